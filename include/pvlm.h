@@ -1,0 +1,217 @@
+/*
+ * pvlm.h -- C ABI of the ParallelVLM verify + UV-Prune + accept hot path
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * The five calls follow the paper's statement of the problem
+ * (ParallelVLM, arXiv 2603.19610):
+ *   pvlm_verify_attn    target verification forward over the video KV cache
+ *                       (Sec. 2.2; Sec. 4.2 Parallel Decoding), fused with the
+ *                       per-token verifier attention mass (Sec. 3, Challenge 2)
+ *   pvlm_uvprune_score  UV-Prune variation score, Eq. (average_similarity),
+ *                       over Eq. (similarity) or over a per-layer criterion
+ *   pvlm_topk_select    Eq. (topk_selection): keep the top 1 - alpha fraction
+ *   pvlm_gather_kv      the draft's compact cache [V*, X] (Sec. 4.2, Stage I)
+ *   pvlm_spec_accept    speculative-sampling accept/reject (Sec. 2.2) with the
+ *                       bonus token of Suppl. B
+ *
+ * Conventions shared by every call
+ *   - Every tensor pointer is a caller-owned DEVICE pointer.  The library never
+ *     allocates, frees or keeps a pointer past the call.
+ *   - Every call is asynchronous on the given stream: no device-wide sync and no
+ *     host<->device copy happens inside a call.  Results are valid once the
+ *     stream reaches the call's completion.
+ *   - Host-side arguments (sizes, capacities, pointer NULL-ness) are validated
+ *     before anything is launched; a failing call launches nothing.
+ *   - Device-resident sizes (lengths, keep counts) are trusted up to the host
+ *     capacities passed alongside them.  A kernel that finds one out of range
+ *     clamps it into range (so memory is never touched out of bounds) and, if
+ *     `status` is non-NULL, ORs PVLM_DEV_RANGE into *status.
+ *   - Outputs must not alias inputs.  Optional outputs may be NULL.
+ *   - No global mutable state: calls are re-entrant; a workspace buffer must
+ *     not be shared by two calls in flight at the same time.
+ *   - Layouts are C-contiguous, innermost index last.  "bf16" is IEEE
+ *     bfloat16 stored in 2 bytes.
+ */
+#ifndef PVLM_H_
+#define PVLM_H_
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PVLM_OK = 0,
+  PVLM_ERR_NULL = 1,         /* a required pointer is NULL                     */
+  PVLM_ERR_SHAPE = 2,        /* inconsistent or out-of-range size argument     */
+  PVLM_ERR_UNSUPPORTED = 3,  /* valid request this build does not implement    */
+  PVLM_ERR_WORKSPACE = 4,    /* workspace NULL or smaller than required        */
+  PVLM_ERR_HIP = 5           /* a HIP call failed; see pvlm_last_hip_error()   */
+} pvlm_status;
+
+typedef enum { PVLM_F32 = 0, PVLM_BF16 = 1 } pvlm_dtype;
+
+/* Criterion fed to UV-Prune's variation operator. */
+typedef enum {
+  PVLM_CRIT_MASS = 0,   /* a precomputed per-layer criterion stack, e.g. the
+                           verifier attention mass of layers 0..L            */
+  PVLM_CRIT_COSSIM = 1  /* vision-text cosine similarity, Eq. (similarity),
+                           computed from layer-wise hidden states            */
+} pvlm_crit;
+
+/* Bits ORed into the optional device status word. */
+#define PVLM_DEV_RANGE 1    /* a device-resident size or index was out of range */
+#define PVLM_DEV_TIMEOUT 2  /* an inter-workgroup wait gave up (results invalid) */
+
+const char* pvlm_status_string(pvlm_status s);
+/* Text of the last HIP error seen by a pvlm call on this host thread. */
+const char* pvlm_last_hip_error(void);
+int pvlm_version(void);
+
+/* ------------------------------------------------------------------------
+ * pvlm_verify_attn -- target verify attention with fused attention mass.
+ *
+ * Defines (Sec. 2.2 verification in one parallel forward; Sec. 4.2 Parallel
+ * Decoding): for batch b, query head h (KV head g = floor(h*Hkv/Hq)), verify
+ * row t in [0, T): the visible cache rows are i = 0 .. ctx_len[b] + t;
+ *   s_i = scale * <q[b,t,h,:], k[b,g,i,:]>,  P_i = softmax_i(s),
+ *   out[b,t,h,:] = sum_i P_i v[b,g,i,:],     lse[b,h,t] = log sum_i exp(s_i),
+ *   mass[b,i] = sum_{h,t} P_{h,t,i}   (normalised probabilities, summed over
+ *                                      every query head and verify row)
+ * so sum_i mass[b,i] = Hq*T.  This is the attention criterion of
+ * attention-guided pruning (Sec. 3, Challenge 2; Suppl. C).
+ *
+ *   dt        PVLM_BF16 (bf16 in/out, fp32 accumulate) or PVLM_F32.
+ *   T         verify rows = gamma + 1, 1..32.  The last T valid cache rows of
+ *             each sequence, [ctx_len[b], ctx_len[b]+T), are the verify block
+ *             (causal among themselves).
+ *   Hq, Hkv   query / KV heads, Hq % Hkv == 0, (Hq/Hkv)*T <= 640.
+ *   D         head dim, 64 or 128.
+ *   n_cap     cache capacity in rows (>= max_ctx + T).
+ *   max_ctx   host upper bound of every ctx_len[b] (used to plan the launch);
+ *             pass n_cap - T when unknown.
+ *   scale     softmax scale, normally 1/sqrt(D).
+ *   q         [B][T][Hq][D] post-RoPE queries.
+ *   k_cache,
+ *   v_cache   [B][Hkv][n_cap][D] post-RoPE keys / values.
+ *   ctx_len   [B] int32 device array, context rows before the verify block.
+ *   out       [B][T][Hq][D], dtype dt.
+ *   mass      [B][n_cap] fp32 or NULL; rows >= ctx_len[b]+T are written 0.
+ *   lse       [B][Hq][T] fp32 (natural log) or NULL.
+ *   ws        device workspace of >= pvlm_verify_attn_workspace_size() bytes,
+ *             zero-filled before its first use; every call leaves its
+ *             synchronisation words zeroed again.
+ *   status    optional device int32, see PVLM_DEV_*.
+ * ---------------------------------------------------------------------- */
+size_t pvlm_verify_attn_workspace_size(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D,
+                                       int64_t n_cap, int64_t max_ctx);
+pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D,
+                             int64_t n_cap, int64_t max_ctx, float scale,
+                             const void* q, const void* k_cache, const void* v_cache,
+                             const int32_t* ctx_len, void* out, float* mass, float* lse,
+                             void* ws, size_t ws_bytes, int32_t* status, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * pvlm_uvprune_score -- UV-Prune score, Eq. (average_similarity):
+ *   score[b,i] = sum_{j<n[b]} sum_{l=1..L} (S^l_ij - S^{l-1}_ij)   (COSSIM)
+ *   score[b,i] = sum_{l=1..L} (c^l_i - c^{l-1}_i)                (MASS)
+ * for visual tokens i < m[b]; score[b, i >= m[b]] is written 0.  S^l is the
+ * cosine similarity of Eq. (similarity) between hidden states at layer l
+ * (layer 0 = decoder input), 0 when either vector has zero norm.  Both sums
+ * telescope exactly, so only layers 0 and L are read.
+ *
+ *   crit        PVLM_CRIT_MASS or PVLM_CRIT_COSSIM.
+ *   L           early layers, >= 1.
+ *   m_cap       visual-row capacity; m: [B] int32 device, m[b] <= m_cap.
+ *   crit_stack  MASS: [L+1][B][m_cap] fp32 (NULL for COSSIM).
+ *   hdt, Dh     COSSIM: hidden-state dtype and hidden size (multiple of 8).
+ *   n_cap,n_txt COSSIM: text-row capacity and [B] int32 device text counts.
+ *   hs_vis      COSSIM: [L+1][B][m_cap][Dh] visual hidden states.
+ *   hs_txt      COSSIM: [L+1][B][n_cap][Dh] text hidden states.
+ *   score       [B][m_cap] fp32 output.
+ *   ws          COSSIM only: >= pvlm_uvprune_workspace_size() bytes.
+ * ---------------------------------------------------------------------- */
+size_t pvlm_uvprune_workspace_size(pvlm_crit crit, int B, int Dh, int64_t n_cap);
+pvlm_status pvlm_uvprune_score(pvlm_crit crit, int B, int L, int64_t m_cap, const int32_t* m,
+                               const float* crit_stack, pvlm_dtype hdt, int Dh, int64_t n_cap,
+                               const int32_t* n_txt, const void* hs_vis, const void* hs_txt,
+                               float* score, void* ws, size_t ws_bytes, int32_t* status,
+                               hipStream_t stream);
+
+/* One layer of the COSSIM criterion, c[b,i] = sum_{j<n[b]} cos(hv[b,i], ht[b,j])
+ * (Eq. similarity summed over text tokens), for streaming use: a caller can
+ * write c^0 and c^L into a criterion stack and call pvlm_uvprune_score(MASS).
+ *   hs_vis [B][m_cap][Dh], hs_txt [B][n_cap][Dh]; crit_out [B][m_cap] fp32. */
+pvlm_status pvlm_uvprune_criterion_cossim(int B, int64_t m_cap, const int32_t* m, pvlm_dtype hdt,
+                                          int Dh, int64_t n_cap, const int32_t* n_txt,
+                                          const void* hs_vis, const void* hs_txt, float* crit_out,
+                                          void* ws, size_t ws_bytes, int32_t* status,
+                                          hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * pvlm_topk_select -- Eq. (topk_selection).  For each b keep the k[b]
+ * visual tokens of largest score[b, 0..m[b]) (k[b] = floor(m[b]*(1-alpha)),
+ * Sec. 4.2), ranking larger scores first, the lower index first among equal
+ * scores, -0.0 equal to +0.0 and NaN below every number.  The kept indices
+ * are written in ascending order to idx[b, 0..k[b]) and idx[b, k[b]..k_cap)
+ * is set to -1.  k[b] = 0 is legal (alpha = 1).
+ *   score [B][m_cap] fp32; m, k: [B] int32 device; idx [B][k_cap] int32.
+ * ---------------------------------------------------------------------- */
+size_t pvlm_topk_workspace_size(int B, int64_t m_cap);
+pvlm_status pvlm_topk_select(int B, int64_t m_cap, const int32_t* m, const int32_t* k,
+                             int32_t k_cap, const float* score, int32_t* idx, void* ws,
+                             size_t ws_bytes, int32_t* status, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * pvlm_gather_kv -- compact draft cache (Sec. 4.2 Stage I: the draft holds
+ * [V*, X]).  For every b and KV head g:
+ *   dst[b,g,r]      = src[b,g,idx[b,r]]             r < k[b]
+ *   dst[b,g,k[b]+r] = src[b,g,tail_begin[b]+r]      r < tail_len[b]
+ * for both K and V; rows keep their original RoPE rotation.  Rows past
+ * k[b]+tail_len[b] are left untouched.
+ *   k_cache, v_cache [B][Hkv][n_cap][D]; k_dst, v_dst [B][Hkv][dst_cap][D];
+ *   idx [B][k_cap] int32 (entries < k[b] must lie in [0, n_cap));
+ *   k, tail_begin, tail_len: [B] int32 device.
+ * ---------------------------------------------------------------------- */
+pvlm_status pvlm_gather_kv(pvlm_dtype dt, int B, int Hkv, int D, int64_t n_cap,
+                           const void* k_cache, const void* v_cache, const int32_t* idx,
+                           const int32_t* k, int32_t k_cap, const int32_t* tail_begin,
+                           const int32_t* tail_len, int64_t dst_cap, void* k_dst, void* v_dst,
+                           int32_t* status, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * pvlm_spec_accept -- speculative-sampling accept/reject (Sec. 2.2) with the
+ * bonus token after full acceptance (Suppl. B).  With p_t = softmax(
+ * target_logits[b,t]/temperature) and q_t = softmax(draft_logits[b,t]/
+ * temperature) (float64, maximum subtracted first):
+ *   draft token x_t is accepted iff u_accept[b,t] * q_t(x_t) < p_t(x_t),
+ *   scanning t = 0..gamma-1 and stopping at the first rejection a;
+ *   n_accepted[b] = a (= gamma if none rejected);
+ *   next_token[b] is drawn by inverse CDF (ascending vocabulary order, first
+ *   y whose cumulative mass exceeds u_sample[b] * total) from
+ *   max(0, p_a - q_a) after a rejection (from p_a if that is all zero), or
+ *   from p_gamma (the bonus) after full acceptance.
+ * temperature == 0 is greedy: accept iff x_t is the target argmax (lowest
+ * index on ties) and next_token is the target argmax at position a.
+ * The library draws no random numbers; decisions are taken in float64.
+ *   draft_logits [B][gamma][V] fp32, target_logits [B][gamma+1][V] fp32
+ *   (finite or -inf, at least one finite per row), draft_tokens [B][gamma],
+ *   u_accept [B][gamma] f64 in [0,1), u_sample [B] f64 in [0,1).
+ *   near_tie (nullable) [B]: 1 when a decision or the draw fell within 1e-9
+ *   (relative) of its boundary, where another summation order could flip it.
+ * ---------------------------------------------------------------------- */
+size_t pvlm_spec_accept_workspace_size(int B, int gamma, int V);
+pvlm_status pvlm_spec_accept(int B, int gamma, int V, float temperature,
+                             const float* draft_logits, const float* target_logits,
+                             const int32_t* draft_tokens, const double* u_accept,
+                             const double* u_sample, int32_t* n_accepted, int32_t* next_token,
+                             int32_t* near_tie, void* ws, size_t ws_bytes, int32_t* status,
+                             hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PVLM_H_ */

@@ -1,0 +1,343 @@
+"""Python binding of libpvlm.so, the MI355X (gfx950) ParallelVLM hot path.
+
+Argument marshalling only: every step runs in the library's HIP kernels.
+Tensors must be CUDA (HIP) tensors on the current device, C-contiguous, with
+the dtypes the C ABI (include/pvlm.h) names.  Calls are enqueued on
+``torch.cuda.current_stream()`` and return without synchronising.
+
+There is no CPU fallback: if libpvlm.so is missing the import of a call's
+library raises, telling the caller to build it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libpvlm.so")
+
+PVLM_F32, PVLM_BF16 = 0, 1
+PVLM_CRIT_MASS, PVLM_CRIT_COSSIM = 0, 1
+PVLM_DEV_RANGE, PVLM_DEV_TIMEOUT = 1, 2
+
+EXPORTS = (
+    "pvlm_status_string", "pvlm_last_hip_error", "pvlm_version",
+    "pvlm_verify_attn_workspace_size", "pvlm_verify_attn",
+    "pvlm_uvprune_workspace_size", "pvlm_uvprune_score", "pvlm_uvprune_criterion_cossim",
+    "pvlm_topk_workspace_size", "pvlm_topk_select",
+    "pvlm_gather_kv",
+    "pvlm_spec_accept_workspace_size", "pvlm_spec_accept",
+)
+
+
+class PvlmError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str = ""):
+        self.status = status
+        msg = f"{where}: pvlm status {status}"
+        if detail:
+            msg += f" ({detail})"
+        super().__init__(msg)
+
+
+_lib = None
+_lib_lock = threading.Lock()
+
+_c = ctypes
+_P = _c.c_void_p
+_I = _c.c_int
+_I64 = _c.c_int64
+_SZ = _c.c_size_t
+_F = _c.c_float
+
+_SIGS = {
+    "pvlm_status_string": (_c.c_char_p, [_I]),
+    "pvlm_last_hip_error": (_c.c_char_p, []),
+    "pvlm_version": (_I, []),
+    "pvlm_verify_attn_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I64, _I64]),
+    "pvlm_verify_attn": (_I, [_I, _I, _I, _I, _I, _I, _I64, _I64, _F, _P, _P, _P, _P, _P, _P, _P,
+                              _P, _SZ, _P, _P]),
+    "pvlm_uvprune_workspace_size": (_SZ, [_I, _I, _I, _I64]),
+    "pvlm_uvprune_score": (_I, [_I, _I, _I, _I64, _P, _P, _I, _I, _I64, _P, _P, _P, _P, _P, _SZ,
+                                _P, _P]),
+    "pvlm_uvprune_criterion_cossim": (_I, [_I, _I64, _P, _I, _I, _I64, _P, _P, _P, _P, _P, _SZ,
+                                           _P, _P]),
+    "pvlm_topk_workspace_size": (_SZ, [_I, _I64]),
+    "pvlm_topk_select": (_I, [_I, _I64, _P, _P, _I, _P, _P, _P, _SZ, _P, _P]),
+    "pvlm_gather_kv": (_I, [_I, _I, _I, _I, _I64, _P, _P, _P, _P, _I, _P, _P, _I64, _P, _P, _P,
+                            _P]),
+    "pvlm_spec_accept_workspace_size": (_SZ, [_I, _I, _I]),
+    "pvlm_spec_accept": (_I, [_I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P]),
+}
+
+
+def lib():
+    """The loaded libpvlm.so (loads it on first use; raises if not built)."""
+    global _lib
+    if _lib is None:
+        with _lib_lock:
+            if _lib is None:
+                if not os.path.exists(LIB_PATH):
+                    raise RuntimeError(
+                        f"{LIB_PATH} is not built; run `python -c 'import __graft_entry__ as g; "
+                        "g.build()'` or `python -m paper_2603_19610_amd.build`")
+                L = ctypes.CDLL(LIB_PATH)
+                for name, (res, args) in _SIGS.items():
+                    fn = getattr(L, name)
+                    fn.restype = res
+                    fn.argtypes = args
+                _lib = L
+    return _lib
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        L = lib()
+        detail = L.pvlm_status_string(status).decode()
+        if status == 5:
+            detail += ": " + L.pvlm_last_hip_error().decode()
+        raise PvlmError(status, where, detail)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _need(t: torch.Tensor, name: str, dtype=None, device=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return PVLM_BF16
+    if t.dtype == torch.float32:
+        return PVLM_F32
+    raise ValueError(f"unsupported dtype {t.dtype}")
+
+
+class Workspace:
+    """A zero-initialised device scratch buffer that grows on demand.
+
+    The library leaves its synchronisation words zeroed after every call, so
+    one buffer can serve successive calls on a stream (not concurrent ones).
+    """
+
+    def __init__(self, device=None):
+        self.device = torch.device("cuda", torch.cuda.current_device()) if device is None else device
+        self.buf = torch.zeros(256, dtype=torch.uint8, device=self.device)
+
+    def get(self, nbytes: int) -> torch.Tensor:
+        if nbytes > self.buf.numel():
+            self.buf = torch.zeros(max(nbytes, 2 * self.buf.numel()), dtype=torch.uint8,
+                                   device=self.device)
+        return self.buf
+
+
+_ws_cache = {}
+
+
+def _default_ws(kind: str) -> Workspace:
+    key = (kind, torch.cuda.current_device())
+    ws = _ws_cache.get(key)
+    if ws is None:
+        ws = _ws_cache[key] = Workspace()
+    return ws
+
+
+# ------------------------------------------------------------------ calls --
+def verify_attn_workspace_size(dtype: int, B, T, Hq, Hkv, D, n_cap, max_ctx) -> int:
+    return int(lib().pvlm_verify_attn_workspace_size(dtype, B, T, Hq, Hkv, D, n_cap, max_ctx))
+
+
+def verify_attn(q, k_cache, v_cache, ctx_len, *, scale: Optional[float] = None,
+                max_ctx: Optional[int] = None, out=None, mass=None, lse=None,
+                want_mass: bool = True, want_lse: bool = True, ws: Optional[Workspace] = None,
+                status=None):
+    """Verify attention + attention mass.  q [B][T][Hq][D]; caches [B][Hkv][n_cap][D];
+    ctx_len [B] int32.  Returns (out, mass or None, lse or None)."""
+    _need(q, "q")
+    dev = q.device
+    _need(k_cache, "k_cache", q.dtype, dev)
+    _need(v_cache, "v_cache", q.dtype, dev)
+    _need(ctx_len, "ctx_len", torch.int32, dev)
+    B, T, Hq, D = q.shape
+    Bk, Hkv, n_cap, Dk = k_cache.shape
+    if Bk != B or Dk != D or tuple(v_cache.shape) != tuple(k_cache.shape) or ctx_len.numel() != B:
+        raise ValueError("inconsistent verify_attn shapes")
+    dt = _dt(q)
+    if scale is None:
+        scale = D ** -0.5
+    if max_ctx is None:
+        max_ctx = n_cap - T
+    if out is None:
+        out = torch.empty_like(q)
+    _need(out, "out", q.dtype, dev)
+    if mass is None and want_mass:
+        mass = torch.empty((B, n_cap), dtype=torch.float32, device=dev)
+    if mass is not None:
+        _need(mass, "mass", torch.float32, dev)
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq, T), dtype=torch.float32, device=dev)
+    if lse is not None:
+        _need(lse, "lse", torch.float32, dev)
+    need = verify_attn_workspace_size(dt, B, T, Hq, Hkv, D, n_cap, max_ctx)
+    wsb = (ws or _default_ws("verify")).get(need)
+    st = lib().pvlm_verify_attn(dt, B, T, Hq, Hkv, D, n_cap, max_ctx, float(scale), _ptr(q),
+                                _ptr(k_cache), _ptr(v_cache), _ptr(ctx_len), _ptr(out), _ptr(mass),
+                                _ptr(lse), _ptr(wsb), wsb.numel(), _ptr(status), _stream())
+    _check(st, "pvlm_verify_attn")
+    return out, mass, lse
+
+
+def uvprune_score_mass(crit_stack, m, *, score=None, status=None):
+    """score = UV-Prune variation over a criterion stack crit_stack [L+1][B][m_cap] fp32."""
+    _need(crit_stack, "crit_stack", torch.float32)
+    dev = crit_stack.device
+    _need(m, "m", torch.int32, dev)
+    Lp1, B, m_cap = crit_stack.shape
+    if score is None:
+        score = torch.empty((B, m_cap), dtype=torch.float32, device=dev)
+    _need(score, "score", torch.float32, dev)
+    st = lib().pvlm_uvprune_score(PVLM_CRIT_MASS, B, Lp1 - 1, m_cap, _ptr(m), _ptr(crit_stack),
+                                  PVLM_F32, 0, 0, None, None, None, _ptr(score), None, 0,
+                                  _ptr(status), _stream())
+    _check(st, "pvlm_uvprune_score")
+    return score
+
+
+def uvprune_score_cossim(hs_vis, hs_txt, m, n_txt, *, score=None, ws=None, status=None):
+    """Eq. (average_similarity) from hidden states hs_vis [L+1][B][m_cap][Dh], hs_txt [L+1][B][n_cap][Dh]."""
+    _need(hs_vis, "hs_vis")
+    dev = hs_vis.device
+    _need(hs_txt, "hs_txt", hs_vis.dtype, dev)
+    _need(m, "m", torch.int32, dev)
+    _need(n_txt, "n_txt", torch.int32, dev)
+    Lp1, B, m_cap, Dh = hs_vis.shape
+    n_cap = hs_txt.shape[2]
+    if hs_txt.shape[0] != Lp1 or hs_txt.shape[1] != B or hs_txt.shape[3] != Dh:
+        raise ValueError("inconsistent hidden-state shapes")
+    if score is None:
+        score = torch.empty((B, m_cap), dtype=torch.float32, device=dev)
+    _need(score, "score", torch.float32, dev)
+    need = int(lib().pvlm_uvprune_workspace_size(PVLM_CRIT_COSSIM, B, Dh, n_cap))
+    wsb = (ws or _default_ws("uvprune")).get(need)
+    st = lib().pvlm_uvprune_score(PVLM_CRIT_COSSIM, B, Lp1 - 1, m_cap, _ptr(m), None,
+                                  _dt(hs_vis), Dh, n_cap, _ptr(n_txt), _ptr(hs_vis), _ptr(hs_txt),
+                                  _ptr(score), _ptr(wsb), wsb.numel(), _ptr(status), _stream())
+    _check(st, "pvlm_uvprune_score")
+    return score
+
+
+def uvprune_criterion_cossim(hv, ht, m, n_txt, *, out=None, ws=None, status=None):
+    """One layer: c[b,i] = sum_j cos(hv[b,i], ht[b,j]); hv [B][m_cap][Dh], ht [B][n_cap][Dh]."""
+    _need(hv, "hv")
+    dev = hv.device
+    _need(ht, "ht", hv.dtype, dev)
+    _need(m, "m", torch.int32, dev)
+    _need(n_txt, "n_txt", torch.int32, dev)
+    B, m_cap, Dh = hv.shape
+    n_cap = ht.shape[1]
+    if out is None:
+        out = torch.empty((B, m_cap), dtype=torch.float32, device=dev)
+    _need(out, "out", torch.float32, dev)
+    need = int(lib().pvlm_uvprune_workspace_size(PVLM_CRIT_COSSIM, B, Dh, n_cap))
+    wsb = (ws or _default_ws("uvprune")).get(need)
+    st = lib().pvlm_uvprune_criterion_cossim(B, m_cap, _ptr(m), _dt(hv), Dh, n_cap, _ptr(n_txt),
+                                             _ptr(hv), _ptr(ht), _ptr(out), _ptr(wsb), wsb.numel(),
+                                             _ptr(status), _stream())
+    _check(st, "pvlm_uvprune_criterion_cossim")
+    return out
+
+
+def topk_select(score, m, k, k_cap: int, *, idx=None, status=None):
+    """Ascending kept indices [B][k_cap] (-1 padded)."""
+    _need(score, "score", torch.float32)
+    dev = score.device
+    _need(m, "m", torch.int32, dev)
+    _need(k, "k", torch.int32, dev)
+    B, m_cap = score.shape
+    if idx is None:
+        idx = torch.empty((B, k_cap), dtype=torch.int32, device=dev)
+    _need(idx, "idx", torch.int32, dev)
+    st = lib().pvlm_topk_select(B, m_cap, _ptr(m), _ptr(k), int(k_cap), _ptr(score), _ptr(idx),
+                                None, 0, _ptr(status), _stream())
+    _check(st, "pvlm_topk_select")
+    return idx
+
+
+def gather_kv(k_cache, v_cache, idx, k, tail_begin, tail_len, dst_cap: int, *, k_dst=None,
+              v_dst=None, status=None):
+    """Compact cache [B][Hkv][dst_cap][D]: kept rows then tail rows."""
+    _need(k_cache, "k_cache")
+    dev = k_cache.device
+    _need(v_cache, "v_cache", k_cache.dtype, dev)
+    _need(idx, "idx", torch.int32, dev)
+    for name, t in (("k", k), ("tail_begin", tail_begin), ("tail_len", tail_len)):
+        _need(t, name, torch.int32, dev)
+    B, Hkv, n_cap, D = k_cache.shape
+    if k_dst is None:
+        k_dst = torch.zeros((B, Hkv, dst_cap, D), dtype=k_cache.dtype, device=dev)
+    if v_dst is None:
+        v_dst = torch.zeros((B, Hkv, dst_cap, D), dtype=k_cache.dtype, device=dev)
+    _need(k_dst, "k_dst", k_cache.dtype, dev)
+    _need(v_dst, "v_dst", k_cache.dtype, dev)
+    st = lib().pvlm_gather_kv(_dt(k_cache), B, Hkv, D, n_cap, _ptr(k_cache), _ptr(v_cache),
+                              _ptr(idx), _ptr(k), idx.shape[1], _ptr(tail_begin), _ptr(tail_len),
+                              dst_cap, _ptr(k_dst), _ptr(v_dst), _ptr(status), _stream())
+    _check(st, "pvlm_gather_kv")
+    return k_dst, v_dst
+
+
+def spec_accept(draft_logits, target_logits, draft_tokens, u_accept, u_sample,
+                temperature: float, *, n_accepted=None, next_token=None, near_tie=None,
+                ws: Optional[Workspace] = None, status=None):
+    """Returns (n_accepted [B], next_token [B], near_tie [B]) int32 tensors."""
+    _need(draft_logits, "draft_logits", torch.float32)
+    dev = draft_logits.device
+    _need(target_logits, "target_logits", torch.float32, dev)
+    _need(draft_tokens, "draft_tokens", torch.int32, dev)
+    _need(u_accept, "u_accept", torch.float64, dev)
+    _need(u_sample, "u_sample", torch.float64, dev)
+    B, gamma, V = draft_logits.shape
+    if tuple(target_logits.shape) != (B, gamma + 1, V):
+        raise ValueError("target_logits must be [B][gamma+1][V]")
+    if n_accepted is None:
+        n_accepted = torch.empty(B, dtype=torch.int32, device=dev)
+    if next_token is None:
+        next_token = torch.empty(B, dtype=torch.int32, device=dev)
+    if near_tie is None:
+        near_tie = torch.empty(B, dtype=torch.int32, device=dev)
+    need = int(lib().pvlm_spec_accept_workspace_size(B, gamma, V))
+    wsb = (ws or _default_ws("accept")).get(need)
+    st = lib().pvlm_spec_accept(B, gamma, V, float(temperature), _ptr(draft_logits),
+                                _ptr(target_logits), _ptr(draft_tokens), _ptr(u_accept),
+                                _ptr(u_sample), _ptr(n_accepted), _ptr(next_token), _ptr(near_tie),
+                                _ptr(wsb), wsb.numel(), _ptr(status), _stream())
+    _check(st, "pvlm_spec_accept")
+    return n_accepted, next_token, near_tie
+
+
+__all__ = [
+    "LIB_PATH", "EXPORTS", "PvlmError", "Workspace", "lib", "verify_attn",
+    "verify_attn_workspace_size", "uvprune_score_mass", "uvprune_score_cossim",
+    "uvprune_criterion_cossim", "topk_select", "gather_kv", "spec_accept",
+    "PVLM_F32", "PVLM_BF16", "PVLM_CRIT_MASS", "PVLM_CRIT_COSSIM", "PVLM_DEV_RANGE",
+    "PVLM_DEV_TIMEOUT",
+]

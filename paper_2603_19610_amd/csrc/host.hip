@@ -1,0 +1,61 @@
+// Host-side helpers of the pvlm library: status strings, HIP error capture and
+// the per-device compute-unit count used to size launches.
+#include <mutex>
+#include <string>
+
+#include "common.h"
+
+namespace pvlm {
+
+namespace {
+thread_local std::string g_last_hip_error;
+std::mutex g_info_mu;
+constexpr int kMaxDevices = 64;
+int g_cus[kMaxDevices] = {0};
+}  // namespace
+
+void set_hip_error(hipError_t e) {
+  g_last_hip_error = std::string(hipGetErrorName(e)) + ": " + hipGetErrorString(e);
+}
+
+pvlm_status hip_check(hipError_t e) {
+  if (e == hipSuccess) return PVLM_OK;
+  set_hip_error(e);
+  return PVLM_ERR_HIP;
+}
+
+pvlm_status device_info(DeviceInfo* out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_check(e);
+  if (dev < 0 || dev >= kMaxDevices) return PVLM_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_info_mu);
+  if (g_cus[dev] == 0) {
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_check(e);
+    if (cus <= 0) return PVLM_ERR_HIP;
+    g_cus[dev] = cus;
+  }
+  out->cus = g_cus[dev];
+  out->xcds = 8;
+  return PVLM_OK;
+}
+
+}  // namespace pvlm
+
+extern "C" const char* pvlm_status_string(pvlm_status s) {
+  switch (s) {
+    case PVLM_OK: return "ok";
+    case PVLM_ERR_NULL: return "a required pointer is NULL";
+    case PVLM_ERR_SHAPE: return "inconsistent or out-of-range size argument";
+    case PVLM_ERR_UNSUPPORTED: return "unsupported dtype, head dim or shape";
+    case PVLM_ERR_WORKSPACE: return "workspace missing or too small";
+    case PVLM_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+extern "C" const char* pvlm_last_hip_error(void) { return pvlm::g_last_hip_error.c_str(); }
+
+extern "C" int pvlm_version(void) { return 1; }

@@ -1,0 +1,851 @@
+// Verify attention with fused per-token attention mass (gfx950).
+//
+// Defines the target's verification forward over the video KV cache
+// (ParallelVLM Sec. 2.2; Sec. 4.2 Parallel Decoding) for the gamma + 1 verify
+// rows, fused with the per-token attention mass that attention-guided pruning
+// ranks visual tokens by (Sec. 3, Challenge 2; Suppl. C attention criterion).
+// The paper runs FlashAttention-2 on NVIDIA GPUs and notes that an explicit
+// score matrix is what makes attention-guided pruning incompatible with
+// block-wise kernels (Sec. 3, Sec. 5.4): here the mass is produced inside the
+// block-wise kernel, with no score matrix in memory.
+//
+// Design (one launch of the main kernel + one small combine launch):
+//  * Work unit = (batch b, KV head g, row group rg, token chunk).  All
+//    (Hq/Hkv) * T query rows of a KV head are packed as the N side of
+//    v_mfma_f32_16x16x32_bf16 tiles (16 rows per tile, at most 5 tiles per
+//    workgroup); tokens are the M side, so each lane ends up owning one query
+//    row and four tokens of every score tile.
+//  * Pass 1 streams K straight from HBM into the MFMA operand registers
+//    (no LDS), forms the scores, and keeps them in registers ("resident"
+//    variant, chunks up to 512 tokens per workgroup) together with each
+//    row's local max and exp-sum.
+//  * The workgroups of one (b, g, rg) exchange those statistics through the
+//    workspace and wait on a counter (cooperative launch: the whole grid is
+//    co-resident), which gives every workgroup each row's exact global
+//    log-sum-exp.
+//  * Pass 2 streams V, turns the resident scores into exactly normalised
+//    probabilities, reduces them over the rows into the per-token mass, and
+//    accumulates P.V on MFMA.  Because P is already normalised, the chunk
+//    partial outputs only need to be summed.
+//  * Chunks too long for registers use the "stream" variant, which recomputes
+//    the scores from K in pass 2 (K is read twice).
+//  * fp32 inputs take a VALU path with the same two-pass structure.
+#include "common.h"
+
+namespace pvlm {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kThreads = kWaves * 64;
+constexpr int kMaxRT = 5;        // 16-row tiles per workgroup
+constexpr int kNB = 4;           // 32-token blocks per wave (resident variant)
+constexpr int kResTokens = kWaves * kNB * 32;
+constexpr int kF32Tile = 64;     // tokens per step of the fp32 path
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kNegInf = -__builtin_huge_valf();
+
+struct VArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const int32_t* ctx_len;
+  float* stats;   // [groups][splits][ROWS][2]  (log2-domain max, exp-sum)
+  float* opart;   // [groups][splits][ROWS][D]
+  float* mpart;   // [B][Hkv*RG][n_cap]
+  int* cnt;       // [groups]
+  int32_t* status;
+  int64_t n_cap;
+  int B, T, Hq, Hkv, G, R, RG, RT, D;
+  int max_ctx;
+  int splits, chunk, grp_base, ngrp, grid;
+  float sl2;      // scale * log2(e)
+};
+
+struct Unit {
+  int grp, split, b, g, rg, ctx, N, c0, c1;
+};
+
+__device__ __forceinline__ bool decode_unit(const VArgs& a, Unit& u) {
+  const int i = blockIdx.x;
+  const int per_xcd = a.grid / 8;
+  const int lg = (i % 8) * per_xcd + i / 8;  // consecutive logical units share an XCD
+  if (lg >= a.ngrp * a.splits) return false;
+  u.grp = a.grp_base + lg / a.splits;
+  u.split = lg % a.splits;
+  u.rg = u.grp % a.RG;
+  const int bg = u.grp / a.RG;
+  u.g = bg % a.Hkv;
+  u.b = bg / a.Hkv;
+  int ctx = a.ctx_len[u.b];
+  if (ctx < 0 || ctx > a.max_ctx) {
+    if (u.split == 0 && threadIdx.x == 0) dev_flag(a.status, PVLM_DEV_RANGE);
+    ctx = ctx < 0 ? 0 : a.max_ctx;
+  }
+  u.ctx = ctx;
+  u.N = ctx + a.T;
+  u.c0 = u.split * a.chunk;
+  u.c1 = min(u.c0 + a.chunk, u.N);
+  return true;
+}
+
+__device__ __forceinline__ void lse_combine(float& m, float& z, float m2, float z2) {
+  const float M = fmaxf(m, m2);
+  if (M == kNegInf) {
+    m = kNegInf;
+    z = 0.f;
+    return;
+  }
+  z = z * exp2f(m - M) + z2 * exp2f(m2 - M);
+  m = M;
+}
+
+// Publish this workgroup's per-row (max, exp-sum), wait for the other chunks
+// of the same (b, g, rg), and leave each row's global log2-sum-exp in s_lse
+// (+inf for padding rows so their probabilities are 0).
+template <int ROWS>
+__device__ void exchange_stats(const VArgs& a, const Unit& u, float* s_m, float* s_z,
+                               float* s_lse, bool wait) {
+  float* st = a.stats + ((size_t)u.grp * a.splits + u.split) * ROWS * 2;
+  for (int r = threadIdx.x; r < ROWS; r += kThreads) {
+    st_agent(st + 2 * r, s_m[r]);
+    st_agent(st + 2 * r + 1, s_z[r]);
+  }
+  wg_arrive_wait(a.cnt + u.grp, a.splits, a.status, wait);
+  if (!wait) return;
+  const float* st0 = a.stats + (size_t)u.grp * a.splits * ROWS * 2;
+  for (int r = threadIdx.x; r < ROWS; r += kThreads) {
+    float M = kNegInf, Z = 0.f;
+    for (int s = 0; s < a.splits; ++s) {
+      const float m2 = ld_agent(st0 + ((size_t)s * ROWS + r) * 2);
+      const float z2 = ld_agent(st0 + ((size_t)s * ROWS + r) * 2 + 1);
+      lse_combine(M, Z, m2, z2);
+    }
+    const int row = u.rg * a.RT * 16 + r;
+    s_lse[r] = (row < a.R && Z > 0.f) ? M + __log2f(Z) : __builtin_huge_valf();
+  }
+  __syncthreads();
+}
+
+// ------------------------------------------------------------ MFMA path --
+template <int D>
+struct VVec;
+template <>
+struct VVec<128> {
+  typedef uint4 T;
+};
+template <>
+struct VVec<64> {
+  typedef uint2 T;
+};
+
+__device__ __forceinline__ uint32_t word_of(const uint4& v, int w) {
+  return w == 0 ? v.x : w == 1 ? v.y : w == 2 ? v.z : v.w;
+}
+__device__ __forceinline__ uint32_t word_of(const uint2& v, int w) { return w == 0 ? v.x : v.y; }
+
+// B operand of P.V for output column group jd: element s is V[token(s)][DPL*n + jd].
+template <typename VT>
+__device__ __forceinline__ bf16x8 pack_v(const VT (&vr)[8], int jd) {
+  const uint32_t sel = (jd & 1) ? 0x07060302u : 0x05040100u;
+  uint32_t w[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p)
+    w[p] = __builtin_amdgcn_perm(word_of(vr[2 * p + 1], jd >> 1), word_of(vr[2 * p], jd >> 1), sel);
+  uint4 u = make_uint4(w[0], w[1], w[2], w[3]);
+  return __builtin_bit_cast(bf16x8, u);
+}
+
+template <int D, int RT>
+__device__ __forceinline__ void load_q(const VArgs& a, const Unit& u, int n, int gq,
+                                       bf16x8 (&Qb)[RT][D / 32]) {
+  const uint16_t* q = static_cast<const uint16_t*>(a.q);
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    const int row = u.rg * a.RT * 16 + rt * 16 + n;
+    const bool ok = row < a.R;
+    const int t = ok ? row / a.G : 0;
+    const int h = u.g * a.G + (ok ? row % a.G : 0);
+    const uint16_t* qp = q + (((size_t)u.b * a.T + t) * a.Hq + h) * D + 8 * gq;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      uint4 v = ok ? *reinterpret_cast<const uint4*>(qp + 32 * ks) : make_uint4(0, 0, 0, 0);
+      Qb[rt][ks] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+}
+
+// K operand of one 32-token block: lane (n, gq) loads token tb + 16*tt + n,
+// d in [32*ks + 8*gq, +8).
+template <int D>
+__device__ __forceinline__ void load_k_block(const uint16_t* kg, int tb, int c1, int n, int gq,
+                                             uint4 (&Kr)[2][D / 32]) {
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt) {
+    const int tok = tb + 16 * tt + n;
+    const uint16_t* kp = kg + (size_t)tok * D + 8 * gq;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks)
+      Kr[tt][ks] = tok < c1 ? *reinterpret_cast<const uint4*>(kp + 32 * ks) : make_uint4(0, 0, 0, 0);
+  }
+}
+
+// V operand rows of one 32-token block: lane (n, gq) loads tokens
+// tb + {4gq..4gq+3, 16+4gq..16+4gq+3}, d in [DPL*n, DPL*n + DPL).
+template <int D>
+__device__ __forceinline__ void load_v_block(const uint16_t* vg, int tb, int c1, int n, int gq,
+                                             typename VVec<D>::T (&Vr)[8]) {
+  typedef typename VVec<D>::T VT;
+  constexpr int DPL = D / 16;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    const int tok = tb + (s < 4 ? 4 * gq + s : 16 + 4 * gq + (s - 4));
+    VT z;
+    __builtin_memset(&z, 0, sizeof(z));
+    Vr[s] = tok < c1 ? *reinterpret_cast<const VT*>(vg + (size_t)tok * D + DPL * n) : z;
+  }
+}
+
+// Scores of one block in the log2 domain, masked to -inf outside the chunk,
+// past the causal limit of each verify row, and on padding rows.
+template <int D, int RT>
+__device__ __forceinline__ void scores_block(const VArgs& a, const Unit& u, const uint4 (&Kr)[2][D / 32],
+                                             const bf16x8 (&Qb)[RT][D / 32], int tb, int n, int gq,
+                                             float (&S)[2][RT][4]) {
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt) {
+    floatx4 acc[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) acc[rt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      const bf16x8 kk = __builtin_bit_cast(bf16x8, Kr[tt][ks]);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+        acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, Qb[rt][ks], acc[rt], 0, 0, 0);
+    }
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int row = u.rg * a.RT * 16 + rt * 16 + n;
+      const int lim = row < a.R ? min(u.c1 - 1, u.ctx + row / a.G) : -1;  // last visible token
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tok = tb + 16 * tt + 4 * gq + i;
+        S[tt][rt][i] = tok <= lim ? acc[rt][i] * a.sl2 : kNegInf;
+      }
+    }
+  }
+}
+
+template <int RT>
+__device__ __forceinline__ void running_stats(const float (&S)[2][RT][4], float (&m)[RT], float (&z)[RT]) {
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    float mx = kNegInf;
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mx = fmaxf(mx, S[tt][rt][i]);
+    const float M = fmaxf(m[rt], mx);
+    if (M != kNegInf) {
+      float acc = z[rt] * exp2f(m[rt] - M);
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc += exp2f(S[tt][rt][i] - M);
+      z[rt] = acc;
+      m[rt] = M;
+    }
+  }
+}
+
+// Reduce the per-lane (m, z) of each row over the four lane groups and the
+// four waves into s_m / s_z.
+template <int RT>
+__device__ __forceinline__ void reduce_stats(float (&m)[RT], float (&z)[RT], int n, int gq, int w,
+                                             float (*s_wm)[RT * 16], float (*s_wz)[RT * 16], float* s_m,
+                                             float* s_z) {
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+    for (int off = 16; off <= 32; off <<= 1) {
+      const float m2 = __shfl_xor(m[rt], off, 64);
+      const float z2 = __shfl_xor(z[rt], off, 64);
+      lse_combine(m[rt], z[rt], m2, z2);
+    }
+    if (gq == 0) {
+      s_wm[w][rt * 16 + n] = m[rt];
+      s_wz[w][rt * 16 + n] = z[rt];
+    }
+  }
+  __syncthreads();
+  for (int r = threadIdx.x; r < RT * 16; r += kThreads) {
+    float M = s_wm[0][r], Z = s_wz[0][r];
+#pragma unroll
+    for (int ww = 1; ww < kWaves; ++ww) lse_combine(M, Z, s_wm[ww][r], s_wz[ww][r]);
+    s_m[r] = M;
+    s_z[r] = Z;
+  }
+  __syncthreads();
+}
+
+// P = exp2(S - lse2): per-token mass (sum over the block's rows, written to
+// mp) and O += P.V on MFMA.
+template <int D, int RT>
+__device__ __forceinline__ void pv_block(const float (&S)[2][RT][4], const float (&lse)[RT],
+                                         const typename VVec<D>::T (&Vr)[8], floatx4 (&O)[RT][D / 16],
+                                         float* mp, int tb, int c1, int n, int gq) {
+  constexpr int DPL = D / 16;
+  float pm[8];
+#pragma unroll
+  for (int v = 0; v < 8; ++v) pm[v] = 0.f;
+  bf16x8 Pa[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = exp2f(S[tt][rt][i] - lse[rt]);
+        pm[4 * tt + i] += p;
+        Pa[rt][4 * tt + i] = static_cast<__bf16>(p);
+      }
+  }
+  // mass: sum the 8 token values over the 16 lanes of a lane group
+  const bool h8 = n & 8, h4 = n & 4, h2 = n & 2;
+  float a8[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float send = h8 ? pm[k] : pm[4 + k];
+    a8[k] = (h8 ? pm[4 + k] : pm[k]) + __shfl_xor(send, 8, 64);
+  }
+  float a4[2];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const float send = h4 ? a8[k] : a8[2 + k];
+    a4[k] = (h4 ? a8[2 + k] : a8[k]) + __shfl_xor(send, 4, 64);
+  }
+  const float send2 = h2 ? a4[0] : a4[1];
+  float a2 = (h2 ? a4[1] : a4[0]) + __shfl_xor(send2, 2, 64);
+  a2 += __shfl_xor(a2, 1, 64);
+  const int v = (h8 ? 4 : 0) + (h4 ? 2 : 0) + (h2 ? 1 : 0);
+  const int tok = tb + 16 * (v >> 2) + 4 * gq + (v & 3);
+  if (!(n & 1) && tok < c1) mp[tok] = a2;
+#pragma unroll
+  for (int jd = 0; jd < DPL; ++jd) {
+    const bf16x8 vb = pack_v(Vr, jd);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+      O[rt][jd] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Pa[rt], vb, O[rt][jd], 0, 0, 0);
+  }
+}
+
+// Sum the four waves' O fragments through LDS and write the chunk partial
+// (row-major [ROWS][D]) to the workspace.
+template <int D, int RT>
+__device__ __forceinline__ void write_opart(const VArgs& a, const Unit& u, floatx4 (&O)[RT][D / 16],
+                                            float* s_o, int lane, int w, int n, int gq) {
+  constexpr int DPL = D / 16;
+  constexpr int F = RT * 16 * D;
+  float* buf0 = s_o;
+  float* buf1 = s_o + F;
+  auto store = [&](float* buf) {
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int jd = 0; jd < DPL; ++jd)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) buf[((rt * DPL + jd) * 4 + i) * 64 + lane] = O[rt][jd][i];
+  };
+  auto add = [&](const float* buf) {
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int jd = 0; jd < DPL; ++jd)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) O[rt][jd][i] += buf[((rt * DPL + jd) * 4 + i) * 64 + lane];
+  };
+  if (w >= 2) store(w == 2 ? buf0 : buf1);
+  __syncthreads();
+  if (w < 2) add(w == 0 ? buf0 : buf1);
+  __syncthreads();
+  if (w == 1) store(buf0);
+  __syncthreads();
+  if (w == 0) {
+    add(buf0);
+    float* op = a.opart + ((size_t)u.grp * a.splits + u.split) * RT * 16 * D;
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float* dst = op + (size_t)(rt * 16 + 4 * gq + i) * D + DPL * n;
+#pragma unroll
+        for (int jd = 0; jd < DPL; jd += 4)
+          *reinterpret_cast<float4*>(dst + jd) =
+              make_float4(O[rt][jd][i], O[rt][jd + 1][i], O[rt][jd + 2][i], O[rt][jd + 3][i]);
+      }
+  }
+}
+
+template <int D, int RT, bool RESIDENT>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+verify_mfma_kernel(VArgs a) {
+  constexpr int ROWS = RT * 16;
+  constexpr int KS = D / 32;
+  constexpr int DPL = D / 16;
+  typedef typename VVec<D>::T VT;
+  __shared__ float s_wm[kWaves][ROWS], s_wz[kWaves][ROWS];
+  __shared__ float s_m[ROWS], s_z[ROWS], s_lse[ROWS];
+  extern __shared__ float s_o[];
+
+  Unit u;
+  if (!decode_unit(a, u)) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n = lane & 15, gq = lane >> 4;
+  if (u.c0 >= u.N) {  // chunk past this sequence's end: empty statistics, no wait
+    for (int r = threadIdx.x; r < ROWS; r += kThreads) {
+      s_m[r] = kNegInf;
+      s_z[r] = 0.f;
+    }
+    __syncthreads();
+    exchange_stats<ROWS>(a, u, s_m, s_z, s_lse, false);
+    return;
+  }
+  const size_t kv_off = ((size_t)u.b * a.Hkv + u.g) * a.n_cap * D;
+  const uint16_t* kg = static_cast<const uint16_t*>(a.k) + kv_off;
+  const uint16_t* vg = static_cast<const uint16_t*>(a.v) + kv_off;
+  float* mp = a.mpart + ((size_t)u.b * a.Hkv * a.RG + u.g * a.RG + u.rg) * a.n_cap;
+
+  bf16x8 Qb[RT][KS];
+  load_q<D, RT>(a, u, n, gq, Qb);
+  float m[RT], z[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    m[rt] = kNegInf;
+    z[rt] = 0.f;
+  }
+  floatx4 O[RT][DPL];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int jd = 0; jd < DPL; ++jd) O[rt][jd] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  if constexpr (RESIDENT) {
+    // ---- pass 1: all K blocks of this wave in flight, scores kept resident
+    float S[kNB][2][RT][4];
+    uint4 Kr[kNB][2][KS];
+#pragma unroll
+    for (int j = 0; j < kNB; ++j) load_k_block<D>(kg, u.c0 + 32 * (w + kWaves * j), u.c1, n, gq, Kr[j]);
+#pragma unroll
+    for (int j = 0; j < kNB; ++j) {
+      const int tb = u.c0 + 32 * (w + kWaves * j);
+      if (tb < u.c1) {
+        scores_block<D, RT>(a, u, Kr[j], Qb, tb, n, gq, S[j]);
+        running_stats<RT>(S[j], m, z);
+      }
+    }
+    // V of the first two blocks goes in flight before the wait
+    VT Vr[2][8];
+    load_v_block<D>(vg, u.c0 + 32 * w, u.c1, n, gq, Vr[0]);
+    load_v_block<D>(vg, u.c0 + 32 * (w + kWaves), u.c1, n, gq, Vr[1]);
+    reduce_stats<RT>(m, z, n, gq, w, s_wm, s_wz, s_m, s_z);
+    exchange_stats<ROWS>(a, u, s_m, s_z, s_lse, true);
+    float lse[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) lse[rt] = s_lse[rt * 16 + n];
+    // ---- pass 2: probabilities, mass, P.V
+#pragma unroll
+    for (int j = 0; j < kNB; ++j) {
+      const int tb = u.c0 + 32 * (w + kWaves * j);
+      if (tb < u.c1) {
+        if (j + 2 < kNB) {
+          VT Vn[8];
+          load_v_block<D>(vg, u.c0 + 32 * (w + kWaves * (j + 2)), u.c1, n, gq, Vn);
+          pv_block<D, RT>(S[j], lse, Vr[j & 1], O, mp, tb, u.c1, n, gq);
+#pragma unroll
+          for (int s = 0; s < 8; ++s) Vr[j & 1][s] = Vn[s];
+        } else {
+          pv_block<D, RT>(S[j], lse, Vr[j & 1], O, mp, tb, u.c1, n, gq);
+        }
+      }
+    }
+  } else {
+    // ---- pass 1: stream K, running statistics only
+    const int nblk = (u.c1 - u.c0 + 31) / 32;
+    for (int blk = w; blk < nblk; blk += kWaves) {
+      const int tb = u.c0 + 32 * blk;
+      uint4 Kr[2][KS];
+      load_k_block<D>(kg, tb, u.c1, n, gq, Kr);
+      float S[2][RT][4];
+      scores_block<D, RT>(a, u, Kr, Qb, tb, n, gq, S);
+      running_stats<RT>(S, m, z);
+    }
+    reduce_stats<RT>(m, z, n, gq, w, s_wm, s_wz, s_m, s_z);
+    exchange_stats<ROWS>(a, u, s_m, s_z, s_lse, true);
+    float lse[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) lse[rt] = s_lse[rt * 16 + n];
+    // ---- pass 2: recompute scores from K, then P, mass and P.V
+    for (int blk = w; blk < nblk; blk += kWaves) {
+      const int tb = u.c0 + 32 * blk;
+      uint4 Kr[2][KS];
+      load_k_block<D>(kg, tb, u.c1, n, gq, Kr);
+      VT Vr[8];
+      load_v_block<D>(vg, tb, u.c1, n, gq, Vr);
+      float S[2][RT][4];
+      scores_block<D, RT>(a, u, Kr, Qb, tb, n, gq, S);
+      pv_block<D, RT>(S, lse, Vr, O, mp, tb, u.c1, n, gq);
+    }
+  }
+  write_opart<D, RT>(a, u, O, s_o, lane, w, n, gq);
+}
+
+// ------------------------------------------------------------ fp32 path --
+template <int D, int RT>
+__global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
+  constexpr int ROWS = RT * 16;
+  constexpr int TC = kF32Tile;
+  constexpr int OPT = ROWS * D / kThreads;
+  extern __shared__ float sm[];
+  float* sQ = sm;                // [ROWS][D]
+  float* sKV = sQ + ROWS * D;    // [TC][D]
+  float* sS = sKV + TC * D;      // [ROWS][TC]
+  __shared__ float s_m[ROWS], s_z[ROWS], s_lse[ROWS];
+
+  Unit u;
+  if (!decode_unit(a, u)) return;
+  const int tid = threadIdx.x;
+  for (int r = tid; r < ROWS; r += kThreads) {
+    s_m[r] = kNegInf;
+    s_z[r] = 0.f;
+  }
+  if (u.c0 >= u.N) {
+    __syncthreads();
+    exchange_stats<ROWS>(a, u, s_m, s_z, s_lse, false);
+    return;
+  }
+  const int row0 = u.rg * a.RT * 16;
+  const float* q = static_cast<const float*>(a.q);
+  for (int e = tid; e < ROWS * D; e += kThreads) {
+    const int r = e / D, d = e % D, row = row0 + r;
+    float val = 0.f;
+    if (row < a.R) {
+      const int t = row / a.G, h = u.g * a.G + row % a.G;
+      val = q[(((size_t)u.b * a.T + t) * a.Hq + h) * D + d];
+    }
+    sQ[e] = val;
+  }
+  const size_t kv_off = ((size_t)u.b * a.Hkv + u.g) * a.n_cap * D;
+  const float* kg = static_cast<const float*>(a.k) + kv_off;
+  const float* vg = static_cast<const float*>(a.v) + kv_off;
+  float* mp = a.mpart + ((size_t)u.b * a.Hkv * a.RG + u.g * a.RG + u.rg) * a.n_cap;
+
+  auto load_rows = [&](const float* src, int base, int nt) {
+    for (int e = tid; e < TC * D; e += kThreads) {
+      const int tt = e / D;
+      sKV[e] = tt < nt ? src[(size_t)(base + tt) * D + e % D] : 0.f;
+    }
+  };
+  auto scores = [&](int base, int nt) {  // sS = scaled, masked scores (log2 domain)
+    for (int e = tid; e < ROWS * TC; e += kThreads) {
+      const int r = e / TC, tt = e % TC, row = row0 + r, tok = base + tt;
+      float s = kNegInf;
+      if (tt < nt && row < a.R && tok <= u.ctx + row / a.G) {
+        float acc = 0.f;
+        for (int d = 0; d < D; ++d) acc = fmaf(sQ[r * D + d], sKV[tt * D + d], acc);
+        s = acc * a.sl2;
+      }
+      sS[e] = s;
+    }
+  };
+
+  // ---- pass 1
+  for (int base = u.c0; base < u.c1; base += TC) {
+    const int nt = min(TC, u.c1 - base);
+    __syncthreads();
+    load_rows(kg, base, nt);
+    __syncthreads();
+    scores(base, nt);
+    __syncthreads();
+    for (int r = tid; r < ROWS; r += kThreads) {
+      float M = s_m[r], Z = s_z[r];
+      for (int tt = 0; tt < nt; ++tt) lse_combine(M, Z, sS[r * TC + tt], 1.f);
+      s_m[r] = M;
+      s_z[r] = Z;
+    }
+  }
+  __syncthreads();
+  exchange_stats<ROWS>(a, u, s_m, s_z, s_lse, true);
+
+  // ---- pass 2
+  float O[OPT];
+#pragma unroll
+  for (int k = 0; k < OPT; ++k) O[k] = 0.f;
+  for (int base = u.c0; base < u.c1; base += TC) {
+    const int nt = min(TC, u.c1 - base);
+    __syncthreads();
+    load_rows(kg, base, nt);
+    __syncthreads();
+    scores(base, nt);
+    __syncthreads();
+    for (int e = tid; e < ROWS * TC; e += kThreads) sS[e] = exp2f(sS[e] - s_lse[e / TC]);
+    __syncthreads();
+    if (tid < nt) {
+      float acc = 0.f;
+      for (int r = 0; r < ROWS; ++r) acc += sS[r * TC + tid];
+      mp[base + tid] = acc;
+    }
+    load_rows(vg, base, nt);
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < OPT; ++k) {
+      const int e = tid + k * kThreads, r = e / D, d = e % D;
+      float acc = O[k];
+      for (int tt = 0; tt < nt; ++tt) acc = fmaf(sS[r * TC + tt], sKV[tt * D + d], acc);
+      O[k] = acc;
+    }
+  }
+  float* op = a.opart + ((size_t)u.grp * a.splits + u.split) * ROWS * D;
+#pragma unroll
+  for (int k = 0; k < OPT; ++k) op[tid + k * kThreads] = O[k];
+}
+
+// --------------------------------------------------------------- combine --
+struct CArgs {
+  const float* stats;
+  const float* opart;
+  const float* mpart;
+  const int32_t* ctx_len;
+  int* cnt;
+  void* out;
+  float* lse;
+  float* mass;
+  int64_t n_cap;
+  int B, T, Hq, Hkv, G, R, RG, RT, D, max_ctx, splits, chunk, groups;
+  int f32;
+};
+
+__device__ __forceinline__ int clamp_ctx(int ctx, int max_ctx) {
+  return ctx < 0 ? 0 : (ctx > max_ctx ? max_ctx : ctx);
+}
+
+// blockIdx.y == 0: output rows (sum of chunk partials) and lse;
+// blockIdx.y == 1: mass (sum over KV heads and row groups) and counter reset.
+__global__ void __launch_bounds__(256) verify_combine_kernel(CArgs a) {
+  const int ROWS = a.RT * 16;
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (blockIdx.y == 0) {
+    const int64_t total = (int64_t)a.groups * ROWS * a.D;
+    if (gid >= total) return;
+    const int d = gid % a.D;
+    const int r = (gid / a.D) % ROWS;
+    const int grp = gid / ((int64_t)a.D * ROWS);
+    const int row = (grp % a.RG) * ROWS + r;
+    if (row >= a.R) return;
+    const int bg = grp / a.RG, g = bg % a.Hkv, b = bg / a.Hkv;
+    const int N = clamp_ctx(a.ctx_len[b], a.max_ctx) + a.T;
+    const int nsp = min(a.splits, (N + a.chunk - 1) / a.chunk);
+    const float* op = a.opart + (size_t)grp * a.splits * ROWS * a.D + (size_t)r * a.D + d;
+    float acc = 0.f;
+    for (int s = 0; s < nsp; ++s) acc += op[(size_t)s * ROWS * a.D];
+    const int t = row / a.G, h = g * a.G + row % a.G;
+    const size_t oi = (((size_t)b * a.T + t) * a.Hq + h) * a.D + d;
+    if (a.f32)
+      static_cast<float*>(a.out)[oi] = acc;
+    else
+      static_cast<uint16_t*>(a.out)[oi] = f32_to_bf16(acc);
+    if (d == 0 && a.lse) {
+      const float* st = a.stats + (size_t)grp * a.splits * ROWS * 2 + (size_t)r * 2;
+      float M = kNegInf, Z = 0.f;
+      for (int s = 0; s < nsp; ++s) lse_combine(M, Z, st[(size_t)s * ROWS * 2], st[(size_t)s * ROWS * 2 + 1]);
+      a.lse[((size_t)b * a.Hq + h) * a.T + t] = (M + __log2f(Z)) * kLn2;
+    }
+  } else {
+    if (gid < a.groups) a.cnt[gid] = 0;
+    if (!a.mass) return;
+    const int64_t total = (int64_t)a.B * a.n_cap;
+    if (gid >= total) return;
+    const int64_t i = gid % a.n_cap;
+    const int b = gid / a.n_cap;
+    const int N = clamp_ctx(a.ctx_len[b], a.max_ctx) + a.T;
+    float acc = 0.f;
+    if (i < N) {
+      const int P = a.Hkv * a.RG;
+      const float* mp = a.mpart + (size_t)b * P * a.n_cap + i;
+      for (int p = 0; p < P; ++p) acc += mp[(size_t)p * a.n_cap];
+    }
+    a.mass[gid] = acc;
+  }
+}
+
+// ------------------------------------------------------------------ host --
+struct VPlan {
+  int G, R, RTT, RG, RT;
+  int64_t n_plan;
+  int splits, chunk, groups, per_launch, grid;
+  bool resident, mfma;
+  int lds_dyn;
+  size_t off_cnt, off_stats, off_opart, off_mpart, bytes;
+};
+
+typedef void (*VKernel)(VArgs);
+
+VKernel pick_kernel(int dt, int D, int RT, bool resident) {
+#define PVLM_VK(DD, R_)                                                                  \
+  if (D == DD && RT == R_) {                                                            \
+    if (dt == PVLM_F32) return verify_f32_kernel<DD, R_>;                               \
+    return resident ? verify_mfma_kernel<DD, R_, true> : verify_mfma_kernel<DD, R_, false>; \
+  }
+  PVLM_VK(128, 1) PVLM_VK(128, 2) PVLM_VK(128, 3) PVLM_VK(128, 4) PVLM_VK(128, 5)
+  PVLM_VK(64, 1) PVLM_VK(64, 2) PVLM_VK(64, 3) PVLM_VK(64, 4) PVLM_VK(64, 5)
+#undef PVLM_VK
+  return nullptr;
+}
+
+int lds_bytes(int dt, int D, int RT) {
+  if (dt == PVLM_F32) return (RT * 16 * D + kF32Tile * D + RT * 16 * kF32Tile) * 4;
+  return 2 * RT * 16 * D * 4;
+}
+
+pvlm_status plan_verify(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int64_t n_cap,
+                        int64_t max_ctx, VPlan* p) {
+  if (dt != PVLM_F32 && dt != PVLM_BF16) return PVLM_ERR_UNSUPPORTED;
+  if (B < 1 || T < 1 || Hq < 1 || Hkv < 1 || n_cap < 1) return PVLM_ERR_SHAPE;
+  if (T > 32 || Hq % Hkv != 0 || (D != 64 && D != 128)) return PVLM_ERR_UNSUPPORTED;
+  if (max_ctx < 0 || max_ctx + T > n_cap || n_cap > (int64_t)1 << 30) return PVLM_ERR_SHAPE;
+  p->G = Hq / Hkv;
+  p->R = p->G * T;
+  if (p->R > 640) return PVLM_ERR_UNSUPPORTED;
+  p->RTT = (p->R + 15) / 16;
+  p->RG = (p->RTT + kMaxRT - 1) / kMaxRT;
+  p->RT = (p->RTT + p->RG - 1) / p->RG;
+  p->n_plan = max_ctx + T;
+  p->mfma = dt == PVLM_BF16;
+  p->groups = B * Hkv * p->RG;
+  DeviceInfo di;
+  pvlm_status st = device_info(&di);
+  if (st != PVLM_OK) return st;
+  const int W = di.cus;  // one workgroup per CU (registers / LDS bound)
+  p->per_launch = p->groups < W ? p->groups : W;
+  int splits = W / p->per_launch;
+  if (splits < 1) splits = 1;
+  if (!p->mfma) {
+    const int64_t want = (p->n_plan + kF32Tile - 1) / kF32Tile;
+    if (splits > want) splits = (int)want;
+  }
+  int64_t chunk = (p->n_plan + splits - 1) / splits;
+  chunk = (chunk + 31) / 32 * 32;
+  p->chunk = (int)chunk;
+  p->splits = (int)((p->n_plan + chunk - 1) / chunk);
+  p->resident = p->mfma && chunk <= kResTokens;
+  p->grid = (p->per_launch * p->splits + 7) / 8 * 8;
+  p->lds_dyn = lds_bytes(dt, D, p->RT);
+  const int ROWS = p->RT * 16;
+  size_t off = 0;
+  p->off_cnt = off;
+  off = align_up(off + sizeof(int) * p->groups, 256);
+  p->off_stats = off;
+  off = align_up(off + sizeof(float) * (size_t)p->groups * p->splits * ROWS * 2, 256);
+  p->off_opart = off;
+  off = align_up(off + sizeof(float) * (size_t)p->groups * p->splits * ROWS * D, 256);
+  p->off_mpart = off;
+  off = align_up(off + sizeof(float) * (size_t)B * Hkv * p->RG * n_cap, 256);
+  p->bytes = off;
+  return PVLM_OK;
+}
+
+}  // namespace
+}  // namespace pvlm
+
+using namespace pvlm;
+
+extern "C" size_t pvlm_verify_attn_workspace_size(pvlm_dtype dt, int B, int T, int Hq, int Hkv,
+                                                  int D, int64_t n_cap, int64_t max_ctx) {
+  VPlan p;
+  if (plan_verify(dt, B, T, Hq, Hkv, D, n_cap, max_ctx, &p) != PVLM_OK) return 0;
+  return p.bytes;
+}
+
+extern "C" pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D,
+                                        int64_t n_cap, int64_t max_ctx, float scale, const void* q,
+                                        const void* k_cache, const void* v_cache,
+                                        const int32_t* ctx_len, void* out, float* mass, float* lse,
+                                        void* ws, size_t ws_bytes, int32_t* status,
+                                        hipStream_t stream) {
+  if (!q || !k_cache || !v_cache || !ctx_len || !out) return PVLM_ERR_NULL;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return PVLM_ERR_SHAPE;
+  VPlan p;
+  pvlm_status st = plan_verify(dt, B, T, Hq, Hkv, D, n_cap, max_ctx, &p);
+  if (st != PVLM_OK) return st;
+  if (!ws) return PVLM_ERR_WORKSPACE;
+  if (ws_bytes < p.bytes) return PVLM_ERR_WORKSPACE;
+  char* wsb = static_cast<char*>(ws);
+  VArgs a;
+  a.q = q;
+  a.k = k_cache;
+  a.v = v_cache;
+  a.ctx_len = ctx_len;
+  a.stats = reinterpret_cast<float*>(wsb + p.off_stats);
+  a.opart = reinterpret_cast<float*>(wsb + p.off_opart);
+  a.mpart = reinterpret_cast<float*>(wsb + p.off_mpart);
+  a.cnt = reinterpret_cast<int*>(wsb + p.off_cnt);
+  a.status = status;
+  a.n_cap = n_cap;
+  a.B = B;
+  a.T = T;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.G = p.G;
+  a.R = p.R;
+  a.RG = p.RG;
+  a.RT = p.RT;
+  a.D = D;
+  a.max_ctx = (int)max_ctx;
+  a.splits = p.splits;
+  a.chunk = p.chunk;
+  a.grid = p.grid;
+  a.sl2 = scale * kLog2e;
+  VKernel kern = pick_kernel(dt, D, p.RT, p.resident);
+  if (!kern) return PVLM_ERR_UNSUPPORTED;
+  PVLM_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, p.lds_dyn));
+  for (int g0 = 0; g0 < p.groups; g0 += p.per_launch) {
+    a.grp_base = g0;
+    a.ngrp = p.groups - g0 < p.per_launch ? p.groups - g0 : p.per_launch;
+    a.grid = (a.ngrp * p.splits + 7) / 8 * 8;
+    void* args[] = {&a};
+    PVLM_HIP(hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3(a.grid),
+                                        dim3(kThreads), args, p.lds_dyn, stream));
+  }
+  CArgs c;
+  c.stats = a.stats;
+  c.opart = a.opart;
+  c.mpart = a.mpart;
+  c.ctx_len = ctx_len;
+  c.cnt = a.cnt;
+  c.out = out;
+  c.lse = lse;
+  c.mass = mass;
+  c.n_cap = n_cap;
+  c.B = B;
+  c.T = T;
+  c.Hq = Hq;
+  c.Hkv = Hkv;
+  c.G = p.G;
+  c.R = p.R;
+  c.RG = p.RG;
+  c.RT = p.RT;
+  c.D = D;
+  c.max_ctx = (int)max_ctx;
+  c.splits = p.splits;
+  c.chunk = p.chunk;
+  c.groups = p.groups;
+  c.f32 = dt == PVLM_F32;
+  const int64_t n0 = (int64_t)p.groups * p.RT * 16 * D;
+  const int64_t n1 = (int64_t)B * n_cap > p.groups ? (int64_t)B * n_cap : p.groups;
+  const int64_t nmax = n0 > n1 ? n0 : n1;
+  hipLaunchKernelGGL(verify_combine_kernel, dim3((unsigned)((nmax + 255) / 256), 2), dim3(256), 0,
+                     stream, c);
+  PVLM_LAUNCHED();
+  return PVLM_OK;
+}

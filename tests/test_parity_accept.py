@@ -1,0 +1,93 @@
+"""GPU parity: pvlm_spec_accept against the float64 oracle.  Accepted lengths
+and emitted tokens must be identical wherever neither side flags a near tie
+(a decision or draw within 1e-9 relative of its boundary)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2603_19610_amd as pv
+import workloads as W
+from gpu_util import note, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(a):
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    n, y, tie = pv.spec_accept(to_dev(a.draft_logits), to_dev(a.target_logits),
+                               to_dev(a.draft_tokens), to_dev(a.u_accept), to_dev(a.u_sample),
+                               a.temperature, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    return n.cpu().numpy(), y.cpu().numpy(), tie.cpu().numpy()
+
+
+def _compare(a, label):
+    note(f"accept {label} B={a.draft_logits.shape[0]} gamma={a.draft_logits.shape[1]} "
+         f"V={a.draft_logits.shape[2]} T={a.temperature}")
+    n, y, tie = _run(a)
+    rn, ry, rt = oracle.spec_accept(a.draft_logits, a.target_logits, a.draft_tokens,
+                                    a.u_accept, a.u_sample, a.temperature)
+    ok = (rt == 0) & (tie == 0)
+    assert ok.mean() >= 0.95, f"too many near ties: {ok.mean()}"
+    assert np.array_equal(n[ok], rn[ok]), (n, rn)
+    assert np.array_equal(y[ok], ry[ok]), (y, ry)
+    return n, rn
+
+
+@pytest.mark.parametrize("temperature", [1.0, 0.7, 0.0])
+def test_tiny_many_salts(temperature):
+    w = W.WORKLOADS["tiny"]
+    a = W.make_accept_inputs(w, temperature=temperature, batch=64, salt=3)
+    n, rn = _compare(a, "tiny")
+    if temperature > 0:
+        assert 0 < rn.mean() < w.gamma           # a mix of accepts and rejects
+
+
+@pytest.mark.parametrize("name", ["llava72b", "qwen32b", "long"])
+def test_workloads(name):
+    w = W.WORKLOADS[name]
+    for salt in range(2):
+        _compare(W.make_accept_inputs(w, salt=salt), f"{name} salt {salt}")
+    _compare(W.make_accept_inputs(w, temperature=0.0), f"{name} greedy")
+
+
+def test_forced_accept_and_reject():
+    w = W.WORKLOADS["tiny"]
+    a = W.make_accept_inputs(w, batch=4, gamma=5, vocab=3000)
+    tl = a.target_logits.copy()
+    tl[:, :5] = a.draft_logits                    # p = q: every draft accepted
+    a_acc = W.AcceptInputs(a.draft_logits, tl, a.draft_tokens,
+                           np.full_like(a.u_accept, 1 - 2.0 ** -53), a.u_sample, 1.0)
+    n, y, _ = _run(a_acc)
+    assert np.all(n == 5)
+    rn, ry, _ = oracle.spec_accept(a_acc.draft_logits, a_acc.target_logits, a_acc.draft_tokens,
+                                   a_acc.u_accept, a_acc.u_sample, 1.0)
+    assert np.array_equal(y, ry)
+    tl2 = tl.copy()
+    for b in range(4):                            # p(x) = 0 at position b
+        tl2[b, b, a.draft_tokens[b, b]] = -np.inf
+    a_rej = W.AcceptInputs(a.draft_logits, tl2, a.draft_tokens, np.zeros_like(a.u_accept),
+                           a.u_sample, 1.0)
+    n, y, _ = _run(a_rej)
+    assert list(n) == [0, 1, 2, 3]
+    for b in range(4):
+        assert y[b] != a.draft_tokens[b, b]
+    rn, ry, _ = oracle.spec_accept(a_rej.draft_logits, a_rej.target_logits, a_rej.draft_tokens,
+                                   a_rej.u_accept, a_rej.u_sample, 1.0)
+    assert np.array_equal(n, rn) and np.array_equal(y, ry)
+
+
+def test_greedy_matches_target_argmax_chain():
+    w = W.WORKLOADS["llava72b"]
+    a = W.make_accept_inputs(w, temperature=0.0, batch=3, vocab=50000)
+    am = a.target_logits.argmax(axis=-1)
+    toks = am[:, :w.gamma].astype(np.int32).copy()
+    toks[1, 3] = (toks[1, 3] + 1) % 50000
+    toks[2, 0] = (toks[2, 0] + 7) % 50000
+    a = W.AcceptInputs(a.draft_logits, a.target_logits, toks, a.u_accept, a.u_sample, 0.0)
+    note("accept greedy chain")
+    n, y, _ = _run(a)
+    assert list(n) == [w.gamma, 3, 0]
+    assert list(y) == [am[0, w.gamma], am[1, 3], am[2, 0]]

@@ -1,0 +1,99 @@
+"""GPU parity: pvlm_topk_select and pvlm_gather_kv, bit-exact against the
+oracle (integer selection and byte copies)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2603_19610_amd as pv
+import workloads as W
+from gpu_util import note, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("kind", ["normal", "ties", "zeros", "special"])
+@pytest.mark.parametrize("m_cap", [1, 1000, 12544, 40000, 131072])
+def test_topk_bit_exact(kind, m_cap):
+    B = 3
+    s = W.make_scores(B, m_cap, kind, seed=m_cap)
+    m = np.array([m_cap, max(1, m_cap - 17), max(1, m_cap // 3)], np.int32)
+    k = np.array([m[0] // 10, m[1], 0], np.int32)
+    k_cap = int(k.max()) + 5
+    note(f"topk {kind} m_cap={m_cap}")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    idx = pv.topk_select(to_dev(s), to_dev(m), to_dev(k), k_cap, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    ref = oracle.topk_select(s, m, k, k_cap)
+    assert np.array_equal(idx.cpu().numpy(), ref)
+
+
+def test_topk_keep_counts_of_workloads():
+    for name in ("tiny", "llava7b", "llava72b", "qwen32b"):
+        w = W.WORKLOADS[name]
+        m = w.m_per_seq().astype(np.int32)
+        k = w.keep_count(m).astype(np.int32)
+        s = W.make_scores(w.batch, int(m.max()), "normal", seed=w.config_id)
+        note(f"topk workload {name}")
+        idx = pv.topk_select(to_dev(s), to_dev(m), to_dev(k), int(k.max()))
+        torch.cuda.synchronize()
+        assert np.array_equal(idx.cpu().numpy(), oracle.topk_select(s, m, k, int(k.max())))
+
+
+def test_topk_range_flag():
+    s = W.make_scores(1, 100, "normal")
+    note("topk k > m flagged")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    idx = pv.topk_select(to_dev(s), to_dev(np.array([50], np.int32)),
+                         to_dev(np.array([80], np.int32)), 60, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) & pv.PVLM_DEV_RANGE
+    assert np.array_equal(idx.cpu().numpy(), oracle.topk_select(s, [50], [50], 60))
+
+
+@pytest.mark.parametrize("dt,D", [("bf16", 128), ("bf16", 64), ("f32", 64), ("f32", 128)])
+def test_gather_bit_exact(dt, D):
+    rng = np.random.default_rng(D)
+    B, Hkv, n_cap = 3, 4, 3000
+    st = np.uint16 if dt == "bf16" else np.float32
+    if dt == "bf16":
+        kc = rng.integers(0, 65535, size=(B, Hkv, n_cap, D), dtype=np.uint16)
+        vc = rng.integers(0, 65535, size=(B, Hkv, n_cap, D), dtype=np.uint16)
+    else:
+        kc = rng.standard_normal((B, Hkv, n_cap, D)).astype(st)
+        vc = rng.standard_normal((B, Hkv, n_cap, D)).astype(st)
+    k = np.array([250, 0, 17], np.int32)
+    k_cap = 256
+    idx = np.full((B, k_cap), -1, np.int32)
+    for b in range(B):
+        idx[b, :k[b]] = np.sort(rng.choice(2000, size=k[b], replace=False))
+    tb = np.array([2000, 2500, 0], np.int32)
+    tl = np.array([256, 500, 5], np.int32)
+    dst_cap = 760
+    note(f"gather {dt} D={D}")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    kd, vd = pv.gather_kv(to_dev(kc), to_dev(vc), to_dev(idx), to_dev(k), to_dev(tb), to_dev(tl),
+                          dst_cap, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    rk, rv = oracle.gather_kv(kc, vc, idx, k, tb, tl, dst_cap)
+    gk = kd.cpu().view(torch.int16).numpy().view(np.uint16) if dt == "bf16" else kd.cpu().numpy()
+    gv = vd.cpu().view(torch.int16).numpy().view(np.uint16) if dt == "bf16" else vd.cpu().numpy()
+    assert np.array_equal(gk.view(np.uint8), rk.view(np.uint8))
+    assert np.array_equal(gv.view(np.uint8), rv.view(np.uint8))
+
+
+def test_gather_rejects_out_of_range_index():
+    kc = np.arange(2 * 64 * 128, dtype=np.float32).reshape(1, 2, 64, 128)
+    idx = np.array([[3, 70, 5]], np.int32)              # 70 >= n_cap
+    note("gather out-of-range index flagged")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    kd, vd = pv.gather_kv(to_dev(kc), to_dev(kc), to_dev(idx), to_dev(np.array([3], np.int32)),
+                          to_dev(np.array([60], np.int32)), to_dev(np.array([4], np.int32)), 8,
+                          status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) & pv.PVLM_DEV_RANGE
+    got = kd.cpu().numpy()
+    assert np.array_equal(got[0, :, 0], kc[0, :, 3]) and np.all(got[0, :, 1] == 0)
+    assert np.array_equal(got[0, :, 3:7], kc[0, :, 60:64])

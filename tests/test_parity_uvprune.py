@@ -1,0 +1,74 @@
+"""GPU parity: pvlm_uvprune_score / pvlm_uvprune_criterion_cossim against the
+float64 oracle, which evaluates Eq. (average_similarity) literally."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2603_19610_amd as pv
+import workloads as W
+from gpu_util import SCORE_REL, f64, note, to_dev, to_host_f64
+
+pytestmark = pytest.mark.gpu
+
+
+def _assert_score(got, ref, scale):
+    err = np.abs(got - ref)
+    lim = SCORE_REL * np.maximum(np.abs(ref), scale)
+    bad = err > lim
+    assert not bad.any(), f"score: {bad.sum()} beyond tolerance, max err {err.max():.3g}"
+
+
+def test_mass_criterion_stack():
+    rng = np.random.default_rng(0)
+    L, B, m_cap = 20, 3, 5000
+    crit = (rng.random((L + 1, B, m_cap)) * 3.0).astype(np.float32)
+    m = np.array([5000, 4321, 1], dtype=np.int32)
+    note("uvprune mass L=20 B=3")
+    s = pv.uvprune_score_mass(to_dev(crit), to_dev(m))
+    torch.cuda.synchronize()
+    ref = oracle.uvprune_score_mass(crit.astype(np.float64), m)
+    _assert_score(to_host_f64(s), ref, np.abs(crit[L]) + np.abs(crit[0]))
+
+
+@pytest.mark.parametrize("dtype,L,Dh", [("f32", 3, 256), ("bf16", 4, 512), ("bf16", 1, 96)])
+def test_cossim_small_literal(dtype, L, Dh):
+    w = W.WORKLOADS["tiny"]
+    w = W.Workload(**{**w.__dict__, "dtype": dtype, "batch": 2, "n_text": 40, "frames": 2,
+                      "tokens_per_frame": 150})
+    h = W.make_hidden_inputs(w, L, hidden=Dh)
+    hv, ht = h.hv.copy(), h.ht.copy()
+    zero = np.uint16(0) if dtype == "bf16" else np.float32(0)
+    hv[:, 0, 7] = zero                 # a zero-norm visual row in every layer
+    ht[:, 1, 3] = zero                 # a zero-norm text row
+    m = np.array([300, 211], np.int32)
+    n = np.array([40, 33], np.int32)
+    note(f"uvprune cossim {dtype} L={L} Dh={Dh}")
+    s = pv.uvprune_score_cossim(to_dev(hv), to_dev(ht), to_dev(m), to_dev(n))
+    c0 = pv.uvprune_criterion_cossim(to_dev(hv[0]), to_dev(ht[0]), to_dev(m), to_dev(n))
+    torch.cuda.synchronize()
+    hv64, ht64 = f64(hv, dtype), f64(ht, dtype)
+    ref = oracle.uvprune_score_cossim(hv64, ht64, m, n)
+    cL = oracle.criterion_cossim(hv64[L], ht64[L], m, n)
+    r0 = oracle.criterion_cossim(hv64[0], ht64[0], m, n)
+    _assert_score(to_host_f64(s), ref, np.abs(cL) + np.abs(r0))
+    _assert_score(to_host_f64(c0), r0, np.abs(r0))
+    assert np.all(to_host_f64(s)[1, 211:] == 0)
+
+
+def test_cossim_72b_shape_sampled():
+    w = W.WORKLOADS["llava72b"]
+    L = w.crit_layers
+    h = W.make_hidden_inputs(w, L, layers=[0, L])
+    note("uvprune cossim 72B shape (layers 0 and L filled)")
+    s = pv.uvprune_score_cossim(to_dev(h.hv), to_dev(h.ht), to_dev(h.m), to_dev(h.n))
+    torch.cuda.synchronize()
+    got = to_host_f64(s)
+    rows = np.random.default_rng(1).choice(int(h.m[0]), size=96, replace=False)
+    hv0 = f64(h.hv[0][:, rows], "bf16")
+    hvL = f64(h.hv[L][:, rows], "bf16")
+    ht0, htL = f64(h.ht[0], "bf16"), f64(h.ht[L], "bf16")
+    mm, nn = [len(rows)], h.n
+    r0 = oracle.criterion_cossim(hv0, ht0, mm, nn)
+    rL = oracle.criterion_cossim(hvL, htL, mm, nn)
+    _assert_score(got[0, rows], (rL - r0)[0], (np.abs(rL) + np.abs(r0))[0])

@@ -1,0 +1,112 @@
+"""GPU parity: pvlm_verify_attn against the float64 oracle (verify attention
+output, log-sum-exp and per-token attention mass), element by element."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2603_19610_amd as pv
+import workloads as W
+from gpu_util import (assert_lse, assert_mass, assert_out, f64, note, to_dev, to_host_f64)
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(inp, max_ctx=None, status=None):
+    q, k, v, ctx = (to_dev(inp.q), to_dev(inp.k), to_dev(inp.v), to_dev(inp.ctx_len))
+    out, mass, lse = pv.verify_attn(q, k, v, ctx, scale=inp.scale, max_ctx=max_ctx, status=status)
+    torch.cuda.synchronize()
+    return out, mass, lse
+
+
+def _check(inp, hq, T, label):
+    note(f"verify {label} q{inp.q.shape} k{inp.k.shape} ctx={list(inp.ctx_len)} {inp.dtype}")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out, mass, lse = _run(inp, status=status)
+    assert int(status.item()) == 0
+    ro, rl, rm = oracle.verify_attn(f64(inp.q, inp.dtype), f64(inp.k, inp.dtype),
+                                    f64(inp.v, inp.dtype), inp.ctx_len, inp.scale)
+    assert_out(to_host_f64(out), ro)
+    assert_lse(to_host_f64(lse), rl)
+    assert_mass(to_host_f64(mass), rm, hq, T)
+    return out, mass, lse
+
+
+SHAPES = [
+    # B, T, Hq, Hkv, D, ctx, dtype
+    (1, 5, 4, 1, 64, [1024], "f32"),
+    (2, 5, 8, 2, 128, [300, 517], "bf16"),        # ragged batch, several tiles
+    (1, 6, 28, 4, 128, [700], "bf16"),             # 7B head layout, 3 row tiles
+    (1, 9, 64, 8, 128, [1111], "bf16"),            # 72B head layout, 5 row tiles
+    (1, 9, 16, 1, 128, [900], "bf16"),             # 144 rows -> two row groups
+    (2, 1, 8, 2, 128, [257, 33], "bf16"),          # T = 1 (pre-verify)
+    (1, 2, 8, 2, 64, [190], "bf16"),               # D = 64 bf16, T = 2
+    (3, 4, 6, 3, 128, [0, 1, 31], "bf16"),         # only the verify block visible
+    (1, 3, 8, 8, 128, [20000], "bf16"),            # chunks > 512 tokens: stream variant
+    (2, 3, 12, 4, 64, [77, 129], "f32"),           # fp32 path, D = 64, 3 row tiles
+    (1, 4, 8, 1, 128, [333], "f32"),               # fp32 path, D = 128
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"B{s[0]}T{s[1]}H{s[2]}/{s[3]}D{s[4]}{s[6]}")
+def test_shapes(shape):
+    B, T, Hq, Hkv, D, ctx, dt = shape
+    inp = W.random_verify_inputs(B, T, Hq, Hkv, D, ctx, dt, seed=sum(ctx) + Hq)
+    _check(inp, Hq, T, "shape")
+
+
+def test_spare_capacity_and_max_ctx_hint():
+    inp = W.random_verify_inputs(2, 5, 8, 2, 128, [400, 250], "bf16", seed=3, n_cap=900)
+    note("verify spare capacity n_cap=900")
+    ro, rl, rm = oracle.verify_attn(f64(inp.q, "bf16"), f64(inp.k, "bf16"), f64(inp.v, "bf16"),
+                                    inp.ctx_len, inp.scale)
+    for max_ctx in (None, 400, 600):
+        out, mass, lse = _run(inp, max_ctx=max_ctx)
+        assert_out(to_host_f64(out), ro)
+        assert_mass(to_host_f64(mass), rm, 8, 5)
+        assert np.all(to_host_f64(mass)[0, 405:] == 0) and np.all(to_host_f64(mass)[1, 255:] == 0)
+
+
+def test_device_length_out_of_range_is_flagged_and_clamped():
+    inp = W.random_verify_inputs(1, 3, 4, 1, 128, [100], "bf16", seed=4, n_cap=200)
+    note("verify ctx_len beyond max_ctx")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    q, k, v = to_dev(inp.q), to_dev(inp.k), to_dev(inp.v)
+    ctx = torch.tensor([150], dtype=torch.int32, device="cuda")   # above max_ctx = 100
+    out, mass, lse = pv.verify_attn(q, k, v, ctx, max_ctx=100, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) & pv.PVLM_DEV_RANGE
+    ro, _, rm = oracle.verify_attn(f64(inp.q, "bf16"), f64(inp.k, "bf16"), f64(inp.v, "bf16"),
+                                   [100], inp.scale)
+    assert_out(to_host_f64(out), ro)
+
+
+@pytest.mark.parametrize("name", ["tiny", "llava7b", "llava72b"])
+def test_workload_layers(name):
+    w = W.WORKLOADS[name]
+    for layer in (0, 1):
+        inp = W.make_verify_inputs(w, layer=layer)
+        _check(inp, w.hq, w.T, f"{name} layer {layer}")
+
+
+def test_qwen32b_ragged_batch():
+    w = W.WORKLOADS["qwen32b"]
+    inp = W.make_verify_inputs(w, layer=1)
+    _check(inp, w.hq, w.T, "qwen32b")
+
+
+def test_long_video_131k():
+    w = W.WORKLOADS["long"]
+    inp = W.make_verify_inputs(w, layer=1)
+    _check(inp, w.hq, w.T, "long")
+
+
+def test_deterministic_and_reusable_workspace():
+    w = W.WORKLOADS["llava72b"]
+    inp = W.make_verify_inputs(w, layer=1)
+    note("verify 72B determinism x3")
+    runs = [_run(inp) for _ in range(3)]
+    for o, m, l in runs[1:]:
+        assert torch.equal(o, runs[0][0]) and torch.equal(m, runs[0][1]) and torch.equal(l, runs[0][2])
+    mass = to_host_f64(runs[0][1])
+    assert abs(mass.sum() - w.hq * w.T) < 1e-3 * w.hq * w.T

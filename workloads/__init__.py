@@ -203,13 +203,14 @@ class VerifyInputs:
 
 
 def make_verify_inputs(w: Workload, layer: int = 1, boost: Optional[float] = None,
-                       seed_layer: Optional[int] = None,
-                       batch_rows: Optional[List[int]] = None) -> VerifyInputs:
+                       seed_layer: Optional[int] = None) -> VerifyInputs:
     """One decoder layer of verify inputs.
 
     For single-layer workloads, ``layer=0`` is the shallow reference layer (same
     base draws, no salient boost) and ``layer=1`` the boosted layer.  For the
     stacked variant pass ``seed_layer=l`` for independent draws per layer.
+    The cache is generated one (batch, KV head) slice at a time so the float64
+    temporaries stay small.
     """
     lens = w.lengths()
     B, T, Hq, Hkv, D = w.batch, w.T, w.hq, w.hkv, w.head_dim
@@ -221,28 +222,49 @@ def make_verify_inputs(w: Workload, layer: int = 1, boost: Optional[float] = Non
     q64 = stream(w.config_id, sl, TID_Q).standard_normal((B, T, Hq, D))
     rk = stream(w.config_id, sl, TID_K)
     rv = stream(w.config_id, sl, TID_V)
-    k64 = np.zeros((B, Hkv, n_cap, D))
-    v64 = np.zeros((B, Hkv, n_cap, D))
+    st_dt = np.float32 if w.dtype == "f32" else np.uint16
+    k = np.zeros((B, Hkv, n_cap, D), dtype=st_dt)
+    v = np.zeros((B, Hkv, n_cap, D), dtype=st_dt)
     for b in range(B):
         N = int(lens[b]) + T
-        k64[b, :, :N] = rk.standard_normal((Hkv, N, D))
-        v64[b, :, :N] = rv.standard_normal((Hkv, N, D))
-        if boost:
-            m_b = int(lens[b]) - w.n_text
-            rows = salient_rows(w, b, m_b)
-            for g in range(Hkv):
+        rows = salient_rows(w, b, int(lens[b]) - w.n_text) if boost else None
+        pos = np.arange(N)
+        for g in range(Hkv):
+            kg = rk.standard_normal((N, D))
+            if boost:
                 mean_q = q64[b, :, g * G:(g + 1) * G, :].reshape(-1, D).mean(axis=0)
-                u = mean_q / np.linalg.norm(mean_q)
-                k64[b, g, rows] += boost * u
+                kg[rows] += boost * (mean_q / np.linalg.norm(mean_q))
+            k[b, g, :N] = round_storage(rope_f64(kg, pos, w.rope_base), w.dtype)
+            v[b, g, :N] = round_storage(rv.standard_normal((N, D)), w.dtype)
     for b in range(B):
-        N = int(lens[b]) + T
-        k64[b, :, :N] = rope_f64(k64[b, :, :N], np.arange(N)[None, :], w.rope_base)
         q64[b] = rope_f64(q64[b], (lens[b] + np.arange(T))[:, None], w.rope_base)
     return VerifyInputs(
-        q=round_storage(q64, w.dtype), k=round_storage(k64, w.dtype),
-        v=round_storage(v64, w.dtype), ctx_len=lens.astype(np.int32),
+        q=round_storage(q64, w.dtype), k=k, v=v, ctx_len=lens.astype(np.int32),
         m=(lens - w.n_text).astype(np.int32), n_cap=n_cap, dtype=w.dtype,
         scale=1.0 / math.sqrt(D))
+
+
+def random_verify_inputs(B: int, T: int, Hq: int, Hkv: int, D: int, ctx: List[int],
+                         dtype: str, seed: int, n_cap: Optional[int] = None,
+                         rope_base: float = 1.0e6) -> VerifyInputs:
+    """Unstructured verify inputs of an arbitrary shape (for edge cases)."""
+    rng = stream(50, seed, TID_Q)
+    ctx = np.asarray(ctx, dtype=np.int64)
+    n_cap = int(n_cap if n_cap is not None else ctx.max() + T)
+    q64 = rng.standard_normal((B, T, Hq, D))
+    st_dt = np.float32 if dtype == "f32" else np.uint16
+    k = np.zeros((B, Hkv, n_cap, D), dtype=st_dt)
+    v = np.zeros((B, Hkv, n_cap, D), dtype=st_dt)
+    for b in range(B):
+        N = int(ctx[b]) + T
+        for g in range(Hkv):
+            k[b, g, :N] = round_storage(rope_f64(rng.standard_normal((N, D)), np.arange(N),
+                                                 rope_base), dtype)
+            v[b, g, :N] = round_storage(rng.standard_normal((N, D)), dtype)
+        q64[b] = rope_f64(q64[b], (ctx[b] + np.arange(T))[:, None], rope_base)
+    return VerifyInputs(q=round_storage(q64, dtype), k=k, v=v, ctx_len=ctx.astype(np.int32),
+                        m=ctx.astype(np.int32), n_cap=n_cap, dtype=dtype,
+                        scale=1.0 / math.sqrt(D))
 
 
 def crit_boost(w: Workload, layer: int) -> float:
