@@ -29,6 +29,10 @@
  *   - Outputs must not alias inputs.  Optional outputs may be NULL.
  *   - No global mutable state: calls are re-entrant; a workspace buffer must
  *     not be shared by two calls in flight at the same time.
+ *   - Workspaces: zero-fill a workspace once before its first use.  Its first
+ *     128 KiB hold the counters of the waits between workgroups, and every
+ *     call leaves them zeroed again, so one buffer (at least as large as each
+ *     call requires) serves calls of any shape in sequence.
  *   - Layouts are C-contiguous, innermost index last.  "bf16" is IEEE
  *     bfloat16 stored in 2 bytes.
  */
@@ -101,9 +105,8 @@ int pvlm_version(void);
  *   out       [B][T][Hq][D], dtype dt.
  *   mass      [B][n_cap] fp32 or NULL; rows >= ctx_len[b]+T are written 0.
  *   lse       [B][Hq][T] fp32 (natural log) or NULL.
- *   ws        device workspace of >= pvlm_verify_attn_workspace_size() bytes,
- *             zero-filled before its first use; every call leaves its
- *             synchronisation words zeroed again.
+ *   ws        device workspace of >= pvlm_verify_attn_workspace_size() bytes
+ *             (see "Workspaces" above).
  *   status    optional device int32, see PVLM_DEV_*.
  * ---------------------------------------------------------------------- */
 size_t pvlm_verify_attn_workspace_size(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D,
@@ -167,16 +170,19 @@ pvlm_status pvlm_topk_select(int B, int64_t m_cap, const int32_t* m, const int32
 
 /* ------------------------------------------------------------------------
  * pvlm_gather_kv -- compact draft cache (Sec. 4.2 Stage I: the draft holds
- * [V*, X]).  For every b and KV head g:
- *   dst[b,g,r]      = src[b,g,idx[b,r]]             r < k[b]
- *   dst[b,g,k[b]+r] = src[b,g,tail_begin[b]+r]      r < tail_len[b]
+ * [V*, X]).  For every layer l, batch b and KV head g:
+ *   dst[l,b,g,r]      = src[l,b,g,idx[b,r]]             r < k[b]
+ *   dst[l,b,g,k[b]+r] = src[l,b,g,tail_begin[b]+r]      r < tail_len[b]
  * for both K and V; rows keep their original RoPE rotation.  Rows past
- * k[b]+tail_len[b] are left untouched.
- *   k_cache, v_cache [B][Hkv][n_cap][D]; k_dst, v_dst [B][Hkv][dst_cap][D];
- *   idx [B][k_cap] int32 (entries < k[b] must lie in [0, n_cap));
- *   k, tail_begin, tail_len: [B] int32 device.
+ * k[b]+tail_len[b] are left untouched.  One kept set serves every layer, so
+ * a stacked cache is gathered in one call (n_layers = 1 for a single layer).
+ *   k_cache, v_cache [n_layers][B][Hkv][n_cap][D];
+ *   k_dst, v_dst     [n_layers][B][Hkv][dst_cap][D];
+ *   idx [B][k_cap] int32 (entries < k[b] must lie in [0, n_cap); an entry
+ *   outside that range is skipped and flagged);
+ *   k, tail_begin, tail_len: [B] int32 device.  n_layers * B <= 65535.
  * ---------------------------------------------------------------------- */
-pvlm_status pvlm_gather_kv(pvlm_dtype dt, int B, int Hkv, int D, int64_t n_cap,
+pvlm_status pvlm_gather_kv(pvlm_dtype dt, int n_layers, int B, int Hkv, int D, int64_t n_cap,
                            const void* k_cache, const void* v_cache, const int32_t* idx,
                            const int32_t* k, int32_t k_cap, const int32_t* tail_begin,
                            const int32_t* tail_len, int64_t dst_cap, void* k_dst, void* v_dst,

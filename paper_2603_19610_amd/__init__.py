@@ -67,8 +67,8 @@ _SIGS = {
                                            _P, _P]),
     "pvlm_topk_workspace_size": (_SZ, [_I, _I64]),
     "pvlm_topk_select": (_I, [_I, _I64, _P, _P, _I, _P, _P, _P, _SZ, _P, _P]),
-    "pvlm_gather_kv": (_I, [_I, _I, _I, _I, _I64, _P, _P, _P, _P, _I, _P, _P, _I64, _P, _P, _P,
-                            _P]),
+    "pvlm_gather_kv": (_I, [_I, _I, _I, _I, _I, _I64, _P, _P, _P, _P, _I, _P, _P, _I64, _P, _P,
+                            _P, _P]),
     "pvlm_spec_accept_workspace_size": (_SZ, [_I, _I, _I]),
     "pvlm_spec_accept": (_I, [_I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P]),
 }
@@ -284,23 +284,36 @@ def topk_select(score, m, k, k_cap: int, *, idx=None, status=None):
 
 def gather_kv(k_cache, v_cache, idx, k, tail_begin, tail_len, dst_cap: int, *, k_dst=None,
               v_dst=None, status=None):
-    """Compact cache [B][Hkv][dst_cap][D]: kept rows then tail rows."""
+    """Compact cache: kept rows then tail rows.  Caches are [B][Hkv][n_cap][D]
+    (one layer) or [L][B][Hkv][n_cap][D] (a stacked cache, one launch);
+    outputs have the same leading dims with dst_cap rows."""
     _need(k_cache, "k_cache")
     dev = k_cache.device
     _need(v_cache, "v_cache", k_cache.dtype, dev)
     _need(idx, "idx", torch.int32, dev)
     for name, t in (("k", k), ("tail_begin", tail_begin), ("tail_len", tail_len)):
         _need(t, name, torch.int32, dev)
-    B, Hkv, n_cap, D = k_cache.shape
+    if k_cache.dim() == 4:
+        n_layers, (B, Hkv, n_cap, D) = 1, k_cache.shape
+    elif k_cache.dim() == 5:
+        n_layers, B, Hkv, n_cap, D = k_cache.shape
+    else:
+        raise ValueError("k_cache must be [B][Hkv][n_cap][D] or [L][B][Hkv][n_cap][D]")
+    if tuple(v_cache.shape) != tuple(k_cache.shape) or idx.shape[0] != B:
+        raise ValueError("inconsistent gather_kv shapes")
+    dst_shape = tuple(k_cache.shape[:-2]) + (dst_cap, D)
     if k_dst is None:
-        k_dst = torch.zeros((B, Hkv, dst_cap, D), dtype=k_cache.dtype, device=dev)
+        k_dst = torch.zeros(dst_shape, dtype=k_cache.dtype, device=dev)
     if v_dst is None:
-        v_dst = torch.zeros((B, Hkv, dst_cap, D), dtype=k_cache.dtype, device=dev)
+        v_dst = torch.zeros(dst_shape, dtype=k_cache.dtype, device=dev)
     _need(k_dst, "k_dst", k_cache.dtype, dev)
     _need(v_dst, "v_dst", k_cache.dtype, dev)
-    st = lib().pvlm_gather_kv(_dt(k_cache), B, Hkv, D, n_cap, _ptr(k_cache), _ptr(v_cache),
-                              _ptr(idx), _ptr(k), idx.shape[1], _ptr(tail_begin), _ptr(tail_len),
-                              dst_cap, _ptr(k_dst), _ptr(v_dst), _ptr(status), _stream())
+    if tuple(k_dst.shape) != dst_shape or tuple(v_dst.shape) != dst_shape:
+        raise ValueError("destination shape mismatch")
+    st = lib().pvlm_gather_kv(_dt(k_cache), n_layers, B, Hkv, D, n_cap, _ptr(k_cache),
+                              _ptr(v_cache), _ptr(idx), _ptr(k), idx.shape[1], _ptr(tail_begin),
+                              _ptr(tail_len), dst_cap, _ptr(k_dst), _ptr(v_dst), _ptr(status),
+                              _stream())
     _check(st, "pvlm_gather_kv")
     return k_dst, v_dst
 

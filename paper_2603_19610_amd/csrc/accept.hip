@@ -23,7 +23,9 @@ constexpr int kAccThreads = 256;
 constexpr int kAccPer = 16;
 constexpr int kChunk = kAccThreads * kAccPer;  // vocabulary entries per item
 constexpr int kAccMaxB = 256;
+constexpr int kMaxChunks = 1024;                // V <= kMaxChunks * kChunk
 constexpr double kNearTie = 1e-9;
+constexpr double kNegInfD = -__builtin_huge_val();
 
 struct AArgs {
   const float* dl;
@@ -35,12 +37,21 @@ struct AArgs {
   int32_t* next;
   int32_t* near;
   int32_t* status;
-  double* pm;   // [B][RW][NC] chunk max
-  double* ps;   // [B][RW][NC] chunk exp-sum
-  int* pi;      // [B][RW][NC] chunk argmax (lowest index)
-  double* rs;   // [B][NC] residual chunk mass
-  double* qs;   // [B][NC] p chunk mass (fallback when the residual is empty)
-  int* bar;     // [0] arrivals, [1] finished workgroups
+  double* pm;     // [B][RW][NC] chunk max
+  double* ps;     // [B][RW][NC] chunk exp-sum (relative to the chunk max)
+  int* pi;        // [B][RW][NC] chunk argmax (lowest index)
+  double* rowM;   // [B][RW] row max
+  double* rowZ;   // [B][RW] row normaliser
+  int* rowA;      // [B][RW] row argmax
+  int* rowcnt;    // [B][RW] chunks finished (last one combines the row)
+  double* rs;     // [B][NC] residual chunk mass
+  double* qs;     // [B][NC] p chunk mass (used when the residual is empty)
+  int* bcnt;      // [B] chunks finished in phase 3
+  double* bZ;     // [B] total mass of the draw distribution
+  double* bPre;   // [B] mass before the crossing chunk
+  int* bCross;    // [B] crossing chunk
+  int* bMode;     // [B] bit 0: draw from the residual; bit 1: rounding fallback
+  int* bar;       // [0] arrivals, [1] finished workgroups
   int B, gamma, V, NC;
   double tau;
   int greedy;
@@ -49,10 +60,6 @@ struct AArgs {
 __device__ __forceinline__ const float* row_ptr(const AArgs& a, int b, int rho) {
   if (rho <= a.gamma) return a.tl + ((size_t)b * (a.gamma + 1) + rho) * a.V;
   return a.dl + ((size_t)b * a.gamma + (rho - a.gamma - 1)) * a.V;
-}
-
-__device__ __forceinline__ void grid_wait(const AArgs& a, int target) {
-  wg_arrive_wait(a.bar, target, a.status, true);
 }
 
 // Exclusive scan of one double per thread over the workgroup (fixed order).
@@ -76,106 +83,149 @@ __device__ double block_scan_f64(double v, double* s_w, double* total) {
   return before + (x - v);
 }
 
+// Workgroup-wide max with lowest-index tie-break (value, index), fixed order.
+__device__ void block_argmax(double& v, int& i, double* s_v, int* s_i) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const double v2 = __shfl_xor(v, o, 64);
+    const int i2 = __shfl_xor(i, o, 64);
+    if (v2 > v || (v2 == v && i2 < i)) {
+      v = v2;
+      i = i2;
+    }
+  }
+  if (lane == 0) {
+    s_v[w] = v;
+    s_i[w] = i;
+  }
+  __syncthreads();
+  v = s_v[0];
+  i = s_i[0];
+  for (int k = 1; k < kAccThreads / 64; ++k)
+    if (s_v[k] > v || (s_v[k] == v && s_i[k] < i)) {
+      v = s_v[k];
+      i = s_i[k];
+    }
+  __syncthreads();
+}
+
+__device__ double block_sum(double x, double* s_v) {
+  x = warp_sum(x);
+  if ((threadIdx.x & 63) == 0) s_v[threadIdx.x >> 6] = x;
+  __syncthreads();
+  double t = 0.0;
+  for (int k = 0; k < kAccThreads / 64; ++k) t += s_v[k];
+  __syncthreads();
+  return t;
+}
+
+__device__ __forceinline__ void finish(const AArgs& a, int* s_flag) {
+  if (wg_signal_last(a.bar + 1, gridDim.x, s_flag) && threadIdx.x == 0) {
+    reset_counter(a.bar);
+    reset_counter(a.bar + 1);
+  }
+}
+
 __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
-  __shared__ double s_red[kAccThreads / 64];
-  __shared__ int s_ired[kAccThreads / 64];
-  __shared__ double s_M[65], s_Z[65];
-  __shared__ int s_arg[65];
+  __shared__ double s_v[kAccThreads / 64];
+  __shared__ int s_i[kAccThreads / 64];
+  __shared__ double s_M[65], s_Z[65], s_px[32], s_qx[32];
+  __shared__ int s_arg[65], s_xok[32];
   __shared__ int s_a[kAccMaxB], s_tie[kAccMaxB];
   __shared__ double s_pM[kAccMaxB], s_pZ[kAccMaxB], s_qM[kAccMaxB], s_qZ[kAccMaxB];
-  __shared__ int s_win;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  __shared__ double s_cr[kMaxChunks], s_cq[kMaxChunks];
+  __shared__ int s_win, s_flag;
+  const int tid = threadIdx.x;
   const int RW = 2 * a.gamma + 1;
   const int W = gridDim.x;
   const double tau = a.tau;
 
-  // ---- phase 1: per-chunk max / argmax / exp-sum
+  // ---- phase 1: chunk max / argmax / exp-sum; the last chunk of a row
+  //      combines the row's totals
   const int items1 = a.B * RW * a.NC;
   for (int it = blockIdx.x; it < items1; it += W) {
     const int c = it % a.NC, rho = (it / a.NC) % RW, b = it / (a.NC * RW);
     if (a.greedy && rho > a.gamma) continue;
     const float* z = row_ptr(a, b, rho);
     const int y0 = c * kChunk, y1 = min(a.V, y0 + kChunk);
-    float mx = -__builtin_huge_valf();
+    double mx = kNegInfD;
     int am = 0x7fffffff;
     for (int y = y0 + tid; y < y1; y += kAccThreads) {
-      const float v = z[y];
+      const double v = z[y];
       if (v > mx) {
         mx = v;
         am = y;
       }
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float m2 = __shfl_xor(mx, o, 64);
-      const int a2 = __shfl_xor(am, o, 64);
-      if (m2 > mx || (m2 == mx && a2 < am)) {
-        mx = m2;
-        am = a2;
-      }
-    }
-    if (lane == 0) {
-      s_red[w] = mx;
-      s_ired[w] = am;
-    }
-    __syncthreads();
-    double M = s_red[0];
-    int AM = s_ired[0];
-    for (int k = 1; k < kAccThreads / 64; ++k)
-      if (s_red[k] > M || (s_red[k] == M && s_ired[k] < AM)) {
-        M = s_red[k];
-        AM = s_ired[k];
-      }
-    __syncthreads();
-    double s = 0.0;
-    if (!a.greedy && M != -__builtin_huge_val()) {
-      for (int y = y0 + tid; y < y1; y += kAccThreads) s += exp(((double)z[y] - M) / tau);
-    }
-    s = warp_sum(s);
-    if (lane == 0) s_red[w] = s;
-    __syncthreads();
+    block_argmax(mx, am, s_v, s_i);
+    double sum = 0.0;
+    if (!a.greedy && mx != kNegInfD)
+      for (int y = y0 + tid; y < y1; y += kAccThreads) sum += exp(((double)z[y] - mx) / tau);
+    sum = block_sum(sum, s_v);
     if (tid == 0) {
-      double S = 0.0;
-      for (int k = 0; k < kAccThreads / 64; ++k) S += s_red[k];
-      st_agent(&a.pm[it], M);
-      st_agent(&a.ps[it], S);
-      st_agent(&a.pi[it], AM);
+      st_agent(a.pm + it, mx);
+      st_agent(a.ps + it, sum);
+      st_agent(a.pi + it, am);
+    }
+    const int r = b * RW + rho;
+    if (wg_signal_last(a.rowcnt + r, a.NC, &s_flag)) {
+      const size_t base = (size_t)r * a.NC;
+      double M = kNegInfD;
+      int A = 0x7fffffff;
+      for (int k = tid; k < a.NC; k += kAccThreads) {
+        const double m2 = ld_agent(a.pm + base + k);
+        const int i2 = ld_agent(a.pi + base + k);
+        if (m2 > M || (m2 == M && i2 < A)) {
+          M = m2;
+          A = i2;
+        }
+      }
+      block_argmax(M, A, s_v, s_i);
+      double Z = 0.0;
+      if (!a.greedy && M != kNegInfD)
+        for (int k = tid; k < a.NC; k += kAccThreads) {
+          const double m2 = ld_agent(a.pm + base + k);
+          if (m2 != kNegInfD) Z += ld_agent(a.ps + base + k) * exp((m2 - M) / tau);
+        }
+      Z = block_sum(Z, s_v);
+      if (tid == 0) {
+        st_agent(a.rowM + r, M);
+        st_agent(a.rowZ + r, Z);
+        st_agent(a.rowA + r, A);
+        reset_counter(a.rowcnt + r);
+      }
     }
     __syncthreads();
   }
-  grid_wait(a, W);
+  wg_signal_wait(a.bar, W, a.status, true);
 
-  // ---- phase 2: row normalisers and the sequential accept decisions
+  // ---- phase 2: the sequential accept decisions (every workgroup with later
+  //      work replays them from the row totals)
   const bool has_late = a.greedy ? blockIdx.x == 0 : blockIdx.x < a.B * a.NC;
   if (has_late) {
     for (int b = 0; b < a.B; ++b) {
       if (tid < RW && (!a.greedy || tid <= a.gamma)) {
-        const size_t base = ((size_t)b * RW + tid) * a.NC;
-        double M = -__builtin_huge_val(), Z = 0.0;
-        int AM = 0;
-        for (int c = 0; c < a.NC; ++c) {
-          const double m2 = ld_agent(&a.pm[base + c]);
-          if (m2 > M) {
-            M = m2;
-            AM = ld_agent(&a.pi[base + c]);
-          }
+        s_M[tid] = ld_agent(a.rowM + b * RW + tid);
+        s_Z[tid] = ld_agent(a.rowZ + b * RW + tid);
+        s_arg[tid] = ld_agent(a.rowA + b * RW + tid);
+      }
+      if (tid >= 64 && tid < 64 + a.gamma) {
+        const int t = tid - 64;
+        const int x = a.tok[(size_t)b * a.gamma + t];
+        const int ok = x >= 0 && x < a.V;
+        s_xok[t] = ok ? x : -1;
+        if (ok && !a.greedy) {
+          s_px[t] = row_ptr(a, b, t)[x];
+          s_qx[t] = row_ptr(a, b, a.gamma + 1 + t)[x];
         }
-        if (!a.greedy && M != -__builtin_huge_val()) {
-          for (int c = 0; c < a.NC; ++c) {
-            const double m2 = ld_agent(&a.pm[base + c]);
-            if (m2 != -__builtin_huge_val()) Z += ld_agent(&a.ps[base + c]) * exp((m2 - M) / tau);
-          }
-        }
-        s_M[tid] = M;
-        s_Z[tid] = Z;
-        s_arg[tid] = AM;
       }
       __syncthreads();
       if (tid == 0) {
         int acc = a.gamma, tie = 0;
         for (int t = 0; t < a.gamma; ++t) {
-          int x = a.tok[(size_t)b * a.gamma + t];
-          if (x < 0 || x >= a.V) {
+          const int x = s_xok[t];
+          if (x < 0) {
             dev_flag(a.status, PVLM_DEV_RANGE);
             acc = t;
             break;
@@ -184,9 +234,9 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
           if (a.greedy) {
             ok = x == s_arg[t];
           } else {
-            const double p = exp(((double)row_ptr(a, b, t)[x] - s_M[t]) / tau) / s_Z[t];
             const int qr = a.gamma + 1 + t;
-            const double q = exp(((double)row_ptr(a, b, qr)[x] - s_M[qr]) / tau) / s_Z[qr];
+            const double p = exp((s_px[t] - s_M[t]) / tau) / s_Z[t];
+            const double q = exp((s_qx[t] - s_M[qr]) / tau) / s_Z[qr];
             const double lhs = a.ua[(size_t)b * a.gamma + t] * q;
             if (fabs(lhs - p) <= kNearTie * fmax(lhs, p)) tie = 1;
             ok = lhs < p;
@@ -214,18 +264,11 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
     }
   }
   if (a.greedy) {
-    __syncthreads();
-    if (tid == 0) {
-      const int done = __hip_atomic_fetch_add(a.bar + 1, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-      if (done == W - 1) {
-        __hip_atomic_store(a.bar, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(a.bar + 1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-    }
+    finish(a, &s_flag);
     return;
   }
 
-  // r(y) of the draw distribution at row a of batch b; also p(y)
+  // r(y) of the draw distribution of batch b; also p(y)
   auto draw_mass = [&](int b, int y, double& p_out) -> double {
     const int acc = s_a[b];
     const double p = exp(((double)row_ptr(a, b, acc)[y] - s_pM[b]) / tau) / s_pZ[b];
@@ -235,7 +278,8 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
     return p > q ? p - q : 0.0;
   };
 
-  // ---- phase 3: chunk masses of the draw distribution
+  // ---- phase 3: chunk masses of the draw distribution; the last chunk of a
+  //      batch row locates the crossing chunk
   const int items3 = a.B * a.NC;
   for (int it = blockIdx.x; it < items3; it += W) {
     const int b = it / a.NC, c = it % a.NC;
@@ -250,40 +294,67 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
       }
     }
     double tr, tp;
-    block_scan_f64(sr, s_red, &tr);
-    block_scan_f64(sp, s_red, &tp);
+    block_scan_f64(sr, s_v, &tr);
+    block_scan_f64(sp, s_v, &tp);
     if (tid == 0) {
-      st_agent(&a.rs[it], tr);
-      st_agent(&a.qs[it], tp);
+      st_agent(a.rs + it, tr);
+      st_agent(a.qs + it, tp);
+    }
+    if (wg_signal_last(a.bcnt + b, a.NC, &s_flag)) {
+      for (int k = tid; k < a.NC; k += kAccThreads) {
+        s_cr[k] = ld_agent(a.rs + (size_t)b * a.NC + k);
+        s_cq[k] = ld_agent(a.qs + (size_t)b * a.NC + k);
+      }
+      __syncthreads();
+      if (tid == 0) {
+        double Zr = 0.0, Zp = 0.0;
+        for (int k = 0; k < a.NC; ++k) {
+          Zr += s_cr[k];
+          Zp += s_cq[k];
+        }
+        const bool use_r = Zr > 0.0;
+        const double* sums = use_r ? s_cr : s_cq;
+        const double Z = use_r ? Zr : Zp;
+        const double thr = a.us[b] * Z;
+        double run = 0.0, pre = 0.0, pre_last = 0.0;
+        int cross = -1, last_pos = -1;
+        for (int k = 0; k < a.NC; ++k) {
+          const double sk = sums[k];
+          if (sk > 0.0) {
+            last_pos = k;
+            pre_last = run;
+          }
+          if (cross < 0 && run + sk > thr) {
+            cross = k;
+            pre = run;
+          }
+          run += sk;
+        }
+        int mode = use_r ? 1 : 0;
+        if (cross < 0) {
+          mode |= 2;
+          cross = last_pos < 0 ? 0 : last_pos;
+          pre = pre_last;
+        }
+        st_agent(a.bZ + b, Z);
+        st_agent(a.bPre + b, pre);
+        st_agent(a.bCross + b, cross);
+        st_agent(a.bMode + b, mode);
+        reset_counter(a.bcnt + b);
+      }
     }
     __syncthreads();
   }
-  grid_wait(a, 2 * W);
+  wg_signal_wait(a.bar, 2 * W, a.status, true);
 
-  // ---- phase 4: locate the crossing chunk, scan it, write the outputs
+  // ---- phase 4: the crossing chunk scans its elements and writes the outputs
   for (int it = blockIdx.x; it < items3; it += W) {
     const int b = it / a.NC, c = it % a.NC;
-    double Zr = 0.0, Zp = 0.0;
-    for (int k = 0; k < a.NC; ++k) {
-      Zr += ld_agent(&a.rs[(size_t)b * a.NC + k]);
-      Zp += ld_agent(&a.qs[(size_t)b * a.NC + k]);
-    }
-    const bool use_r = Zr > 0.0;
-    const double* sums = use_r ? a.rs : a.qs;
-    const double Z = use_r ? Zr : Zp;
+    if (c != ld_agent(a.bCross + b)) continue;  // uniform across the workgroup
+    const int mode = ld_agent(a.bMode + b);
+    const bool use_r = mode & 1, fallback = mode & 2;
+    const double Z = ld_agent(a.bZ + b), pre = ld_agent(a.bPre + b);
     const double thr = a.us[b] * Z;
-    double run = 0.0, pre = 0.0;
-    int cross = -1, last_pos = -1;
-    for (int k = 0; k < a.NC; ++k) {
-      const double sk = ld_agent(&sums[(size_t)b * a.NC + k]);
-      if (k == c) pre = run;
-      if (sk > 0.0) last_pos = k;
-      run += sk;
-      if (cross < 0 && run > thr) cross = k;
-    }
-    const bool fallback = cross < 0;
-    if (fallback) cross = last_pos < 0 ? 0 : last_pos;
-    if (c != cross) continue;  // uniform across the workgroup
     const int y0 = c * kChunk + tid * kAccPer;
     double r[kAccPer];
     double own = 0.0;
@@ -298,7 +369,7 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
       own += r[e];
     }
     double tot;
-    const double excl = block_scan_f64(own, s_red, &tot);
+    const double excl = block_scan_f64(own, s_v, &tot);
     if (tid == 0) s_win = fallback ? -1 : 0x7fffffff;
     __syncthreads();
     double cum = pre + excl;
@@ -356,39 +427,50 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
     }
     __syncthreads();
   }
-  __syncthreads();
-  if (tid == 0) {
-    const int done = __hip_atomic_fetch_add(a.bar + 1, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    if (done == W - 1) {
-      __hip_atomic_store(a.bar, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(a.bar + 1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-  }
+  finish(a, &s_flag);
 }
 
 struct APlan {
   int NC;
-  size_t off_bar, off_pm, off_ps, off_pi, off_rs, off_qs, bytes;
+  size_t off_bar, off_pm, off_ps, off_pi, off_rowM, off_rowZ, off_rowA, off_rowcnt, off_rs, off_qs,
+      off_bcnt, off_bZ, off_bPre, off_bCross, off_bMode, bytes;
 };
 
 pvlm_status plan_accept(int B, int gamma, int V, APlan* p) {
   if (B < 1 || gamma < 1 || V < 1) return PVLM_ERR_SHAPE;
-  if (B > kAccMaxB || gamma > 32 || V > (1 << 30)) return PVLM_ERR_UNSUPPORTED;
+  if (B > kAccMaxB || gamma > 32 || V > kMaxChunks * kChunk) return PVLM_ERR_UNSUPPORTED;
   p->NC = (V + kChunk - 1) / kChunk;
-  const size_t rows = (size_t)B * (2 * gamma + 1) * p->NC;
-  size_t off = 0;
-  p->off_bar = off;
-  off = align_up(off + 2 * sizeof(int), 256);
-  p->off_pm = off;
-  off = align_up(off + rows * sizeof(double), 256);
-  p->off_ps = off;
-  off = align_up(off + rows * sizeof(double), 256);
-  p->off_pi = off;
-  off = align_up(off + rows * sizeof(int), 256);
-  p->off_rs = off;
-  off = align_up(off + (size_t)B * p->NC * sizeof(double), 256);
-  p->off_qs = off;
-  off = align_up(off + (size_t)B * p->NC * sizeof(double), 256);
+  const size_t rows = (size_t)B * (2 * gamma + 1);
+  const size_t parts = rows * p->NC;
+  // counters first (inside the fixed synchronisation region), data after it
+  size_t sync = 0;
+  auto take_sync = [&](size_t bytes) {
+    const size_t at = sync;
+    sync += bytes;
+    return at;
+  };
+  p->off_bar = take_sync(2 * sizeof(int));
+  p->off_rowcnt = take_sync(rows * sizeof(int));
+  p->off_bcnt = take_sync(B * sizeof(int));
+  if (sync > kSyncRegion) return PVLM_ERR_UNSUPPORTED;
+  size_t off = kSyncRegion;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, 256);
+    return at;
+  };
+  p->off_pm = take(parts * sizeof(double));
+  p->off_ps = take(parts * sizeof(double));
+  p->off_pi = take(parts * sizeof(int));
+  p->off_rowM = take(rows * sizeof(double));
+  p->off_rowZ = take(rows * sizeof(double));
+  p->off_rowA = take(rows * sizeof(int));
+  p->off_rs = take((size_t)B * p->NC * sizeof(double));
+  p->off_qs = take((size_t)B * p->NC * sizeof(double));
+  p->off_bZ = take(B * sizeof(double));
+  p->off_bPre = take(B * sizeof(double));
+  p->off_bCross = take(B * sizeof(int));
+  p->off_bMode = take(B * sizeof(int));
   p->bytes = off;
   return PVLM_OK;
 }
@@ -435,8 +517,17 @@ extern "C" pvlm_status pvlm_spec_accept(int B, int gamma, int V, float temperatu
   a.pm = reinterpret_cast<double*>(wsb + p.off_pm);
   a.ps = reinterpret_cast<double*>(wsb + p.off_ps);
   a.pi = reinterpret_cast<int*>(wsb + p.off_pi);
+  a.rowM = reinterpret_cast<double*>(wsb + p.off_rowM);
+  a.rowZ = reinterpret_cast<double*>(wsb + p.off_rowZ);
+  a.rowA = reinterpret_cast<int*>(wsb + p.off_rowA);
+  a.rowcnt = reinterpret_cast<int*>(wsb + p.off_rowcnt);
   a.rs = reinterpret_cast<double*>(wsb + p.off_rs);
   a.qs = reinterpret_cast<double*>(wsb + p.off_qs);
+  a.bcnt = reinterpret_cast<int*>(wsb + p.off_bcnt);
+  a.bZ = reinterpret_cast<double*>(wsb + p.off_bZ);
+  a.bPre = reinterpret_cast<double*>(wsb + p.off_bPre);
+  a.bCross = reinterpret_cast<int*>(wsb + p.off_bCross);
+  a.bMode = reinterpret_cast<int*>(wsb + p.off_bMode);
   a.bar = reinterpret_cast<int*>(wsb + p.off_bar);
   a.B = B;
   a.gamma = gamma;
@@ -448,7 +539,7 @@ extern "C" pvlm_status pvlm_spec_accept(int B, int gamma, int V, float temperatu
   int grid = di.cus < items ? di.cus : items;
   if (grid < 1) grid = 1;
   void* args[] = {&a};
-  PVLM_HIP(hipLaunchCooperativeKernel(reinterpret_cast<const void*>(accept_kernel), dim3(grid),
-                                      dim3(kAccThreads), args, 0, stream));
+  PVLM_HIP(launch_coresident(reinterpret_cast<const void*>(accept_kernel), dim3(grid),
+                             dim3(kAccThreads), args, 0, stream));
   return PVLM_OK;
 }

@@ -34,6 +34,22 @@ pvlm_status device_info(DeviceInfo* out);
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Every workspace starts with a fixed-size region that holds all counters of
+// the inter-workgroup waits.  Each call leaves that region zeroed, so a zeroed
+// workspace can be reused by calls of any shape: their data areas (after the
+// region) may overlap earlier data, their counters never do.
+constexpr size_t kSyncRegion = 128 * 1024;
+constexpr int kSyncInts = (int)(kSyncRegion / sizeof(int));
+
+// Raise a kernel's dynamic-LDS limit to `bytes` (done once per kernel and size).
+hipError_t allow_dynamic_lds(const void* kernel, int bytes);
+
+// Launch a kernel whose workgroups wait on each other: cooperatively (the
+// runtime guarantees co-residency), or as an ordinary launch while the stream
+// is being captured into a graph.  Grids are at most one workgroup per CU.
+hipError_t launch_coresident(const void* kernel, dim3 grid, dim3 block, void** args, int lds,
+                             hipStream_t stream);
+
 // ---------------------------------------------------------------- device --
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
@@ -50,8 +66,11 @@ __device__ __forceinline__ void dev_flag(int32_t* status, int bit) {
   if (status) __hip_atomic_fetch_or(status, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Coherent (agent-scope) scalar loads/stores for data exchanged between
-// workgroups that may sit on different XCDs.
+// Coherent (agent-scope) loads/stores for data exchanged between workgroups
+// that may sit on different XCDs.  Each XCD has its own L2; a plain load can
+// hit a stale line in the reader's L2 even after an acquire, so every read of
+// another workgroup's data goes through these (they are independent loads and
+// pipeline when issued back to back).
 __device__ __forceinline__ float ld_agent(const float* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -63,6 +82,15 @@ __device__ __forceinline__ double ld_agent(const double* p) {
 }
 __device__ __forceinline__ void st_agent(double* p, double v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_agent(float2* p, float2 v) {
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), __builtin_bit_cast(uint64_t, v),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 ld_agent(const float2* p) {
+  const uint64_t u = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+  return __builtin_bit_cast(float2, u);
 }
 __device__ __forceinline__ int ld_agent(const int* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -76,20 +104,27 @@ __device__ __forceinline__ void st_agent(int* p, int v) {
 // wave always exits.
 constexpr int kSpinLimit = 1 << 20;
 
-// Arrive at a counter and wait until it reaches `target`.  Must be called by
-// every thread of the workgroup (thread 0 does the atomics).  All global
-// writes made by the workgroup before the call are visible (agent scope) to
-// every workgroup that returns from a wait on the same counter.
-__device__ __forceinline__ void wg_arrive_wait(int* counter, int target, int32_t* status,
-                                               bool wait = true) {
-  // every thread publishes its own prior writes before the workgroup arrives
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+// Inter-workgroup exchange protocol.  Data another workgroup will read is
+// written with st_agent (device-coherent stores) and read with ld_agent
+// (device-coherent loads).  A workgroup signals with wg_signal*: every wave
+// first waits for its own memory operations to complete (s_waitcnt 0, after
+// which its coherent stores are visible device-wide), then thread 0 bumps the
+// counter with a relaxed atomic.  Waiters poll with relaxed atomic loads.  No
+// cache-wide fence is needed because no exchanged datum ever lives only in a
+// non-coherent cache.
+// `writer_wave0` limits the completion wait to wave 0 when only wave 0 wrote
+// data other workgroups will read (the other waves may keep loads in flight).
+__device__ __forceinline__ void wg_signal_wait(int* counter, int target, int32_t* status,
+                                               bool wait, bool writer_wave0 = false) {
+  // wave-uniform (scalar) branch: an exec-masked one would still run the wait
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (!writer_wave0 || wave == 0) __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0) {
-    __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (wait) {
       int spins = 0;
-      while (__hip_atomic_load(counter, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target) {
+      while (__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
         __builtin_amdgcn_s_sleep(1);
         if (++spins > kSpinLimit) {
           dev_flag(status, PVLM_DEV_TIMEOUT);
@@ -99,7 +134,25 @@ __device__ __forceinline__ void wg_arrive_wait(int* counter, int target, int32_t
     }
   }
   __syncthreads();
-  if (wait) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
+
+// Signal without waiting; true in every thread of the workgroup whose signal
+// brought the counter to `target` (the last arriver).  `s_flag` is a
+// __shared__ int.
+__device__ __forceinline__ bool wg_signal_last(int* counter, int target, int* s_flag) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0)
+    *s_flag = __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+              target - 1;
+  __syncthreads();
+  const bool last = *s_flag != 0;
+  __syncthreads();
+  return last;
+}
+
+__device__ __forceinline__ void reset_counter(int* counter) {
+  __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ float warp_max(float v) {

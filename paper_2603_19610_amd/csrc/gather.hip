@@ -1,8 +1,9 @@
 // Compact draft cache gather (gfx950): the draft holds [V*, X] (ParallelVLM
 // Sec. 4.2, Stage I): the kept visual rows in ascending index order followed
-// by the text (tail) rows, for every KV head, K and V alike.  Pure bit copy
-// with 16-byte loads/stores; a cache row is D * elem bytes (256 B for bf16,
-// D = 128), i.e. 16 lanes per row.
+// by the text (tail) rows, for every layer and KV head, K and V alike.  Pure
+// bit copy with 16-byte loads/stores; a cache row is D * elem bytes (256 B for
+// bf16, D = 128), i.e. 16 lanes per row.  One launch covers all layers of a
+// stacked cache.
 #include "common.h"
 
 namespace pvlm {
@@ -19,12 +20,13 @@ struct GArgs {
   uint4* vd;
   int32_t* status;
   int64_t n_cap, dst_cap;
-  int Hkv, k_cap, row_vec;  // row_vec = 16-byte vectors per cache row
+  int B, Hkv, k_cap, row_vec;  // row_vec = 16-byte vectors per cache row
 };
 
-// grid: x = dst-row blocks, y = KV head, z = batch.
+// grid: x = dst-row blocks, y = KV head, z = layer * B + batch.
 __global__ void __launch_bounds__(256) gather_kernel(GArgs a) {
-  const int b = blockIdx.z, g = blockIdx.y;
+  const int b = blockIdx.z % a.B, g = blockIdx.y;
+  const size_t lb = blockIdx.z;  // layer * B + b
   const int rows_per_block = 256 / a.row_vec;
   const int r = blockIdx.x * rows_per_block + threadIdx.x / a.row_vec;
   const int c = threadIdx.x % a.row_vec;
@@ -47,19 +49,20 @@ __global__ void __launch_bounds__(256) gather_kernel(GArgs a) {
     int64_t lim = a.n_cap - tb < a.dst_cap - kb ? a.n_cap - tb : a.dst_cap - kb;
     tl = tl < 0 ? 0 : (int)(tl < lim ? tl : lim);
   }
-  if (bad && blockIdx.x == 0 && g == 0 && threadIdx.x == 0) dev_flag(a.status, PVLM_DEV_RANGE);
+  if (bad && blockIdx.x == 0 && g == 0 && lb == (size_t)b && threadIdx.x == 0)
+    dev_flag(a.status, PVLM_DEV_RANGE);
   if (r >= kb + tl) return;
   int src;
   if (r < kb) {
     src = a.idx[(size_t)b * a.k_cap + r];
     if (src < 0 || src >= a.n_cap) {
-      if (c == 0) dev_flag(a.status, PVLM_DEV_RANGE);
+      if (c == 0 && lb == (size_t)b) dev_flag(a.status, PVLM_DEV_RANGE);
       return;
     }
   } else {
     src = tb + (r - kb);
   }
-  const size_t bg = (size_t)b * a.Hkv + g;
+  const size_t bg = lb * a.Hkv + g;
   const size_t si = (bg * a.n_cap + src) * a.row_vec + c;
   const size_t di = (bg * a.dst_cap + r) * a.row_vec + c;
   const uint4 kv = a.k[si];
@@ -73,7 +76,8 @@ __global__ void __launch_bounds__(256) gather_kernel(GArgs a) {
 
 using namespace pvlm;
 
-extern "C" pvlm_status pvlm_gather_kv(pvlm_dtype dt, int B, int Hkv, int D, int64_t n_cap,
+extern "C" pvlm_status pvlm_gather_kv(pvlm_dtype dt, int n_layers, int B, int Hkv, int D,
+                                      int64_t n_cap,
                                       const void* k_cache, const void* v_cache,
                                       const int32_t* idx, const int32_t* k, int32_t k_cap,
                                       const int32_t* tail_begin, const int32_t* tail_len,
@@ -83,8 +87,10 @@ extern "C" pvlm_status pvlm_gather_kv(pvlm_dtype dt, int B, int Hkv, int D, int6
     return PVLM_ERR_NULL;
   if (k_cap > 0 && !idx) return PVLM_ERR_NULL;
   if (dt != PVLM_F32 && dt != PVLM_BF16) return PVLM_ERR_UNSUPPORTED;
-  if (B < 1 || Hkv < 1 || n_cap < 1 || k_cap < 0 || dst_cap < 0) return PVLM_ERR_SHAPE;
-  if (n_cap > ((int64_t)1 << 30) || dst_cap > ((int64_t)1 << 30) || B > 65535 || Hkv > 65535)
+  if (n_layers < 1 || B < 1 || Hkv < 1 || n_cap < 1 || k_cap < 0 || dst_cap < 0)
+    return PVLM_ERR_SHAPE;
+  if (n_cap > ((int64_t)1 << 30) || dst_cap > ((int64_t)1 << 30) || (int64_t)n_layers * B > 65535 ||
+      Hkv > 65535)
     return PVLM_ERR_SHAPE;
   const int esize = dt == PVLM_F32 ? 4 : 2;
   const int row_bytes = D * esize;
@@ -103,12 +109,13 @@ extern "C" pvlm_status pvlm_gather_kv(pvlm_dtype dt, int B, int Hkv, int D, int6
   a.status = status;
   a.n_cap = n_cap;
   a.dst_cap = dst_cap;
+  a.B = B;
   a.Hkv = Hkv;
   a.k_cap = k_cap;
   a.row_vec = row_bytes / 16;
   const int rows_per_block = 256 / a.row_vec;
   const int64_t xb = (dst_cap + rows_per_block - 1) / rows_per_block;
-  hipLaunchKernelGGL(gather_kernel, dim3((unsigned)xb, Hkv, B), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(gather_kernel, dim3((unsigned)xb, Hkv, n_layers * B), dim3(256), 0, stream, a);
   PVLM_LAUNCHED();
   return PVLM_OK;
 }

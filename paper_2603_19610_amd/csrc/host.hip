@@ -1,7 +1,9 @@
 // Host-side helpers of the pvlm library: status strings, HIP error capture and
 // the per-device compute-unit count used to size launches.
 #include <mutex>
+#include <set>
 #include <string>
+#include <utility>
 
 #include "common.h"
 
@@ -12,7 +14,27 @@ thread_local std::string g_last_hip_error;
 std::mutex g_info_mu;
 constexpr int kMaxDevices = 64;
 int g_cus[kMaxDevices] = {0};
+std::mutex g_lds_mu;
+std::set<std::pair<const void*, int>> g_lds_done;
 }  // namespace
+
+hipError_t allow_dynamic_lds(const void* kernel, int bytes) {
+  std::lock_guard<std::mutex> lock(g_lds_mu);
+  if (g_lds_done.count({kernel, bytes})) return hipSuccess;
+  hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e == hipSuccess) g_lds_done.insert({kernel, bytes});
+  return e;
+}
+
+hipError_t launch_coresident(const void* kernel, dim3 grid, dim3 block, void** args, int lds,
+                             hipStream_t stream) {
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(stream, &cap);
+  if (e != hipSuccess) return e;
+  if (cap == hipStreamCaptureStatusNone)
+    return hipLaunchCooperativeKernel(kernel, grid, block, args, lds, stream);
+  return hipLaunchKernel(kernel, grid, block, args, lds, stream);
+}
 
 void set_hip_error(hipError_t e) {
   g_last_hip_error = std::string(hipGetErrorName(e)) + ": " + hipGetErrorString(e);

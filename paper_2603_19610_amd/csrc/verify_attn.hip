@@ -9,7 +9,7 @@
 // block-wise kernels (Sec. 3, Sec. 5.4): here the mass is produced inside the
 // block-wise kernel, with no score matrix in memory.
 //
-// Design (one launch of the main kernel + one small combine launch):
+// Design (one cooperative launch):
 //  * Work unit = (batch b, KV head g, row group rg, token chunk).  All
 //    (Hq/Hkv) * T query rows of a KV head are packed as the N side of
 //    v_mfma_f32_16x16x32_bf16 tiles (16 rows per tile, at most 5 tiles per
@@ -29,6 +29,11 @@
 //    partial outputs only need to be summed.
 //  * Chunks too long for registers use the "stream" variant, which recomputes
 //    the scores from K in pass 2 (K is read twice).
+//  * Epilogue: the chunk partials of O are summed after a second wait on the
+//    group counter, each workgroup summing one slice (the group's workgroups
+//    sit on one XCD, so the partials stay in its L2); the per-token mass is
+//    summed over KV heads by whichever workgroup of a chunk arrives last.
+//    Sums run in a fixed order, so results are bit-reproducible.
 //  * fp32 inputs take a VALU path with the same two-pass structure.
 #include "common.h"
 
@@ -53,13 +58,20 @@ struct VArgs {
   float* stats;   // [groups][splits][ROWS][2]  (log2-domain max, exp-sum)
   float* opart;   // [groups][splits][ROWS][D]
   float* mpart;   // [B][Hkv*RG][n_cap]
-  int* cnt;       // [groups]
+  int* cnt;       // [groups]   first wait (statistics)
+  int* cnt2;      // [groups]   second wait (O partials)
+  int* done;      // [groups]   finished workgroups (resets the counters)
+  int* mcnt;      // [B][splits] arrivals per chunk for the mass sum
+  void* out;
+  float* lse;
+  float* mass;
   int32_t* status;
   int64_t n_cap;
   int B, T, Hq, Hkv, G, R, RG, RT, D;
   int max_ctx;
   int splits, chunk, grp_base, ngrp, grid;
   float sl2;      // scale * log2(e)
+  int f32;
 };
 
 struct Unit {
@@ -102,29 +114,120 @@ __device__ __forceinline__ void lse_combine(float& m, float& z, float m2, float 
 
 // Publish this workgroup's per-row (max, exp-sum), wait for the other chunks
 // of the same (b, g, rg), and leave each row's global log2-sum-exp in s_lse
-// (+inf for padding rows so their probabilities are 0).
+// (+inf for padding rows so their probabilities are 0).  The statistics are
+// written by wave 0 only, so only that wave needs to publish its stores.
 template <int ROWS>
 __device__ void exchange_stats(const VArgs& a, const Unit& u, float* s_m, float* s_z,
                                float* s_lse, bool wait) {
+  constexpr int kU = 16;  // splits loaded per round trip
   float* st = a.stats + ((size_t)u.grp * a.splits + u.split) * ROWS * 2;
-  for (int r = threadIdx.x; r < ROWS; r += kThreads) {
-    st_agent(st + 2 * r, s_m[r]);
-    st_agent(st + 2 * r + 1, s_z[r]);
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    for (int r = threadIdx.x; r < ROWS; r += 64) {
+      st_agent(st + 2 * r, s_m[r]);
+      st_agent(st + 2 * r + 1, s_z[r]);
+    }
   }
-  wg_arrive_wait(a.cnt + u.grp, a.splits, a.status, wait);
+  wg_signal_wait(a.cnt + u.grp, a.splits, a.status, wait, /*writer_wave0=*/true);
   if (!wait) return;
   const float* st0 = a.stats + (size_t)u.grp * a.splits * ROWS * 2;
   for (int r = threadIdx.x; r < ROWS; r += kThreads) {
     float M = kNegInf, Z = 0.f;
-    for (int s = 0; s < a.splits; ++s) {
-      const float m2 = ld_agent(st0 + ((size_t)s * ROWS + r) * 2);
-      const float z2 = ld_agent(st0 + ((size_t)s * ROWS + r) * 2 + 1);
-      lse_combine(M, Z, m2, z2);
+    for (int s0 = 0; s0 < a.splits; s0 += kU) {
+      float2 v[kU];
+#pragma unroll
+      for (int j = 0; j < kU; ++j)
+        v[j] = s0 + j < a.splits
+                   ? ld_agent(reinterpret_cast<const float2*>(st0 + ((size_t)(s0 + j) * ROWS + r) * 2))
+                   : make_float2(kNegInf, 0.f);
+#pragma unroll
+      for (int j = 0; j < kU; ++j) lse_combine(M, Z, v[j].x, v[j].y);
     }
     const int row = u.rg * a.RT * 16 + r;
     s_lse[r] = (row < a.R && Z > 0.f) ? M + __log2f(Z) : __builtin_huge_valf();
   }
   __syncthreads();
+}
+
+// After pass 2: O (sum of the chunk partials after a second wait on the group
+// counter, one slice per workgroup), lse, then the per-token mass (summed over
+// KV heads and row groups by the last workgroup of each chunk -- done last so
+// that work never delays the group's wait), and counter reset.
+template <int ROWS, int D>
+__device__ void verify_epilogue(const VArgs& a, const Unit& u, const float* s_lse, bool empty,
+                                int* s_flag) {
+  const int tid = threadIdx.x;
+  wg_signal_wait(a.cnt2 + u.grp, a.splits, a.status, !empty);
+  if (!empty) {
+    const int row0 = u.rg * a.RT * 16;
+    const int nsp = (u.N + a.chunk - 1) / a.chunk;
+    const int rows = min(ROWS, a.R - row0);
+    const int E2 = rows * D / 2;  // float pairs
+    const int per = (E2 + nsp - 1) / nsp;
+    const int e0 = u.split * per, e1 = min(E2, e0 + per);
+    const float2* op = reinterpret_cast<const float2*>(a.opart + (size_t)u.grp * a.splits * ROWS * D);
+    for (int e = e0 + tid; e < e1; e += kThreads) {
+      float2 acc = make_float2(0.f, 0.f);
+      for (int s0 = 0; s0 < nsp; s0 += 16) {
+        float2 v[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          v[j] = s0 + j < nsp ? ld_agent(op + (size_t)(s0 + j) * ROWS * D / 2 + e) : make_float2(0.f, 0.f);
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          acc.x += v[j].x;
+          acc.y += v[j].y;
+        }
+      }
+      const int row = row0 + (2 * e) / D, d = (2 * e) % D;
+      const int t = row / a.G, h = u.g * a.G + row % a.G;
+      const size_t oi = (((size_t)u.b * a.T + t) * a.Hq + h) * D + d;
+      if (a.f32) {
+        *reinterpret_cast<float2*>(static_cast<float*>(a.out) + oi) = acc;
+      } else {
+        const uint32_t pk = (uint32_t)f32_to_bf16(acc.x) | ((uint32_t)f32_to_bf16(acc.y) << 16);
+        *reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(a.out) + oi) = pk;
+      }
+    }
+    if (a.lse && u.split == 0) {
+      for (int r = tid; r < rows; r += kThreads) {
+        const int row = row0 + r, t = row / a.G, h = u.g * a.G + row % a.G;
+        a.lse[((size_t)u.b * a.Hq + h) * a.T + t] = s_lse[r] * kLn2;
+      }
+    }
+  }
+  if (a.mass) {
+    const int P = a.Hkv * a.RG;
+    int* mc = a.mcnt + (size_t)u.b * a.splits + u.split;
+    if (wg_signal_last(mc, P, s_flag)) {
+      const int64_t lo = u.c0;
+      const int64_t hi_sum = u.c1 > u.c0 ? u.c1 : u.c0;
+      const int64_t chunk_end = (int64_t)u.c0 + a.chunk;
+      const int64_t hi = u.split == a.splits - 1 ? a.n_cap : (chunk_end < a.n_cap ? chunk_end : a.n_cap);
+      const float* mp = a.mpart + (size_t)u.b * P * a.n_cap;
+      float* ms = a.mass + (size_t)u.b * a.n_cap;
+      for (int64_t i = lo + tid; i < hi; i += kThreads) {
+        float acc = 0.f;
+        if (i < hi_sum) {
+          for (int p0 = 0; p0 < P; p0 += 8) {
+            float v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+              v[j] = p0 + j < P ? ld_agent(mp + (size_t)(p0 + j) * a.n_cap + i) : 0.f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc += v[j];
+          }
+        }
+        ms[i] = acc;
+      }
+      if (tid == 0) reset_counter(mc);
+    }
+  }
+  if (wg_signal_last(a.done + u.grp, a.splits, s_flag) && tid == 0) {
+    reset_counter(a.cnt + u.grp);
+    reset_counter(a.cnt2 + u.grp);
+    reset_counter(a.done + u.grp);
+  }
 }
 
 // ------------------------------------------------------------ MFMA path --
@@ -156,42 +259,44 @@ __device__ __forceinline__ bf16x8 pack_v(const VT (&vr)[8], int jd) {
   return __builtin_bit_cast(bf16x8, u);
 }
 
+// Q operand of every row tile (B side of S^T = K Q^T): lane (n, gq) holds
+// q[row][32*ks + 8*gq .. +8] of row 16*rt + n.  Padding rows load a real row
+// (their scores are masked), so the loads are unconditional.
 template <int D, int RT>
 __device__ __forceinline__ void load_q(const VArgs& a, const Unit& u, int n, int gq,
                                        bf16x8 (&Qb)[RT][D / 32]) {
   const uint16_t* q = static_cast<const uint16_t*>(a.q);
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
-    const int row = u.rg * a.RT * 16 + rt * 16 + n;
-    const bool ok = row < a.R;
-    const int t = ok ? row / a.G : 0;
-    const int h = u.g * a.G + (ok ? row % a.G : 0);
+    const int row = min(u.rg * a.RT * 16 + rt * 16 + n, a.R - 1);
+    const int t = row / a.G;
+    const int h = u.g * a.G + row % a.G;
     const uint16_t* qp = q + (((size_t)u.b * a.T + t) * a.Hq + h) * D + 8 * gq;
 #pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) {
-      uint4 v = ok ? *reinterpret_cast<const uint4*>(qp + 32 * ks) : make_uint4(0, 0, 0, 0);
-      Qb[rt][ks] = __builtin_bit_cast(bf16x8, v);
-    }
+    for (int ks = 0; ks < D / 32; ++ks)
+      Qb[rt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(qp + 32 * ks));
   }
 }
 
 // K operand of one 32-token block: lane (n, gq) loads token tb + 16*tt + n,
-// d in [32*ks + 8*gq, +8).
+// d in [32*ks + 8*gq, +8).  Tokens past the chunk load the chunk's last row
+// (their scores are masked), keeping the loads unconditional so the
+// compiler can wait for one block while the later ones stay in flight.
 template <int D>
 __device__ __forceinline__ void load_k_block(const uint16_t* kg, int tb, int c1, int n, int gq,
                                              uint4 (&Kr)[2][D / 32]) {
 #pragma unroll
   for (int tt = 0; tt < 2; ++tt) {
-    const int tok = tb + 16 * tt + n;
+    const int tok = min(tb + 16 * tt + n, c1 - 1);
     const uint16_t* kp = kg + (size_t)tok * D + 8 * gq;
 #pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks)
-      Kr[tt][ks] = tok < c1 ? *reinterpret_cast<const uint4*>(kp + 32 * ks) : make_uint4(0, 0, 0, 0);
+    for (int ks = 0; ks < D / 32; ++ks) Kr[tt][ks] = *reinterpret_cast<const uint4*>(kp + 32 * ks);
   }
 }
 
 // V operand rows of one 32-token block: lane (n, gq) loads tokens
-// tb + {4gq..4gq+3, 16+4gq..16+4gq+3}, d in [DPL*n, DPL*n + DPL).
+// tb + {4gq..4gq+3, 16+4gq..16+4gq+3}, d in [DPL*n, DPL*n + DPL).  Tokens past
+// the chunk load its last row (their probabilities are 0).
 template <int D>
 __device__ __forceinline__ void load_v_block(const uint16_t* vg, int tb, int c1, int n, int gq,
                                              typename VVec<D>::T (&Vr)[8]) {
@@ -199,10 +304,48 @@ __device__ __forceinline__ void load_v_block(const uint16_t* vg, int tb, int c1,
   constexpr int DPL = D / 16;
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
-    const int tok = tb + (s < 4 ? 4 * gq + s : 16 + 4 * gq + (s - 4));
-    VT z;
-    __builtin_memset(&z, 0, sizeof(z));
-    Vr[s] = tok < c1 ? *reinterpret_cast<const VT*>(vg + (size_t)tok * D + DPL * n) : z;
+    const int tok = min(tb + (s < 4 ? 4 * gq + s : 16 + 4 * gq + (s - 4)), c1 - 1);
+    Vr[s] = *reinterpret_cast<const VT*>(vg + (size_t)tok * D + DPL * n);
+  }
+}
+
+// Stream one 32-token block of V into LDS with coalesced global->LDS loads:
+// instruction k of the wave covers cache rows tb + k*RPI .. +RPI (RPI = 512/D),
+// lane l writes the 16 bytes at column (l % (D/8)) of row (l / (D/8)).  Rows
+// past the chunk re-read its last row (their probabilities are 0).
+// The loads are issued through inline asm so the compiler's wait insertion
+// does not track them (it would otherwise wait for them before any later LDS
+// access); untracked loads can only lengthen the compiler's own vmcnt waits.
+// The consumer waits explicitly (s_waitcnt vmcnt(0) + workgroup barrier).
+template <int D>
+__device__ __forceinline__ void issue_v_lds(const uint16_t* vg, int tb, int c1, uint16_t* lds_blk,
+                                            int lane) {
+  constexpr int CPR = D / 8;    // 16-byte columns per row
+  constexpr int RPI = 64 / CPR; // rows per instruction
+#pragma unroll
+  for (int k = 0; k < 32 / RPI; ++k) {
+    const int row = k * RPI + lane / CPR;
+    const int tok = min(tb + row, c1 - 1);
+    const uint16_t* src = vg + (size_t)tok * D + 8 * (lane % CPR);
+    const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
+        reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint16_t*)(lds_blk + k * RPI * D))));
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(lds), "v"(src)
+                 : "memory", "m0");
+  }
+}
+
+// V operand rows of one block from LDS (row-major [32][D] bf16).
+template <int D>
+__device__ __forceinline__ void read_v_lds(const uint16_t* lds_blk, int n, int gq,
+                                           typename VVec<D>::T (&Vr)[8]) {
+  typedef typename VVec<D>::T VT;
+  constexpr int DPL = D / 16;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    const int row = s < 4 ? 4 * gq + s : 16 + 4 * gq + (s - 4);
+    Vr[s] = *reinterpret_cast<const VT*>(lds_blk + row * D + DPL * n);
   }
 }
 
@@ -330,7 +473,7 @@ __device__ __forceinline__ void pv_block(const float (&S)[2][RT][4], const float
   a2 += __shfl_xor(a2, 1, 64);
   const int v = (h8 ? 4 : 0) + (h4 ? 2 : 0) + (h2 ? 1 : 0);
   const int tok = tb + 16 * (v >> 2) + 4 * gq + (v & 3);
-  if (!(n & 1) && tok < c1) mp[tok] = a2;
+  if (!(n & 1) && tok < c1) st_agent(mp + tok, a2);
 #pragma unroll
   for (int jd = 0; jd < DPL; ++jd) {
     const bf16x8 vb = pack_v(Vr, jd);
@@ -373,18 +516,22 @@ __device__ __forceinline__ void write_opart(const VArgs& a, const Unit& u, float
   __syncthreads();
   if (w == 0) {
     add(buf0);
-    float* op = a.opart + ((size_t)u.grp * a.splits + u.split) * RT * 16 * D;
+    // row-major copy of the sum in buf1 (each lane writes DPL consecutive d)
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        float* dst = op + (size_t)(rt * 16 + 4 * gq + i) * D + DPL * n;
+        float* dst = buf1 + (rt * 16 + 4 * gq + i) * D + DPL * n;
 #pragma unroll
         for (int jd = 0; jd < DPL; jd += 4)
           *reinterpret_cast<float4*>(dst + jd) =
               make_float4(O[rt][jd][i], O[rt][jd + 1][i], O[rt][jd + 2][i], O[rt][jd + 3][i]);
       }
   }
+  __syncthreads();
+  float* op = a.opart + ((size_t)u.grp * a.splits + u.split) * RT * 16 * D;
+  for (int e = threadIdx.x; e < F / 2; e += kThreads)
+    st_agent(reinterpret_cast<float2*>(op) + e, reinterpret_cast<const float2*>(buf1)[e]);
 }
 
 template <int D, int RT, bool RESIDENT>
@@ -396,6 +543,7 @@ verify_mfma_kernel(VArgs a) {
   typedef typename VVec<D>::T VT;
   __shared__ float s_wm[kWaves][ROWS], s_wz[kWaves][ROWS];
   __shared__ float s_m[ROWS], s_z[ROWS], s_lse[ROWS];
+  __shared__ int s_flag;
   extern __shared__ float s_o[];
 
   Unit u;
@@ -409,6 +557,7 @@ verify_mfma_kernel(VArgs a) {
     }
     __syncthreads();
     exchange_stats<ROWS>(a, u, s_m, s_z, s_lse, false);
+    verify_epilogue<ROWS, D>(a, u, s_lse, true, &s_flag);
     return;
   }
   const size_t kv_off = ((size_t)u.b * a.Hkv + u.g) * a.n_cap * D;
@@ -431,44 +580,57 @@ verify_mfma_kernel(VArgs a) {
     for (int jd = 0; jd < DPL; ++jd) O[rt][jd] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   if constexpr (RESIDENT) {
-    // ---- pass 1: all K blocks of this wave in flight, scores kept resident
+    // ---- pass 1: all K blocks of this wave in flight (registers), then the
+    //      whole chunk's V streamed into LDS by waves 1-3 (wave 0 keeps no
+    //      loads in flight so it can publish the statistics without waiting
+    //      for them); scores kept resident.
+    uint16_t* s_v = reinterpret_cast<uint16_t*>(s_o);
     float S[kNB][2][RT][4];
     uint4 Kr[kNB][2][KS];
-#pragma unroll
-    for (int j = 0; j < kNB; ++j) load_k_block<D>(kg, u.c0 + 32 * (w + kWaves * j), u.c1, n, gq, Kr[j]);
+    // keep the issue order Q, K block 0, 1, ... so block j's wait leaves the
+    // later blocks in flight (the scheduler would otherwise reorder the loads)
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
+      load_k_block<D>(kg, u.c0 + 32 * (w + kWaves * j), u.c1, n, gq, Kr[j]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    const int nblk = (u.c1 - u.c0 + 31) / 32;
+#pragma unroll
+    for (int j = 0; j < kNB; ++j) {
+      if (j == kNB - 1) {
+        // all of this wave's K has landed: queue V behind it so HBM keeps
+        // streaming through the last block, the statistics and the wait
+        __builtin_amdgcn_s_waitcnt(0);
+        if (w > 0)
+          for (int blk = w - 1; blk < nblk; blk += kWaves - 1)
+            issue_v_lds<D>(vg, u.c0 + 32 * blk, u.c1, s_v + blk * 32 * D, lane);
+      }
       const int tb = u.c0 + 32 * (w + kWaves * j);
       if (tb < u.c1) {
         scores_block<D, RT>(a, u, Kr[j], Qb, tb, n, gq, S[j]);
         running_stats<RT>(S[j], m, z);
       }
     }
-    // V of the first two blocks goes in flight before the wait
-    VT Vr[2][8];
-    load_v_block<D>(vg, u.c0 + 32 * w, u.c1, n, gq, Vr[0]);
-    load_v_block<D>(vg, u.c0 + 32 * (w + kWaves), u.c1, n, gq, Vr[1]);
     reduce_stats<RT>(m, z, n, gq, w, s_wm, s_wz, s_m, s_z);
     exchange_stats<ROWS>(a, u, s_m, s_z, s_lse, true);
     float lse[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) lse[rt] = s_lse[rt * 16 + n];
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's V loads have landed in LDS
+    __syncthreads();                // ... and every other wave's
     // ---- pass 2: probabilities, mass, P.V
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
-      const int tb = u.c0 + 32 * (w + kWaves * j);
+      const int blk = w + kWaves * j;
+      const int tb = u.c0 + 32 * blk;
       if (tb < u.c1) {
-        if (j + 2 < kNB) {
-          VT Vn[8];
-          load_v_block<D>(vg, u.c0 + 32 * (w + kWaves * (j + 2)), u.c1, n, gq, Vn);
-          pv_block<D, RT>(S[j], lse, Vr[j & 1], O, mp, tb, u.c1, n, gq);
-#pragma unroll
-          for (int s = 0; s < 8; ++s) Vr[j & 1][s] = Vn[s];
-        } else {
-          pv_block<D, RT>(S[j], lse, Vr[j & 1], O, mp, tb, u.c1, n, gq);
-        }
+        VT Vr[8];
+        read_v_lds<D>(s_v + blk * 32 * D, n, gq, Vr);
+        pv_block<D, RT>(S[j], lse, Vr, O, mp, tb, u.c1, n, gq);
       }
     }
+    __syncthreads();  // V region of LDS is reused below
   } else {
     // ---- pass 1: stream K, running statistics only
     const int nblk = (u.c1 - u.c0 + 31) / 32;
@@ -498,6 +660,7 @@ verify_mfma_kernel(VArgs a) {
     }
   }
   write_opart<D, RT>(a, u, O, s_o, lane, w, n, gq);
+  verify_epilogue<ROWS, D>(a, u, s_lse, false, &s_flag);
 }
 
 // ------------------------------------------------------------ fp32 path --
@@ -511,6 +674,7 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
   float* sKV = sQ + ROWS * D;    // [TC][D]
   float* sS = sKV + TC * D;      // [ROWS][TC]
   __shared__ float s_m[ROWS], s_z[ROWS], s_lse[ROWS];
+  __shared__ int s_flag;
 
   Unit u;
   if (!decode_unit(a, u)) return;
@@ -522,6 +686,7 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
   if (u.c0 >= u.N) {
     __syncthreads();
     exchange_stats<ROWS>(a, u, s_m, s_z, s_lse, false);
+    verify_epilogue<ROWS, D>(a, u, s_lse, true, &s_flag);
     return;
   }
   const int row0 = u.rg * a.RT * 16;
@@ -593,7 +758,7 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
     if (tid < nt) {
       float acc = 0.f;
       for (int r = 0; r < ROWS; ++r) acc += sS[r * TC + tid];
-      mp[base + tid] = acc;
+      st_agent(mp + base + tid, acc);
     }
     load_rows(vg, base, nt);
     __syncthreads();
@@ -607,75 +772,8 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
   }
   float* op = a.opart + ((size_t)u.grp * a.splits + u.split) * ROWS * D;
 #pragma unroll
-  for (int k = 0; k < OPT; ++k) op[tid + k * kThreads] = O[k];
-}
-
-// --------------------------------------------------------------- combine --
-struct CArgs {
-  const float* stats;
-  const float* opart;
-  const float* mpart;
-  const int32_t* ctx_len;
-  int* cnt;
-  void* out;
-  float* lse;
-  float* mass;
-  int64_t n_cap;
-  int B, T, Hq, Hkv, G, R, RG, RT, D, max_ctx, splits, chunk, groups;
-  int f32;
-};
-
-__device__ __forceinline__ int clamp_ctx(int ctx, int max_ctx) {
-  return ctx < 0 ? 0 : (ctx > max_ctx ? max_ctx : ctx);
-}
-
-// blockIdx.y == 0: output rows (sum of chunk partials) and lse;
-// blockIdx.y == 1: mass (sum over KV heads and row groups) and counter reset.
-__global__ void __launch_bounds__(256) verify_combine_kernel(CArgs a) {
-  const int ROWS = a.RT * 16;
-  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (blockIdx.y == 0) {
-    const int64_t total = (int64_t)a.groups * ROWS * a.D;
-    if (gid >= total) return;
-    const int d = gid % a.D;
-    const int r = (gid / a.D) % ROWS;
-    const int grp = gid / ((int64_t)a.D * ROWS);
-    const int row = (grp % a.RG) * ROWS + r;
-    if (row >= a.R) return;
-    const int bg = grp / a.RG, g = bg % a.Hkv, b = bg / a.Hkv;
-    const int N = clamp_ctx(a.ctx_len[b], a.max_ctx) + a.T;
-    const int nsp = min(a.splits, (N + a.chunk - 1) / a.chunk);
-    const float* op = a.opart + (size_t)grp * a.splits * ROWS * a.D + (size_t)r * a.D + d;
-    float acc = 0.f;
-    for (int s = 0; s < nsp; ++s) acc += op[(size_t)s * ROWS * a.D];
-    const int t = row / a.G, h = g * a.G + row % a.G;
-    const size_t oi = (((size_t)b * a.T + t) * a.Hq + h) * a.D + d;
-    if (a.f32)
-      static_cast<float*>(a.out)[oi] = acc;
-    else
-      static_cast<uint16_t*>(a.out)[oi] = f32_to_bf16(acc);
-    if (d == 0 && a.lse) {
-      const float* st = a.stats + (size_t)grp * a.splits * ROWS * 2 + (size_t)r * 2;
-      float M = kNegInf, Z = 0.f;
-      for (int s = 0; s < nsp; ++s) lse_combine(M, Z, st[(size_t)s * ROWS * 2], st[(size_t)s * ROWS * 2 + 1]);
-      a.lse[((size_t)b * a.Hq + h) * a.T + t] = (M + __log2f(Z)) * kLn2;
-    }
-  } else {
-    if (gid < a.groups) a.cnt[gid] = 0;
-    if (!a.mass) return;
-    const int64_t total = (int64_t)a.B * a.n_cap;
-    if (gid >= total) return;
-    const int64_t i = gid % a.n_cap;
-    const int b = gid / a.n_cap;
-    const int N = clamp_ctx(a.ctx_len[b], a.max_ctx) + a.T;
-    float acc = 0.f;
-    if (i < N) {
-      const int P = a.Hkv * a.RG;
-      const float* mp = a.mpart + (size_t)b * P * a.n_cap + i;
-      for (int p = 0; p < P; ++p) acc += mp[(size_t)p * a.n_cap];
-    }
-    a.mass[gid] = acc;
-  }
+  for (int k = 0; k < OPT; ++k) st_agent(op + tid + k * kThreads, O[k]);
+  verify_epilogue<ROWS, D>(a, u, s_lse, false, &s_flag);
 }
 
 // ------------------------------------------------------------------ host --
@@ -685,7 +783,7 @@ struct VPlan {
   int splits, chunk, groups, per_launch, grid;
   bool resident, mfma;
   int lds_dyn;
-  size_t off_cnt, off_stats, off_opart, off_mpart, bytes;
+  size_t off_cnt, off_cnt2, off_done, off_mcnt, off_stats, off_opart, off_mpart, bytes;
 };
 
 typedef void (*VKernel)(VArgs);
@@ -702,9 +800,11 @@ VKernel pick_kernel(int dt, int D, int RT, bool resident) {
   return nullptr;
 }
 
-int lds_bytes(int dt, int D, int RT) {
+int lds_bytes(int dt, int D, int RT, bool resident) {
   if (dt == PVLM_F32) return (RT * 16 * D + kF32Tile * D + RT * 16 * kF32Tile) * 4;
-  return 2 * RT * 16 * D * 4;
+  const int ored = 2 * RT * 16 * D * 4;              // O partial reduction
+  const int vres = resident ? kResTokens * D * 2 : 0;  // the chunk's V (bf16)
+  return ored > vres ? ored : vres;
 }
 
 pvlm_status plan_verify(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int64_t n_cap,
@@ -739,11 +839,15 @@ pvlm_status plan_verify(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int
   p->splits = (int)((p->n_plan + chunk - 1) / chunk);
   p->resident = p->mfma && chunk <= kResTokens;
   p->grid = (p->per_launch * p->splits + 7) / 8 * 8;
-  p->lds_dyn = lds_bytes(dt, D, p->RT);
+  p->lds_dyn = lds_bytes(dt, D, p->RT, p->resident);
   const int ROWS = p->RT * 16;
-  size_t off = 0;
-  p->off_cnt = off;
-  off = align_up(off + sizeof(int) * p->groups, 256);
+  const size_t n_sync = 3 * (size_t)p->groups + (size_t)B * p->splits;
+  if (n_sync > (size_t)kSyncInts) return PVLM_ERR_UNSUPPORTED;
+  p->off_cnt = 0;
+  p->off_cnt2 = p->off_cnt + sizeof(int) * p->groups;
+  p->off_done = p->off_cnt2 + sizeof(int) * p->groups;
+  p->off_mcnt = p->off_done + sizeof(int) * p->groups;
+  size_t off = kSyncRegion;
   p->off_stats = off;
   off = align_up(off + sizeof(float) * (size_t)p->groups * p->splits * ROWS * 2, 256);
   p->off_opart = off;
@@ -789,6 +893,13 @@ extern "C" pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int
   a.opart = reinterpret_cast<float*>(wsb + p.off_opart);
   a.mpart = reinterpret_cast<float*>(wsb + p.off_mpart);
   a.cnt = reinterpret_cast<int*>(wsb + p.off_cnt);
+  a.cnt2 = reinterpret_cast<int*>(wsb + p.off_cnt2);
+  a.done = reinterpret_cast<int*>(wsb + p.off_done);
+  a.mcnt = reinterpret_cast<int*>(wsb + p.off_mcnt);
+  a.out = out;
+  a.lse = lse;
+  a.mass = mass;
+  a.f32 = dt == PVLM_F32;
   a.status = status;
   a.n_cap = n_cap;
   a.B = B;
@@ -807,45 +918,14 @@ extern "C" pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int
   a.sl2 = scale * kLog2e;
   VKernel kern = pick_kernel(dt, D, p.RT, p.resident);
   if (!kern) return PVLM_ERR_UNSUPPORTED;
-  PVLM_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                               hipFuncAttributeMaxDynamicSharedMemorySize, p.lds_dyn));
+  PVLM_HIP(allow_dynamic_lds(reinterpret_cast<const void*>(kern), p.lds_dyn));
   for (int g0 = 0; g0 < p.groups; g0 += p.per_launch) {
     a.grp_base = g0;
     a.ngrp = p.groups - g0 < p.per_launch ? p.groups - g0 : p.per_launch;
     a.grid = (a.ngrp * p.splits + 7) / 8 * 8;
     void* args[] = {&a};
-    PVLM_HIP(hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3(a.grid),
-                                        dim3(kThreads), args, p.lds_dyn, stream));
+    PVLM_HIP(launch_coresident(reinterpret_cast<const void*>(kern), dim3(a.grid), dim3(kThreads),
+                               args, p.lds_dyn, stream));
   }
-  CArgs c;
-  c.stats = a.stats;
-  c.opart = a.opart;
-  c.mpart = a.mpart;
-  c.ctx_len = ctx_len;
-  c.cnt = a.cnt;
-  c.out = out;
-  c.lse = lse;
-  c.mass = mass;
-  c.n_cap = n_cap;
-  c.B = B;
-  c.T = T;
-  c.Hq = Hq;
-  c.Hkv = Hkv;
-  c.G = p.G;
-  c.R = p.R;
-  c.RG = p.RG;
-  c.RT = p.RT;
-  c.D = D;
-  c.max_ctx = (int)max_ctx;
-  c.splits = p.splits;
-  c.chunk = p.chunk;
-  c.groups = p.groups;
-  c.f32 = dt == PVLM_F32;
-  const int64_t n0 = (int64_t)p.groups * p.RT * 16 * D;
-  const int64_t n1 = (int64_t)B * n_cap > p.groups ? (int64_t)B * n_cap : p.groups;
-  const int64_t nmax = n0 > n1 ? n0 : n1;
-  hipLaunchKernelGGL(verify_combine_kernel, dim3((unsigned)((nmax + 255) / 256), 2), dim3(256), 0,
-                     stream, c);
-  PVLM_LAUNCHED();
   return PVLM_OK;
 }

@@ -56,10 +56,12 @@ def test_other_calls_reject():
     assert L.pvlm_topk_select(1, 10, FAKE, FAKE, 4, None, FAKE, None, 0, None, None) == 1
     assert L.pvlm_topk_select(0, 10, FAKE, FAKE, 4, FAKE, FAKE, None, 0, None, None) == 2
     # gather: unsupported row size, NULL destination
-    assert L.pvlm_gather_kv(1, 1, 1, 3, 10, FAKE, FAKE, FAKE, FAKE, 4, FAKE, FAKE, 8, FAKE, FAKE,
-                            None, None) == 3
-    assert L.pvlm_gather_kv(1, 1, 1, 128, 10, FAKE, FAKE, FAKE, FAKE, 4, FAKE, FAKE, 8, None,
+    assert L.pvlm_gather_kv(1, 1, 1, 1, 3, 10, FAKE, FAKE, FAKE, FAKE, 4, FAKE, FAKE, 8, FAKE,
+                            FAKE, None, None) == 3
+    assert L.pvlm_gather_kv(1, 1, 1, 1, 128, 10, FAKE, FAKE, FAKE, FAKE, 4, FAKE, FAKE, 8, None,
                             FAKE, None, None) == 1
+    assert L.pvlm_gather_kv(1, 0, 1, 1, 128, 10, FAKE, FAKE, FAKE, FAKE, 4, FAKE, FAKE, 8, FAKE,
+                            FAKE, None, None) == 2
     # accept: gamma 0, too many rows, negative temperature, tiny workspace
     args = [FAKE] * 8
     assert L.pvlm_spec_accept(1, 0, 10, 1.0, *args, FAKE, 1 << 20, None, None) == 2

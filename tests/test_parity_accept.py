@@ -91,3 +91,24 @@ def test_greedy_matches_target_argmax_chain():
     n, y, _ = _run(a)
     assert list(n) == [w.gamma, 3, 0]
     assert list(y) == [am[0, w.gamma], am[1, 3], am[2, 0]]
+
+
+def test_workspace_reused_across_shapes():
+    """One workspace serves calls of different shapes in sequence (the
+    synchronisation counters live in a fixed region every call leaves zeroed)."""
+    ws = pv.Workspace(torch.device("cuda", 0))
+    cases = [W.make_accept_inputs(W.WORKLOADS["tiny"], batch=64, salt=5),
+             W.make_accept_inputs(W.WORKLOADS["llava72b"], salt=7),
+             W.make_accept_inputs(W.WORKLOADS["qwen32b"], vocab=50000, salt=8),
+             W.make_accept_inputs(W.WORKLOADS["tiny"], batch=64, salt=6)]
+    for a in cases:
+        note(f"accept ws reuse B={a.draft_logits.shape[0]} V={a.draft_logits.shape[2]}")
+        n, y, tie = pv.spec_accept(to_dev(a.draft_logits), to_dev(a.target_logits),
+                                   to_dev(a.draft_tokens), to_dev(a.u_accept), to_dev(a.u_sample),
+                                   a.temperature, ws=ws)
+        torch.cuda.synchronize()
+        rn, ry, rt = oracle.spec_accept(a.draft_logits, a.target_logits, a.draft_tokens,
+                                        a.u_accept, a.u_sample, a.temperature)
+        ok = (rt == 0) & (tie.cpu().numpy() == 0)
+        assert np.array_equal(n.cpu().numpy()[ok], rn[ok])
+        assert np.array_equal(y.cpu().numpy()[ok], ry[ok])

@@ -110,3 +110,19 @@ def test_deterministic_and_reusable_workspace():
         assert torch.equal(o, runs[0][0]) and torch.equal(m, runs[0][1]) and torch.equal(l, runs[0][2])
     mass = to_host_f64(runs[0][1])
     assert abs(mass.sum() - w.hq * w.T) < 1e-3 * w.hq * w.T
+
+
+def test_workspace_reused_across_shapes():
+    ws = pv.Workspace(torch.device("cuda", 0))
+    shapes = [(2, 5, 8, 2, 128, [300, 517]), (1, 9, 64, 8, 128, [1111]),
+              (1, 3, 8, 8, 128, [3000]), (3, 4, 6, 3, 128, [0, 1, 31]), (1, 9, 16, 1, 128, [900])]
+    for (B, T, Hq, Hkv, D, ctx) in shapes:
+        inp = W.random_verify_inputs(B, T, Hq, Hkv, D, ctx, "bf16", seed=B + T + Hq)
+        note(f"verify ws reuse {inp.q.shape} {inp.k.shape}")
+        out, mass, lse = pv.verify_attn(to_dev(inp.q), to_dev(inp.k), to_dev(inp.v),
+                                        to_dev(inp.ctx_len), ws=ws)
+        torch.cuda.synchronize()
+        ro, rl, rm = oracle.verify_attn(f64(inp.q, "bf16"), f64(inp.k, "bf16"),
+                                        f64(inp.v, "bf16"), inp.ctx_len, inp.scale)
+        assert_out(to_host_f64(out), ro)
+        assert_mass(to_host_f64(mass), rm, Hq, T)

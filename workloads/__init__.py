@@ -376,3 +376,57 @@ def make_scores(n_rows: int, m: int, kind: str = "normal", seed: int = 0) -> np.
         s[(sel >= 0.2) & (sel < 0.3)] = -0.0
         return s
     raise ValueError(kind)
+
+
+# ------------------------------------------------- device-side generation --
+def make_verify_layer_torch(w: Workload, seed_layer: int, boost: float, device,
+                            k_out=None, v_out=None, q_out=None):
+    """Same recipe as ``make_verify_inputs`` (N(0,1) draws in float64, salient
+    boost along the group's unit mean query before RoPE, rotate-half RoPE in
+    float64, rounding to the storage dtype), drawn with torch's generator on
+    ``device`` so large stacked caches can be built quickly.  The values differ
+    from the numpy stream of the same seed.  Writes into the given tensors
+    ([B][Hkv][n_cap][D] and [B][T][Hq][D]) or allocates them.
+    """
+    import torch
+    lens = w.lengths()
+    B, T, Hq, Hkv, D = w.batch, w.T, w.hq, w.hkv, w.head_dim
+    n_cap = w.n_cap()
+    G = w.group
+    tdt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    gen = torch.Generator(device=device)
+    gen.manual_seed(SEED_ROOT * 1000003 + w.config_id * 10007 + seed_layer)
+    if k_out is None:
+        k_out = torch.zeros((B, Hkv, n_cap, D), dtype=tdt, device=device)
+    if v_out is None:
+        v_out = torch.zeros((B, Hkv, n_cap, D), dtype=tdt, device=device)
+    if q_out is None:
+        q_out = torch.zeros((B, T, Hq, D), dtype=tdt, device=device)
+    f64 = torch.float64
+    h = D // 2
+    theta = w.rope_base ** (-2.0 * torch.arange(h, dtype=f64, device=device) / D)
+
+    def rope(x, pos):
+        ang = pos.to(f64)[..., None] * theta
+        c, s = torch.cos(ang), torch.sin(ang)
+        a, b = x[..., :h], x[..., h:]
+        return torch.cat([a * c - b * s, a * s + b * c], dim=-1)
+
+    q64 = torch.randn((B, T, Hq, D), dtype=f64, device=device, generator=gen)
+    for b in range(B):
+        N = int(lens[b]) + T
+        pos = torch.arange(N, device=device)
+        rows = None
+        if boost:
+            rows = torch.from_numpy(salient_rows(w, b, int(lens[b]) - w.n_text)).to(device)
+        for g in range(Hkv):
+            kg = torch.randn((N, D), dtype=f64, device=device, generator=gen)
+            if boost:
+                mq = q64[b, :, g * G:(g + 1) * G, :].reshape(-1, D).mean(dim=0)
+                kg[rows] += boost * mq / torch.linalg.norm(mq)
+            k_out[b, g, :N] = rope(kg, pos).to(torch.float32).to(tdt)
+            v_out[b, g, :N] = torch.randn((N, D), dtype=f64, device=device,
+                                          generator=gen).to(torch.float32).to(tdt)
+        qpos = torch.arange(T, device=device) + int(lens[b])
+        q_out[b] = rope(q64[b], qpos[:, None]).to(torch.float32).to(tdt)
+    return q_out, k_out, v_out
