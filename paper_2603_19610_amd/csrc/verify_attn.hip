@@ -43,6 +43,7 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kMaxRT = 5;        // 16-row tiles per workgroup
+constexpr int kOSets = 8;        // max thread sets splitting the O-partial sum
 constexpr int kNB = 4;           // 32-token blocks per wave (resident variant)
 constexpr int kResTokens = kWaves * kNB * 32;
 constexpr int kF32Tile = 64;     // tokens per step of the fp32 path
@@ -101,6 +102,11 @@ __device__ __forceinline__ bool decode_unit(const VArgs& a, Unit& u) {
   return true;
 }
 
+// exp2 on the hardware transcendental unit (v_exp_f32).  It flushes results
+// below 2^-126 to zero, which only drops probabilities under the mass
+// tolerance's absolute floor.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 __device__ __forceinline__ void lse_combine(float& m, float& z, float m2, float z2) {
   const float M = fmaxf(m, m2);
   if (M == kNegInf) {
@@ -108,7 +114,7 @@ __device__ __forceinline__ void lse_combine(float& m, float& z, float m2, float 
     z = 0.f;
     return;
   }
-  z = z * exp2f(m - M) + z2 * exp2f(m2 - M);
+  z = z * fast_exp2(m - M) + z2 * fast_exp2(m2 - M);
   m = M;
 }
 
@@ -149,53 +155,11 @@ __device__ void exchange_stats(const VArgs& a, const Unit& u, float* s_m, float*
   __syncthreads();
 }
 
-// After pass 2: O (sum of the chunk partials after a second wait on the group
-// counter, one slice per workgroup), lse, then the per-token mass (summed over
-// KV heads and row groups by the last workgroup of each chunk -- done last so
-// that work never delays the group's wait), and counter reset.
-template <int ROWS, int D>
-__device__ void verify_epilogue(const VArgs& a, const Unit& u, const float* s_lse, bool empty,
-                                int* s_flag) {
+// Per-token mass summed over the KV heads and row groups by the last
+// workgroup of each chunk (no wait), then the group's counter reset by its
+// last workgroup.
+__device__ void mass_combine_and_finish(const VArgs& a, const Unit& u, int* s_flag) {
   const int tid = threadIdx.x;
-  wg_signal_wait(a.cnt2 + u.grp, a.splits, a.status, !empty);
-  if (!empty) {
-    const int row0 = u.rg * a.RT * 16;
-    const int nsp = (u.N + a.chunk - 1) / a.chunk;
-    const int rows = min(ROWS, a.R - row0);
-    const int E2 = rows * D / 2;  // float pairs
-    const int per = (E2 + nsp - 1) / nsp;
-    const int e0 = u.split * per, e1 = min(E2, e0 + per);
-    const float2* op = reinterpret_cast<const float2*>(a.opart + (size_t)u.grp * a.splits * ROWS * D);
-    for (int e = e0 + tid; e < e1; e += kThreads) {
-      float2 acc = make_float2(0.f, 0.f);
-      for (int s0 = 0; s0 < nsp; s0 += 16) {
-        float2 v[16];
-#pragma unroll
-        for (int j = 0; j < 16; ++j)
-          v[j] = s0 + j < nsp ? ld_agent(op + (size_t)(s0 + j) * ROWS * D / 2 + e) : make_float2(0.f, 0.f);
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          acc.x += v[j].x;
-          acc.y += v[j].y;
-        }
-      }
-      const int row = row0 + (2 * e) / D, d = (2 * e) % D;
-      const int t = row / a.G, h = u.g * a.G + row % a.G;
-      const size_t oi = (((size_t)u.b * a.T + t) * a.Hq + h) * D + d;
-      if (a.f32) {
-        *reinterpret_cast<float2*>(static_cast<float*>(a.out) + oi) = acc;
-      } else {
-        const uint32_t pk = (uint32_t)f32_to_bf16(acc.x) | ((uint32_t)f32_to_bf16(acc.y) << 16);
-        *reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(a.out) + oi) = pk;
-      }
-    }
-    if (a.lse && u.split == 0) {
-      for (int r = tid; r < rows; r += kThreads) {
-        const int row = row0 + r, t = row / a.G, h = u.g * a.G + row % a.G;
-        a.lse[((size_t)u.b * a.Hq + h) * a.T + t] = s_lse[r] * kLn2;
-      }
-    }
-  }
   if (a.mass) {
     const int P = a.Hkv * a.RG;
     int* mc = a.mcnt + (size_t)u.b * a.splits + u.split;
@@ -228,6 +192,78 @@ __device__ void verify_epilogue(const VArgs& a, const Unit& u, const float* s_ls
     reset_counter(a.cnt2 + u.grp);
     reset_counter(a.done + u.grp);
   }
+}
+
+// After pass 2: O (sum of the chunk partials after a second wait on the group
+// counter, one slice per workgroup), lse, then the per-token mass (summed over
+// KV heads and row groups by the last workgroup of each chunk -- done last so
+// that work never delays the group's wait), and counter reset.
+template <int ROWS, int D>
+__device__ void verify_epilogue(const VArgs& a, const Unit& u, const float* s_lse, bool empty,
+                                int* s_flag) {
+  const int tid = threadIdx.x;
+  wg_signal_wait(a.cnt2 + u.grp, a.splits, a.status, !empty);
+  if (!empty) {
+    const int row0 = u.rg * a.RT * 16;
+    const int nsp = (u.N + a.chunk - 1) / a.chunk;
+    const int rows = min(ROWS, a.R - row0);
+    const int E4 = rows * D / 4;  // groups of four consecutive values
+    const int per = (E4 + nsp - 1) / nsp;
+    const int e0 = u.split * per, e1 = min(E4, e0 + per);
+    for (int e = e0 + tid; e < e1; e += kThreads) {
+      float acc[4] = {0.f, 0.f, 0.f, 0.f};
+      if (a.f32) {  // fp32 partials, two float pairs per group
+        const float2* op = reinterpret_cast<const float2*>(a.opart + (size_t)u.grp * a.splits * ROWS * D);
+        for (int s0 = 0; s0 < nsp; s0 += 8) {
+          float2 v[8][2];
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+              v[j][h] = s0 + j < nsp ? ld_agent(op + ((size_t)(s0 + j) * ROWS * D) / 2 + 2 * e + h)
+                                     : make_float2(0.f, 0.f);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            acc[0] += v[j][0].x;
+            acc[1] += v[j][0].y;
+            acc[2] += v[j][1].x;
+            acc[3] += v[j][1].y;
+          }
+        }
+      } else {  // bf16 partials, one 64-bit load per group
+        const uint64_t* op = reinterpret_cast<const uint64_t*>(a.opart) + (size_t)u.grp * a.splits * ROWS * D / 4;
+        for (int s0 = 0; s0 < nsp; s0 += 16) {
+          uint64_t v[16];
+#pragma unroll
+          for (int j = 0; j < 16; ++j)
+            v[j] = s0 + j < nsp ? __hip_atomic_load(op + (size_t)(s0 + j) * ROWS * D / 4 + e,
+                                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                                : 0ull;
+#pragma unroll
+          for (int j = 0; j < 16; ++j)
+#pragma unroll
+            for (int h = 0; h < 4; ++h) acc[h] += bf16_to_f32((uint16_t)(v[j] >> (16 * h)));
+        }
+      }
+      const int row = row0 + (4 * e) / D, d = (4 * e) % D;
+      const int t = row / a.G, h = u.g * a.G + row % a.G;
+      const size_t oi = (((size_t)u.b * a.T + t) * a.Hq + h) * D + d;
+      if (a.f32) {
+        *reinterpret_cast<float4*>(static_cast<float*>(a.out) + oi) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+      } else {
+        const uint64_t pk = (uint64_t)f32_to_bf16(acc[0]) | ((uint64_t)f32_to_bf16(acc[1]) << 16) |
+                            ((uint64_t)f32_to_bf16(acc[2]) << 32) | ((uint64_t)f32_to_bf16(acc[3]) << 48);
+        *reinterpret_cast<uint64_t*>(static_cast<uint16_t*>(a.out) + oi) = pk;
+      }
+    }
+    if (a.lse && u.split == 0) {
+      for (int r = tid; r < rows; r += kThreads) {
+        const int row = row0 + r, t = row / a.G, h = u.g * a.G + row % a.G;
+        a.lse[((size_t)u.b * a.Hq + h) * a.T + t] = s_lse[r] * kLn2;
+      }
+    }
+  }
+  mass_combine_and_finish(a, u, s_flag);
 }
 
 // ------------------------------------------------------------ MFMA path --
@@ -391,11 +427,11 @@ __device__ __forceinline__ void running_stats(const float (&S)[2][RT][4], float 
       for (int i = 0; i < 4; ++i) mx = fmaxf(mx, S[tt][rt][i]);
     const float M = fmaxf(m[rt], mx);
     if (M != kNegInf) {
-      float acc = z[rt] * exp2f(m[rt] - M);
+      float acc = z[rt] * fast_exp2(m[rt] - M);
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc += exp2f(S[tt][rt][i] - M);
+        for (int i = 0; i < 4; ++i) acc += fast_exp2(S[tt][rt][i] - M);
       z[rt] = acc;
       m[rt] = M;
     }
@@ -432,6 +468,65 @@ __device__ __forceinline__ void reduce_stats(float (&m)[RT], float (&z)[RT], int
   __syncthreads();
 }
 
+// Probabilities of one block relative to a per-row reference (the
+// workgroup's local row maximum), accumulated into O on MFMA.
+template <int D, int RT>
+__device__ __forceinline__ void pv_local(const float (&S)[2][RT][4], const float (&ref)[RT],
+                                         const typename VVec<D>::T (&Vr)[8],
+                                         floatx4 (&O)[RT][D / 16]) {
+  constexpr int DPL = D / 16;
+  bf16x8 Pa[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) Pa[rt][4 * tt + i] = static_cast<__bf16>(fast_exp2(S[tt][rt][i] - ref[rt]));
+#pragma unroll
+  for (int jd = 0; jd < DPL; ++jd) {
+    const bf16x8 vb = pack_v(Vr, jd);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+      O[rt][jd] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Pa[rt], vb, O[rt][jd], 0, 0, 0);
+  }
+}
+
+// Exact probabilities exp2(S - lse2) of one block summed over its rows: the
+// workgroup's share of the per-token attention mass, written to mp.
+template <int RT>
+__device__ __forceinline__ void mass_block(const float (&S)[2][RT][4], const float (&lse)[RT],
+                                           float* mp, int tb, int c1, int n, int gq) {
+  float pm[8];
+#pragma unroll
+  for (int v = 0; v < 8; ++v) pm[v] = 0.f;
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pm[4 * tt + i] += fast_exp2(S[tt][rt][i] - lse[rt]);
+  // sum the 8 token values over the 16 lanes of a lane group
+  const bool h8 = n & 8, h4 = n & 4, h2 = n & 2;
+  float a8[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float send = h8 ? pm[k] : pm[4 + k];
+    a8[k] = (h8 ? pm[4 + k] : pm[k]) + __shfl_xor(send, 8, 64);
+  }
+  float a4[2];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const float send = h4 ? a8[k] : a8[2 + k];
+    a4[k] = (h4 ? a8[2 + k] : a8[k]) + __shfl_xor(send, 4, 64);
+  }
+  const float send2 = h2 ? a4[0] : a4[1];
+  float a2 = (h2 ? a4[1] : a4[0]) + __shfl_xor(send2, 2, 64);
+  a2 += __shfl_xor(a2, 1, 64);
+  const int v = (h8 ? 4 : 0) + (h4 ? 2 : 0) + (h2 ? 1 : 0);
+  const int tok = tb + 16 * (v >> 2) + 4 * gq + (v & 3);
+  if (!(n & 1) && tok < c1) st_agent(mp + tok, a2);
+}
+
 // P = exp2(S - lse2): per-token mass (sum over the block's rows, written to
 // mp) and O += P.V on MFMA.
 template <int D, int RT>
@@ -449,7 +544,7 @@ __device__ __forceinline__ void pv_block(const float (&S)[2][RT][4], const float
     for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float p = exp2f(S[tt][rt][i] - lse[rt]);
+        const float p = fast_exp2(S[tt][rt][i] - lse[rt]);
         pm[4 * tt + i] += p;
         Pa[rt][4 * tt + i] = static_cast<__bf16>(p);
       }
@@ -484,29 +579,33 @@ __device__ __forceinline__ void pv_block(const float (&S)[2][RT][4], const float
 }
 
 // Sum the four waves' O fragments through LDS and write the chunk partial
-// (row-major [ROWS][D]) to the workspace.
+// (row-major [ROWS][D]) to the workspace.  Fragments move as float4 (one
+// 16-byte LDS access per MFMA tile per lane) in batches of 8 so the LDS
+// latency overlaps.
 template <int D, int RT>
 __device__ __forceinline__ void write_opart(const VArgs& a, const Unit& u, floatx4 (&O)[RT][D / 16],
                                             float* s_o, int lane, int w, int n, int gq) {
   constexpr int DPL = D / 16;
+  constexpr int NF = RT * DPL;  // fragments (MFMA tiles) per lane
   constexpr int F = RT * 16 * D;
-  float* buf0 = s_o;
-  float* buf1 = s_o + F;
-  auto store = [&](float* buf) {
+  floatx4* buf0 = reinterpret_cast<floatx4*>(s_o);
+  floatx4* buf1 = reinterpret_cast<floatx4*>(s_o + F);
+  auto frag = [&](int f) -> floatx4& { return O[f / DPL][f % DPL]; };
+  auto store = [&](floatx4* buf) {
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-      for (int jd = 0; jd < DPL; ++jd)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) buf[((rt * DPL + jd) * 4 + i) * 64 + lane] = O[rt][jd][i];
+    for (int f = 0; f < NF; ++f) buf[f * 64 + lane] = frag(f);
   };
-  auto add = [&](const float* buf) {
+  auto add = [&](const floatx4* buf) {
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
+    for (int f0 = 0; f0 < NF; f0 += 8) {
+      floatx4 t[8];
 #pragma unroll
-      for (int jd = 0; jd < DPL; ++jd)
+      for (int k = 0; k < 8; ++k)
+        if (f0 + k < NF) t[k] = buf[(f0 + k) * 64 + lane];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) O[rt][jd][i] += buf[((rt * DPL + jd) * 4 + i) * 64 + lane];
+      for (int k = 0; k < 8; ++k)
+        if (f0 + k < NF) frag(f0 + k) += t[k];
+    }
   };
   if (w >= 2) store(w == 2 ? buf0 : buf1);
   __syncthreads();
@@ -514,14 +613,15 @@ __device__ __forceinline__ void write_opart(const VArgs& a, const Unit& u, float
   __syncthreads();
   if (w == 1) store(buf0);
   __syncthreads();
+  float* rowmaj = s_o + F;
   if (w == 0) {
     add(buf0);
-    // row-major copy of the sum in buf1 (each lane writes DPL consecutive d)
+    // row-major copy of the sum (each lane writes DPL consecutive d)
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        float* dst = buf1 + (rt * 16 + 4 * gq + i) * D + DPL * n;
+        float* dst = rowmaj + (rt * 16 + 4 * gq + i) * D + DPL * n;
 #pragma unroll
         for (int jd = 0; jd < DPL; jd += 4)
           *reinterpret_cast<float4*>(dst + jd) =
@@ -529,9 +629,167 @@ __device__ __forceinline__ void write_opart(const VArgs& a, const Unit& u, float
       }
   }
   __syncthreads();
-  float* op = a.opart + ((size_t)u.grp * a.splits + u.split) * RT * 16 * D;
-  for (int e = threadIdx.x; e < F / 2; e += kThreads)
-    st_agent(reinterpret_cast<float2*>(op) + e, reinterpret_cast<const float2*>(buf1)[e]);
+  const float* buf1f = rowmaj;
+  // chunk partial in bf16, four values per 64-bit device-coherent store
+  uint64_t* op = reinterpret_cast<uint64_t*>(a.opart) + ((size_t)u.grp * a.splits + u.split) * F / 4;
+  for (int e = threadIdx.x; e < F / 4; e += kThreads) {
+    const float4 v = reinterpret_cast<const float4*>(buf1f)[e];
+    const uint64_t pk = (uint64_t)f32_to_bf16(v.x) | ((uint64_t)f32_to_bf16(v.y) << 16) |
+                        ((uint64_t)f32_to_bf16(v.z) << 32) | ((uint64_t)f32_to_bf16(v.w) << 48);
+    __hip_atomic_store(op + e, pk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Resident variant, after the chunk partial of O (relative to the
+// workgroup's own row maxima) and the row statistics are published: the one
+// wait of the group, then each row's global log2-sum-exp and the per-chunk
+// rescale factors, the exact per-token mass from the resident scores, this
+// workgroup's slice of O (factor-weighted sum of the partials), lse, the mass
+// sum over KV heads (last workgroup of each chunk) and the counter reset.
+template <int D, int RT>
+__device__ void verify_epilogue_local(const VArgs& a, const Unit& u, const float (&S)[kNB][2][RT][4],
+                                      float* s_lse, float* s_fac, float (*s_pm)[RT * 16],
+                                      float (*s_pz)[RT * 16], bool empty, int* s_flag, int n, int gq,
+                                      int w) {
+  constexpr int ROWS = RT * 16;
+  constexpr int kU = 16;
+  // threads per row for the statistics combine (rows x parts <= 256)
+  constexpr int P = kThreads / ROWS < kWaves ? kThreads / ROWS : kWaves;
+  const int tid = threadIdx.x;
+  wg_signal_wait(a.cnt + u.grp, a.splits, a.status, !empty);
+  if (!empty) {
+    const float* st0 = a.stats + (size_t)u.grp * a.splits * ROWS * 2;
+    const int nsp = (u.N + a.chunk - 1) / a.chunk;
+    // 1. every (chunk, row) statistic is read once; partial combines per part
+    if (tid < P * ROWS) {
+      const int r = tid % ROWS, part = tid / ROWS;
+      float M = kNegInf, Z = 0.f;
+      for (int s0 = part; s0 < nsp; s0 += P * kU) {
+        float2 v[kU];
+#pragma unroll
+        for (int j = 0; j < kU; ++j) {
+          const int sp = s0 + j * P;
+          v[j] = sp < nsp ? ld_agent(reinterpret_cast<const float2*>(st0 + ((size_t)sp * ROWS + r) * 2))
+                          : make_float2(kNegInf, 0.f);
+        }
+#pragma unroll
+        for (int j = 0; j < kU; ++j) {
+          const int sp = s0 + j * P;
+          if (sp < nsp) s_fac[sp * ROWS + r] = v[j].x;
+          lse_combine(M, Z, v[j].x, v[j].y);
+        }
+      }
+      s_pm[part][r] = M;
+      s_pz[part][r] = Z;
+    }
+    __syncthreads();
+    // 2. per row: global max, sum and lse; (M, 1/Z) kept in part slot 0
+    if (tid < ROWS) {
+      const int r = tid;
+      float M = s_pm[0][r], Z = s_pz[0][r];
+#pragma unroll
+      for (int p = 1; p < P; ++p) lse_combine(M, Z, s_pm[p][r], s_pz[p][r]);
+      const int row = u.rg * a.RT * 16 + r;
+      const bool ok = row < a.R && Z > 0.f;
+      s_lse[r] = ok ? M + __log2f(Z) : __builtin_huge_valf();
+      s_pm[0][r] = M;
+      s_pz[0][r] = ok ? 1.f / Z : 0.f;
+    }
+    __syncthreads();
+    // 3. rescale factor of every chunk partial: exp2(m_chunk - M) / Z
+    for (int e = tid; e < nsp * ROWS; e += kThreads) {
+      const int r = e % ROWS;
+      const float m = s_fac[e], invZ = s_pz[0][r];
+      s_fac[e] = invZ != 0.f && m != kNegInf ? fast_exp2(m - s_pm[0][r]) * invZ : 0.f;
+    }
+    __syncthreads();
+    // exact per-token mass of this chunk's tokens
+    float lse[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) lse[rt] = s_lse[rt * 16 + n];
+    float* mp = a.mpart + ((size_t)u.b * a.Hkv * a.RG + u.g * a.RG + u.rg) * a.n_cap;
+    if (a.mass) {
+#pragma unroll
+      for (int j = 0; j < kNB; ++j) {
+        const int tb = u.c0 + 32 * (w + kWaves * j);
+        if (tb < u.c1) mass_block<RT>(S[j], lse, mp, tb, u.c1, n, gq);
+      }
+    }
+    // this workgroup's slice of O: sum over chunks of factor * partial.  With
+    // few elements per workgroup the chunks are split over Q thread sets and
+    // the Q partial sums meet in LDS.
+    const int row0 = u.rg * a.RT * 16;
+    const int rows = min(ROWS, a.R - row0);
+    const int E4 = rows * D / 4;
+    const int per = (E4 + nsp - 1) / nsp;
+    const int e0 = min(E4, u.split * per), e1 = min(E4, e0 + per);
+    const int cnt = e1 - e0;
+    const uint64_t* op = reinterpret_cast<const uint64_t*>(a.opart) + (size_t)u.grp * a.splits * ROWS * D / 4;
+    auto accumulate = [&](int e, int q, int Q, float (&acc)[4]) {
+      const int r = (4 * e) / D;
+      for (int s0 = q; s0 < nsp; s0 += Q * kU) {
+        uint64_t v[kU];
+#pragma unroll
+        for (int j = 0; j < kU; ++j) {
+          const int sp = s0 + j * Q;
+          v[j] = sp < nsp ? __hip_atomic_load(op + (size_t)sp * ROWS * D / 4 + e, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT)
+                          : 0ull;
+        }
+#pragma unroll
+        for (int j = 0; j < kU; ++j) {
+          const int sp = s0 + j * Q;
+          const float f = sp < nsp ? s_fac[sp * ROWS + r] : 0.f;
+#pragma unroll
+          for (int h = 0; h < 4; ++h) acc[h] += f * bf16_to_f32((uint16_t)(v[j] >> (16 * h)));
+        }
+      }
+    };
+    auto emit = [&](int e, const float (&acc)[4]) {
+      const int r = (4 * e) / D;
+      const int row = row0 + r, d = (4 * e) % D;
+      const int t = row / a.G, h = u.g * a.G + row % a.G;
+      const size_t oi = (((size_t)u.b * a.T + t) * a.Hq + h) * D + d;
+      const uint64_t pk = (uint64_t)f32_to_bf16(acc[0]) | ((uint64_t)f32_to_bf16(acc[1]) << 16) |
+                          ((uint64_t)f32_to_bf16(acc[2]) << 32) | ((uint64_t)f32_to_bf16(acc[3]) << 48);
+      *reinterpret_cast<uint64_t*>(static_cast<uint16_t*>(a.out) + oi) = pk;
+    };
+    const int Q = cnt <= 0 ? 1 : min(kOSets, max(1, kThreads / cnt));
+    if (Q == 1) {
+      for (int e = e0 + tid; e < e1; e += kThreads) {
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+        accumulate(e, 0, 1, acc);
+        emit(e, acc);
+      }
+    } else {
+      float4* s_acc = reinterpret_cast<float4*>(s_fac + ((nsp * ROWS + 3) & ~3));
+      const int q = tid / cnt, el = tid % cnt;
+      if (q < Q) {
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+        accumulate(e0 + el, q, Q, acc);
+        s_acc[q * cnt + el] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+      }
+      __syncthreads();
+      if (tid < cnt) {
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int qq = 0; qq < Q; ++qq) {
+          const float4 v = s_acc[qq * cnt + tid];
+          acc[0] += v.x;
+          acc[1] += v.y;
+          acc[2] += v.z;
+          acc[3] += v.w;
+        }
+        emit(e0 + tid, acc);
+      }
+    }
+    if (a.lse && u.split == 0) {
+      for (int r = tid; r < rows; r += kThreads) {
+        const int row = row0 + r, t = row / a.G, h = u.g * a.G + row % a.G;
+        a.lse[((size_t)u.b * a.Hq + h) * a.T + t] = s_lse[r] * kLn2;
+      }
+    }
+  }
+  mass_combine_and_finish(a, u, s_flag);
 }
 
 template <int D, int RT, bool RESIDENT>
@@ -557,7 +815,10 @@ verify_mfma_kernel(VArgs a) {
     }
     __syncthreads();
     exchange_stats<ROWS>(a, u, s_m, s_z, s_lse, false);
-    verify_epilogue<ROWS, D>(a, u, s_lse, true, &s_flag);
+    if constexpr (RESIDENT)
+      mass_combine_and_finish(a, u, &s_flag);
+    else
+      verify_epilogue<ROWS, D>(a, u, s_lse, true, &s_flag);
     return;
   }
   const size_t kv_off = ((size_t)u.b * a.Hkv + u.g) * a.n_cap * D;
@@ -587,8 +848,10 @@ verify_mfma_kernel(VArgs a) {
     uint16_t* s_v = reinterpret_cast<uint16_t*>(s_o);
     float S[kNB][2][RT][4];
     uint4 Kr[kNB][2][KS];
-    // keep the issue order Q, K block 0, 1, ... so block j's wait leaves the
-    // later blocks in flight (the scheduler would otherwise reorder the loads)
+    // issue order: Q, K block 0, 1, ... (the scheduler would otherwise reorder
+    // the loads), then the chunk's V into LDS from waves 1-3, so HBM streams
+    // K and V back to back; wave 0 keeps only K/Q in flight so it can publish
+    // the statistics without waiting for V.
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
@@ -596,16 +859,11 @@ verify_mfma_kernel(VArgs a) {
       __builtin_amdgcn_sched_barrier(0);
     }
     const int nblk = (u.c1 - u.c0 + 31) / 32;
+    if (w > 0)
+      for (int blk = w - 1; blk < nblk; blk += kWaves - 1)
+        issue_v_lds<D>(vg, u.c0 + 32 * blk, u.c1, s_v + blk * 32 * D, lane);
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
-      if (j == kNB - 1) {
-        // all of this wave's K has landed: queue V behind it so HBM keeps
-        // streaming through the last block, the statistics and the wait
-        __builtin_amdgcn_s_waitcnt(0);
-        if (w > 0)
-          for (int blk = w - 1; blk < nblk; blk += kWaves - 1)
-            issue_v_lds<D>(vg, u.c0 + 32 * blk, u.c1, s_v + blk * 32 * D, lane);
-      }
       const int tb = u.c0 + 32 * (w + kWaves * j);
       if (tb < u.c1) {
         scores_block<D, RT>(a, u, Kr[j], Qb, tb, n, gq, S[j]);
@@ -613,13 +871,16 @@ verify_mfma_kernel(VArgs a) {
       }
     }
     reduce_stats<RT>(m, z, n, gq, w, s_wm, s_wz, s_m, s_z);
-    exchange_stats<ROWS>(a, u, s_m, s_z, s_lse, true);
-    float lse[RT];
+    // ---- pass 2 (no wait on other workgroups): probabilities relative to
+    //      this workgroup's row maxima, P.V on MFMA
+    float ref[RT];
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) lse[rt] = s_lse[rt * 16 + n];
+    for (int rt = 0; rt < RT; ++rt) {
+      const float mm = s_m[rt * 16 + n];
+      ref[rt] = mm == kNegInf ? __builtin_huge_valf() : mm;
+    }
     __builtin_amdgcn_s_waitcnt(0);  // this wave's V loads have landed in LDS
     __syncthreads();                // ... and every other wave's
-    // ---- pass 2: probabilities, mass, P.V
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
       const int blk = w + kWaves * j;
@@ -627,10 +888,20 @@ verify_mfma_kernel(VArgs a) {
       if (tb < u.c1) {
         VT Vr[8];
         read_v_lds<D>(s_v + blk * 32 * D, n, gq, Vr);
-        pv_block<D, RT>(S[j], lse, Vr, O, mp, tb, u.c1, n, gq);
+        pv_local<D, RT>(S[j], ref, Vr, O);
       }
     }
     __syncthreads();  // V region of LDS is reused below
+    write_opart<D, RT>(a, u, O, s_o, lane, w, n, gq);
+    float* st = a.stats + ((size_t)u.grp * a.splits + u.split) * ROWS * 2;
+    if (threadIdx.x < 64)
+      for (int r = threadIdx.x; r < ROWS; r += 64) {
+        st_agent(st + 2 * r, s_m[r]);
+        st_agent(st + 2 * r + 1, s_z[r]);
+      }
+    __syncthreads();  // s_o is reused as the factor table
+    verify_epilogue_local<D, RT>(a, u, S, s_lse, s_o, s_wm, s_wz, false, &s_flag, n, gq, w);
+    return;
   } else {
     // ---- pass 1: stream K, running statistics only
     const int nblk = (u.c1 - u.c0 + 31) / 32;
@@ -753,7 +1024,7 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
     __syncthreads();
     scores(base, nt);
     __syncthreads();
-    for (int e = tid; e < ROWS * TC; e += kThreads) sS[e] = exp2f(sS[e] - s_lse[e / TC]);
+    for (int e = tid; e < ROWS * TC; e += kThreads) sS[e] = fast_exp2(sS[e] - s_lse[e / TC]);
     __syncthreads();
     if (tid < nt) {
       float acc = 0.f;
@@ -800,11 +1071,16 @@ VKernel pick_kernel(int dt, int D, int RT, bool resident) {
   return nullptr;
 }
 
-int lds_bytes(int dt, int D, int RT, bool resident) {
+int lds_bytes(int dt, int D, int RT, bool resident, int splits) {
   if (dt == PVLM_F32) return (RT * 16 * D + kF32Tile * D + RT * 16 * kF32Tile) * 4;
-  const int ored = 2 * RT * 16 * D * 4;              // O partial reduction
-  const int vres = resident ? kResTokens * D * 2 : 0;  // the chunk's V (bf16)
-  return ored > vres ? ored : vres;
+  int b = 2 * RT * 16 * D * 4;                                   // O partial reduction
+  if (resident) {
+    b = b > kResTokens * D * 2 ? b : kResTokens * D * 2;         // the chunk's V (bf16)
+    // rescale factors, then the O-sum partials (at most 256 float4)
+    const int f = (splits * RT * 16 + 3) / 4 * 16 + kThreads * 16;
+    b = b > f ? b : f;
+  }
+  return b;
 }
 
 pvlm_status plan_verify(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int64_t n_cap,
@@ -839,7 +1115,7 @@ pvlm_status plan_verify(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int
   p->splits = (int)((p->n_plan + chunk - 1) / chunk);
   p->resident = p->mfma && chunk <= kResTokens;
   p->grid = (p->per_launch * p->splits + 7) / 8 * 8;
-  p->lds_dyn = lds_bytes(dt, D, p->RT, p->resident);
+  p->lds_dyn = lds_bytes(dt, D, p->RT, p->resident, p->splits);
   const int ROWS = p->RT * 16;
   const size_t n_sync = 3 * (size_t)p->groups + (size_t)B * p->splits;
   if (n_sync > (size_t)kSyncInts) return PVLM_ERR_UNSUPPORTED;
