@@ -12,8 +12,8 @@ HIP graph replay (falls back to eager launches if capture fails).
 
 Prints ONE JSON line.  `value` is microseconds per decoder layer (step time /
 80); `achieved_hbm_tbs` is algorithmic bytes / step time.  `roofline` covers the
-dominant kernel (verify attention) timed with HIP events around each launch on
-the launching stream.  `cpu_baseline` times the float64 oracle on the host for
+dominant kernel (verify attention): its mean launch duration comes from HIP
+events around replays of a graph of 80 verify launches on the replaying stream.  `cpu_baseline` times the float64 oracle on the host for
 a bounded sample of the same step.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--mode stacked|layer]
@@ -36,7 +36,9 @@ sys.path.insert(0, ROOT)
 METRIC = "verify+prune step us/layer & achieved HBM TB/s, LLaVA-OV-72B layer shape"
 HBM_PEAK_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
-VERIFY_SRC = os.path.join(ROOT, "paper_2603_19610_amd", "csrc", "verify_attn.hip")
+VERIFY_SRCS = [os.path.join(ROOT, "paper_2603_19610_amd", "csrc", f)
+               for f in ("verify_attn.hip", "common.h")]
+COPY_BYTES = 512 << 20
 
 
 def log(msg):
@@ -52,10 +54,12 @@ def parse():
     ap.add_argument("--mode", choices=["stacked", "layer"], default="stacked")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--kernel-reps", type=int, default=40,
-                    help="verify launches timed one by one for the roofline")
+    ap.add_argument("--kernel-reps", type=int, default=80,
+                    help="verify launches per graph replay timed for the roofline")
     ap.add_argument("--verify-only", type=int, default=0,
                     help="profiling helper: run N verify launches and exit")
+    ap.add_argument("--copy-only", type=int, default=0,
+                    help="profiling helper: N device copies of 512 MiB (counter calibration)")
     return ap.parse_args()
 
 
@@ -97,12 +101,14 @@ def measured_traffic():
     if not os.path.exists(path):
         return None
     text = open(path).read()
-    h = re.search(r"verify_attn\.hip sha256: ([0-9a-f]{64})", text)
+    h = re.search(r"kernel source sha256 \(verify_attn\.hip \+ common\.h\): ([0-9a-f]{64})", text)
     t = re.search(r"traffic_bytes_per_launch: ([0-9.eE+]+)", text)
     if not h or not t:
         return None
-    cur = hashlib.sha256(open(VERIFY_SRC, "rb").read()).hexdigest()
-    return float(t.group(1)) if cur == h.group(1) else None
+    cur = hashlib.sha256()
+    for f in VERIFY_SRCS:
+        cur.update(open(f, "rb").read())
+    return float(t.group(1)) if cur.hexdigest() == h.group(1) else None
 
 
 # ------------------------------------------------------------ CPU baseline --
@@ -171,6 +177,15 @@ def main():
 
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
+    if args.copy_only:  # a plain copy of known size: 512 MiB read + 512 MiB written
+        src = torch.ones(COPY_BYTES // 2, dtype=torch.bfloat16, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(args.copy_only):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_only": args.copy_only, "bytes_read": COPY_BYTES,
+                          "bytes_written": COPY_BYTES}))
+        return
     w = W.WORKLOADS[args.workload]
     stacked = args.mode == "stacked"
     NL = w.n_layers if stacked else 1
@@ -296,24 +311,47 @@ def main():
     if st:
         log(f"device status {st} during the timed steps")
 
-    # ---- dominant kernel: verify attention, one launch at a time
-    blocker = torch.randn((4096, 4096), device=dev, dtype=torch.bfloat16)
+    # ---- dominant kernel: verify attention.  `reps` launches (cycling over
+    # the layers) captured in one graph; events on the replaying stream around
+    # whole replays give the mean launch duration, inter-kernel gaps included.
     reps = args.kernel_reps
+    vb = verify_bytes(w)
+    k_mean = None
+    if graph_used:
+        gv = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gv):
+            for r in range(reps):
+                verify((7 * r + 3) % NL, mass_x)
+        gv.replay()
+        torch.cuda.synchronize()
+        n_rep = 5
+        a_ev = torch.cuda.Event(enable_timing=True)
+        b_ev = torch.cuda.Event(enable_timing=True)
+        a_ev.record()
+        for _ in range(n_rep):
+            gv.replay()
+        b_ev.record()
+        torch.cuda.synchronize()
+        k_mean = a_ev.elapsed_time(b_ev) * 1e3 / (n_rep * reps)
+    # one eager (cooperative) launch at a time behind a busy stream: the
+    # per-launch cost a caller outside a graph sees
+    blocker = torch.randn((4096, 4096), device=dev, dtype=torch.bfloat16)
+    n_eager = 40
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(reps)]
+           for _ in range(n_eager)]
     torch.cuda.synchronize()
     for _ in range(48):         # keep the GPU busy while the launches are enqueued
         blocker = blocker @ blocker
         blocker = blocker / blocker.abs().max()
-    for r in range(reps):
+    for r in range(n_eager):
         a, b = evs[r]
         a.record()
         verify((7 * r + 3) % NL, mass_x)
         b.record()
     torch.cuda.synchronize()
-    kus = [a.elapsed_time(b) * 1e3 for a, b in evs]
-    k_mean = float(np.mean(kus[2:]))
-    vb = verify_bytes(w)
+    eager_us = float(np.mean([a.elapsed_time(b) * 1e3 for a, b in evs][2:]))
+    if k_mean is None:
+        k_mean = eager_us
     achieved = vb / (k_mean * 1e-6) / 1e9
 
     step_bytes = NL * (verify_bytes(w) + gather_bytes(w)) + uvprune_bytes(w) + topk_bytes(w) \
@@ -364,6 +402,9 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
             "bytes_per_launch": vb, "launch_us": round(k_mean, 3),
+            "launch_timing": ("graph of %d launches, events around replays" % reps
+                              if graph_used else "eager launches, events around each"),
+            "eager_launch_us": round(eager_us, 3),
         },
         "cpu_baseline": cpu,
         "device_status": st,

@@ -151,6 +151,20 @@ __device__ __forceinline__ bool wg_signal_last(int* counter, int target, int* s_
   return last;
 }
 
+// Workgroup barrier that orders LDS only: global loads and stores stay in
+// flight across it (a full __syncthreads waits for every outstanding memory
+// operation of the wave first).
+__device__ __forceinline__ void lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+__device__ __forceinline__ uint64_t pack_bf16x4(float x, float y, float z, float w) {
+  return (uint64_t)f32_to_bf16(x) | ((uint64_t)f32_to_bf16(y) << 16) | ((uint64_t)f32_to_bf16(z) << 32) |
+         ((uint64_t)f32_to_bf16(w) << 48);
+}
+
 __device__ __forceinline__ void reset_counter(int* counter) {
   __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }

@@ -578,65 +578,54 @@ __device__ __forceinline__ void pv_block(const float (&S)[2][RT][4], const float
   }
 }
 
-// Sum the four waves' O fragments through LDS and write the chunk partial
-// (row-major [ROWS][D]) to the workspace.  Fragments move as float4 (one
-// 16-byte LDS access per MFMA tile per lane) in batches of 8 so the LDS
-// latency overlaps.
+// Sum the four waves' O fragments and write the chunk partial (row-major
+// [ROWS][D], bf16) to the workspace.  Reduce-scatter through LDS: the MFMA
+// tiles of O form units of four tiles (one 16-row tile, four consecutive d per
+// lane); unit k belongs to wave k % 4.  Every wave parks the units it does not
+// own, one barrier, then each owner adds the three parked copies to its own
+// and stores the sum (8 bytes per lane and row) straight from registers.
 template <int D, int RT>
 __device__ __forceinline__ void write_opart(const VArgs& a, const Unit& u, floatx4 (&O)[RT][D / 16],
                                             float* s_o, int lane, int w, int n, int gq) {
   constexpr int DPL = D / 16;
-  constexpr int NF = RT * DPL;  // fragments (MFMA tiles) per lane
-  constexpr int F = RT * 16 * D;
-  floatx4* buf0 = reinterpret_cast<floatx4*>(s_o);
-  floatx4* buf1 = reinterpret_cast<floatx4*>(s_o + F);
-  auto frag = [&](int f) -> floatx4& { return O[f / DPL][f % DPL]; };
-  auto store = [&](floatx4* buf) {
+  constexpr int FU = 4;          // tiles per unit
+  constexpr int HU = DPL / FU;   // units per 16-row tile
+  constexpr int U = RT * HU;
+  static_assert(DPL % FU == 0, "head dim must be a multiple of 64");
+  floatx4* buf = reinterpret_cast<floatx4*>(s_o);
+  const int wu = __builtin_amdgcn_readfirstlane(w);
 #pragma unroll
-    for (int f = 0; f < NF; ++f) buf[f * 64 + lane] = frag(f);
-  };
-  auto add = [&](const floatx4* buf) {
+  for (int k = 0; k < U; ++k) {
+    const int own = k % kWaves;
+    if (own != wu) {
+      const int s = (wu - own + kWaves) % kWaves - 1;  // 0..2
+      floatx4* dst = buf + (k * 3 + s) * FU * 64 + lane;
 #pragma unroll
-    for (int f0 = 0; f0 < NF; f0 += 8) {
-      floatx4 t[8];
-#pragma unroll
-      for (int k = 0; k < 8; ++k)
-        if (f0 + k < NF) t[k] = buf[(f0 + k) * 64 + lane];
-#pragma unroll
-      for (int k = 0; k < 8; ++k)
-        if (f0 + k < NF) frag(f0 + k) += t[k];
+      for (int j = 0; j < FU; ++j) dst[j * 64] = O[k / HU][(k % HU) * FU + j];
     }
-  };
-  if (w >= 2) store(w == 2 ? buf0 : buf1);
-  __syncthreads();
-  if (w < 2) add(w == 0 ? buf0 : buf1);
-  __syncthreads();
-  if (w == 1) store(buf0);
-  __syncthreads();
-  float* rowmaj = s_o + F;
-  if (w == 0) {
-    add(buf0);
-    // row-major copy of the sum (each lane writes DPL consecutive d)
+  }
+  lds_sync();
+  uint64_t* op = reinterpret_cast<uint64_t*>(a.opart) + ((size_t)u.grp * a.splits + u.split) * RT * 16 * D / 4;
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
+  for (int k = 0; k < U; ++k) {
+    if (k % kWaves == wu) {
+      const int rt = k / HU, h = k % HU;
+      floatx4 t[3][FU];
+#pragma unroll
+      for (int s = 0; s < 3; ++s)
+#pragma unroll
+        for (int j = 0; j < FU; ++j) t[s][j] = buf[(k * 3 + s) * FU * 64 + j * 64 + lane];
+      floatx4 acc[FU];
+#pragma unroll
+      for (int j = 0; j < FU; ++j) acc[j] = O[rt][h * FU + j] + t[0][j] + t[1][j] + t[2][j];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        float* dst = rowmaj + (rt * 16 + 4 * gq + i) * D + DPL * n;
-#pragma unroll
-        for (int jd = 0; jd < DPL; jd += 4)
-          *reinterpret_cast<float4*>(dst + jd) =
-              make_float4(O[rt][jd][i], O[rt][jd + 1][i], O[rt][jd + 2][i], O[rt][jd + 3][i]);
+        const int row = rt * 16 + 4 * gq + i;
+        __hip_atomic_store(op + (row * D + DPL * n + FU * h) / 4,
+                           pack_bf16x4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
       }
-  }
-  __syncthreads();
-  const float* buf1f = rowmaj;
-  // chunk partial in bf16, four values per 64-bit device-coherent store
-  uint64_t* op = reinterpret_cast<uint64_t*>(a.opart) + ((size_t)u.grp * a.splits + u.split) * F / 4;
-  for (int e = threadIdx.x; e < F / 4; e += kThreads) {
-    const float4 v = reinterpret_cast<const float4*>(buf1f)[e];
-    const uint64_t pk = (uint64_t)f32_to_bf16(v.x) | ((uint64_t)f32_to_bf16(v.y) << 16) |
-                        ((uint64_t)f32_to_bf16(v.z) << 32) | ((uint64_t)f32_to_bf16(v.w) << 48);
-    __hip_atomic_store(op + e, pk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
 }
 
@@ -660,50 +649,112 @@ __device__ void verify_epilogue_local(const VArgs& a, const Unit& u, const float
   if (!empty) {
     const float* st0 = a.stats + (size_t)u.grp * a.splits * ROWS * 2;
     const int nsp = (u.N + a.chunk - 1) / a.chunk;
-    // 1. every (chunk, row) statistic is read once; partial combines per part
-    if (tid < P * ROWS) {
-      const int r = tid % ROWS, part = tid / ROWS;
-      float M = kNegInf, Z = 0.f;
-      for (int s0 = part; s0 < nsp; s0 += P * kU) {
+    // This workgroup's slice of O is the factor-weighted sum over chunks of
+    // the partials.  With few elements per workgroup the chunks are split
+    // over Q thread sets whose sums meet in LDS.
+    const int row0 = u.rg * a.RT * 16;
+    const int rows = min(ROWS, a.R - row0);
+    const int E4 = rows * D / 4;
+    const int per = (E4 + nsp - 1) / nsp;
+    const int e0 = min(E4, u.split * per), e1 = min(E4, e0 + per);
+    const int cnt = e1 - e0;
+    const int Q = cnt <= 0 ? 1 : min(kOSets, max(1, kThreads / cnt));
+    const int q = cnt <= 0 ? 0 : tid / cnt, el = cnt <= 0 ? 0 : tid % cnt;
+    const bool act = cnt > 0 && q < Q;  // first element e0 + el (Q = 1: el = tid)
+    const uint64_t* op = reinterpret_cast<const uint64_t*>(a.opart) + (size_t)u.grp * a.splits * ROWS * D / 4;
+    auto load_parts = [&](int e, int s0, int Qs, uint64_t (&v)[kU]) {
+      // unconditional (clamped) loads keep the wait counts fine-grained
+#pragma unroll
+      for (int j = 0; j < kU; ++j) {
+        const int sp = min(s0 + j * Qs, nsp - 1);
+        v[j] = __hip_atomic_load(op + (size_t)sp * ROWS * D / 4 + e, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+      }
+    };
+    auto fma_parts = [&](int e, int s0, int Qs, const uint64_t (&v)[kU], float (&acc)[4]) {
+      const int r = (4 * e) / D;
+#pragma unroll
+      for (int j = 0; j < kU; ++j) {
+        const int sp = s0 + j * Qs;
+        const float f = sp < nsp ? s_fac[sp * ROWS + r] : 0.f;
+#pragma unroll
+        for (int h = 0; h < 4; ++h) acc[h] += f * bf16_to_f32((uint16_t)(v[j] >> (16 * h)));
+      }
+    };
+    auto emit = [&](int e, const float (&acc)[4]) {
+      const int r = (4 * e) / D;
+      const int row = row0 + r, d = (4 * e) % D;
+      const int t = row / a.G, h = u.g * a.G + row % a.G;
+      const size_t oi = (((size_t)u.b * a.T + t) * a.Hq + h) * D + d;
+      *reinterpret_cast<uint64_t*>(static_cast<uint16_t*>(a.out) + oi) =
+          pack_bf16x4(acc[0], acc[1], acc[2], acc[3]);
+    };
+    // 1. statistics of every (chunk, row) pair, read once: first round trip,
+    //    with the first batch of O partials issued right behind it
+    const int r_st = tid % ROWS, part = tid / ROWS;
+    const bool st_thr = tid < P * ROWS;
+    float2 sv[kU];
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      const int sp = min(part + j * P, nsp - 1);
+      sv[j] = ld_agent(reinterpret_cast<const float2*>(st0 + ((size_t)sp * ROWS + r_st) * 2));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    const int e_first = act ? e0 + el : 0;
+    uint64_t pre[kU];
+    load_parts(e_first, q, Q, pre);
+    __builtin_amdgcn_sched_barrier(0);
+    float M = kNegInf, Z = 0.f;
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      const int sp = part + j * P;
+      if (st_thr && sp < nsp) {
+        s_fac[sp * ROWS + r_st] = sv[j].x;
+        lse_combine(M, Z, sv[j].x, sv[j].y);
+      }
+    }
+    if (st_thr) {
+      for (int s0 = part + P * kU; s0 < nsp; s0 += P * kU) {  // more than P * kU chunks
         float2 v[kU];
 #pragma unroll
         for (int j = 0; j < kU; ++j) {
-          const int sp = s0 + j * P;
-          v[j] = sp < nsp ? ld_agent(reinterpret_cast<const float2*>(st0 + ((size_t)sp * ROWS + r) * 2))
-                          : make_float2(kNegInf, 0.f);
+          const int sp = min(s0 + j * P, nsp - 1);
+          v[j] = ld_agent(reinterpret_cast<const float2*>(st0 + ((size_t)sp * ROWS + r_st) * 2));
         }
 #pragma unroll
         for (int j = 0; j < kU; ++j) {
           const int sp = s0 + j * P;
-          if (sp < nsp) s_fac[sp * ROWS + r] = v[j].x;
-          lse_combine(M, Z, v[j].x, v[j].y);
+          if (sp < nsp) {
+            s_fac[sp * ROWS + r_st] = v[j].x;
+            lse_combine(M, Z, v[j].x, v[j].y);
+          }
         }
       }
-      s_pm[part][r] = M;
-      s_pz[part][r] = Z;
+      s_pm[part][r_st] = M;
+      s_pz[part][r_st] = Z;
     }
-    __syncthreads();
+    lds_sync();
     // 2. per row: global max, sum and lse; (M, 1/Z) kept in part slot 0
     if (tid < ROWS) {
       const int r = tid;
-      float M = s_pm[0][r], Z = s_pz[0][r];
+      float Mr = s_pm[0][r], Zr = s_pz[0][r];
 #pragma unroll
-      for (int p = 1; p < P; ++p) lse_combine(M, Z, s_pm[p][r], s_pz[p][r]);
-      const int row = u.rg * a.RT * 16 + r;
-      const bool ok = row < a.R && Z > 0.f;
-      s_lse[r] = ok ? M + __log2f(Z) : __builtin_huge_valf();
-      s_pm[0][r] = M;
-      s_pz[0][r] = ok ? 1.f / Z : 0.f;
+      for (int p = 1; p < P; ++p) lse_combine(Mr, Zr, s_pm[p][r], s_pz[p][r]);
+      const int row = row0 + r;
+      const bool ok = row < a.R && Zr > 0.f;
+      s_lse[r] = ok ? Mr + __log2f(Zr) : __builtin_huge_valf();
+      s_pm[0][r] = Mr;
+      s_pz[0][r] = ok ? 1.f / Zr : 0.f;
     }
-    __syncthreads();
+    lds_sync();
     // 3. rescale factor of every chunk partial: exp2(m_chunk - M) / Z
     for (int e = tid; e < nsp * ROWS; e += kThreads) {
       const int r = e % ROWS;
       const float m = s_fac[e], invZ = s_pz[0][r];
       s_fac[e] = invZ != 0.f && m != kNegInf ? fast_exp2(m - s_pm[0][r]) * invZ : 0.f;
     }
-    __syncthreads();
-    // exact per-token mass of this chunk's tokens
+    lds_sync();
+    // 4. exact per-token mass of this chunk's tokens (resident scores)
     float lse[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) lse[rt] = s_lse[rt * 16 + n];
@@ -715,62 +766,35 @@ __device__ void verify_epilogue_local(const VArgs& a, const Unit& u, const float
         if (tb < u.c1) mass_block<RT>(S[j], lse, mp, tb, u.c1, n, gq);
       }
     }
-    // this workgroup's slice of O: sum over chunks of factor * partial.  With
-    // few elements per workgroup the chunks are split over Q thread sets and
-    // the Q partial sums meet in LDS.
-    const int row0 = u.rg * a.RT * 16;
-    const int rows = min(ROWS, a.R - row0);
-    const int E4 = rows * D / 4;
-    const int per = (E4 + nsp - 1) / nsp;
-    const int e0 = min(E4, u.split * per), e1 = min(E4, e0 + per);
-    const int cnt = e1 - e0;
-    const uint64_t* op = reinterpret_cast<const uint64_t*>(a.opart) + (size_t)u.grp * a.splits * ROWS * D / 4;
-    auto accumulate = [&](int e, int q, int Q, float (&acc)[4]) {
-      const int r = (4 * e) / D;
-      for (int s0 = q; s0 < nsp; s0 += Q * kU) {
+    // 5. O slice
+    if (act) {
+      float acc[4] = {0.f, 0.f, 0.f, 0.f};
+      fma_parts(e_first, q, Q, pre, acc);
+      for (int s0 = q + Q * kU; s0 < nsp; s0 += Q * kU) {
         uint64_t v[kU];
-#pragma unroll
-        for (int j = 0; j < kU; ++j) {
-          const int sp = s0 + j * Q;
-          v[j] = sp < nsp ? __hip_atomic_load(op + (size_t)sp * ROWS * D / 4 + e, __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT)
-                          : 0ull;
-        }
-#pragma unroll
-        for (int j = 0; j < kU; ++j) {
-          const int sp = s0 + j * Q;
-          const float f = sp < nsp ? s_fac[sp * ROWS + r] : 0.f;
-#pragma unroll
-          for (int h = 0; h < 4; ++h) acc[h] += f * bf16_to_f32((uint16_t)(v[j] >> (16 * h)));
-        }
+        load_parts(e_first, s0, Q, v);
+        fma_parts(e_first, s0, Q, v, acc);
       }
-    };
-    auto emit = [&](int e, const float (&acc)[4]) {
-      const int r = (4 * e) / D;
-      const int row = row0 + r, d = (4 * e) % D;
-      const int t = row / a.G, h = u.g * a.G + row % a.G;
-      const size_t oi = (((size_t)u.b * a.T + t) * a.Hq + h) * D + d;
-      const uint64_t pk = (uint64_t)f32_to_bf16(acc[0]) | ((uint64_t)f32_to_bf16(acc[1]) << 16) |
-                          ((uint64_t)f32_to_bf16(acc[2]) << 32) | ((uint64_t)f32_to_bf16(acc[3]) << 48);
-      *reinterpret_cast<uint64_t*>(static_cast<uint16_t*>(a.out) + oi) = pk;
-    };
-    const int Q = cnt <= 0 ? 1 : min(kOSets, max(1, kThreads / cnt));
+      if (Q == 1)
+        emit(e_first, acc);
+      else
+        reinterpret_cast<float4*>(s_fac + ((nsp * ROWS + 3) & ~3))[q * cnt + el] =
+            make_float4(acc[0], acc[1], acc[2], acc[3]);
+    }
     if (Q == 1) {
-      for (int e = e0 + tid; e < e1; e += kThreads) {
+      for (int e = e0 + tid + kThreads; e < e1; e += kThreads) {
         float acc[4] = {0.f, 0.f, 0.f, 0.f};
-        accumulate(e, 0, 1, acc);
+        for (int s0 = 0; s0 < nsp; s0 += kU) {
+          uint64_t v[kU];
+          load_parts(e, s0, 1, v);
+          fma_parts(e, s0, 1, v, acc);
+        }
         emit(e, acc);
       }
     } else {
-      float4* s_acc = reinterpret_cast<float4*>(s_fac + ((nsp * ROWS + 3) & ~3));
-      const int q = tid / cnt, el = tid % cnt;
-      if (q < Q) {
-        float acc[4] = {0.f, 0.f, 0.f, 0.f};
-        accumulate(e0 + el, q, Q, acc);
-        s_acc[q * cnt + el] = make_float4(acc[0], acc[1], acc[2], acc[3]);
-      }
-      __syncthreads();
+      lds_sync();
       if (tid < cnt) {
+        const float4* s_acc = reinterpret_cast<const float4*>(s_fac + ((nsp * ROWS + 3) & ~3));
         float acc[4] = {0.f, 0.f, 0.f, 0.f};
         for (int qq = 0; qq < Q; ++qq) {
           const float4 v = s_acc[qq * cnt + tid];
@@ -1073,7 +1097,7 @@ VKernel pick_kernel(int dt, int D, int RT, bool resident) {
 
 int lds_bytes(int dt, int D, int RT, bool resident, int splits) {
   if (dt == PVLM_F32) return (RT * 16 * D + kF32Tile * D + RT * 16 * kF32Tile) * 4;
-  int b = 2 * RT * 16 * D * 4;                                   // O partial reduction
+  int b = 3 * RT * 16 * D * 4;                                   // O partial reduce-scatter
   if (resident) {
     b = b > kResTokens * D * 2 ? b : kResTokens * D * 2;         // the chunk's V (bf16)
     // rescale factors, then the O-sum partials (at most 256 float4)
