@@ -13,8 +13,12 @@ HIP graph replay (falls back to eager launches if capture fails).
 Prints ONE JSON line.  `value` is microseconds per decoder layer (step time /
 80); `achieved_hbm_tbs` is algorithmic bytes / step time.  `roofline` covers the
 dominant kernel (verify attention): its mean launch duration comes from HIP
-events around replays of a graph of 80 verify launches on the replaying stream.  `cpu_baseline` times the float64 oracle on the host for
-a bounded sample of the same step.
+events around replays of a graph of 80 verify launches on the replaying stream.
+`stages_us` times each stage the same way; `copy_gbs` is the device-to-device
+copy bandwidth measured in the same run; `other_configs` times the single-layer
+step of the other model shapes; `cossim` times the similarity criterion.
+`cpu_baseline` times the float64 oracle on the host for a bounded sample of the
+same step.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--mode stacked|layer]
 """
@@ -39,6 +43,7 @@ PROFILES = os.path.join(ROOT, "profiles")
 VERIFY_SRCS = [os.path.join(ROOT, "paper_2603_19610_amd", "csrc", f)
                for f in ("verify_attn.hip", "common.h")]
 COPY_BYTES = 512 << 20
+OTHER_CONFIGS = ("llava7b", "llava72b", "qwen32b", "long")
 
 
 def log(msg):
@@ -54,6 +59,8 @@ def parse():
     ap.add_argument("--mode", choices=["stacked", "layer"], default="stacked")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the other model shapes and the similarity criterion")
     ap.add_argument("--kernel-reps", type=int, default=80,
                     help="verify launches per graph replay timed for the roofline")
     ap.add_argument("--verify-only", type=int, default=0,
@@ -93,22 +100,37 @@ def accept_bytes(w):
     return 4 * w.batch * (2 * w.gamma + 1) * w.vocab
 
 
+def cossim_bytes(w, esize=2):
+    """Hidden states of layers 0 and L (the layer sum telescopes), score out."""
+    m = int(w.m_per_seq().sum())
+    return 2 * (m + w.batch * w.n_text) * w.hidden * esize + 4 * m
+
+
 # ---------------------------------------------------------------- traffic --
 def measured_traffic():
     """HBM bytes per verify launch from the committed rocprofv3 counter runs,
-    or None when the kernel source changed since they were taken."""
+    or None when the kernel code changed since they were taken."""
     path = os.path.join(PROFILES, "verify_attn_llava72b_traffic.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
-    h = re.search(r"kernel source sha256 \(verify_attn\.hip \+ common\.h\): ([0-9a-f]{64})", text)
+    h = re.search(r"kernel code sha256: ([0-9a-f]{64})", text)
     t = re.search(r"traffic_bytes_per_launch: ([0-9.eE+]+)", text)
     if not h or not t:
         return None
+    return float(t.group(1)) if kernel_code_digest() == h.group(1) else None
+
+
+def kernel_code_digest():
+    """sha256 of verify_attn.hip + common.h with comments and blank lines
+    stripped: changes whenever the verify kernel's code does."""
     cur = hashlib.sha256()
     for f in VERIFY_SRCS:
-        cur.update(open(f, "rb").read())
-    return float(t.group(1)) if cur.hexdigest() == h.group(1) else None
+        for line in open(f):
+            code = re.sub(r"//.*", "", line).rstrip()
+            if code:
+                cur.update(code.encode() + b"\n")
+    return cur.hexdigest()
 
 
 # ------------------------------------------------------------ CPU baseline --
@@ -151,6 +173,14 @@ def cpu_baseline(w, layers_host, crit_layers, per_layer_ok):
     once = t_uv + t_topk + t_acc
     L = per_layer_ok
     us_per_layer = (per_layer + once / L) * 1e6
+    cpu_model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {
         "value": round(us_per_layer, 1), "unit": "us/layer", "cores": int(threads),
         "kind": "oracle",
@@ -158,8 +188,233 @@ def cpu_baseline(w, layers_host, crit_layers, per_layer_ok):
                    f"(mean {np.mean(t_verify):.2f} s/layer), gather of one layer "
                    f"({t_gather:.3f} s), UV-Prune over {crit_layers + 1} masses ({t_uv:.3f} s), "
                    f"top-k ({t_topk:.3f} s) and accept ({t_acc:.3f} s); per layer = verify + "
-                   f"gather + (UV-Prune + top-k + accept) / {L}; host cores available {cores}"),
+                   f"gather + (UV-Prune + top-k + accept) / {L}; host cores available {cores}; "
+                   f"cpu {cpu_model}"),
     }
+
+
+# ------------------------------------------------------------- the step --
+class Step:
+    """Inputs resident in HBM and the step's launches for one workload.
+
+    Stacked: n_layers independent seeded layers (verify per layer; UV-Prune
+    and top-k after layer L over the masses of layers 0..L; gather of every
+    layer; accept).  Single layer: layer 0 (no salient boost) is the shallow
+    reference whose mass exists before the step; the step verifies layer 1,
+    scores, selects, gathers and accepts."""
+
+    def __init__(self, torch, pv, W, w, stacked, dev):
+        self.torch, self.pv, self.w, self.stacked = torch, pv, w, stacked
+        NL = w.n_layers if stacked else 1
+        L = w.crit_layers if stacked else 1
+        self.NL, self.L = NL, L
+        B, T, Hq, Hkv, D = w.batch, w.T, w.hq, w.hkv, w.head_dim
+        n_cap = w.n_cap()
+        lens = w.lengths()
+        m_np = w.m_per_seq().astype(np.int32)
+        K_np = w.keep_count(m_np).astype(np.int32)
+        k_cap = max(1, int(K_np.max()))
+        dst_cap = k_cap + w.n_text
+        self.m_np, self.lens = m_np, lens
+        tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        self.Kc = torch.zeros((NL, B, Hkv, n_cap, D), dtype=tdt, device=dev)
+        self.Vc = torch.zeros_like(self.Kc)
+        self.Q = torch.zeros((NL, B, T, Hq, D), dtype=tdt, device=dev)
+        for l in range(NL):
+            layer_id = l if stacked else 1
+            boost = W.crit_boost(w, layer_id) if stacked else 3.0
+            W.make_verify_layer_torch(w, layer_id, boost, dev,
+                                      k_out=self.Kc[l], v_out=self.Vc[l], q_out=self.Q[l])
+        q0 = k0 = v0 = None
+        if not stacked:
+            q0, k0, v0 = W.make_verify_layer_torch(w, 1, 0.0, dev)
+        self.ctx = torch.from_numpy(lens.astype(np.int32)).to(dev)
+        self.m_t = torch.from_numpy(m_np).to(dev)
+        self.k_t = torch.from_numpy(K_np).to(dev)
+        self.tail_b = self.m_t.clone()
+        self.tail_l = torch.full((B,), w.n_text, dtype=torch.int32, device=dev)
+        acc = W.make_accept_inputs(w)
+        self.temperature = acc.temperature
+        self.dl = torch.from_numpy(acc.draft_logits).to(dev)
+        self.tl = torch.from_numpy(acc.target_logits).to(dev)
+        self.tok = torch.from_numpy(acc.draft_tokens).to(dev)
+        self.ua = torch.from_numpy(acc.u_accept).to(dev)
+        self.us = torch.from_numpy(acc.u_sample).to(dev)
+        self.out = torch.empty((B, T, Hq, D), dtype=tdt, device=dev)
+        self.lse = torch.empty((B, Hq, T), dtype=torch.float32, device=dev)
+        self.crit = torch.zeros((L + 1, B, n_cap), dtype=torch.float32, device=dev)
+        self.mass_x = torch.empty((B, n_cap), dtype=torch.float32, device=dev)
+        self.score = torch.empty((B, n_cap), dtype=torch.float32, device=dev)
+        self.k_cap, self.dst_cap = k_cap, dst_cap
+        self.idx = torch.empty((B, k_cap), dtype=torch.int32, device=dev)
+        self.kd = torch.zeros((NL, B, Hkv, dst_cap, D), dtype=tdt, device=dev)
+        self.vd = torch.zeros_like(self.kd)
+        self.na = torch.empty(B, dtype=torch.int32, device=dev)
+        self.nt = torch.empty(B, dtype=torch.int32, device=dev)
+        self.tie = torch.empty(B, dtype=torch.int32, device=dev)
+        self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.ws_v = pv.Workspace(dev)
+        self.ws_a = pv.Workspace(dev)
+        self.max_ctx = int(lens.max())
+        if not stacked:  # the shallow reference layer's mass exists before the step
+            pv.verify_attn(q0, k0, v0, self.ctx, max_ctx=self.max_ctx, out=self.out,
+                           mass=self.crit[0], lse=self.lse, ws=self.ws_v, status=self.status)
+        torch.cuda.synchronize()
+
+    def verify(self, l, mass=None):
+        self.pv.verify_attn(self.Q[l], self.Kc[l], self.Vc[l], self.ctx, max_ctx=self.max_ctx,
+                            out=self.out, mass=self.mass_x if mass is None else mass,
+                            lse=self.lse, ws=self.ws_v, status=self.status)
+
+    def prune(self):
+        self.pv.uvprune_score_mass(self.crit, self.m_t, score=self.score, status=self.status)
+        self.pv.topk_select(self.score, self.m_t, self.k_t, self.k_cap, idx=self.idx,
+                            status=self.status)
+
+    def gather(self):
+        self.pv.gather_kv(self.Kc, self.Vc, self.idx, self.k_t, self.tail_b, self.tail_l,
+                          self.dst_cap, k_dst=self.kd, v_dst=self.vd, status=self.status)
+
+    def accept(self):
+        self.pv.spec_accept(self.dl, self.tl, self.tok, self.ua, self.us, self.temperature,
+                            n_accepted=self.na, next_token=self.nt, near_tie=self.tie,
+                            ws=self.ws_a, status=self.status)
+
+    def step(self):
+        for l in range(self.NL):
+            if self.stacked:
+                self.verify(l, self.crit[l] if l <= self.L else self.mass_x)
+            else:
+                self.verify(0, self.crit[1])
+            if l == (self.L if self.stacked else 0):
+                self.prune()
+        self.gather()
+        self.accept()
+
+    def bytes(self):
+        w = self.w
+        return self.NL * (verify_bytes(w) + gather_bytes(w)) + uvprune_bytes(w) \
+            + topk_bytes(w) + accept_bytes(w)
+
+
+def capture(torch, fn):
+    """A HIP graph of fn() (after one eager warm-up run on a side stream)."""
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        fn()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    torch.cuda.synchronize()
+    return g
+
+
+def time_replays(torch, run, n):
+    """Mean ms per call of run() over n calls, HIP events on the current stream."""
+    run()
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(n):
+        run()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / n
+
+
+def copy_bandwidth(torch, dev, nbytes, reps):
+    """Device-to-device copy GB/s (bytes read + written) for copies moving
+    nbytes each.  The copies cycle over enough distinct buffers (>= 2 GiB in
+    all) that no source is still in the 256 MB Infinity Cache when it is read
+    again, as the verify launches cycle over the layers' caches."""
+    n = max(1, -(-(2 << 30) // nbytes))
+    bufs = [(torch.ones(nbytes // 4, dtype=torch.bfloat16, device=dev),
+             torch.empty(nbytes // 4, dtype=torch.bfloat16, device=dev)) for _ in range(n)]
+
+    def run():
+        for s, d in bufs:
+            d.copy_(s)
+
+    g = capture(torch, run)
+    ms = time_replays(torch, g.replay, reps) / n
+    del bufs, g
+    torch.cuda.empty_cache()
+    return nbytes / (ms * 1e-3) / 1e9
+
+
+def stage_times(torch, st, reps):
+    """Graph-timed mean us of each stage of the step (`reps` verify launches,
+    cycling over the layers, or 10 launches of another stage per graph)."""
+    out = {}
+    g = capture(torch, lambda: [st.verify((7 * r + 3) % st.NL) for r in range(reps)])
+    out["verify"] = time_replays(torch, g.replay, 5) * 1e3 / reps
+    for name, fn in (("uvprune+topk", st.prune), ("gather", st.gather), ("accept", st.accept)):
+        g = capture(torch, lambda: [fn() for _ in range(10)])
+        out[name] = time_replays(torch, g.replay, 5) * 1e3 / 10
+    return out
+
+
+def single_layer_record(torch, pv, W, name, dev, steps):
+    w = W.WORKLOADS[name]
+    st = Step(torch, pv, W, w, False, dev)
+    g = capture(torch, st.step)
+    ms = time_replays(torch, g.replay, steps)
+    stg = stage_times(torch, st, 20)
+    vb = verify_bytes(w)
+    rec = {
+        "us_per_step": round(ms * 1e3, 2),
+        "step_bytes": st.bytes(),
+        "step_tbs": round(st.bytes() / (ms * 1e-3) / 1e12, 3),
+        "stages_us": {k: round(v, 2) for k, v in stg.items()},
+        "verify_tbs": round(vb / (stg["verify"] * 1e-6) / 1e12, 3),
+        "verify_frac_of_peak": round(vb / (stg["verify"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+        "device_status": int(st.status.item()),
+    }
+    del st, g
+    torch.cuda.empty_cache()
+    return rec
+
+
+def cossim_record(torch, pv, W, dev):
+    """UV-Prune similarity criterion on the 72B shape: layers 0 and L of the
+    hidden states (the layer sum telescopes), bf16, hidden size 8192."""
+    w = W.WORKLOADS["llava72b"]
+    B, m, n, Dh = w.batch, int(w.m_per_seq().max()), w.n_text, w.hidden
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(260319610)
+    hv = torch.randn((2, B, m, Dh), device=dev, generator=gen).to(torch.bfloat16)
+    ht = torch.randn((2, B, n, Dh), device=dev, generator=gen).to(torch.bfloat16)
+    m_t = torch.full((B,), m, dtype=torch.int32, device=dev)
+    n_t = torch.full((B,), n, dtype=torch.int32, device=dev)
+    score = torch.empty((B, m), dtype=torch.float32, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    ws = pv.Workspace(dev)
+
+    def fn():
+        pv.uvprune_score_cossim(hv, ht, m_t, n_t, score=score, ws=ws, status=status)
+
+    g = capture(torch, fn)
+    ms = time_replays(torch, g.replay, 20)
+    nb = cossim_bytes(w)
+    rec = {"workload": "llava72b hidden states, layers 0 and 20, D_h 8192, bf16",
+           "us": round(ms * 1e3, 2), "bytes": nb,
+           "tbs": round(nb / (ms * 1e-3) / 1e12, 3),
+           "frac_of_peak": round(nb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+           "device_status": int(status.item())}
+    del hv, ht, g
+    torch.cuda.empty_cache()
+    return rec
+
+
+def tiles(w):
+    """16-row MFMA tiles per workgroup for the packed query rows of a KV head."""
+    rtt = -(-w.group * w.T // 16)
+    rg = -(-rtt // 5)
+    return -(-rtt // rg)
 
 
 def main():
@@ -186,108 +441,30 @@ def main():
         print(json.dumps({"copy_only": args.copy_only, "bytes_read": COPY_BYTES,
                           "bytes_written": COPY_BYTES}))
         return
+
     w = W.WORKLOADS[args.workload]
     stacked = args.mode == "stacked"
-    NL = w.n_layers if stacked else 1
-    L = w.crit_layers if stacked else 1
-    B, T, Hq, Hkv, D = w.batch, w.T, w.hq, w.hkv, w.head_dim
-    n_cap = w.n_cap()
-    lens = w.lengths()
-    m_np = w.m_per_seq().astype(np.int32)
-    K_np = w.keep_count(m_np).astype(np.int32)
-    k_cap = int(K_np.max())
-    dst_cap = k_cap + w.n_text
-
-    # ---- inputs resident in HBM
     t0 = time.time()
-    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
-    Kc = torch.zeros((NL, B, Hkv, n_cap, D), dtype=tdt, device=dev)
-    Vc = torch.zeros_like(Kc)
-    Q = torch.zeros((NL, B, T, Hq, D), dtype=tdt, device=dev)
-    for l in range(NL):
-        layer_id = l if stacked else 1
-        W.make_verify_layer_torch(w, layer_id, W.crit_boost(w, layer_id), dev,
-                                  k_out=Kc[l], v_out=Vc[l], q_out=Q[l])
-    q0 = k0 = v0 = None
-    if not stacked:  # layer 0 = the same draws without the salient boost
-        q0, k0, v0 = W.make_verify_layer_torch(w, 1, 0.0, dev)
-    torch.cuda.synchronize()
-    log(f"inputs: {NL} layer(s), cache {2 * Kc.numel() * Kc.element_size() / 1e9:.2f} GB, "
+    st = Step(torch, pv, W, w, stacked, dev)
+    NL = st.NL
+    log(f"inputs: {NL} layer(s), cache {2 * st.Kc.numel() * st.Kc.element_size() / 1e9:.2f} GB, "
         f"{time.time() - t0:.1f} s")
-    ctx = torch.from_numpy(lens.astype(np.int32)).to(dev)
-    m_t = torch.from_numpy(m_np).to(dev)
-    k_t = torch.from_numpy(K_np).to(dev)
-    tail_b = m_t.clone()
-    tail_l = torch.full((B,), w.n_text, dtype=torch.int32, device=dev)
-    acc = W.make_accept_inputs(w)
-    dl = torch.from_numpy(acc.draft_logits).to(dev)
-    tl = torch.from_numpy(acc.target_logits).to(dev)
-    tok = torch.from_numpy(acc.draft_tokens).to(dev)
-    ua = torch.from_numpy(acc.u_accept).to(dev)
-    us = torch.from_numpy(acc.u_sample).to(dev)
-
-    out = torch.empty((B, T, Hq, D), dtype=tdt, device=dev)
-    lse = torch.empty((B, Hq, T), dtype=torch.float32, device=dev)
-    crit = torch.zeros((L + 1, B, n_cap), dtype=torch.float32, device=dev)
-    mass_x = torch.empty((B, n_cap), dtype=torch.float32, device=dev)
-    score = torch.empty((B, n_cap), dtype=torch.float32, device=dev)
-    idx = torch.empty((B, k_cap), dtype=torch.int32, device=dev)
-    kd = torch.zeros((NL, B, Hkv, dst_cap, D), dtype=tdt, device=dev)
-    vd = torch.zeros_like(kd)
-    na = torch.empty(B, dtype=torch.int32, device=dev)
-    nt = torch.empty(B, dtype=torch.int32, device=dev)
-    tie = torch.empty(B, dtype=torch.int32, device=dev)
-    status = torch.zeros(1, dtype=torch.int32, device=dev)
-    ws_v = pv.Workspace(dev)
-    ws_a = pv.Workspace(dev)
-    max_ctx = int(lens.max())
-
-    if not stacked:  # the shallow reference layer's mass exists before the step
-        pv.verify_attn(q0, k0, v0, ctx, max_ctx=max_ctx, out=out, mass=crit[0], lse=lse, ws=ws_v,
-                       status=status)
-
-    def verify(l, mass):
-        pv.verify_attn(Q[l], Kc[l], Vc[l], ctx, max_ctx=max_ctx, out=out, mass=mass, lse=lse,
-                       ws=ws_v, status=status)
-
-    def step():
-        for l in range(NL):
-            if stacked:
-                verify(l, crit[l] if l <= L else mass_x)
-            else:
-                verify(0, crit[1])
-            if l == (L if stacked else 0):
-                pv.uvprune_score_mass(crit, m_t, score=score, status=status)
-                pv.topk_select(score, m_t, k_t, k_cap, idx=idx, status=status)
-        pv.gather_kv(Kc, Vc, idx, k_t, tail_b, tail_l, dst_cap, k_dst=kd, v_dst=vd, status=status)
-        pv.spec_accept(dl, tl, tok, ua, us, acc.temperature, n_accepted=na, next_token=nt,
-                       near_tie=tie, ws=ws_a, status=status)
 
     if args.verify_only:
         for r in range(args.verify_only):
-            verify(r % NL, mass_x)
+            st.verify(r % NL)
         torch.cuda.synchronize()
-        print(json.dumps({"verify_only": args.verify_only, "status": int(status.item())}))
+        print(json.dumps({"verify_only": args.verify_only, "status": int(st.status.item())}))
         return
 
     # eager warm-up (also sizes the workspaces before any capture)
-    step()
+    st.step()
     torch.cuda.synchronize()
-    run = step
+    run = st.step
     graph_used = False
     if not args.no_graph:
         try:
-            s = torch.cuda.Stream()
-            s.wait_stream(torch.cuda.current_stream())
-            with torch.cuda.stream(s):
-                step()
-            torch.cuda.current_stream().wait_stream(s)
-            torch.cuda.synchronize()
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g):
-                step()
-            torch.cuda.synchronize()
-            run = g.replay
+            run = capture(torch, st.step).replay
             graph_used = True
         except Exception as e:  # capture unsupported: time eager launches
             log(f"graph capture failed ({type(e).__name__}: {e}); timing eager launches")
@@ -295,7 +472,7 @@ def main():
     for _ in range(args.warmup):
         run()
     torch.cuda.synchronize()
-    status.zero_()
+    st.status.zero_()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -307,32 +484,20 @@ def main():
     torch.cuda.synchronize()
     host_s = time.perf_counter() - h0
     ms_step = e0.elapsed_time(e1) / args.steps
-    st = int(status.item())
-    if st:
-        log(f"device status {st} during the timed steps")
+    status = int(st.status.item())
+    if status:
+        log(f"device status {status} during the timed steps")
 
-    # ---- dominant kernel: verify attention.  `reps` launches (cycling over
-    # the layers) captured in one graph; events on the replaying stream around
-    # whole replays give the mean launch duration, inter-kernel gaps included.
+    # ---- per-stage times; verify is the dominant kernel: `reps` launches
+    # (cycling over the layers) in one graph, events on the replaying stream
+    # around whole replays give its mean launch duration, inter-kernel gaps
+    # included.
     reps = args.kernel_reps
     vb = verify_bytes(w)
-    k_mean = None
+    stages = None
     if graph_used:
-        gv = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(gv):
-            for r in range(reps):
-                verify((7 * r + 3) % NL, mass_x)
-        gv.replay()
-        torch.cuda.synchronize()
-        n_rep = 5
-        a_ev = torch.cuda.Event(enable_timing=True)
-        b_ev = torch.cuda.Event(enable_timing=True)
-        a_ev.record()
-        for _ in range(n_rep):
-            gv.replay()
-        b_ev.record()
-        torch.cuda.synchronize()
-        k_mean = a_ev.elapsed_time(b_ev) * 1e3 / (n_rep * reps)
+        stages = stage_times(torch, st, reps)
+        k_mean = stages["verify"]
     # one eager (cooperative) launch at a time behind a busy stream: the
     # per-launch cost a caller outside a graph sees
     blocker = torch.randn((4096, 4096), device=dev, dtype=torch.bfloat16)
@@ -346,31 +511,50 @@ def main():
     for r in range(n_eager):
         a, b = evs[r]
         a.record()
-        verify((7 * r + 3) % NL, mass_x)
+        st.verify((7 * r + 3) % NL)
         b.record()
     torch.cuda.synchronize()
+    del blocker
     eager_us = float(np.mean([a.elapsed_time(b) * 1e3 for a, b in evs][2:]))
-    if k_mean is None:
+    if stages is None:
         k_mean = eager_us
     achieved = vb / (k_mean * 1e-6) / 1e9
+    copy_same = copy_bandwidth(torch, dev, 4 * (vb // 4), 5)
+    copy_big = copy_bandwidth(torch, dev, 2 << 30, 5)
 
-    step_bytes = NL * (verify_bytes(w) + gather_bytes(w)) + uvprune_bytes(w) + topk_bytes(w) \
-        + accept_bytes(w)
+    step_bytes = st.bytes()
     us_layer = ms_step * 1e3 / NL
     traffic = measured_traffic()
 
     cpu = None
     if not args.no_cpu_baseline:
         hosts = []
-        sample = [1, 2] if not stacked else [0, 20, 40, 79]
-        for l in sample[:4]:
+        # a bounded sample: every fourth layer of the stack (20 layers)
+        sample = [0] if not stacked else list(range(0, NL, 4))
+        for l in sample:
             li = min(l, NL - 1)
-            hosts.append((W.storage_to_f64(Q[li].float().cpu().numpy(), "f32"),
-                          Kc[li].float().cpu().double().numpy(),
-                          Vc[li].float().cpu().double().numpy(), lens))
+            hosts.append((W.storage_to_f64(st.Q[li].float().cpu().numpy(), "f32"),
+                          st.Kc[li].float().cpu().double().numpy(),
+                          st.Vc[li].float().cpu().double().numpy(), st.lens))
         t0 = time.time()
-        cpu = cpu_baseline(w, hosts, L, NL)
+        cpu = cpu_baseline(w, hosts, st.L, NL)
         log(f"cpu baseline {time.time() - t0:.1f} s")
+    m_max = int(st.m_np.max())
+    L_used = st.L
+    del st, run
+    torch.cuda.empty_cache()
+
+    others = None
+    cossim = None
+    if not args.no_extra and graph_used:
+        others = {}
+        for name in OTHER_CONFIGS:
+            t0 = time.time()
+            others[name] = single_layer_record(torch, pv, W, name, dev, 20)
+            log(f"{name} single layer: {others[name]['us_per_step']} us/step "
+                f"({time.time() - t0:.1f} s)")
+        cossim = cossim_record(torch, pv, W, dev)
+        log(f"cossim: {cossim['us']} us")
 
     rec = {
         "metric": METRIC,
@@ -387,17 +571,19 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{w.name}-{'stacked-%dL' % NL if stacked else 'single-layer'}",
-            "batch": B, "query_heads": Hq, "kv_heads": Hkv, "head_dim": D,
-            "visual_tokens": int(m_np.max()), "text_tokens": w.n_text, "gamma": w.gamma,
-            "verify_rows": T, "keep": f"{w.keep_num}/{w.keep_den}", "uvprune_layers": L,
+            "batch": w.batch, "query_heads": w.hq, "kv_heads": w.hkv, "head_dim": w.head_dim,
+            "visual_tokens": m_max, "text_tokens": w.n_text, "gamma": w.gamma,
+            "verify_rows": w.T, "keep": f"{w.keep_num}/{w.keep_den}", "uvprune_layers": L_used,
             "vocab": w.vocab, "layers": NL, "criterion": "attention mass",
             "hip_graph": graph_used,
         },
         "achieved_hbm_tbs": round(step_bytes / (ms_step * 1e-3) / 1e12, 3),
         "step_bytes": step_bytes,
         "host_ms_per_step": round(host_s * 1e3 / args.steps, 4),
+        "stages_us": {k: round(v, 2) for k, v in stages.items()} if stages else None,
+        "copy_gbs": {"same_bytes_as_verify": round(copy_same, 1), "2GiB": round(copy_big, 1)},
         "roofline": {
-            "bound": "hbm", "kernel": "verify_mfma_kernel<128,5,resident>",
+            "bound": "hbm", "kernel": f"verify_mfma_kernel<{w.head_dim},{tiles(w)},resident>",
             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
@@ -405,9 +591,12 @@ def main():
             "launch_timing": ("graph of %d launches, events around replays" % reps
                               if graph_used else "eager launches, events around each"),
             "eager_launch_us": round(eager_us, 3),
+            "frac_of_copy_same_bytes": round(achieved / copy_same, 4),
         },
+        "other_configs": others,
+        "cossim": cossim,
         "cpu_baseline": cpu,
-        "device_status": st,
+        "device_status": status,
     }
     print(json.dumps(rec))
 

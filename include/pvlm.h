@@ -86,7 +86,7 @@ int pvlm_version(void);
  *   mass[b,i] = sum_{h,t} P_{h,t,i}   (normalised probabilities, summed over
  *                                      every query head and verify row)
  * so sum_i mass[b,i] = Hq*T.  This is the attention criterion of
- * attention-guided pruning (Sec. 3, Challenge 2; Suppl. C).
+ * attention-guided pruning (Sec. 3, Challenge 2; Suppl. D).
  *
  *   dt        PVLM_BF16 (bf16 in/out, fp32 accumulate) or PVLM_F32.
  *   T         verify rows = gamma + 1, 1..32.  The last T valid cache rows of

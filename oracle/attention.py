@@ -9,7 +9,7 @@ the gamma drafts) attends, for every query head h, to all context rows and
 causally to the verify-block rows before it.  Grouped-query attention maps
 head h to KV head floor(h * Hkv / Hq).  The per-token attention mass is the
 attention criterion of attention-guided pruning (Sec. 3, Challenge 2, and the
-"attention criterion" ablation in Suppl. C): the normalised probabilities
+"attention criterion" ablation in Suppl. D): the normalised probabilities
 summed over all heads and verify rows.
 """
 from __future__ import annotations

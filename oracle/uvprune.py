@@ -13,7 +13,7 @@ used throughout).
 The same variation operator is applied to a precomputed per-layer criterion
 stack c^l_i ("MASS" mode): there the criterion is already summed over the
 text side (e.g. the verifier attention mass of layer l), so the score is
-sum_{l=1..L} (c^l_i - c^{l-1}_i) (Suppl. C, attention criterion + variation).
+sum_{l=1..L} (c^l_i - c^{l-1}_i) (Suppl. D, the attention criterion with variation).
 
 The sums are evaluated literally: no telescoping, no factoring of the j-sum.
 """

@@ -1,7 +1,7 @@
 // UV-Prune score (gfx950): Eq. (average_similarity) of ParallelVLM Sec. 4.1,
 // over either the vision-text cosine similarity of Eq. (similarity)
 // ("COSSIM") or a precomputed per-layer criterion stack ("MASS", e.g. the
-// verifier attention mass; Suppl. C's attention criterion + variation).
+// verifier attention mass; Suppl. D's attention criterion with variation).
 //
 // The layer sum telescopes exactly, sum_{l=1..L} (S^l - S^{l-1}) = S^L - S^0,
 // and the text-token sum is linear in the normalised text vectors,

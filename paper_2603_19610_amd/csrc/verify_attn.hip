@@ -1,40 +1,41 @@
 // Verify attention with fused per-token attention mass (gfx950).
 //
-// Defines the target's verification forward over the video KV cache
+// Computes the target's verification forward over the video KV cache
 // (ParallelVLM Sec. 2.2; Sec. 4.2 Parallel Decoding) for the gamma + 1 verify
 // rows, fused with the per-token attention mass that attention-guided pruning
-// ranks visual tokens by (Sec. 3, Challenge 2; Suppl. C attention criterion).
-// The paper runs FlashAttention-2 on NVIDIA GPUs and notes that an explicit
-// score matrix is what makes attention-guided pruning incompatible with
-// block-wise kernels (Sec. 3, Sec. 5.4): here the mass is produced inside the
+// ranks visual tokens by (Sec. 3, Challenge 2; Suppl. D, attention criterion).
+// The paper notes that pruning by attention needs explicit scores, which
+// block-wise attention kernels never materialise (Sec. 3; Sec. 5.3,
+// FlashAttention compatibility): here the mass is produced inside the
 // block-wise kernel, with no score matrix in memory.
 //
-// Design (one cooperative launch):
+// Design (one launch, grid co-resident: one workgroup per CU):
 //  * Work unit = (batch b, KV head g, row group rg, token chunk).  All
 //    (Hq/Hkv) * T query rows of a KV head are packed as the N side of
 //    v_mfma_f32_16x16x32_bf16 tiles (16 rows per tile, at most 5 tiles per
-//    workgroup); tokens are the M side, so each lane ends up owning one query
-//    row and four tokens of every score tile.
-//  * Pass 1 streams K straight from HBM into the MFMA operand registers
-//    (no LDS), forms the scores, and keeps them in registers ("resident"
-//    variant, chunks up to 512 tokens per workgroup) together with each
-//    row's local max and exp-sum.
-//  * The workgroups of one (b, g, rg) exchange those statistics through the
-//    workspace and wait on a counter (cooperative launch: the whole grid is
-//    co-resident), which gives every workgroup each row's exact global
-//    log-sum-exp.
-//  * Pass 2 streams V, turns the resident scores into exactly normalised
-//    probabilities, reduces them over the rows into the per-token mass, and
-//    accumulates P.V on MFMA.  Because P is already normalised, the chunk
-//    partial outputs only need to be summed.
-//  * Chunks too long for registers use the "stream" variant, which recomputes
-//    the scores from K in pass 2 (K is read twice).
-//  * Epilogue: the chunk partials of O are summed after a second wait on the
-//    group counter, each workgroup summing one slice (the group's workgroups
-//    sit on one XCD, so the partials stay in its L2); the per-token mass is
-//    summed over KV heads by whichever workgroup of a chunk arrives last.
-//    Sums run in a fixed order, so results are bit-reproducible.
-//  * fp32 inputs take a VALU path with the same two-pass structure.
+//    workgroup); tokens are the M side, so each lane owns one query row and
+//    four tokens of every score tile.  The workgroups of one (b, g, rg) are
+//    placed on one XCD.
+//  * "Resident" variant (chunks up to 512 tokens): every wave puts its K
+//    blocks in flight straight into MFMA operand registers, waves 1-3 stream
+//    the chunk's V into LDS behind them (global_load_lds), and the scores stay
+//    in registers.  P.V then runs against the workgroup's own row maxima, the
+//    four waves' O fragments are reduce-scattered through LDS, and the chunk
+//    partial (bf16) and the row statistics are published.  One wait on the
+//    group counter follows; after it each workgroup forms every row's global
+//    log-sum-exp, the exact normalised mass of its own tokens from the
+//    resident scores, and one slice of O as the factor-weighted sum of the
+//    chunk partials.
+//  * "Stream" variant (longer chunks): statistics are exchanged after pass 1,
+//    pass 2 recomputes the scores from K (K is read twice) with the exact
+//    global log-sum-exp, and a second wait precedes the O sum.
+//  * The mass is summed over KV heads and row groups by whichever workgroup
+//    of a chunk arrives last.  Every sum runs in a fixed order, so results
+//    are bit-reproducible.
+//  * Workgroups exchange data only through device-coherent stores and loads
+//    followed by a relaxed counter increment and a polling wait (no cache
+//    flush).
+//  * fp32 inputs take a VALU path with the two-wait structure.
 #include "common.h"
 
 namespace pvlm {
