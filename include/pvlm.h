@@ -30,9 +30,10 @@
  *   - No global mutable state: calls are re-entrant; a workspace buffer must
  *     not be shared by two calls in flight at the same time.
  *   - Workspaces: zero-fill a workspace once before its first use.  Its first
- *     128 KiB hold the counters of the waits between workgroups, and every
- *     call leaves them zeroed again, so one buffer (at least as large as each
- *     call requires) serves calls of any shape in sequence.
+ *     1 MiB holds the counters of the waits between workgroups, and every
+ *     call leaves them in a consistent state (zero again, or, for verify's
+ *     monotonic counters, advanced together), so one buffer (at least as large
+ *     as each call requires) serves calls of any kind and shape in sequence.
  *   - Layouts are C-contiguous, innermost index last.  "bf16" is IEEE
  *     bfloat16 stored in 2 bytes.
  */
@@ -68,7 +69,10 @@ typedef enum {
 
 /* Bits ORed into the optional device status word. */
 #define PVLM_DEV_RANGE 1    /* a device-resident size or index was out of range */
-#define PVLM_DEV_TIMEOUT 2  /* an inter-workgroup wait gave up (results invalid) */
+#define PVLM_DEV_TIMEOUT 2  /* an inter-workgroup wait gave up (results invalid;
+                               zero-fill the workspace again before reusing it) */
+#define PVLM_DEV_PLACEMENT 4 /* a workgroup ran on another XCD than the launch
+                               planned for (results may be invalid)          */
 
 const char* pvlm_status_string(pvlm_status s);
 /* Text of the last HIP error seen by a pvlm call on this host thread. */

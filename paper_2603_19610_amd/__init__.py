@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(_PKG, "libpvlm.so")
 
 PVLM_F32, PVLM_BF16 = 0, 1
 PVLM_CRIT_MASS, PVLM_CRIT_COSSIM = 0, 1
-PVLM_DEV_RANGE, PVLM_DEV_TIMEOUT = 1, 2
+PVLM_DEV_RANGE, PVLM_DEV_TIMEOUT, PVLM_DEV_PLACEMENT = 1, 2, 4
 
 EXPORTS = (
     "pvlm_status_string", "pvlm_last_hip_error", "pvlm_version",
@@ -135,8 +135,8 @@ def _dt(t: torch.Tensor) -> int:
 class Workspace:
     """A zero-initialised device scratch buffer that grows on demand.
 
-    The library leaves its synchronisation words zeroed after every call, so
-    one buffer can serve successive calls on a stream (not concurrent ones).
+    The library leaves its synchronisation words consistent after every call,
+    so one buffer can serve successive calls on a stream (not concurrent ones).
     """
 
     def __init__(self, device=None):
@@ -352,5 +352,5 @@ __all__ = [
     "verify_attn_workspace_size", "uvprune_score_mass", "uvprune_score_cossim",
     "uvprune_criterion_cossim", "topk_select", "gather_kv", "spec_accept",
     "PVLM_F32", "PVLM_BF16", "PVLM_CRIT_MASS", "PVLM_CRIT_COSSIM", "PVLM_DEV_RANGE",
-    "PVLM_DEV_TIMEOUT",
+    "PVLM_DEV_TIMEOUT", "PVLM_DEV_PLACEMENT",
 ]

@@ -452,7 +452,7 @@ pvlm_status plan_accept(int B, int gamma, int V, APlan* p) {
   p->off_bar = take_sync(2 * sizeof(int));
   p->off_rowcnt = take_sync(rows * sizeof(int));
   p->off_bcnt = take_sync(B * sizeof(int));
-  if (sync > kSyncRegion) return PVLM_ERR_UNSUPPORTED;
+  if (sync > kSyncMonoOff) return PVLM_ERR_UNSUPPORTED;
   size_t off = kSyncRegion;
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -536,7 +536,10 @@ extern "C" pvlm_status pvlm_spec_accept(int B, int gamma, int V, float temperatu
   a.tau = (double)temperature;
   a.greedy = temperature == 0.f;
   const int items = B * (2 * gamma + 1) * p.NC;
-  int grid = di.cus < items ? di.cus : items;
+  // a multiple of 8 workgroups (the XCD count) keeps the cooperative queue's
+  // round-robin XCD placement aligned for the launches that follow
+  int grid = (items + 7) / 8 * 8;
+  if (grid > di.cus) grid = di.cus;
   if (grid < 1) grid = 1;
   void* args[] = {&a};
   PVLM_HIP(launch_coresident(reinterpret_cast<const void*>(accept_kernel), dim3(grid),

@@ -27,19 +27,24 @@ pvlm_status hip_check(hipError_t e);
 
 struct DeviceInfo {
   int cus = 0;
-  int xcds = 8;
+  int xcds = 0;  // accelerator complex dies (workgroup i runs on die i % xcds); 0 = unknown
 };
-// Compute-unit count of the current device (queried once per device).
+// Compute-unit and XCD counts of the current device (queried once per device).
 pvlm_status device_info(DeviceInfo* out);
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Every workspace starts with a fixed-size region that holds all counters of
-// the inter-workgroup waits.  Each call leaves that region zeroed, so a zeroed
-// workspace can be reused by calls of any shape: their data areas (after the
-// region) may overlap earlier data, their counters never do.
-constexpr size_t kSyncRegion = 128 * 1024;
-constexpr int kSyncInts = (int)(kSyncRegion / sizeof(int));
+// the inter-workgroup waits, so a zero-filled workspace can be reused by calls
+// of any shape: their data areas (after the region) may overlap earlier data,
+// their counters never do.  Calls whose counters return to zero use the low
+// part of the region; verify's monotonic counters (each call leaves them
+// consistent, never reset) use the part from kSyncMonoOff on.
+constexpr size_t kSyncRegion = 1024 * 1024;
+constexpr size_t kSyncMonoOff = 256 * 1024;
+// Counters that many workgroups update or poll get a 128-byte line each, so
+// the memory-side atomics and polls of different counters never contend.
+constexpr size_t kSyncLine = 128;
 
 // Raise a kernel's dynamic-LDS limit to `bytes` (done once per kernel and size).
 hipError_t allow_dynamic_lds(const void* kernel, int bytes);
@@ -163,6 +168,59 @@ __device__ __forceinline__ void lds_sync() {
 __device__ __forceinline__ uint64_t pack_bf16x4(float x, float y, float z, float w) {
   return (uint64_t)f32_to_bf16(x) | ((uint64_t)f32_to_bf16(y) << 16) | ((uint64_t)f32_to_bf16(z) << 32) |
          ((uint64_t)f32_to_bf16(w) << 48);
+}
+
+// Monotonic group counters.  Every launch adds one arrival per workgroup of a
+// group to that group's counter and never resets it; the count the counter
+// had when the launch began ("base") is kept beside it.  Every workgroup reads
+// the base at kernel start, waits for base + (workgroups in the group) with
+// wrapping arithmetic, and the launch's last arrival at the group's final
+// counter advances the base.  No end-of-kernel reset round trip is needed.
+__device__ __forceinline__ unsigned grp_arrive(unsigned* counter) {
+  return __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned grp_read(const unsigned* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Bounded poll until *counter has reached `target`; flags PVLM_DEV_TIMEOUT
+// and gives up after kSpinLimit polls.
+__device__ __forceinline__ void grp_poll(const unsigned* counter, unsigned target, int32_t* status) {
+  int spins = 0;
+  while ((int)(grp_read(counter) - target) < 0) {
+    __builtin_amdgcn_s_sleep(1);
+    if (++spins > kSpinLimit) {
+      dev_flag(status, PVLM_DEV_TIMEOUT);
+      break;
+    }
+  }
+}
+
+// Stores and loads of data exchanged between workgroups.  LOCAL: every
+// workgroup of the exchange runs on one XCD and so shares one L2; data is
+// written and read once per launch at addresses the reader has not touched
+// before in the launch (its L1 holds no copy), so plain accesses through that
+// L2 are coherent.  Otherwise device-coherent accesses are used.
+template <bool LOCAL>
+__device__ __forceinline__ void x_store(float* p, float v) {
+  if constexpr (LOCAL) *p = v; else st_agent(p, v);
+}
+template <bool LOCAL>
+__device__ __forceinline__ void x_store(uint64_t* p, uint64_t v) {
+  if constexpr (LOCAL) *p = v;
+  else __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <bool LOCAL>
+__device__ __forceinline__ void x_store(float2* p, float2 v) {
+  if constexpr (LOCAL) *p = v; else st_agent(p, v);
+}
+template <bool LOCAL>
+__device__ __forceinline__ float2 x_load(const float2* p) {
+  if constexpr (LOCAL) return *p; else return ld_agent(p);
+}
+template <bool LOCAL>
+__device__ __forceinline__ uint64_t x_load(const uint64_t* p) {
+  if constexpr (LOCAL) return *p;
+  else return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ void reset_counter(int* counter) {

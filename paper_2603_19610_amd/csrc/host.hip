@@ -14,6 +14,7 @@ thread_local std::string g_last_hip_error;
 std::mutex g_info_mu;
 constexpr int kMaxDevices = 64;
 int g_cus[kMaxDevices] = {0};
+int g_xcds[kMaxDevices] = {0};
 std::mutex g_lds_mu;
 std::set<std::pair<const void*, int>> g_lds_done;
 }  // namespace
@@ -57,10 +58,15 @@ pvlm_status device_info(DeviceInfo* out) {
     e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return hip_check(e);
     if (cus <= 0) return PVLM_ERR_HIP;
+    int xcds = 0;
+    if (hipDeviceGetAttribute(&xcds, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess || xcds < 1)
+      xcds = 0;  // unknown: no exchange relies on sharing an XCD
+    (void)hipGetLastError();
+    g_xcds[dev] = xcds;
     g_cus[dev] = cus;
   }
   out->cus = g_cus[dev];
-  out->xcds = 8;
+  out->xcds = g_xcds[dev];
   return PVLM_OK;
 }
 

@@ -57,13 +57,14 @@ struct VArgs {
   const void* k;
   const void* v;
   const int32_t* ctx_len;
-  float* stats;   // [groups][splits][ROWS][2]  (log2-domain max, exp-sum)
-  float* opart;   // [groups][splits][ROWS][D]
-  float* mpart;   // [B][Hkv*RG][n_cap]
-  int* cnt;       // [groups]   first wait (statistics)
-  int* cnt2;      // [groups]   second wait (O partials)
-  int* done;      // [groups]   finished workgroups (resets the counters)
-  int* mcnt;      // [B][splits] arrivals per chunk for the mass sum
+  float* stats;     // [groups][splits] records of ROWS + 1 float2 (padded to 128 B):
+                    // (log2-domain max, exp-sum) per row, then the launch tag
+  float* opart;     // [groups][splits][ROWS][D] (bf16 pairs, or fp32)
+  float* mpart;     // [B][Hkv*RG][n_cap]
+  unsigned* slots;  // [groups][3] monotonic, one 128-byte line each: arrivals
+                    // with published statistics, arrivals with published O
+                    // partials, and the counters' value when the launch began
+  int* mcnt;        // [B][splits] arrivals per chunk for the mass sum (128 B apart)
   void* out;
   float* lse;
   float* mass;
@@ -72,7 +73,9 @@ struct VArgs {
   int B, T, Hq, Hkv, G, R, RG, RT, D;
   int max_ctx;
   int splits, chunk, grp_base, ngrp, grid;
-  float sl2;      // scale * log2(e)
+  int xmap;         // workgroup i runs on XCD i % xmap (1: no XCD-aware mapping)
+  int local;        // every group's workgroups share one XCD
+  float sl2;        // scale * log2(e)
   int f32;
 };
 
@@ -82,8 +85,20 @@ struct Unit {
 
 __device__ __forceinline__ bool decode_unit(const VArgs& a, Unit& u) {
   const int i = blockIdx.x;
-  const int per_xcd = a.grid / 8;
-  const int lg = (i % 8) * per_xcd + i / 8;  // consecutive logical units share an XCD
+  const int per_xcd = a.grid / a.xmap;
+  // Consecutive logical units share an XCD.  Workgroup i runs on XCD
+  // (i + s) % xmap for a launch-wide offset s (s = 0 on an idle queue), so in
+  // the same-XCD exchange mode the logical index is built from the XCD the
+  // workgroup actually runs on, which keeps every group on one XCD for any s.
+  int x = i % a.xmap;
+  if (a.local) {
+    int xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    xcc &= 0xf;
+    if (xcc < a.xmap) x = xcc;
+    else if (threadIdx.x == 0) dev_flag(a.status, PVLM_DEV_PLACEMENT);
+  }
+  const int lg = x * per_xcd + i / a.xmap;
   if (lg >= a.ngrp * a.splits) return false;
   u.grp = a.grp_base + lg / a.splits;
   u.split = lg % a.splits;
@@ -119,91 +134,176 @@ __device__ __forceinline__ void lse_combine(float& m, float& z, float m2, float 
   m = M;
 }
 
-// Publish this workgroup's per-row (max, exp-sum), wait for the other chunks
-// of the same (b, g, rg), and leave each row's global log2-sum-exp in s_lse
-// (+inf for padding rows so their probabilities are 0).  The statistics are
-// written by wave 0 only, so only that wave needs to publish its stores.
+// ---------------------------------------------------- group exchanges --
+// The workgroups of one (b, g, rg) group meet at two monotonic counters
+// (common.h): cnt_s once their row statistics are published, cnt_o once their
+// O partials are.  Every workgroup arrives at cnt_s before cnt_o, and the
+// launch's last arrival at cnt_o advances the group's base.
+
+constexpr int kLineU = (int)(kSyncLine / sizeof(unsigned));  // counters per 128-byte line
+__device__ __forceinline__ unsigned* cnt_s(const VArgs& a, const Unit& u) {
+  return a.slots + (3 * u.grp) * kLineU;
+}
+__device__ __forceinline__ unsigned* cnt_o(const VArgs& a, const Unit& u) {
+  return a.slots + (3 * u.grp + 1) * kLineU;
+}
+__device__ __forceinline__ unsigned* cnt_base(const VArgs& a, const Unit& u) {
+  return a.slots + (3 * u.grp + 2) * kLineU;
+}
+
+// The group's counter base for this launch (every thread reads it).
+__device__ __forceinline__ unsigned read_base(const VArgs& a, const Unit& u) {
+  return grp_read(cnt_base(a, u));
+}
+
+// Each workgroup's statistics record holds ROWS (max, exp-sum) pairs and a
+// header stamped with the launch's tag (base + 1, different in every launch
+// of the group), which readers check: a record missing from this launch
+// (misplaced workgroup, stale data) raises PVLM_DEV_PLACEMENT.
+// Records are padded to whole 128-byte lines so no two workgroups' records
+// share a cache line.
 template <int ROWS>
-__device__ void exchange_stats(const VArgs& a, const Unit& u, float* s_m, float* s_z,
-                               float* s_lse, bool wait) {
-  constexpr int kU = 16;  // splits loaded per round trip
-  float* st = a.stats + ((size_t)u.grp * a.splits + u.split) * ROWS * 2;
-  __syncthreads();
+constexpr int rec_stride() { return (ROWS + 1 + 15) / 16 * 16; }  // float2 units
+template <int ROWS>
+__device__ __forceinline__ float2* stats_rec(const VArgs& a, const Unit& u, int split) {
+  return reinterpret_cast<float2*>(a.stats) + ((size_t)u.grp * a.splits + split) * rec_stride<ROWS>();
+}
+
+// Wave 0 publishes this workgroup's per-row (max, exp-sum) and the tag.
+template <int ROWS, bool LOCAL>
+__device__ __forceinline__ void stats_store(const VArgs& a, const Unit& u, const float* s_m,
+                                            const float* s_z, unsigned base) {
   if (threadIdx.x < 64) {
-    for (int r = threadIdx.x; r < ROWS; r += 64) {
-      st_agent(st + 2 * r, s_m[r]);
-      st_agent(st + 2 * r + 1, s_z[r]);
-    }
+    float2* st = stats_rec<ROWS>(a, u, u.split);
+    for (int r = threadIdx.x; r < ROWS; r += 64) x_store<LOCAL>(st + r, make_float2(s_m[r], s_z[r]));
+    if (threadIdx.x == 0) x_store<LOCAL>(st + ROWS, make_float2(__uint_as_float(base + 1u), 0.f));
   }
-  wg_signal_wait(a.cnt + u.grp, a.splits, a.status, wait, /*writer_wave0=*/true);
-  if (!wait) return;
-  const float* st0 = a.stats + (size_t)u.grp * a.splits * ROWS * 2;
-  for (int r = threadIdx.x; r < ROWS; r += kThreads) {
+}
+
+// Thread 0, after its O-partial arrival returned `old`: the launch's last
+// arrival advances the base, every other workgroup waits (if asked) for all.
+__device__ __forceinline__ void o_finish(const VArgs& a, const Unit& u, unsigned base, unsigned old,
+                                         bool wait) {
+  if (old - base == (unsigned)a.splits - 1u)
+    __hip_atomic_store(cnt_base(a, u), base + (unsigned)a.splits, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  else if (wait)
+    grp_poll(cnt_o(a, u), base + (unsigned)a.splits, a.status);
+}
+
+// Every row's statistics over the group's nsp chunks, combined in parallel
+// (P thread sets per row): leaves the row's log2-sum-exp in s_lse (+inf for
+// padding rows, whose probabilities are then 0), its global max in s_pm[0]
+// and 1/sum in s_pz[0] (0 for padding rows) and, if s_fac is given, each
+// chunk's row max in s_fac[chunk * ROWS + row].
+template <int ROWS, bool LOCAL>
+__device__ void stats_combine(const VArgs& a, const Unit& u, int nsp, float* s_lse, float* s_fac,
+                              float (*s_pm)[ROWS], float (*s_pz)[ROWS], unsigned base) {
+  constexpr int kU = 16;
+  constexpr int P = kThreads / ROWS < kWaves ? kThreads / ROWS : kWaves;
+  const int tid = threadIdx.x;
+  const float2* st0 = stats_rec<ROWS>(a, u, 0);
+  for (int sp = tid; sp < nsp; sp += kThreads) {  // every chunk's record is from this launch
+    const float2 h = x_load<LOCAL>(st0 + (size_t)sp * rec_stride<ROWS>() + ROWS);
+    if (__float_as_uint(h.x) != base + 1u) dev_flag(a.status, PVLM_DEV_PLACEMENT);
+  }
+  if (tid < P * ROWS) {
+    const int r = tid % ROWS, part = tid / ROWS;
     float M = kNegInf, Z = 0.f;
-    for (int s0 = 0; s0 < a.splits; s0 += kU) {
+    for (int s0 = part; s0 < nsp; s0 += P * kU) {
       float2 v[kU];
 #pragma unroll
-      for (int j = 0; j < kU; ++j)
-        v[j] = s0 + j < a.splits
-                   ? ld_agent(reinterpret_cast<const float2*>(st0 + ((size_t)(s0 + j) * ROWS + r) * 2))
-                   : make_float2(kNegInf, 0.f);
+      for (int j = 0; j < kU; ++j)  // unconditional (clamped) loads: fine-grained waits
+        v[j] = x_load<LOCAL>(st0 + (size_t)min(s0 + j * P, nsp - 1) * rec_stride<ROWS>() + r);
 #pragma unroll
-      for (int j = 0; j < kU; ++j) lse_combine(M, Z, v[j].x, v[j].y);
+      for (int j = 0; j < kU; ++j) {
+        const int sp = s0 + j * P;
+        if (sp < nsp) {
+          if (s_fac) s_fac[sp * ROWS + r] = v[j].x;
+          lse_combine(M, Z, v[j].x, v[j].y);
+        }
+      }
     }
-    const int row = u.rg * a.RT * 16 + r;
-    s_lse[r] = (row < a.R && Z > 0.f) ? M + __log2f(Z) : __builtin_huge_valf();
+    s_pm[part][r] = M;
+    s_pz[part][r] = Z;
+  }
+  lds_sync();
+  if (tid < ROWS) {
+    const int r = tid;
+    float M = s_pm[0][r], Z = s_pz[0][r];
+#pragma unroll
+    for (int p = 1; p < P; ++p) lse_combine(M, Z, s_pm[p][r], s_pz[p][r]);
+    const bool ok = u.rg * a.RT * 16 + r < a.R && Z > 0.f;
+    s_lse[r] = ok ? M + __log2f(Z) : __builtin_huge_valf();
+    s_pm[0][r] = M;
+    s_pz[0][r] = ok ? 1.f / Z : 0.f;
+  }
+  lds_sync();
+}
+
+// Statistics exchange of the two-pass variants: publish, arrive, and (unless
+// the chunk is empty) wait for the whole group and combine into s_lse.
+template <int ROWS, bool LOCAL>
+__device__ void exchange_stats(const VArgs& a, const Unit& u, const float* s_m, const float* s_z,
+                               float* s_lse, float (*s_pm)[ROWS], float (*s_pz)[ROWS],
+                               unsigned base, bool wait) {
+  __syncthreads();
+  stats_store<ROWS, LOCAL>(a, u, s_m, s_z, base);
+  // wave-uniform branch: only wave 0 wrote, only it waits for its stores
+  if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) == 0) __builtin_amdgcn_s_waitcnt(0);
+  if (threadIdx.x == 0) {
+    grp_arrive(cnt_s(a, u));
+    if (wait) grp_poll(cnt_s(a, u), base + (unsigned)a.splits, a.status);
   }
   __syncthreads();
+  if (wait)
+    stats_combine<ROWS, LOCAL>(a, u, (u.N + a.chunk - 1) / a.chunk, s_lse, nullptr, s_pm, s_pz, base);
 }
 
 // Per-token mass summed over the KV heads and row groups by the last
-// workgroup of each chunk (no wait), then the group's counter reset by its
-// last workgroup.
-__device__ void mass_combine_and_finish(const VArgs& a, const Unit& u, int* s_flag) {
+// workgroup of each chunk to arrive (the chunk's workgroups sit on different
+// XCDs, so these exchanges are device-coherent).
+__device__ void mass_combine(const VArgs& a, const Unit& u, int* s_flag) {
   const int tid = threadIdx.x;
-  if (a.mass) {
-    const int P = a.Hkv * a.RG;
-    int* mc = a.mcnt + (size_t)u.b * a.splits + u.split;
-    if (wg_signal_last(mc, P, s_flag)) {
-      const int64_t lo = u.c0;
-      const int64_t hi_sum = u.c1 > u.c0 ? u.c1 : u.c0;
-      const int64_t chunk_end = (int64_t)u.c0 + a.chunk;
-      const int64_t hi = u.split == a.splits - 1 ? a.n_cap : (chunk_end < a.n_cap ? chunk_end : a.n_cap);
-      const float* mp = a.mpart + (size_t)u.b * P * a.n_cap;
-      float* ms = a.mass + (size_t)u.b * a.n_cap;
-      for (int64_t i = lo + tid; i < hi; i += kThreads) {
-        float acc = 0.f;
-        if (i < hi_sum) {
-          for (int p0 = 0; p0 < P; p0 += 8) {
-            float v[8];
+  if (!a.mass) return;
+  const int P = a.Hkv * a.RG;
+  int* mc = a.mcnt + ((size_t)u.b * a.splits + u.split) * (kSyncLine / sizeof(int));
+  if (wg_signal_last(mc, P, s_flag)) {
+    const int64_t lo = u.c0;
+    const int64_t hi_sum = u.c1 > u.c0 ? u.c1 : u.c0;
+    const int64_t chunk_end = (int64_t)u.c0 + a.chunk;
+    const int64_t hi = u.split == a.splits - 1 ? a.n_cap : (chunk_end < a.n_cap ? chunk_end : a.n_cap);
+    const float* mp = a.mpart + (size_t)u.b * P * a.n_cap;
+    float* ms = a.mass + (size_t)u.b * a.n_cap;
+    for (int64_t i = lo + tid; i < hi; i += kThreads) {
+      float acc = 0.f;
+      if (i < hi_sum) {
+        for (int p0 = 0; p0 < P; p0 += 8) {
+          float v[8];
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-              v[j] = p0 + j < P ? ld_agent(mp + (size_t)(p0 + j) * a.n_cap + i) : 0.f;
+          for (int j = 0; j < 8; ++j)
+            v[j] = p0 + j < P ? ld_agent(mp + (size_t)(p0 + j) * a.n_cap + i) : 0.f;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) acc += v[j];
-          }
+          for (int j = 0; j < 8; ++j) acc += v[j];
         }
-        ms[i] = acc;
       }
-      if (tid == 0) reset_counter(mc);
+      ms[i] = acc;
     }
-  }
-  if (wg_signal_last(a.done + u.grp, a.splits, s_flag) && tid == 0) {
-    reset_counter(a.cnt + u.grp);
-    reset_counter(a.cnt2 + u.grp);
-    reset_counter(a.done + u.grp);
+    if (tid == 0) reset_counter(mc);
   }
 }
 
-// After pass 2: O (sum of the chunk partials after a second wait on the group
-// counter, one slice per workgroup), lse, then the per-token mass (summed over
-// KV heads and row groups by the last workgroup of each chunk -- done last so
-// that work never delays the group's wait), and counter reset.
-template <int ROWS, int D>
+// End of the two-pass variants: the O partials are published (every wave's
+// stores complete), arrive at cnt_o and wait; O = sum of the chunk partials
+// (one slice per workgroup), lse; then the mass sum.
+template <int ROWS, int D, bool LOCAL>
 __device__ void verify_epilogue(const VArgs& a, const Unit& u, const float* s_lse, bool empty,
-                                int* s_flag) {
+                                int* s_flag, unsigned base) {
   const int tid = threadIdx.x;
-  wg_signal_wait(a.cnt2 + u.grp, a.splits, a.status, !empty);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (tid == 0) o_finish(a, u, base, grp_arrive(cnt_o(a, u)), !empty);
+  __syncthreads();
   if (!empty) {
     const int row0 = u.rg * a.RT * 16;
     const int nsp = (u.N + a.chunk - 1) / a.chunk;
@@ -221,14 +321,15 @@ __device__ void verify_epilogue(const VArgs& a, const Unit& u, const float* s_ls
           for (int j = 0; j < 8; ++j)
 #pragma unroll
             for (int h = 0; h < 2; ++h)
-              v[j][h] = s0 + j < nsp ? ld_agent(op + ((size_t)(s0 + j) * ROWS * D) / 2 + 2 * e + h)
-                                     : make_float2(0.f, 0.f);
+              v[j][h] = x_load<LOCAL>(op + ((size_t)min(s0 + j, nsp - 1) * ROWS * D) / 2 + 2 * e + h);
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
-            acc[0] += v[j][0].x;
-            acc[1] += v[j][0].y;
-            acc[2] += v[j][1].x;
-            acc[3] += v[j][1].y;
+            if (s0 + j < nsp) {
+              acc[0] += v[j][0].x;
+              acc[1] += v[j][0].y;
+              acc[2] += v[j][1].x;
+              acc[3] += v[j][1].y;
+            }
           }
         }
       } else {  // bf16 partials, one 64-bit load per group
@@ -237,25 +338,23 @@ __device__ void verify_epilogue(const VArgs& a, const Unit& u, const float* s_ls
           uint64_t v[16];
 #pragma unroll
           for (int j = 0; j < 16; ++j)
-            v[j] = s0 + j < nsp ? __hip_atomic_load(op + (size_t)(s0 + j) * ROWS * D / 4 + e,
-                                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                                : 0ull;
+            v[j] = x_load<LOCAL>(op + (size_t)min(s0 + j, nsp - 1) * ROWS * D / 4 + e);
 #pragma unroll
           for (int j = 0; j < 16; ++j)
+            if (s0 + j < nsp) {
 #pragma unroll
-            for (int h = 0; h < 4; ++h) acc[h] += bf16_to_f32((uint16_t)(v[j] >> (16 * h)));
+              for (int h = 0; h < 4; ++h) acc[h] += bf16_to_f32((uint16_t)(v[j] >> (16 * h)));
+            }
         }
       }
       const int row = row0 + (4 * e) / D, d = (4 * e) % D;
       const int t = row / a.G, h = u.g * a.G + row % a.G;
       const size_t oi = (((size_t)u.b * a.T + t) * a.Hq + h) * D + d;
-      if (a.f32) {
+      if (a.f32)
         *reinterpret_cast<float4*>(static_cast<float*>(a.out) + oi) = make_float4(acc[0], acc[1], acc[2], acc[3]);
-      } else {
-        const uint64_t pk = (uint64_t)f32_to_bf16(acc[0]) | ((uint64_t)f32_to_bf16(acc[1]) << 16) |
-                            ((uint64_t)f32_to_bf16(acc[2]) << 32) | ((uint64_t)f32_to_bf16(acc[3]) << 48);
-        *reinterpret_cast<uint64_t*>(static_cast<uint16_t*>(a.out) + oi) = pk;
-      }
+      else
+        *reinterpret_cast<uint64_t*>(static_cast<uint16_t*>(a.out) + oi) =
+            pack_bf16x4(acc[0], acc[1], acc[2], acc[3]);
     }
     if (a.lse && u.split == 0) {
       for (int r = tid; r < rows; r += kThreads) {
@@ -264,7 +363,7 @@ __device__ void verify_epilogue(const VArgs& a, const Unit& u, const float* s_ls
       }
     }
   }
-  mass_combine_and_finish(a, u, s_flag);
+  mass_combine(a, u, s_flag);
 }
 
 // ------------------------------------------------------------ MFMA path --
@@ -458,7 +557,7 @@ __device__ __forceinline__ void reduce_stats(float (&m)[RT], float (&z)[RT], int
       s_wz[w][rt * 16 + n] = z[rt];
     }
   }
-  __syncthreads();
+  lds_sync();
   for (int r = threadIdx.x; r < RT * 16; r += kThreads) {
     float M = s_wm[0][r], Z = s_wz[0][r];
 #pragma unroll
@@ -466,7 +565,7 @@ __device__ __forceinline__ void reduce_stats(float (&m)[RT], float (&z)[RT], int
     s_m[r] = M;
     s_z[r] = Z;
   }
-  __syncthreads();
+  lds_sync();
 }
 
 // Probabilities of one block relative to a per-row reference (the
@@ -585,7 +684,7 @@ __device__ __forceinline__ void pv_block(const float (&S)[2][RT][4], const float
 // lane); unit k belongs to wave k % 4.  Every wave parks the units it does not
 // own, one barrier, then each owner adds the three parked copies to its own
 // and stores the sum (8 bytes per lane and row) straight from registers.
-template <int D, int RT>
+template <int D, int RT, bool LOCAL>
 __device__ __forceinline__ void write_opart(const VArgs& a, const Unit& u, floatx4 (&O)[RT][D / 16],
                                             float* s_o, int lane, int w, int n, int gq) {
   constexpr int DPL = D / 16;
@@ -622,202 +721,161 @@ __device__ __forceinline__ void write_opart(const VArgs& a, const Unit& u, float
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = rt * 16 + 4 * gq + i;
-        __hip_atomic_store(op + (row * D + DPL * n + FU * h) / 4,
-                           pack_bf16x4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]), __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
+        x_store<LOCAL>(op + (row * D + DPL * n + FU * h) / 4,
+                       pack_bf16x4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]));
       }
     }
   }
 }
 
 // Resident variant, after the chunk partial of O (relative to the
-// workgroup's own row maxima) and the row statistics are published: the one
-// wait of the group, then each row's global log2-sum-exp and the per-chunk
-// rescale factors, the exact per-token mass from the resident scores, this
-// workgroup's slice of O (factor-weighted sum of the partials), lse, the mass
-// sum over KV heads (last workgroup of each chunk) and the counter reset.
-template <int D, int RT>
+// workgroup's own row maxima) is published and the workgroup has arrived at
+// cnt_o (thread 0 holds the value the arrival returned): wait for the group's
+// statistics (published right after pass 1, so normally complete), form each
+// row's global log2-sum-exp and the per-chunk rescale factors, wait for the O
+// partials and put the loads of this workgroup's O slice in flight, compute
+// the exact per-token mass from the resident scores meanwhile, then the
+// factor-weighted O sum, lse, and the mass sum over KV heads.
+template <int D, int RT, bool LOCAL>
 __device__ void verify_epilogue_local(const VArgs& a, const Unit& u, const float (&S)[kNB][2][RT][4],
                                       float* s_lse, float* s_fac, float (*s_pm)[RT * 16],
-                                      float (*s_pz)[RT * 16], bool empty, int* s_flag, int n, int gq,
-                                      int w) {
+                                      float (*s_pz)[RT * 16], int* s_flag, int n, int gq, int w,
+                                      unsigned base, unsigned old) {
   constexpr int ROWS = RT * 16;
   constexpr int kU = 16;
-  // threads per row for the statistics combine (rows x parts <= 256)
-  constexpr int P = kThreads / ROWS < kWaves ? kThreads / ROWS : kWaves;
   const int tid = threadIdx.x;
-  wg_signal_wait(a.cnt + u.grp, a.splits, a.status, !empty);
-  if (!empty) {
-    const float* st0 = a.stats + (size_t)u.grp * a.splits * ROWS * 2;
-    const int nsp = (u.N + a.chunk - 1) / a.chunk;
-    // This workgroup's slice of O is the factor-weighted sum over chunks of
-    // the partials.  With few elements per workgroup the chunks are split
-    // over Q thread sets whose sums meet in LDS.
-    const int row0 = u.rg * a.RT * 16;
-    const int rows = min(ROWS, a.R - row0);
-    const int E4 = rows * D / 4;
-    const int per = (E4 + nsp - 1) / nsp;
-    const int e0 = min(E4, u.split * per), e1 = min(E4, e0 + per);
-    const int cnt = e1 - e0;
-    const int Q = cnt <= 0 ? 1 : min(kOSets, max(1, kThreads / cnt));
-    const int q = cnt <= 0 ? 0 : tid / cnt, el = cnt <= 0 ? 0 : tid % cnt;
-    const bool act = cnt > 0 && q < Q;  // first element e0 + el (Q = 1: el = tid)
-    const uint64_t* op = reinterpret_cast<const uint64_t*>(a.opart) + (size_t)u.grp * a.splits * ROWS * D / 4;
-    auto load_parts = [&](int e, int s0, int Qs, uint64_t (&v)[kU]) {
-      // unconditional (clamped) loads keep the wait counts fine-grained
+  const int nsp = (u.N + a.chunk - 1) / a.chunk;
+  if (tid == 0) grp_poll(cnt_s(a, u), base + (unsigned)a.splits, a.status);
+  __syncthreads();
+  stats_combine<ROWS, LOCAL>(a, u, nsp, s_lse, s_fac, s_pm, s_pz, base);
+  // rescale factor of every chunk partial: exp2(m_chunk - M) / Z
+  for (int e = tid; e < nsp * ROWS; e += kThreads) {
+    const int r = e % ROWS;
+    const float m = s_fac[e], invZ = s_pz[0][r];
+    s_fac[e] = invZ != 0.f && m != kNegInf ? fast_exp2(m - s_pm[0][r]) * invZ : 0.f;
+  }
+  if (tid == 0) o_finish(a, u, base, old, true);
+  __syncthreads();
+  // This workgroup's slice of O is the factor-weighted sum over chunks of the
+  // partials.  With few elements per workgroup the chunks are split over Q
+  // thread sets whose sums meet in LDS.
+  const int row0 = u.rg * a.RT * 16;
+  const int rows = min(ROWS, a.R - row0);
+  const int E4 = rows * D / 4;
+  const int per = (E4 + nsp - 1) / nsp;
+  const int e0 = min(E4, u.split * per), e1 = min(E4, e0 + per);
+  const int cnt = e1 - e0;
+  const int Q = cnt <= 0 ? 1 : min(kOSets, max(1, kThreads / cnt));
+  const int q = cnt <= 0 ? 0 : tid / cnt, el = cnt <= 0 ? 0 : tid % cnt;
+  const bool act = cnt > 0 && q < Q;  // first element e0 + el (Q = 1: el = tid)
+  const uint64_t* op = reinterpret_cast<const uint64_t*>(a.opart) + (size_t)u.grp * a.splits * ROWS * D / 4;
+  auto load_parts = [&](int e, int s0, int Qs, uint64_t (&v)[kU]) {
+    // unconditional (clamped) loads keep the wait counts fine-grained
 #pragma unroll
-      for (int j = 0; j < kU; ++j) {
-        const int sp = min(s0 + j * Qs, nsp - 1);
-        v[j] = __hip_atomic_load(op + (size_t)sp * ROWS * D / 4 + e, __ATOMIC_RELAXED,
-                                 __HIP_MEMORY_SCOPE_AGENT);
-      }
-    };
-    auto fma_parts = [&](int e, int s0, int Qs, const uint64_t (&v)[kU], float (&acc)[4]) {
-      const int r = (4 * e) / D;
-#pragma unroll
-      for (int j = 0; j < kU; ++j) {
-        const int sp = s0 + j * Qs;
-        const float f = sp < nsp ? s_fac[sp * ROWS + r] : 0.f;
-#pragma unroll
-        for (int h = 0; h < 4; ++h) acc[h] += f * bf16_to_f32((uint16_t)(v[j] >> (16 * h)));
-      }
-    };
-    auto emit = [&](int e, const float (&acc)[4]) {
-      const int r = (4 * e) / D;
-      const int row = row0 + r, d = (4 * e) % D;
-      const int t = row / a.G, h = u.g * a.G + row % a.G;
-      const size_t oi = (((size_t)u.b * a.T + t) * a.Hq + h) * D + d;
-      *reinterpret_cast<uint64_t*>(static_cast<uint16_t*>(a.out) + oi) =
-          pack_bf16x4(acc[0], acc[1], acc[2], acc[3]);
-    };
-    // 1. statistics of every (chunk, row) pair, read once: first round trip,
-    //    with the first batch of O partials issued right behind it
-    const int r_st = tid % ROWS, part = tid / ROWS;
-    const bool st_thr = tid < P * ROWS;
-    float2 sv[kU];
+    for (int j = 0; j < kU; ++j)
+      v[j] = x_load<LOCAL>(op + (size_t)min(s0 + j * Qs, nsp - 1) * ROWS * D / 4 + e);
+  };
+  auto fma_parts = [&](int e, int s0, int Qs, const uint64_t (&v)[kU], float (&acc)[4]) {
+    const int r = (4 * e) / D;
 #pragma unroll
     for (int j = 0; j < kU; ++j) {
-      const int sp = min(part + j * P, nsp - 1);
-      sv[j] = ld_agent(reinterpret_cast<const float2*>(st0 + ((size_t)sp * ROWS + r_st) * 2));
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    const int e_first = act ? e0 + el : 0;
-    uint64_t pre[kU];
-    load_parts(e_first, q, Q, pre);
-    __builtin_amdgcn_sched_barrier(0);
-    float M = kNegInf, Z = 0.f;
+      const int sp = s0 + j * Qs;
+      const float f = sp < nsp ? s_fac[sp * ROWS + r] : 0.f;
 #pragma unroll
-    for (int j = 0; j < kU; ++j) {
-      const int sp = part + j * P;
-      if (st_thr && sp < nsp) {
-        s_fac[sp * ROWS + r_st] = sv[j].x;
-        lse_combine(M, Z, sv[j].x, sv[j].y);
-      }
+      for (int h = 0; h < 4; ++h) acc[h] += f * bf16_to_f32((uint16_t)(v[j] >> (16 * h)));
     }
-    if (st_thr) {
-      for (int s0 = part + P * kU; s0 < nsp; s0 += P * kU) {  // more than P * kU chunks
-        float2 v[kU];
+  };
+  auto emit = [&](int e, const float (&acc)[4]) {
+    const int r = (4 * e) / D;
+    const int row = row0 + r, d = (4 * e) % D;
+    const int t = row / a.G, h = u.g * a.G + row % a.G;
+    const size_t oi = (((size_t)u.b * a.T + t) * a.Hq + h) * D + d;
+    *reinterpret_cast<uint64_t*>(static_cast<uint16_t*>(a.out) + oi) =
+        pack_bf16x4(acc[0], acc[1], acc[2], acc[3]);
+  };
+  const int e_first = act ? e0 + el : 0;
+  uint64_t pre[kU];
+  load_parts(e_first, q, Q, pre);
+  __builtin_amdgcn_sched_barrier(0);
+  // exact per-token mass of this chunk's tokens (resident scores)
+  float lse[RT];
 #pragma unroll
-        for (int j = 0; j < kU; ++j) {
-          const int sp = min(s0 + j * P, nsp - 1);
-          v[j] = ld_agent(reinterpret_cast<const float2*>(st0 + ((size_t)sp * ROWS + r_st) * 2));
-        }
+  for (int rt = 0; rt < RT; ++rt) lse[rt] = s_lse[rt * 16 + n];
+  float* mp = a.mpart + ((size_t)u.b * a.Hkv * a.RG + u.g * a.RG + u.rg) * a.n_cap;
+  if (a.mass) {
 #pragma unroll
-        for (int j = 0; j < kU; ++j) {
-          const int sp = s0 + j * P;
-          if (sp < nsp) {
-            s_fac[sp * ROWS + r_st] = v[j].x;
-            lse_combine(M, Z, v[j].x, v[j].y);
-          }
-        }
-      }
-      s_pm[part][r_st] = M;
-      s_pz[part][r_st] = Z;
-    }
-    lds_sync();
-    // 2. per row: global max, sum and lse; (M, 1/Z) kept in part slot 0
-    if (tid < ROWS) {
-      const int r = tid;
-      float Mr = s_pm[0][r], Zr = s_pz[0][r];
-#pragma unroll
-      for (int p = 1; p < P; ++p) lse_combine(Mr, Zr, s_pm[p][r], s_pz[p][r]);
-      const int row = row0 + r;
-      const bool ok = row < a.R && Zr > 0.f;
-      s_lse[r] = ok ? Mr + __log2f(Zr) : __builtin_huge_valf();
-      s_pm[0][r] = Mr;
-      s_pz[0][r] = ok ? 1.f / Zr : 0.f;
-    }
-    lds_sync();
-    // 3. rescale factor of every chunk partial: exp2(m_chunk - M) / Z
-    for (int e = tid; e < nsp * ROWS; e += kThreads) {
-      const int r = e % ROWS;
-      const float m = s_fac[e], invZ = s_pz[0][r];
-      s_fac[e] = invZ != 0.f && m != kNegInf ? fast_exp2(m - s_pm[0][r]) * invZ : 0.f;
-    }
-    lds_sync();
-    // 4. exact per-token mass of this chunk's tokens (resident scores)
-    float lse[RT];
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) lse[rt] = s_lse[rt * 16 + n];
-    float* mp = a.mpart + ((size_t)u.b * a.Hkv * a.RG + u.g * a.RG + u.rg) * a.n_cap;
-    if (a.mass) {
-#pragma unroll
-      for (int j = 0; j < kNB; ++j) {
-        const int tb = u.c0 + 32 * (w + kWaves * j);
-        if (tb < u.c1) mass_block<RT>(S[j], lse, mp, tb, u.c1, n, gq);
-      }
-    }
-    // 5. O slice
-    if (act) {
-      float acc[4] = {0.f, 0.f, 0.f, 0.f};
-      fma_parts(e_first, q, Q, pre, acc);
-      for (int s0 = q + Q * kU; s0 < nsp; s0 += Q * kU) {
-        uint64_t v[kU];
-        load_parts(e_first, s0, Q, v);
-        fma_parts(e_first, s0, Q, v, acc);
-      }
-      if (Q == 1)
-        emit(e_first, acc);
-      else
-        reinterpret_cast<float4*>(s_fac + ((nsp * ROWS + 3) & ~3))[q * cnt + el] =
-            make_float4(acc[0], acc[1], acc[2], acc[3]);
-    }
-    if (Q == 1) {
-      for (int e = e0 + tid + kThreads; e < e1; e += kThreads) {
-        float acc[4] = {0.f, 0.f, 0.f, 0.f};
-        for (int s0 = 0; s0 < nsp; s0 += kU) {
-          uint64_t v[kU];
-          load_parts(e, s0, 1, v);
-          fma_parts(e, s0, 1, v, acc);
-        }
-        emit(e, acc);
-      }
-    } else {
-      lds_sync();
-      if (tid < cnt) {
-        const float4* s_acc = reinterpret_cast<const float4*>(s_fac + ((nsp * ROWS + 3) & ~3));
-        float acc[4] = {0.f, 0.f, 0.f, 0.f};
-        for (int qq = 0; qq < Q; ++qq) {
-          const float4 v = s_acc[qq * cnt + tid];
-          acc[0] += v.x;
-          acc[1] += v.y;
-          acc[2] += v.z;
-          acc[3] += v.w;
-        }
-        emit(e0 + tid, acc);
-      }
-    }
-    if (a.lse && u.split == 0) {
-      for (int r = tid; r < rows; r += kThreads) {
-        const int row = row0 + r, t = row / a.G, h = u.g * a.G + row % a.G;
-        a.lse[((size_t)u.b * a.Hq + h) * a.T + t] = s_lse[r] * kLn2;
-      }
+    for (int j = 0; j < kNB; ++j) {
+      const int tb = u.c0 + 32 * (w + kWaves * j);
+      if (tb < u.c1) mass_block<RT>(S[j], lse, mp, tb, u.c1, n, gq);
     }
   }
-  mass_combine_and_finish(a, u, s_flag);
+  // O slice
+  if (act) {
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    fma_parts(e_first, q, Q, pre, acc);
+    for (int s0 = q + Q * kU; s0 < nsp; s0 += Q * kU) {
+      uint64_t v[kU];
+      load_parts(e_first, s0, Q, v);
+      fma_parts(e_first, s0, Q, v, acc);
+    }
+    if (Q == 1)
+      emit(e_first, acc);
+    else
+      reinterpret_cast<float4*>(s_fac + ((nsp * ROWS + 3) & ~3))[q * cnt + el] =
+          make_float4(acc[0], acc[1], acc[2], acc[3]);
+  }
+  if (Q == 1) {
+    for (int e = e0 + tid + kThreads; e < e1; e += kThreads) {
+      float acc[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int s0 = 0; s0 < nsp; s0 += kU) {
+        uint64_t v[kU];
+        load_parts(e, s0, 1, v);
+        fma_parts(e, s0, 1, v, acc);
+      }
+      emit(e, acc);
+    }
+  } else {
+    lds_sync();
+    if (tid < cnt) {
+      const float4* s_acc = reinterpret_cast<const float4*>(s_fac + ((nsp * ROWS + 3) & ~3));
+      float acc[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int qq = 0; qq < Q; ++qq) {
+        const float4 v = s_acc[qq * cnt + tid];
+        acc[0] += v.x;
+        acc[1] += v.y;
+        acc[2] += v.z;
+        acc[3] += v.w;
+      }
+      emit(e0 + tid, acc);
+    }
+  }
+  if (a.lse && u.split == 0) {
+    for (int r = tid; r < rows; r += kThreads) {
+      const int row = row0 + r, t = row / a.G, h = u.g * a.G + row % a.G;
+      a.lse[((size_t)u.b * a.Hq + h) * a.T + t] = s_lse[r] * kLn2;
+    }
+  }
+  mass_combine(a, u, s_flag);
 }
 
-template <int D, int RT, bool RESIDENT>
+// A chunk past this sequence's end: publish empty statistics, arrive at both
+// counters without waiting (advancing the base if last), join the mass sum.
+template <int ROWS, bool LOCAL>
+__device__ void empty_chunk(const VArgs& a, const Unit& u, const float* s_m, const float* s_z,
+                            unsigned base, int* s_flag) {
+  stats_store<ROWS, LOCAL>(a, u, s_m, s_z, base);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    grp_arrive(cnt_s(a, u));
+    __builtin_amdgcn_s_waitcnt(0);  // the statistics arrival lands before the O arrival
+    o_finish(a, u, base, grp_arrive(cnt_o(a, u)), false);
+  }
+  __syncthreads();
+  mass_combine(a, u, s_flag);
+}
+
+template <int D, int RT, bool RESIDENT, bool LOCAL>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 verify_mfma_kernel(VArgs a) {
   constexpr int ROWS = RT * 16;
@@ -831,6 +889,7 @@ verify_mfma_kernel(VArgs a) {
 
   Unit u;
   if (!decode_unit(a, u)) return;
+  const unsigned base = read_base(a, u);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n = lane & 15, gq = lane >> 4;
   if (u.c0 >= u.N) {  // chunk past this sequence's end: empty statistics, no wait
@@ -839,11 +898,7 @@ verify_mfma_kernel(VArgs a) {
       s_z[r] = 0.f;
     }
     __syncthreads();
-    exchange_stats<ROWS>(a, u, s_m, s_z, s_lse, false);
-    if constexpr (RESIDENT)
-      mass_combine_and_finish(a, u, &s_flag);
-    else
-      verify_epilogue<ROWS, D>(a, u, s_lse, true, &s_flag);
+    empty_chunk<ROWS, LOCAL>(a, u, s_m, s_z, base, &s_flag);
     return;
   }
   const size_t kv_off = ((size_t)u.b * a.Hkv + u.g) * a.n_cap * D;
@@ -896,6 +951,8 @@ verify_mfma_kernel(VArgs a) {
       }
     }
     reduce_stats<RT>(m, z, n, gq, w, s_wm, s_wz, s_m, s_z);
+    // publish the statistics (wave 0); the arrival follows at the V wait
+    stats_store<ROWS, LOCAL>(a, u, s_m, s_z, base);
     // ---- pass 2 (no wait on other workgroups): probabilities relative to
     //      this workgroup's row maxima, P.V on MFMA
     float ref[RT];
@@ -904,8 +961,9 @@ verify_mfma_kernel(VArgs a) {
       const float mm = s_m[rt * 16 + n];
       ref[rt] = mm == kNegInf ? __builtin_huge_valf() : mm;
     }
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's V loads have landed in LDS
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's V loads (wave 0: its statistics stores) are done
     __syncthreads();                // ... and every other wave's
+    if (threadIdx.x == 0) grp_arrive(cnt_s(a, u));
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
       const int blk = w + kWaves * j;
@@ -917,15 +975,12 @@ verify_mfma_kernel(VArgs a) {
       }
     }
     __syncthreads();  // V region of LDS is reused below
-    write_opart<D, RT>(a, u, O, s_o, lane, w, n, gq);
-    float* st = a.stats + ((size_t)u.grp * a.splits + u.split) * ROWS * 2;
-    if (threadIdx.x < 64)
-      for (int r = threadIdx.x; r < ROWS; r += 64) {
-        st_agent(st + 2 * r, s_m[r]);
-        st_agent(st + 2 * r + 1, s_z[r]);
-      }
-    __syncthreads();  // s_o is reused as the factor table
-    verify_epilogue_local<D, RT>(a, u, S, s_lse, s_o, s_wm, s_wz, false, &s_flag, n, gq, w);
+    write_opart<D, RT, LOCAL>(a, u, O, s_o, lane, w, n, gq);
+    __builtin_amdgcn_s_waitcnt(0);  // every wave's partial stores are complete
+    __syncthreads();                // (s_o is reused as the factor table)
+    unsigned old = 0;
+    if (threadIdx.x == 0) old = grp_arrive(cnt_o(a, u));
+    verify_epilogue_local<D, RT, LOCAL>(a, u, S, s_lse, s_o, s_wm, s_wz, &s_flag, n, gq, w, base, old);
     return;
   } else {
     // ---- pass 1: stream K, running statistics only
@@ -939,7 +994,7 @@ verify_mfma_kernel(VArgs a) {
       running_stats<RT>(S, m, z);
     }
     reduce_stats<RT>(m, z, n, gq, w, s_wm, s_wz, s_m, s_z);
-    exchange_stats<ROWS>(a, u, s_m, s_z, s_lse, true);
+    exchange_stats<ROWS, LOCAL>(a, u, s_m, s_z, s_lse, s_wm, s_wz, base, true);
     float lse[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) lse[rt] = s_lse[rt * 16 + n];
@@ -955,8 +1010,8 @@ verify_mfma_kernel(VArgs a) {
       pv_block<D, RT>(S, lse, Vr, O, mp, tb, u.c1, n, gq);
     }
   }
-  write_opart<D, RT>(a, u, O, s_o, lane, w, n, gq);
-  verify_epilogue<ROWS, D>(a, u, s_lse, false, &s_flag);
+  write_opart<D, RT, LOCAL>(a, u, O, s_o, lane, w, n, gq);
+  verify_epilogue<ROWS, D, LOCAL>(a, u, s_lse, false, &s_flag, base);
 }
 
 // ------------------------------------------------------------ fp32 path --
@@ -970,10 +1025,12 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
   float* sKV = sQ + ROWS * D;    // [TC][D]
   float* sS = sKV + TC * D;      // [ROWS][TC]
   __shared__ float s_m[ROWS], s_z[ROWS], s_lse[ROWS];
+  __shared__ float s_pm[kWaves][ROWS], s_pz[kWaves][ROWS];
   __shared__ int s_flag;
 
   Unit u;
   if (!decode_unit(a, u)) return;
+  const unsigned base = read_base(a, u);
   const int tid = threadIdx.x;
   for (int r = tid; r < ROWS; r += kThreads) {
     s_m[r] = kNegInf;
@@ -981,8 +1038,7 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
   }
   if (u.c0 >= u.N) {
     __syncthreads();
-    exchange_stats<ROWS>(a, u, s_m, s_z, s_lse, false);
-    verify_epilogue<ROWS, D>(a, u, s_lse, true, &s_flag);
+    empty_chunk<ROWS, false>(a, u, s_m, s_z, base, &s_flag);
     return;
   }
   const int row0 = u.rg * a.RT * 16;
@@ -1036,7 +1092,7 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
     }
   }
   __syncthreads();
-  exchange_stats<ROWS>(a, u, s_m, s_z, s_lse, true);
+  exchange_stats<ROWS, false>(a, u, s_m, s_z, s_lse, s_pm, s_pz, base, true);
 
   // ---- pass 2
   float O[OPT];
@@ -1069,7 +1125,7 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
   float* op = a.opart + ((size_t)u.grp * a.splits + u.split) * ROWS * D;
 #pragma unroll
   for (int k = 0; k < OPT; ++k) st_agent(op + tid + k * kThreads, O[k]);
-  verify_epilogue<ROWS, D>(a, u, s_lse, false, &s_flag);
+  verify_epilogue<ROWS, D, false>(a, u, s_lse, false, &s_flag, base);
 }
 
 // ------------------------------------------------------------------ host --
@@ -1079,16 +1135,21 @@ struct VPlan {
   int splits, chunk, groups, per_launch, grid;
   bool resident, mfma;
   int lds_dyn;
-  size_t off_cnt, off_cnt2, off_done, off_mcnt, off_stats, off_opart, off_mpart, bytes;
+  int xcds;
+  size_t off_cnt_s, off_mcnt, off_stats, off_opart, off_mpart, bytes;
 };
 
 typedef void (*VKernel)(VArgs);
 
-VKernel pick_kernel(int dt, int D, int RT, bool resident) {
+VKernel pick_kernel(int dt, int D, int RT, bool resident, bool local) {
 #define PVLM_VK(DD, R_)                                                                  \
   if (D == DD && RT == R_) {                                                            \
     if (dt == PVLM_F32) return verify_f32_kernel<DD, R_>;                               \
-    return resident ? verify_mfma_kernel<DD, R_, true> : verify_mfma_kernel<DD, R_, false>; \
+    if (local)                                                                          \
+      return resident ? verify_mfma_kernel<DD, R_, true, true>                           \
+                      : verify_mfma_kernel<DD, R_, false, true>;                         \
+    return resident ? verify_mfma_kernel<DD, R_, true, false>                            \
+                    : verify_mfma_kernel<DD, R_, false, false>;                          \
   }
   PVLM_VK(128, 1) PVLM_VK(128, 2) PVLM_VK(128, 3) PVLM_VK(128, 4) PVLM_VK(128, 5)
   PVLM_VK(64, 1) PVLM_VK(64, 2) PVLM_VK(64, 3) PVLM_VK(64, 4) PVLM_VK(64, 5)
@@ -1127,6 +1188,7 @@ pvlm_status plan_verify(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int
   pvlm_status st = device_info(&di);
   if (st != PVLM_OK) return st;
   const int W = di.cus;  // one workgroup per CU (registers / LDS bound)
+  p->xcds = di.xcds;
   p->per_launch = p->groups < W ? p->groups : W;
   int splits = W / p->per_launch;
   if (splits < 1) splits = 1;
@@ -1142,15 +1204,18 @@ pvlm_status plan_verify(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int
   p->grid = (p->per_launch * p->splits + 7) / 8 * 8;
   p->lds_dyn = lds_bytes(dt, D, p->RT, p->resident, p->splits);
   const int ROWS = p->RT * 16;
-  const size_t n_sync = 3 * (size_t)p->groups + (size_t)B * p->splits;
-  if (n_sync > (size_t)kSyncInts) return PVLM_ERR_UNSUPPORTED;
-  p->off_cnt = 0;
-  p->off_cnt2 = p->off_cnt + sizeof(int) * p->groups;
-  p->off_done = p->off_cnt2 + sizeof(int) * p->groups;
-  p->off_mcnt = p->off_done + sizeof(int) * p->groups;
+  // Monotonic group counters sit at fixed per-group slots (cnt_s, cnt_o, base
+  // of group g on lines 3g..3g+2 of the monotonic part), so calls of any shape
+  // keep every slot consistent; the mass-sum counters return to zero and live
+  // in the low part.
+  if (3 * kSyncLine * (size_t)p->groups > kSyncRegion - kSyncMonoOff) return PVLM_ERR_UNSUPPORTED;
+  if (kSyncLine * (size_t)B * p->splits > kSyncMonoOff) return PVLM_ERR_UNSUPPORTED;
+  p->off_cnt_s = kSyncMonoOff;
+  p->off_mcnt = 0;
   size_t off = kSyncRegion;
   p->off_stats = off;
-  off = align_up(off + sizeof(float) * (size_t)p->groups * p->splits * ROWS * 2, 256);
+  off = align_up(off + sizeof(float) * 2 * (size_t)p->groups * p->splits * ((ROWS + 1 + 15) / 16 * 16),
+                 256);
   p->off_opart = off;
   off = align_up(off + sizeof(float) * (size_t)p->groups * p->splits * ROWS * D, 256);
   p->off_mpart = off;
@@ -1193,9 +1258,7 @@ extern "C" pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int
   a.stats = reinterpret_cast<float*>(wsb + p.off_stats);
   a.opart = reinterpret_cast<float*>(wsb + p.off_opart);
   a.mpart = reinterpret_cast<float*>(wsb + p.off_mpart);
-  a.cnt = reinterpret_cast<int*>(wsb + p.off_cnt);
-  a.cnt2 = reinterpret_cast<int*>(wsb + p.off_cnt2);
-  a.done = reinterpret_cast<int*>(wsb + p.off_done);
+  a.slots = reinterpret_cast<unsigned*>(wsb + p.off_cnt_s);
   a.mcnt = reinterpret_cast<int*>(wsb + p.off_mcnt);
   a.out = out;
   a.lse = lse;
@@ -1217,13 +1280,18 @@ extern "C" pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int
   a.chunk = p.chunk;
   a.grid = p.grid;
   a.sl2 = scale * kLog2e;
-  VKernel kern = pick_kernel(dt, D, p.RT, p.resident);
-  if (!kern) return PVLM_ERR_UNSUPPORTED;
-  PVLM_HIP(allow_dynamic_lds(reinterpret_cast<const void*>(kern), p.lds_dyn));
+  if (!pick_kernel(dt, D, p.RT, p.resident, false)) return PVLM_ERR_UNSUPPORTED;
   for (int g0 = 0; g0 < p.groups; g0 += p.per_launch) {
     a.grp_base = g0;
     a.ngrp = p.groups - g0 < p.per_launch ? p.groups - g0 : p.per_launch;
     a.grid = (a.ngrp * p.splits + 7) / 8 * 8;
+    // XCD-aware placement: logical units i*per_xcd.. run on XCD i.  When each
+    // group's workgroups then share one XCD (and so one L2), the group's
+    // exchanges use plain loads and stores (fp32 path: always device-coherent).
+    a.xmap = p.xcds > 0 && a.grid % p.xcds == 0 ? p.xcds : 1;
+    a.local = p.mfma && p.xcds > 0 && a.xmap == p.xcds && (a.grid / a.xmap) % p.splits == 0;
+    VKernel kern = pick_kernel(dt, D, p.RT, p.resident, a.local != 0);
+    PVLM_HIP(allow_dynamic_lds(reinterpret_cast<const void*>(kern), p.lds_dyn));
     void* args[] = {&a};
     PVLM_HIP(launch_coresident(reinterpret_cast<const void*>(kern), dim3(a.grid), dim3(kThreads),
                                args, p.lds_dyn, stream));

@@ -95,7 +95,7 @@ def test_greedy_matches_target_argmax_chain():
 
 def test_workspace_reused_across_shapes():
     """One workspace serves calls of different shapes in sequence (the
-    synchronisation counters live in a fixed region every call leaves zeroed)."""
+    synchronisation counters live in a fixed region every call leaves consistent)."""
     ws = pv.Workspace(torch.device("cuda", 0))
     cases = [W.make_accept_inputs(W.WORKLOADS["tiny"], batch=64, salt=5),
              W.make_accept_inputs(W.WORKLOADS["llava72b"], salt=7),

@@ -126,3 +126,35 @@ def test_workspace_reused_across_shapes():
                                         f64(inp.v, "bf16"), inp.ctx_len, inp.scale)
         assert_out(to_host_f64(out), ro)
         assert_mass(to_host_f64(mass), rm, Hq, T)
+
+
+def test_one_workspace_across_call_kinds():
+    """One zero-filled workspace serves verify and accept calls in any order:
+    verify's monotonic group counters (same-XCD and cross-XCD exchange
+    launches alike) and accept's counters that return to zero share its
+    synchronisation region without disturbing each other."""
+    ws = pv.Workspace(torch.device("cuda", 0))
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    acc = W.make_accept_inputs(W.WORKLOADS["tiny"], batch=8, salt=11)
+    rn, ry, rt = oracle.spec_accept(acc.draft_logits, acc.target_logits, acc.draft_tokens,
+                                    acc.u_accept, acc.u_sample, acc.temperature)
+    shapes = [(1, 9, 64, 8, 128, [1111]), (1, 6, 28, 4, 128, [700]), (1, 9, 64, 8, 128, [1111]),
+              (2, 5, 8, 2, 128, [300, 517]), (1, 6, 28, 4, 128, [700])]
+    for i, (B, T, Hq, Hkv, D, ctx) in enumerate(shapes):
+        inp = W.random_verify_inputs(B, T, Hq, Hkv, D, ctx, "bf16", seed=40 + i)
+        note(f"mixed workspace: verify {inp.q.shape} ctx={ctx}, then accept")
+        out, mass, lse = pv.verify_attn(to_dev(inp.q), to_dev(inp.k), to_dev(inp.v),
+                                        to_dev(inp.ctx_len), ws=ws, status=status)
+        n, y, tie = pv.spec_accept(to_dev(acc.draft_logits), to_dev(acc.target_logits),
+                                   to_dev(acc.draft_tokens), to_dev(acc.u_accept),
+                                   to_dev(acc.u_sample), acc.temperature, ws=ws, status=status)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0
+        ro, rl, rm = oracle.verify_attn(f64(inp.q, "bf16"), f64(inp.k, "bf16"),
+                                        f64(inp.v, "bf16"), inp.ctx_len, inp.scale)
+        assert_out(to_host_f64(out), ro)
+        assert_lse(to_host_f64(lse), rl)
+        assert_mass(to_host_f64(mass), rm, Hq, T)
+        ok = rt == 0
+        assert np.array_equal(n.cpu().numpy()[ok], rn[ok])
+        assert np.array_equal(y.cpu().numpy()[ok], ry[ok])
