@@ -538,6 +538,30 @@ __device__ __forceinline__ void running_stats(const float (&S)[2][RT][4], float 
   }
 }
 
+// Reduce a per-lane value of each row over the four lane groups (max or sum)
+// and the four waves into s_out[row] (scaled by `scale`); LDS barriers only.
+template <int RT, bool MAX>
+__device__ __forceinline__ void reduce_rows(float (&v)[RT], int n, int gq, int w, float (*s_w)[RT * 16],
+                                            float* s_out, float scale) {
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+    for (int off = 16; off <= 32; off <<= 1) {
+      const float o = __shfl_xor(v[rt], off, 64);
+      v[rt] = MAX ? fmaxf(v[rt], o) : v[rt] + o;
+    }
+    if (gq == 0) s_w[w][rt * 16 + n] = v[rt];
+  }
+  lds_sync();
+  for (int r = threadIdx.x; r < RT * 16; r += kThreads) {
+    float acc = s_w[0][r];
+#pragma unroll
+    for (int ww = 1; ww < kWaves; ++ww) acc = MAX ? fmaxf(acc, s_w[ww][r]) : acc + s_w[ww][r];
+    s_out[r] = acc == kNegInf ? kNegInf : acc * scale;
+  }
+  lds_sync();
+}
+
 // Reduce the per-lane (m, z) of each row over the four lane groups and the
 // four waves into s_m / s_z.
 template <int RT>
@@ -591,21 +615,10 @@ __device__ __forceinline__ void pv_local(const float (&S)[2][RT][4], const float
   }
 }
 
-// Exact probabilities exp2(S - lse2) of one block summed over its rows: the
-// workgroup's share of the per-token attention mass, written to mp.
-template <int RT>
-__device__ __forceinline__ void mass_block(const float (&S)[2][RT][4], const float (&lse)[RT],
-                                           float* mp, int tb, int c1, int n, int gq) {
-  float pm[8];
-#pragma unroll
-  for (int v = 0; v < 8; ++v) pm[v] = 0.f;
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) pm[4 * tt + i] += fast_exp2(S[tt][rt][i] - lse[rt]);
-  // sum the 8 token values over the 16 lanes of a lane group
+// Sum each lane's 8 token values over the 16 lanes (rows) of its lane group
+// and store the per-token sums (lanes with even n hold one token each).
+__device__ __forceinline__ void mass_reduce_store(const float (&pm)[8], float* mp, int tb, int c1, int n,
+                                                  int gq) {
   const bool h8 = n & 8, h4 = n & 4, h2 = n & 2;
   float a8[4];
 #pragma unroll
@@ -626,6 +639,144 @@ __device__ __forceinline__ void mass_block(const float (&S)[2][RT][4], const flo
   const int tok = tb + 16 * (v >> 2) + 4 * gq + (v & 3);
   if (!(n & 1) && tok < c1) st_agent(mp + tok, a2);
 }
+
+// ---- resident variant: the raw score accumulators stay exactly as the MFMA
+// produced them (unscaled, unmasked), which lets the compiler keep them in
+// accumulation registers; the scale and the causal / chunk-end mask are
+// applied where the scores are used.  vis[rt] is the last token visible to
+// the lane's row of tile rt (-1 for padding rows); element (tt, i) of a block
+// starting at token tb is token tb + 16 tt + 4 gq + i.
+// The workgroup's Q tile in LDS for the resident variant: ROWS rows of D/8
+// 16-byte chunks, chunk c of row r stored at position c ^ (r mod D/8) of the
+// row (an XOR swizzle: the 16 rows a B-operand read touches then fall on
+// distinct banks).  It is loaded straight into LDS (global_load_lds, no
+// registers), one 64-chunk run per instruction; padding rows repeat the last
+// real row (their scores are masked).
+template <int D, int RT>
+__device__ __forceinline__ void issue_q_lds(const VArgs& a, const Unit& u, uint16_t* s_q, int w,
+                                            int lane) {
+  constexpr int CH = D / 8;
+  constexpr int NI = RT * 16 * CH / 64;  // instructions per workgroup
+  const uint16_t* q = static_cast<const uint16_t*>(a.q);
+#pragma unroll
+  for (int k = 0; k < (NI + kWaves - 1) / kWaves; ++k) {
+    const int ins = w + kWaves * k;
+    if (ins < NI) {
+      const int slot = ins * 64 + lane, r = slot / CH, c = (slot % CH) ^ (r % CH);
+      const int row = min(u.rg * a.RT * 16 + r, a.R - 1);
+      const int t = row / a.G, h = u.g * a.G + row % a.G;
+      const uint16_t* src = q + (((size_t)u.b * a.T + t) * a.Hq + h) * D + 8 * c;
+      const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
+          reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint16_t*)(s_q + ins * 64 * 8))));
+      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+                   :
+                   : "s"(lds), "v"(src)
+                   : "memory", "m0");
+    }
+  }
+}
+
+template <int D, int RT>
+__device__ __forceinline__ bf16x8 q_operand(const uint16_t* s_q, int rt, int ks, int n, int gq) {
+  constexpr int CH = D / 8;
+  const int r = rt * 16 + n, c = 4 * ks + gq;
+  return __builtin_bit_cast(
+      bf16x8, *reinterpret_cast<const uint4*>(s_q + (r * CH + (c ^ (r % CH))) * 8));
+}
+
+template <int D, int RT>
+__device__ __forceinline__ void scores_raw(const uint4 (&Kr)[2][D / 32], const uint16_t* s_q, int n,
+                                           int gq, floatx4 (&S)[2][RT]) {
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt) {
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) S[tt][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      const bf16x8 kk = __builtin_bit_cast(bf16x8, Kr[tt][ks]);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+        S[tt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, q_operand<D, RT>(s_q, rt, ks, n, gq),
+                                                            S[tt][rt], 0, 0, 0);
+    }
+  }
+}
+
+// Per-lane maximum of the visible raw scores of one block, per row tile.
+template <int RT>
+__device__ __forceinline__ void block_max_raw(const floatx4 (&S)[2][RT], const int (&vis)[RT], int tb,
+                                              int gq, float (&mx)[RT]) {
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    const int off = vis[rt] - tb - 4 * gq;  // element (tt, i) visible iff 16 tt + i <= off
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mx[rt] = fmaxf(mx[rt], 16 * tt + i <= off ? S[tt][rt][i] : kNegInf);
+  }
+}
+
+// Raw scores -> probabilities relative to the workgroup's row maxima,
+// P = exp2(scale * s - ref) (0 where masked), in place; per-lane row sums.
+template <int RT>
+__device__ __forceinline__ void block_probs(floatx4 (&S)[2][RT], const int (&vis)[RT], int tb, int gq,
+                                            float sl2, const float (&ref)[RT], float (&z)[RT]) {
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    const int off = vis[rt] - tb - 4 * gq;
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = 16 * tt + i <= off ? fast_exp2(fmaf(S[tt][rt][i], sl2, -ref[rt])) : 0.f;
+        S[tt][rt][i] = p;
+        z[rt] += p;
+      }
+  }
+}
+
+// O += P.V of one block (P resident, converted to bf16 for the MFMA).
+template <int D, int RT>
+__device__ __forceinline__ void pv_resident(const floatx4 (&P)[2][RT], const typename VVec<D>::T (&Vr)[8],
+                                            floatx4 (&O)[RT][D / 16]) {
+  constexpr int DPL = D / 16;
+  bf16x8 Pa[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) Pa[rt][4 * tt + i] = static_cast<__bf16>(P[tt][rt][i]);
+#pragma unroll
+  for (int jd = 0; jd < DPL; ++jd) {
+    const bf16x8 vb = pack_v(Vr, jd);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+      O[rt][jd] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Pa[rt], vb, O[rt][jd], 0, 0, 0);
+  }
+}
+
+// Exact probabilities of one block summed over its rows (the workgroup's
+// share of the per-token mass), written to mp: the resident P relative to
+// the workgroup's row maximum times c = exp2(ref - lse) per row.
+template <int RT>
+__device__ __forceinline__ void mass_block_resident(const floatx4 (&P)[2][RT], const float (&c)[RT],
+                                                    float* mp, int tb, int c1, int n, int gq) {
+  float pm[8];
+#pragma unroll
+  for (int v = 0; v < 8; ++v) pm[v] = 0.f;
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pm[4 * tt + i] = fmaf(P[tt][rt][i], c[rt], pm[4 * tt + i]);
+  mass_reduce_store(pm, mp, tb, c1, n, gq);
+}
+
+// Exact probabilities exp2(S - lse2) of one block summed over its rows: the
+// workgroup's share of the per-token attention mass, written to mp.
+
 
 // P = exp2(S - lse2): per-token mass (sum over the block's rows, written to
 // mp) and O += P.V on MFMA.
@@ -737,7 +888,8 @@ __device__ __forceinline__ void write_opart(const VArgs& a, const Unit& u, float
 // the exact per-token mass from the resident scores meanwhile, then the
 // factor-weighted O sum, lse, and the mass sum over KV heads.
 template <int D, int RT, bool LOCAL>
-__device__ void verify_epilogue_local(const VArgs& a, const Unit& u, const float (&S)[kNB][2][RT][4],
+__device__ void verify_epilogue_local(const VArgs& a, const Unit& u, const floatx4 (&P)[kNB][2][RT],
+                                      const float (&ref)[RT],
                                       float* s_lse, float* s_fac, float (*s_pm)[RT * 16],
                                       float (*s_pz)[RT * 16], int* s_flag, int n, int gq, int w,
                                       unsigned base, unsigned old) {
@@ -797,16 +949,17 @@ __device__ void verify_epilogue_local(const VArgs& a, const Unit& u, const float
   uint64_t pre[kU];
   load_parts(e_first, q, Q, pre);
   __builtin_amdgcn_sched_barrier(0);
-  // exact per-token mass of this chunk's tokens (resident scores)
-  float lse[RT];
+  // exact per-token mass of this chunk's tokens: resident P times
+  // exp2(ref - lse) per row (0 for padding rows, whose lse is +inf)
+  float c[RT];
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) lse[rt] = s_lse[rt * 16 + n];
+  for (int rt = 0; rt < RT; ++rt) c[rt] = fast_exp2(ref[rt] - s_lse[rt * 16 + n]);
   float* mp = a.mpart + ((size_t)u.b * a.Hkv * a.RG + u.g * a.RG + u.rg) * a.n_cap;
   if (a.mass) {
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
       const int tb = u.c0 + 32 * (w + kWaves * j);
-      if (tb < u.c1) mass_block<RT>(S[j], lse, mp, tb, u.c1, n, gq);
+      if (tb < u.c1) mass_block_resident<RT>(P[j], c, mp, tb, u.c1, n, gq);
     }
   }
   // O slice
@@ -906,8 +1059,6 @@ verify_mfma_kernel(VArgs a) {
   const uint16_t* vg = static_cast<const uint16_t*>(a.v) + kv_off;
   float* mp = a.mpart + ((size_t)u.b * a.Hkv * a.RG + u.g * a.RG + u.rg) * a.n_cap;
 
-  bf16x8 Qb[RT][KS];
-  load_q<D, RT>(a, u, n, gq, Qb);
   float m[RT], z[RT];
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
@@ -915,29 +1066,42 @@ verify_mfma_kernel(VArgs a) {
     z[rt] = 0.f;
   }
   floatx4 O[RT][DPL];
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-    for (int jd = 0; jd < DPL; ++jd) O[rt][jd] = floatx4{0.f, 0.f, 0.f, 0.f};
-
   if constexpr (RESIDENT) {
     // ---- pass 1: all K blocks of this wave in flight (registers), then the
     //      whole chunk's V streamed into LDS by waves 1-3 (wave 0 keeps no
     //      loads in flight so it can publish the statistics without waiting
     //      for them); scores kept resident.
     uint16_t* s_v = reinterpret_cast<uint16_t*>(s_o);
-    float S[kNB][2][RT][4];
+    uint16_t* s_q = s_v + kResTokens * D;  // after the V region
+    floatx4 S[kNB][2][RT];
     uint4 Kr[kNB][2][KS];
-    // issue order: Q, K block 0, 1, ... (the scheduler would otherwise reorder
-    // the loads), then the chunk's V into LDS from waves 1-3, so HBM streams
-    // K and V back to back; wave 0 keeps only K/Q in flight so it can publish
-    // the statistics without waiting for V.
+    int vis[RT];  // last token visible to this lane's row of each tile (-1: padding row)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int row = u.rg * a.RT * 16 + rt * 16 + n;
+      vis[rt] = row < a.R ? min(u.c1 - 1, u.ctx + row / a.G) : -1;
+    }
+    // issue order: Q (into LDS), K block 0, 1, ... (the scheduler would
+    // otherwise reorder the loads), then, once Q has landed, the chunk's V
+    // into LDS from waves 1-3, so HBM streams K and V back to back; wave 0
+    // keeps only K in flight so it can publish the statistics without waiting
+    // for V.
+    issue_q_lds<D, RT>(a, u, s_q, w, lane);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
       load_k_block<D>(kg, u.c0 + 32 * (w + kWaves * j), u.c1, n, gq, Kr[j]);
       __builtin_amdgcn_sched_barrier(0);
     }
+    // this wave's Q chunks have landed once at most the 8 * KS K loads issued
+    // after them are outstanding; then every wave's (barrier), then V behind K
+    static_assert(kNB * 2 * KS == 32 || kNB * 2 * KS == 16, "the wait below counts the K loads");
+    if constexpr (kNB * 2 * KS == 32)
+      asm volatile("s_waitcnt vmcnt(32)" ::: "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+    lds_sync();
+    __builtin_amdgcn_sched_barrier(0);
     const int nblk = (u.c1 - u.c0 + 31) / 32;
     if (w > 0)
       for (int blk = w - 1; blk < nblk; blk += kWaves - 1)
@@ -946,24 +1110,35 @@ verify_mfma_kernel(VArgs a) {
     for (int j = 0; j < kNB; ++j) {
       const int tb = u.c0 + 32 * (w + kWaves * j);
       if (tb < u.c1) {
-        scores_block<D, RT>(a, u, Kr[j], Qb, tb, n, gq, S[j]);
-        running_stats<RT>(S[j], m, z);
+        scores_raw<D, RT>(Kr[j], s_q, n, gq, S[j]);
+        block_max_raw<RT>(S[j], vis, tb, gq, m);
       }
     }
-    reduce_stats<RT>(m, z, n, gq, w, s_wm, s_wz, s_m, s_z);
-    // publish the statistics (wave 0); the arrival follows at the V wait
-    stats_store<ROWS, LOCAL>(a, u, s_m, s_z, base);
-    // ---- pass 2 (no wait on other workgroups): probabilities relative to
-    //      this workgroup's row maxima, P.V on MFMA
+    // the workgroup's row maxima (log2 domain), then the resident scores
+    // become probabilities relative to them, one exp2 per score
+    reduce_rows<RT, true>(m, n, gq, w, s_wm, s_m, a.sl2);
     float ref[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       const float mm = s_m[rt * 16 + n];
-      ref[rt] = mm == kNegInf ? __builtin_huge_valf() : mm;
+      ref[rt] = mm == kNegInf ? 0.f : mm;  // rows with no visible token: P = 0 anyway
     }
+#pragma unroll
+    for (int j = 0; j < kNB; ++j) {
+      const int tb = u.c0 + 32 * (w + kWaves * j);
+      if (tb < u.c1) block_probs<RT>(S[j], vis, tb, gq, a.sl2, ref, z);
+    }
+    reduce_rows<RT, false>(z, n, gq, w, s_wz, s_z, 1.f);
+    // publish the statistics (wave 0); the arrival follows at the V wait
+    stats_store<ROWS, LOCAL>(a, u, s_m, s_z, base);
+    // ---- pass 2 (no wait on other workgroups): P.V on MFMA
     __builtin_amdgcn_s_waitcnt(0);  // this wave's V loads (wave 0: its statistics stores) are done
     __syncthreads();                // ... and every other wave's
     if (threadIdx.x == 0) grp_arrive(cnt_s(a, u));
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int jd = 0; jd < DPL; ++jd) O[rt][jd] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
       const int blk = w + kWaves * j;
@@ -971,7 +1146,7 @@ verify_mfma_kernel(VArgs a) {
       if (tb < u.c1) {
         VT Vr[8];
         read_v_lds<D>(s_v + blk * 32 * D, n, gq, Vr);
-        pv_local<D, RT>(S[j], ref, Vr, O);
+        pv_resident<D, RT>(S[j], Vr, O);
       }
     }
     __syncthreads();  // V region of LDS is reused below
@@ -980,9 +1155,16 @@ verify_mfma_kernel(VArgs a) {
     __syncthreads();                // (s_o is reused as the factor table)
     unsigned old = 0;
     if (threadIdx.x == 0) old = grp_arrive(cnt_o(a, u));
-    verify_epilogue_local<D, RT, LOCAL>(a, u, S, s_lse, s_o, s_wm, s_wz, &s_flag, n, gq, w, base, old);
+    verify_epilogue_local<D, RT, LOCAL>(a, u, S, ref, s_lse, s_o, s_wm, s_wz, &s_flag, n, gq, w, base,
+                                        old);
     return;
   } else {
+    bf16x8 Qb[RT][KS];
+    load_q<D, RT>(a, u, n, gq, Qb);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int jd = 0; jd < DPL; ++jd) O[rt][jd] = floatx4{0.f, 0.f, 0.f, 0.f};
     // ---- pass 1: stream K, running statistics only
     const int nblk = (u.c1 - u.c0 + 31) / 32;
     for (int blk = w; blk < nblk; blk += kWaves) {
@@ -1161,7 +1343,8 @@ int lds_bytes(int dt, int D, int RT, bool resident, int splits) {
   if (dt == PVLM_F32) return (RT * 16 * D + kF32Tile * D + RT * 16 * kF32Tile) * 4;
   int b = 3 * RT * 16 * D * 4;                                   // O partial reduce-scatter
   if (resident) {
-    b = b > kResTokens * D * 2 ? b : kResTokens * D * 2;         // the chunk's V (bf16)
+    const int vq = kResTokens * D * 2 + RT * 16 * D * 2;          // the chunk's V, then Q (bf16)
+    b = b > vq ? b : vq;
     // rescale factors, then the O-sum partials (at most 256 float4)
     const int f = (splits * RT * 16 + 3) / 4 * 16 + kThreads * 16;
     b = b > f ? b : f;
