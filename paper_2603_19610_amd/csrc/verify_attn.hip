@@ -1038,7 +1038,7 @@ verify_mfma_kernel(VArgs a) {
   __shared__ float s_wm[kWaves][ROWS], s_wz[kWaves][ROWS];
   __shared__ float s_m[ROWS], s_z[ROWS], s_lse[ROWS];
   __shared__ int s_flag;
-  extern __shared__ float s_o[];
+  extern __shared__ __align__(256) float s_o[];  // 16-byte LDS accesses need 16-byte alignment
 
   Unit u;
   if (!decode_unit(a, u)) return;
@@ -1202,7 +1202,7 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
   constexpr int ROWS = RT * 16;
   constexpr int TC = kF32Tile;
   constexpr int OPT = ROWS * D / kThreads;
-  extern __shared__ float sm[];
+  extern __shared__ __align__(256) float sm[];
   float* sQ = sm;                // [ROWS][D]
   float* sKV = sQ + ROWS * D;    // [TC][D]
   float* sS = sKV + TC * D;      // [ROWS][TC]
