@@ -223,6 +223,41 @@ __device__ __forceinline__ uint64_t x_load(const uint64_t* p) {
   else return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Cross-lane exchanges that stay in the VALU (no LDS crossbar round trip):
+// DPP row operations and the gfx950 permlane swaps.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf,
+                                                               0xf, false));
+}
+__device__ __forceinline__ float lane_xor1(float x) { return dpp_mov<0xB1>(x); }   // quad_perm 1,0,3,2
+__device__ __forceinline__ float lane_xor2(float x) { return dpp_mov<0x4E>(x); }   // quad_perm 2,3,0,1
+__device__ __forceinline__ float lane_xor8(float x) { return dpp_mov<0x128>(x); }  // row_ror:8
+// lane i of every 8 receives lane 7 - i (row_half_mirror): partners differ in bit 2
+__device__ __forceinline__ float lane_mirror8(float x) { return dpp_mov<0x141>(x); }
+// Sum / max over the four lanes l, l^16, l^32, l^48 (every lane gets the result).
+__device__ __forceinline__ float rows4_sum(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);  // lower row + upper row
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);            // lower half + upper half
+}
+__device__ __forceinline__ float rows4_max(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+// The value of lane l ^ 16 and of lane l ^ 32.
+__device__ __forceinline__ float lane_xor16(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float((threadIdx.x & 16) ? a[0] : a[1]);
+}
+__device__ __forceinline__ float lane_xor32(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float((threadIdx.x & 32) ? a[0] : a[1]);
+}
+
 __device__ __forceinline__ void reset_counter(int* counter) {
   __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }

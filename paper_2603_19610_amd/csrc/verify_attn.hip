@@ -545,11 +545,7 @@ __device__ __forceinline__ void reduce_rows(float (&v)[RT], int n, int gq, int w
                                             float* s_out, float scale) {
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
-#pragma unroll
-    for (int off = 16; off <= 32; off <<= 1) {
-      const float o = __shfl_xor(v[rt], off, 64);
-      v[rt] = MAX ? fmaxf(v[rt], o) : v[rt] + o;
-    }
+    v[rt] = MAX ? rows4_max(v[rt]) : rows4_sum(v[rt]);
     if (gq == 0) s_w[w][rt * 16 + n] = v[rt];
   }
   lds_sync();
@@ -572,8 +568,8 @@ __device__ __forceinline__ void reduce_stats(float (&m)[RT], float (&z)[RT], int
   for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
     for (int off = 16; off <= 32; off <<= 1) {
-      const float m2 = __shfl_xor(m[rt], off, 64);
-      const float z2 = __shfl_xor(z[rt], off, 64);
+      const float m2 = off == 16 ? lane_xor16(m[rt]) : lane_xor32(m[rt]);
+      const float z2 = off == 16 ? lane_xor16(z[rt]) : lane_xor32(z[rt]);
       lse_combine(m[rt], z[rt], m2, z2);
     }
     if (gq == 0) {
@@ -619,22 +615,25 @@ __device__ __forceinline__ void pv_local(const float (&S)[2][RT][4], const float
 // and store the per-token sums (lanes with even n hold one token each).
 __device__ __forceinline__ void mass_reduce_store(const float (&pm)[8], float* mp, int tb, int c1, int n,
                                                   int gq) {
+  // transpose-reduce: each step a lane keeps half of its values (chosen by
+  // one bit of n) and adds the partner's copy of that half; partners differ
+  // in that bit (n^8, then n^7 within each 8, n^2, n^1)
   const bool h8 = n & 8, h4 = n & 4, h2 = n & 2;
   float a8[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const float send = h8 ? pm[k] : pm[4 + k];
-    a8[k] = (h8 ? pm[4 + k] : pm[k]) + __shfl_xor(send, 8, 64);
+    a8[k] = (h8 ? pm[4 + k] : pm[k]) + lane_xor8(send);
   }
   float a4[2];
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     const float send = h4 ? a8[k] : a8[2 + k];
-    a4[k] = (h4 ? a8[2 + k] : a8[k]) + __shfl_xor(send, 4, 64);
+    a4[k] = (h4 ? a8[2 + k] : a8[k]) + lane_mirror8(send);
   }
   const float send2 = h2 ? a4[0] : a4[1];
-  float a2 = (h2 ? a4[1] : a4[0]) + __shfl_xor(send2, 2, 64);
-  a2 += __shfl_xor(a2, 1, 64);
+  float a2 = (h2 ? a4[1] : a4[0]) + lane_xor2(send2);
+  a2 += lane_xor1(a2);
   const int v = (h8 ? 4 : 0) + (h4 ? 2 : 0) + (h2 ? 1 : 0);
   const int tok = tb + 16 * (v >> 2) + 4 * gq + (v & 3);
   if (!(n & 1) && tok < c1) st_agent(mp + tok, a2);
@@ -801,22 +800,25 @@ __device__ __forceinline__ void pv_block(const float (&S)[2][RT][4], const float
       }
   }
   // mass: sum the 8 token values over the 16 lanes of a lane group
+  // transpose-reduce: each step a lane keeps half of its values (chosen by
+  // one bit of n) and adds the partner's copy of that half; partners differ
+  // in that bit (n^8, then n^7 within each 8, n^2, n^1)
   const bool h8 = n & 8, h4 = n & 4, h2 = n & 2;
   float a8[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const float send = h8 ? pm[k] : pm[4 + k];
-    a8[k] = (h8 ? pm[4 + k] : pm[k]) + __shfl_xor(send, 8, 64);
+    a8[k] = (h8 ? pm[4 + k] : pm[k]) + lane_xor8(send);
   }
   float a4[2];
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     const float send = h4 ? a8[k] : a8[2 + k];
-    a4[k] = (h4 ? a8[2 + k] : a8[k]) + __shfl_xor(send, 4, 64);
+    a4[k] = (h4 ? a8[2 + k] : a8[k]) + lane_mirror8(send);
   }
   const float send2 = h2 ? a4[0] : a4[1];
-  float a2 = (h2 ? a4[1] : a4[0]) + __shfl_xor(send2, 2, 64);
-  a2 += __shfl_xor(a2, 1, 64);
+  float a2 = (h2 ? a4[1] : a4[0]) + lane_xor2(send2);
+  a2 += lane_xor1(a2);
   const int v = (h8 ? 4 : 0) + (h4 ? 2 : 0) + (h2 ? 1 : 0);
   const int tok = tb + 16 * (v >> 2) + 4 * gq + (v & 3);
   if (!(n & 1) && tok < c1) st_agent(mp + tok, a2);
