@@ -417,6 +417,25 @@ def tiles(w):
     return -(-rtt // rg)
 
 
+def verify_kernel_label(w, cus=256, xcds=8):
+    """The verify kernel variant the library's launch plan picks for this shape
+    (one workgroup per CU; resident scores for chunks of at most 512 tokens;
+    same-XCD exchange when every group's workgroups share an XCD)."""
+    rtt = -(-w.group * w.T // 16)
+    rg = -(-rtt // 5)
+    groups = w.batch * w.hkv * rg
+    per_launch = min(groups, cus)
+    splits = max(1, cus // per_launch)
+    n = int(w.lengths().max()) + w.T
+    chunk = -(-(-(-n // splits)) // 32) * 32
+    splits = -(-n // chunk)
+    grid = -(-per_launch * splits // 8) * 8
+    resident = chunk <= 512
+    local = grid % xcds == 0 and (grid // xcds) % splits == 0
+    return (f"verify_mfma_kernel<{w.head_dim},{tiles(w)},{'resident' if resident else 'stream'},"
+            f"{'same-XCD' if local else 'cross-XCD'}>")
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -583,7 +602,7 @@ def main():
         "stages_us": {k: round(v, 2) for k, v in stages.items()} if stages else None,
         "copy_gbs": {"same_bytes_as_verify": round(copy_same, 1), "2GiB": round(copy_big, 1)},
         "roofline": {
-            "bound": "hbm", "kernel": f"verify_mfma_kernel<{w.head_dim},{tiles(w)},resident>",
+            "bound": "hbm", "kernel": verify_kernel_label(w),
             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
