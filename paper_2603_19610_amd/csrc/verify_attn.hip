@@ -395,25 +395,6 @@ __device__ __forceinline__ bf16x8 pack_v(const VT (&vr)[8], int jd) {
   return __builtin_bit_cast(bf16x8, u);
 }
 
-// Q operand of every row tile (B side of S^T = K Q^T): lane (n, gq) holds
-// q[row][32*ks + 8*gq .. +8] of row 16*rt + n.  Padding rows load a real row
-// (their scores are masked), so the loads are unconditional.
-template <int D, int RT>
-__device__ __forceinline__ void load_q(const VArgs& a, const Unit& u, int n, int gq,
-                                       bf16x8 (&Qb)[RT][D / 32]) {
-  const uint16_t* q = static_cast<const uint16_t*>(a.q);
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    const int row = min(u.rg * a.RT * 16 + rt * 16 + n, a.R - 1);
-    const int t = row / a.G;
-    const int h = u.g * a.G + row % a.G;
-    const uint16_t* qp = q + (((size_t)u.b * a.T + t) * a.Hq + h) * D + 8 * gq;
-#pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks)
-      Qb[rt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(qp + 32 * ks));
-  }
-}
-
 // K operand of one 32-token block: lane (n, gq) loads token tb + 16*tt + n,
 // d in [32*ks + 8*gq, +8).  Tokens past the chunk load the chunk's last row
 // (their scores are masked), keeping the loads unconditional so the
@@ -489,32 +470,8 @@ __device__ __forceinline__ void read_v_lds(const uint16_t* lds_blk, int n, int g
 // past the causal limit of each verify row, and on padding rows.
 template <int D, int RT>
 __device__ __forceinline__ void scores_block(const VArgs& a, const Unit& u, const uint4 (&Kr)[2][D / 32],
-                                             const bf16x8 (&Qb)[RT][D / 32], int tb, int n, int gq,
-                                             float (&S)[2][RT][4]) {
-#pragma unroll
-  for (int tt = 0; tt < 2; ++tt) {
-    floatx4 acc[RT];
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) acc[rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) {
-      const bf16x8 kk = __builtin_bit_cast(bf16x8, Kr[tt][ks]);
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-        acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, Qb[rt][ks], acc[rt], 0, 0, 0);
-    }
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      const int row = u.rg * a.RT * 16 + rt * 16 + n;
-      const int lim = row < a.R ? min(u.c1 - 1, u.ctx + row / a.G) : -1;  // last visible token
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int tok = tb + 16 * tt + 4 * gq + i;
-        S[tt][rt][i] = tok <= lim ? acc[rt][i] * a.sl2 : kNegInf;
-      }
-    }
-  }
-}
+                                             const uint16_t* s_q, int tb, int n, int gq,
+                                             float (&S)[2][RT][4]);
 
 template <int RT>
 __device__ __forceinline__ void running_stats(const float (&S)[2][RT][4], float (&m)[RT], float (&z)[RT]) {
@@ -681,6 +638,39 @@ __device__ __forceinline__ bf16x8 q_operand(const uint16_t* s_q, int rt, int ks,
   const int r = rt * 16 + n, c = 4 * ks + gq;
   return __builtin_bit_cast(
       bf16x8, *reinterpret_cast<const uint4*>(s_q + (r * CH + (c ^ (r % CH))) * 8));
+}
+
+// Scaled (log2 domain), masked scores of one block for the stream variant
+// (Q operands from the LDS tile): -inf past the chunk, past the causal limit
+// of each verify row, and on padding rows.
+template <int D, int RT>
+__device__ __forceinline__ void scores_block(const VArgs& a, const Unit& u, const uint4 (&Kr)[2][D / 32],
+                                             const uint16_t* s_q, int tb, int n, int gq,
+                                             float (&S)[2][RT][4]) {
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt) {
+    floatx4 acc[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) acc[rt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      const bf16x8 kk = __builtin_bit_cast(bf16x8, Kr[tt][ks]);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+        acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, q_operand<D, RT>(s_q, rt, ks, n, gq), acc[rt],
+                                                          0, 0, 0);
+    }
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int row = u.rg * a.RT * 16 + rt * 16 + n;
+      const int lim = row < a.R ? min(u.c1 - 1, u.ctx + row / a.G) : -1;  // last visible token
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tok = tb + 16 * tt + 4 * gq + i;
+        S[tt][rt][i] = tok <= lim ? acc[rt][i] * a.sl2 : kNegInf;
+      }
+    }
+  }
 }
 
 template <int D, int RT>
@@ -1161,39 +1151,86 @@ verify_mfma_kernel(VArgs a) {
                                         old);
     return;
   } else {
-    bf16x8 Qb[RT][KS];
-    load_q<D, RT>(a, u, n, gq, Qb);
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-      for (int jd = 0; jd < DPL; ++jd) O[rt][jd] = floatx4{0.f, 0.f, 0.f, 0.f};
-    // ---- pass 1: stream K, running statistics only
+    // the Q tile in LDS (the region is reused for the O partials at the end)
+    uint16_t* s_q = reinterpret_cast<uint16_t*>(s_o);
+    issue_q_lds<D, RT>(a, u, s_q, w, lane);
+    __builtin_amdgcn_s_waitcnt(0);
+    lds_sync();
+    // ---- pass 1: stream K, running statistics only.  Software-pipelined:
+    //      the loads of the wave's next two blocks are in flight while the
+    //      current two are scored (loads past the chunk are clamped, their
+    //      scores masked, so every load is unconditional).
     const int nblk = (u.c1 - u.c0 + 31) / 32;
-    for (int blk = w; blk < nblk; blk += kWaves) {
-      const int tb = u.c0 + 32 * blk;
-      uint4 Kr[2][KS];
-      load_k_block<D>(kg, tb, u.c1, n, gq, Kr);
-      float S[2][RT][4];
-      scores_block<D, RT>(a, u, Kr, Qb, tb, n, gq, S);
-      running_stats<RT>(S, m, z);
+    auto score_pair = [&](const uint4 (&K2)[2][2][KS], int blk0) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int blk = blk0 + h * kWaves;
+        if (blk < nblk) {
+          float S[2][RT][4];
+          scores_block<D, RT>(a, u, K2[h], s_q, u.c0 + 32 * blk, n, gq, S);
+          running_stats<RT>(S, m, z);
+        }
+      }
+    };
+    auto load_pair = [&](uint4 (&K2)[2][2][KS], int blk0) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) load_k_block<D>(kg, u.c0 + 32 * (blk0 + h * kWaves), u.c1, n, gq, K2[h]);
+    };
+    {
+      uint4 Ka[2][2][KS], Kb[2][2][KS];
+      load_pair(Ka, w);
+      for (int blk = w; blk < nblk; blk += 4 * kWaves) {
+        load_pair(Kb, blk + 2 * kWaves);
+        score_pair(Ka, blk);
+        if (blk + 2 * kWaves >= nblk) break;
+        load_pair(Ka, blk + 4 * kWaves);
+        score_pair(Kb, blk + 2 * kWaves);
+      }
     }
     reduce_stats<RT>(m, z, n, gq, w, s_wm, s_wz, s_m, s_z);
     exchange_stats<ROWS, LOCAL>(a, u, s_m, s_z, s_lse, s_wm, s_wz, base, true);
     float lse[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) lse[rt] = s_lse[rt * 16 + n];
-    // ---- pass 2: recompute scores from K, then P, mass and P.V
-    for (int blk = w; blk < nblk; blk += kWaves) {
+    // ---- pass 2: recompute scores from K, then P, mass and P.V.  Up to 3
+    //      row tiles the next block's K and V load during this one; with more
+    //      the O accumulators leave no registers for a second block.
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int jd = 0; jd < DPL; ++jd) O[rt][jd] = floatx4{0.f, 0.f, 0.f, 0.f};
+    auto step = [&](const uint4 (&Kr)[2][KS], const VT (&Vr)[8], int blk) {
       const int tb = u.c0 + 32 * blk;
-      uint4 Kr[2][KS];
-      load_k_block<D>(kg, tb, u.c1, n, gq, Kr);
-      VT Vr[8];
-      load_v_block<D>(vg, tb, u.c1, n, gq, Vr);
       float S[2][RT][4];
-      scores_block<D, RT>(a, u, Kr, Qb, tb, n, gq, S);
+      scores_block<D, RT>(a, u, Kr, s_q, tb, n, gq, S);
       pv_block<D, RT>(S, lse, Vr, O, mp, tb, u.c1, n, gq);
+    };
+    if constexpr (RT <= 3) {
+      uint4 Ka[2][KS], Kb[2][KS];
+      VT Va[8], Vb[8];
+      load_k_block<D>(kg, u.c0 + 32 * w, u.c1, n, gq, Ka);
+      load_v_block<D>(vg, u.c0 + 32 * w, u.c1, n, gq, Va);
+      for (int blk = w; blk < nblk; blk += 2 * kWaves) {
+        const int b2 = blk + kWaves;
+        load_k_block<D>(kg, u.c0 + 32 * b2, u.c1, n, gq, Kb);
+        load_v_block<D>(vg, u.c0 + 32 * b2, u.c1, n, gq, Vb);
+        step(Ka, Va, blk);
+        if (b2 >= nblk) break;
+        load_k_block<D>(kg, u.c0 + 32 * (b2 + kWaves), u.c1, n, gq, Ka);
+        load_v_block<D>(vg, u.c0 + 32 * (b2 + kWaves), u.c1, n, gq, Va);
+        step(Kb, Vb, b2);
+      }
+    } else {
+      for (int blk = w; blk < nblk; blk += kWaves) {
+        uint4 Kr[2][KS];
+        load_k_block<D>(kg, u.c0 + 32 * blk, u.c1, n, gq, Kr);
+        VT Vr[8];
+        load_v_block<D>(vg, u.c0 + 32 * blk, u.c1, n, gq, Vr);
+        step(Kr, Vr, blk);
+      }
     }
   }
+  lds_sync();  // every wave is done with the Q tile, whose LDS the partials reuse
   write_opart<D, RT, LOCAL>(a, u, O, s_o, lane, w, n, gq);
   verify_epilogue<ROWS, D, LOCAL>(a, u, s_lse, false, &s_flag, base);
 }
