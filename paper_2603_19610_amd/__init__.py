@@ -266,7 +266,7 @@ def uvprune_criterion_cossim(hv, ht, m, n_txt, *, out=None, ws=None, status=None
     return out
 
 
-def topk_select(score, m, k, k_cap: int, *, idx=None, status=None):
+def topk_select(score, m, k, k_cap: int, *, idx=None, ws=None, status=None):
     """Ascending kept indices [B][k_cap] (-1 padded)."""
     _need(score, "score", torch.float32)
     dev = score.device
@@ -276,8 +276,10 @@ def topk_select(score, m, k, k_cap: int, *, idx=None, status=None):
     if idx is None:
         idx = torch.empty((B, k_cap), dtype=torch.int32, device=dev)
     _need(idx, "idx", torch.int32, dev)
+    need = int(lib().pvlm_topk_workspace_size(B, m_cap))
+    wsb = (ws or _default_ws("topk")).get(need)
     st = lib().pvlm_topk_select(B, m_cap, _ptr(m), _ptr(k), int(k_cap), _ptr(score), _ptr(idx),
-                                None, 0, _ptr(status), _stream())
+                                _ptr(wsb), wsb.numel(), _ptr(status), _stream())
     _check(st, "pvlm_topk_select")
     return idx
 

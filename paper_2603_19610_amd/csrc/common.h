@@ -38,10 +38,12 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // the inter-workgroup waits, so a zero-filled workspace can be reused by calls
 // of any shape: their data areas (after the region) may overlap earlier data,
 // their counters never do.  Calls whose counters return to zero use the low
-// part of the region; verify's monotonic counters (each call leaves them
-// consistent, never reset) use the part from kSyncMonoOff on.
+// part of the region; monotonic counters (each call leaves them consistent,
+// never resets them) use the rest: verify's from kSyncMonoOff, top-k's from
+// kSyncTopkOff.
 constexpr size_t kSyncRegion = 1024 * 1024;
 constexpr size_t kSyncMonoOff = 256 * 1024;
+constexpr size_t kSyncTopkOff = 768 * 1024;
 // Counters that many workgroups update or poll get a 128-byte line each, so
 // the memory-side atomics and polls of different counters never contend.
 constexpr size_t kSyncLine = 128;

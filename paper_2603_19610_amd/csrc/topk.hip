@@ -4,19 +4,27 @@
 // Ranking: larger score first, lower index first among equal scores, -0.0
 // equal to +0.0, NaN below every number.  Each score maps to a 32-bit key
 // whose unsigned order is that ranking (ties aside); the K-th largest key is
-// found by an MSB-first radix select (four 8-bit digits, LDS histograms), and
-// one ordered pass then emits, in ascending index order, every index whose key
-// is above the threshold plus the lowest-indexed ones equal to it.
-// One 1024-thread workgroup per batch row; the whole selection is integer
-// work, so the result is bit-exact.
+// found by an MSB-first radix select (four 8-bit digits), and one ordered
+// pass then emits, in ascending index order, every index whose key is above
+// the threshold plus the lowest-indexed ones equal to it.  The whole
+// selection is integer work, so the result is bit-exact.
+//
+// Each batch row is split over NW workgroups (one launch, grid co-resident):
+// per digit, every workgroup histograms its slice in LDS and publishes it;
+// the last to arrive sums the NW histograms, picks the digit and publishes
+// it; the others wait for it.  The emission step exchanges per-slice counts
+// the same way so every workgroup knows where its slice's output starts.
 #include "common.h"
 
 namespace pvlm {
 namespace {
 
-constexpr int kTopkThreads = 1024;
+constexpr int kTopkThreads = 256;
 constexpr int kTopkWaves = kTopkThreads / 64;
-constexpr int kPerThread = 16;  // consecutive elements per thread in the ordered pass
+constexpr int kPerThread = 16;   // consecutive scores per thread (register slice, ordered pass)
+constexpr int kSlice = kTopkThreads * kPerThread;  // scores per workgroup unless B*NW would exceed the CUs
+constexpr int kBarriers = 5;     // four digits and the emission counts
+static_assert(kTopkThreads == 256, "one histogram bin per thread");
 
 __device__ __forceinline__ uint32_t rank_key(float f) {
   if (f != f) return 0u;                 // NaN: lowest
@@ -37,134 +45,290 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* s_warp, int* tot
   }
   if (lane == 63) s_warp[w] = x;
   __syncthreads();
-  if (w == 0) {
-    int t = lane < kTopkWaves ? s_warp[lane] : 0;
+  int before = 0;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(t, o, 64);
-      if (lane >= o) t += y;
-    }
-    if (lane < kTopkWaves) s_warp[lane] = t;  // inclusive over waves
-  }
-  __syncthreads();
-  const int before = w > 0 ? s_warp[w - 1] : 0;
-  *total = s_warp[kTopkWaves - 1];
+  for (int ww = 0; ww < kTopkWaves; ++ww) before += ww < w ? s_warp[ww] : 0;
+  int tot = 0;
+#pragma unroll
+  for (int ww = 0; ww < kTopkWaves; ++ww) tot += s_warp[ww];
+  *total = tot;
   __syncthreads();
   return before + x - v;
 }
 
-__global__ void __launch_bounds__(kTopkThreads) topk_kernel(const float* score, const int32_t* m,
-                                                            const int32_t* k, int64_t m_cap,
-                                                            int k_cap, int32_t* idx,
-                                                            int32_t* status) {
+struct TArgs {
+  const float* score;
+  const int32_t* m;
+  const int32_t* k;
+  int32_t* idx;
+  int32_t* status;
+  int* hist;       // [B][NW][256] per-slice digit histograms
+  int* res;        // [B][4]: digit, keys above the prefix range
+  int* cnt;        // [B][NW][2]: keys above the threshold, keys equal to it
+  int* arrive;     // [B] arrivals (128 B apart), back to zero after each call
+  unsigned* gen;   // [B] generation words (128 B apart), advanced per barrier
+  int64_t m_cap;
+  int k_cap, NW, slice;
+};
+
+constexpr int kLine = (int)(kSyncLine / sizeof(int));
+
+// Barrier `p` (0-based) of row b.  Thread 0 arrives; the launch's last arrival
+// runs `last` (with the whole workgroup) and then releases the others, which
+// wait for the generation word to reach g0 + p + 1.  Returns in every thread.
+template <typename F>
+__device__ __forceinline__ void row_barrier(const TArgs& a, int b, int p, unsigned g0, int* s_flag,
+                                            F last) {
+  __builtin_amdgcn_s_waitcnt(0);  // this workgroup's published data is visible
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int old = __hip_atomic_fetch_add(a.arrive + b * kLine, 1, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+    *s_flag = old == a.NW * (p + 1) - 1;
+  }
+  __syncthreads();
+  if (*s_flag) {
+    last();
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      if (p == kBarriers - 1)  // every workgroup has arrived for the last time
+        __hip_atomic_store(a.arrive + b * kLine, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(a.gen + b * kLine, g0 + (unsigned)p + 1u, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
+  } else if (threadIdx.x == 0) {
+    grp_poll(a.gen + b * kLine, g0 + (unsigned)p + 1u, a.status);
+  }
+  __syncthreads();
+}
+
+// REG: the slice (at most kTopkThreads * kPerThread scores) is read once into
+// registers, thread t holding the scores s0 + kPerThread*t + e; otherwise it
+// is read again from memory for every pass, in chunks of that size.
+template <bool REG>
+__global__ void __launch_bounds__(kTopkThreads) topk_kernel(TArgs a) {
+  constexpr int kChunk = kTopkThreads * kPerThread;
   __shared__ int hist[256];
   __shared__ int s_warp[kTopkWaves];
-  __shared__ int s_digit, s_above;
-  const int b = blockIdx.x;
+  __shared__ int s_flag, s_res[2];
+  const int b = blockIdx.x / a.NW, j = blockIdx.x % a.NW;
   const int tid = threadIdx.x;
-  const float* sc = score + (size_t)b * m_cap;
-  int32_t* out = idx + (size_t)b * k_cap;
+  const float* sc = a.score + (size_t)b * a.m_cap;
+  int32_t* out = a.idx + (size_t)b * a.k_cap;
+  // the generation at launch start, read before this workgroup first arrives
+  // (only thread 0 arrives and waits)
+  const unsigned g0 = tid == 0 ? grp_read(a.gen + b * kLine) : 0u;
 
-  int mb = m[b], kb = k[b];
+  int mb = a.m[b], kb = a.k[b];
   bool bad = false;
-  if (mb < 0 || mb > m_cap) {
+  if (mb < 0 || mb > a.m_cap) {
     bad = true;
-    mb = mb < 0 ? 0 : (int)m_cap;
+    mb = mb < 0 ? 0 : (int)a.m_cap;
   }
-  const int kmax = mb < k_cap ? mb : k_cap;
+  const int kmax = mb < a.k_cap ? mb : a.k_cap;
   if (kb < 0 || kb > kmax) {
     bad = true;
     kb = kb < 0 ? 0 : kmax;
   }
-  if (bad && tid == 0) dev_flag(status, PVLM_DEV_RANGE);
-  for (int r = kb + tid; r < k_cap; r += kTopkThreads) out[r] = -1;
-  if (kb == 0) return;
+  if (bad && j == 0 && tid == 0) dev_flag(a.status, PVLM_DEV_RANGE);
+  if (j == 0)
+    for (int r = kb + tid; r < a.k_cap; r += kTopkThreads) out[r] = -1;
+  const int s0 = min(mb, j * a.slice), s1 = min(mb, s0 + a.slice);
+  int* hrow = a.hist + (size_t)b * a.NW * 256;
 
-  // ---- radix select of the kb-th largest key
+  uint32_t kr[kPerThread];
+  if constexpr (REG) {
+    const int i0 = s0 + tid * kPerThread;
+#pragma unroll
+    for (int e = 0; e < kPerThread; ++e) kr[e] = i0 + e < s1 ? rank_key(sc[i0 + e]) : 0u;
+  }
+  // f(key) over this thread's scores of the slice
+  auto visit = [&](auto f) {
+    if constexpr (REG) {
+      const int nv = s1 - (s0 + tid * kPerThread);
+#pragma unroll
+      for (int e = 0; e < kPerThread; ++e)
+        if (e < nv) f(kr[e]);
+    } else {
+      for (int i = s0 + tid; i < s1; i += kTopkThreads) f(rank_key(sc[i]));
+    }
+  };
+
+  // ---- radix select of the kb-th largest key.  With kb == 0 nothing is
+  //      counted, but every barrier is still passed.
   uint32_t prefix = 0, mask = 0;
   int above = 0;  // keys strictly above the current prefix range
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
-    for (int i = tid; i < 256; i += kTopkThreads) hist[i] = 0;
+    hist[tid] = 0;
     __syncthreads();
-    for (int i = tid; i < mb; i += kTopkThreads) {
-      const uint32_t key = rank_key(sc[i]);
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255], 1);
-    }
+    if (kb > 0)
+      visit([&](uint32_t key) {
+        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255], 1);
+      });
     __syncthreads();
-    if (tid < 64) {
-      // lane l owns digits 255-4l .. 252-4l (descending); scan from the top
-      int c[4], own = 0;
+    st_agent(hrow + j * 256 + tid, hist[tid]);
+    row_barrier(a, b, pass, g0, &s_flag, [&]() {
+      // the last workgroup: total histogram, then the digit holding the
+      // kb-th largest key (scanning digits from the top)
+      int t = 0;
+      for (int j0 = 0; j0 < a.NW; j0 += 8) {
+        int v[8];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        c[q] = hist[255 - 4 * tid - q];
-        own += c[q];
-      }
-      int incl = own;
+        for (int q = 0; q < 8; ++q) v[q] = j0 + q < a.NW ? ld_agent(hrow + (j0 + q) * 256 + tid) : 0;
 #pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(incl, o, 64);
-        if (tid >= o) incl += y;
+        for (int q = 0; q < 8; ++q) t += v[q];
       }
-      const int excl = incl - own;
-      const int need = kb - above;
-      if (excl < need && need <= incl) {
-        int acc = excl;
+      hist[tid] = t;
+      __syncthreads();
+      if (tid < 64) {
+        // lane l owns digits 255-4l .. 252-4l (descending)
+        int c[4], own = 0;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          if (acc + c[q] >= need) {
-            s_digit = 255 - 4 * tid - q;
-            s_above = above + acc;
-            break;
+          c[q] = hist[255 - 4 * tid - q];
+          own += c[q];
+        }
+        int incl = own;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(incl, o, 64);
+          if (tid >= o) incl += y;
+        }
+        const int excl = incl - own;
+        const int need = kb - above;
+        if (excl < need && need <= incl) {
+          int acc = excl;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            if (acc + c[q] >= need) {
+              st_agent(a.res + b * 4, 255 - 4 * tid - q);
+              st_agent(a.res + b * 4 + 1, above + acc);
+              break;
+            }
+            acc += c[q];
           }
-          acc += c[q];
         }
       }
+    });
+    if (tid == 0) {
+      s_res[0] = ld_agent(a.res + b * 4);
+      s_res[1] = ld_agent(a.res + b * 4 + 1);
     }
     __syncthreads();
-    prefix |= (uint32_t)s_digit << shift;
-    mask |= 255u << shift;
-    above = s_above;
+    if (kb > 0) {
+      prefix |= (uint32_t)s_res[0] << shift;
+      mask |= 255u << shift;
+      above = s_res[1];
+    }
     __syncthreads();
   }
   const uint32_t tau = prefix;
-  const int need_eq = kb - above;  // >= 1 keys equal to tau, lowest indices first
+  const int need_eq = kb - above;  // keys equal to tau to keep, lowest indices first
 
-  // ---- ordered emission in ascending index order
-  int carry_eq = 0, carry_out = 0;
-  for (int base = 0; base < mb; base += kTopkThreads * kPerThread) {
+  // ---- this slice's counts, exchanged: where its output starts
+  int n_gt = 0, n_eq = 0;
+  if (kb > 0)
+    visit([&](uint32_t key) {
+      n_gt += key > tau;
+      n_eq += key == tau;
+    });
+  int slice_gt, slice_eq;
+  block_exclusive_scan(n_gt, s_warp, &slice_gt);
+  block_exclusive_scan(n_eq, s_warp, &slice_eq);
+  if (tid == 0) {
+    st_agent(a.cnt + ((size_t)b * a.NW + j) * 2, slice_gt);
+    st_agent(a.cnt + ((size_t)b * a.NW + j) * 2 + 1, slice_eq);
+  }
+  row_barrier(a, b, 4, g0, &s_flag, []() {});
+  if (kb == 0) return;
+  if (tid < 64) {  // counts of the slices before this one
+    int gt = 0, eq = 0;
+    for (int q = tid; q < j; q += 64) {
+      gt += ld_agent(a.cnt + ((size_t)b * a.NW + q) * 2);
+      eq += ld_agent(a.cnt + ((size_t)b * a.NW + q) * 2 + 1);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      gt += __shfl_xor(gt, o, 64);
+      eq += __shfl_xor(eq, o, 64);
+    }
+    if (tid == 0) {
+      s_res[0] = gt;
+      s_res[1] = eq;
+    }
+  }
+  __syncthreads();
+  int carry_out = s_res[0] + min(s_res[1], need_eq);
+  int carry_eq = s_res[1];
+
+  // ---- ordered emission of the slice in ascending index order
+  for (int base = s0; base < s1; base += kChunk) {
     const int i0 = base + tid * kPerThread;
     uint32_t keys[kPerThread];
-    int n_gt = 0, n_eq = 0;
+    int g = 0, e_ = 0;
 #pragma unroll
     for (int e = 0; e < kPerThread; ++e) {
-      const int i = i0 + e;
-      keys[e] = i < mb ? rank_key(sc[i]) : 0u;
-      const bool valid = i < mb;
-      n_gt += valid && keys[e] > tau;
-      n_eq += valid && keys[e] == tau;
+      const bool valid = i0 + e < s1;
+      if constexpr (REG) keys[e] = kr[e];
+      else keys[e] = valid ? rank_key(sc[i0 + e]) : 0u;
+      g += valid && keys[e] > tau;
+      e_ += valid && keys[e] == tau;
     }
     int tot_eq;
-    const int eq_before = carry_eq + block_exclusive_scan(n_eq, s_warp, &tot_eq);
+    const int eq_before = carry_eq + block_exclusive_scan(e_, s_warp, &tot_eq);
     int take_eq = need_eq - eq_before;
-    take_eq = take_eq < 0 ? 0 : (take_eq > n_eq ? n_eq : take_eq);
+    take_eq = take_eq < 0 ? 0 : (take_eq > e_ ? e_ : take_eq);
     int tot_sel;
-    int pos = carry_out + block_exclusive_scan(n_gt + take_eq, s_warp, &tot_sel);
+    int pos = carry_out + block_exclusive_scan(g + take_eq, s_warp, &tot_sel);
 #pragma unroll
     for (int e = 0; e < kPerThread; ++e) {
-      const int i = i0 + e;
-      if (i < mb) {
+      if (i0 + e < s1) {
         bool sel = keys[e] > tau;
         if (keys[e] == tau && take_eq > 0) {
           sel = true;
           --take_eq;
         }
-        if (sel && pos < kb) out[pos++] = i;
+        if (sel && pos < kb) out[pos++] = i0 + e;
       }
     }
     carry_eq += tot_eq;
     carry_out += tot_sel;
   }
+}
+
+struct TPlan {
+  int NW, slice;
+  size_t off_arrive, off_gen, off_hist, off_res, off_cnt, bytes;
+};
+
+pvlm_status plan_topk(int B, int64_t m_cap, TPlan* p) {
+  if (B < 1 || m_cap < 1 || m_cap > ((int64_t)1 << 30)) return PVLM_ERR_SHAPE;
+  DeviceInfo di;
+  pvlm_status st = device_info(&di);
+  if (st != PVLM_OK) return st;
+  if (B > di.cus) return PVLM_ERR_UNSUPPORTED;
+  const int nw_max = di.cus / B;  // co-resident: at most one workgroup per CU
+  int64_t nw = (m_cap + kSlice - 1) / kSlice;
+  if (nw > nw_max) nw = nw_max;
+  if (nw < 1) nw = 1;
+  p->NW = (int)nw;
+  p->slice = (int)((m_cap + nw - 1) / nw);
+  // counters: arrivals return to zero (low part), generations are monotonic
+  // (their own part of the monotonic region)
+  if (kSyncLine * (size_t)B > kSyncRegion - kSyncTopkOff) return PVLM_ERR_UNSUPPORTED;
+  p->off_arrive = 0;
+  p->off_gen = kSyncTopkOff;
+  size_t off = kSyncRegion;
+  p->off_hist = off;
+  off = align_up(off + sizeof(int) * (size_t)B * p->NW * 256, 256);
+  p->off_res = off;
+  off = align_up(off + sizeof(int) * (size_t)B * 4, 256);
+  p->off_cnt = off;
+  off = align_up(off + sizeof(int) * (size_t)B * p->NW * 2, 256);
+  p->bytes = off;
+  return PVLM_OK;
 }
 
 }  // namespace
@@ -173,21 +337,42 @@ __global__ void __launch_bounds__(kTopkThreads) topk_kernel(const float* score, 
 using namespace pvlm;
 
 extern "C" size_t pvlm_topk_workspace_size(int B, int64_t m_cap) {
-  (void)B;
-  (void)m_cap;
-  return 0;
+  TPlan p;
+  if (plan_topk(B, m_cap, &p) != PVLM_OK) return 0;
+  return p.bytes;
 }
 
 extern "C" pvlm_status pvlm_topk_select(int B, int64_t m_cap, const int32_t* m, const int32_t* k,
                                         int32_t k_cap, const float* score, int32_t* idx, void* ws,
                                         size_t ws_bytes, int32_t* status, hipStream_t stream) {
-  (void)ws;
-  (void)ws_bytes;
   if (!m || !k || !score || !idx) return PVLM_ERR_NULL;
   if (B < 1 || m_cap < 1 || k_cap < 0 || m_cap > ((int64_t)1 << 30)) return PVLM_ERR_SHAPE;
   if (k_cap == 0) return PVLM_OK;
-  hipLaunchKernelGGL(topk_kernel, dim3(B), dim3(kTopkThreads), 0, stream, score, m, k, m_cap,
-                     k_cap, idx, status);
-  PVLM_LAUNCHED();
+  TPlan p;
+  pvlm_status st = plan_topk(B, m_cap, &p);
+  if (st != PVLM_OK) return st;
+  if (!ws || ws_bytes < p.bytes) return PVLM_ERR_WORKSPACE;
+  char* wsb = static_cast<char*>(ws);
+  TArgs a;
+  a.score = score;
+  a.m = m;
+  a.k = k;
+  a.idx = idx;
+  a.status = status;
+  a.hist = reinterpret_cast<int*>(wsb + p.off_hist);
+  a.res = reinterpret_cast<int*>(wsb + p.off_res);
+  a.cnt = reinterpret_cast<int*>(wsb + p.off_cnt);
+  a.arrive = reinterpret_cast<int*>(wsb + p.off_arrive);
+  a.gen = reinterpret_cast<unsigned*>(wsb + p.off_gen);
+  a.m_cap = m_cap;
+  a.k_cap = k_cap;
+  a.NW = p.NW;
+  a.slice = p.slice;
+  void* args[] = {&a};
+  const void* kern = p.slice <= kTopkThreads * kPerThread
+                         ? reinterpret_cast<const void*>(topk_kernel<true>)
+                         : reinterpret_cast<const void*>(topk_kernel<false>);
+  PVLM_HIP(launch_coresident(kern, dim3(B * p.NW),
+                             dim3(kTopkThreads), args, 0, stream));
   return PVLM_OK;
 }

@@ -1430,7 +1430,7 @@ pvlm_status plan_verify(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int
   // of group g on lines 3g..3g+2 of the monotonic part), so calls of any shape
   // keep every slot consistent; the mass-sum counters return to zero and live
   // in the low part.
-  if (3 * kSyncLine * (size_t)p->groups > kSyncRegion - kSyncMonoOff) return PVLM_ERR_UNSUPPORTED;
+  if (3 * kSyncLine * (size_t)p->groups > kSyncTopkOff - kSyncMonoOff) return PVLM_ERR_UNSUPPORTED;
   if (kSyncLine * (size_t)B * p->splits > kSyncMonoOff) return PVLM_ERR_UNSUPPORTED;
   p->off_cnt_s = kSyncMonoOff;
   p->off_mcnt = 0;
