@@ -216,6 +216,9 @@ pvlm_status pvlm_gather_kv(pvlm_dtype dt, int n_layers, int B, int Hkv, int D, i
  *   u_accept [B][gamma] f64 in [0,1), u_sample [B] f64 in [0,1).
  *   near_tie (nullable) [B]: 1 when a decision or the draw fell within 1e-9
  *   (relative) of its boundary, where another summation order could flip it.
+ * Limits: B <= 256, gamma <= 32, V <= 1048576 (PVLM_ERR_UNSUPPORTED).  The
+ * workgroups of the one launch exchange partial sums through `ws`
+ * (pvlm_spec_accept_workspace_size bytes, zero-filled before first use).
  * ---------------------------------------------------------------------- */
 size_t pvlm_spec_accept_workspace_size(int B, int gamma, int V);
 pvlm_status pvlm_spec_accept(int B, int gamma, int V, float temperature,

@@ -2,28 +2,39 @@
 // with probability min(1, p/q); on rejection draw from norm(max(0, p - q)))
 // and the bonus token after full acceptance (Suppl. B).
 //
-// One cooperative launch, four phases separated by grid-wide waits:
-//  1. every (batch, row, vocab chunk) item: chunk max (and lowest argmax) and
-//     sum of exp((z - max) / temperature) in float64;
-//  2. every workgroup with later work combines those into each row's max and
-//     normaliser and replays the sequential accept decisions (float64) to find
-//     the first rejection a -- redundantly, so no extra wait is needed;
-//  3. every (batch, chunk) item: the chunk's mass of the draw distribution
-//     (the residual max(0, p_a - q_a), or p_gamma for the bonus), summed with
-//     the same blocked scan phase 4 uses;
-//  4. the chunk where the cumulative mass first exceeds u' * total scans its
-//     elements and writes the outputs.
-// temperature == 0 stops after phase 2 (greedy argmax).
+// One cooperative launch of 512-thread workgroups, three phases separated by
+// two grid-wide waits:
+//  1. every (batch, row, vocabulary chunk) item: the chunk's max (lowest
+//     argmax) and sum of exp((z - max) / temperature) in float64, from one
+//     coalesced read of the chunk held in registers;
+//  2. every workgroup with draw work combines the chunk results of its batch
+//     into each row's max and normaliser, evaluates the accept test of every
+//     drafted position in parallel (float64) and takes the first rejection a,
+//     then computes the mass of its small chunk of the draw distribution (the
+//     residual max(0, p_a - q_a), or p_gamma for the bonus), keeping the
+//     values; the draw chunks are spread over the whole grid;
+//  3. after the second wait every such workgroup scans the chunk masses to
+//     locate the chunk where the cumulative mass first exceeds u' * total;
+//     that chunk's workgroup scans its kept values and writes the outputs.
+// temperature == 0 stops after the first wait (greedy argmax).
+//
+// The waits: see grid_wait (no end-of-kernel round trip returns anything to
+// zero).
 #include "common.h"
 
 namespace pvlm {
 namespace {
 
-constexpr int kAccThreads = 256;
-constexpr int kAccPer = 16;
+constexpr int kAccThreads = 512;
+constexpr int kAccWaves = kAccThreads / 64;
+constexpr int kAccPer = 24;
 constexpr int kChunk = kAccThreads * kAccPer;  // vocabulary entries per item
 constexpr int kAccMaxB = 256;
-constexpr int kMaxChunks = 1024;                // V <= kMaxChunks * kChunk
+constexpr int kDrawPer = 2;                      // entries per thread in the draw phases
+constexpr int kDrawChunk = kAccThreads * kDrawPer;
+constexpr int kMaxDraw = 1024;                   // draw chunks per batch row: V <= kMaxDraw * kDrawChunk
+constexpr int kSumPer = kMaxDraw / kAccThreads;  // draw-chunk sums per thread in the crossing search
+constexpr int kMaxRows = 65;                    // 2 * gamma + 1, gamma <= 32
 constexpr double kNearTie = 1e-9;
 constexpr double kNegInfD = -__builtin_huge_val();
 
@@ -37,22 +48,15 @@ struct AArgs {
   int32_t* next;
   int32_t* near;
   int32_t* status;
-  double* pm;     // [B][RW][NC] chunk max
-  double* ps;     // [B][RW][NC] chunk exp-sum (relative to the chunk max)
-  int* pi;        // [B][RW][NC] chunk argmax (lowest index)
-  double* rowM;   // [B][RW] row max
-  double* rowZ;   // [B][RW] row normaliser
-  int* rowA;      // [B][RW] row argmax
-  int* rowcnt;    // [B][RW] chunks finished (last one combines the row)
-  double* rs;     // [B][NC] residual chunk mass
-  double* qs;     // [B][NC] p chunk mass (used when the residual is empty)
-  int* bcnt;      // [B] chunks finished in phase 3
-  double* bZ;     // [B] total mass of the draw distribution
-  double* bPre;   // [B] mass before the crossing chunk
-  int* bCross;    // [B] crossing chunk
-  int* bMode;     // [B] bit 0: draw from the residual; bit 1: rounding fallback
-  int* bar;       // [0] arrivals, [1] finished workgroups
-  int B, gamma, V, NC;
+  double* pm;       // [B][RW][NC] chunk max
+  double* ps;       // [B][RW][NC] chunk exp-sum (relative to the chunk max)
+  int* pi;          // [B][RW][NC] chunk argmax (lowest index)
+  double* rs;       // [B][ND] residual mass of each draw chunk
+  double* qs;       // [B][ND] p mass of each draw chunk (used when the residual is empty)
+  int* arrive;      // [2] arrivals at the two waits (128 bytes apart), zero at rest
+  unsigned* gen;    // generation word, advanced once per wait
+  int B, gamma, V, NC;  // NC: phase-1 chunks per row
+  int ND;               // draw chunks per batch row
   double tau;
   int greedy;
 };
@@ -60,6 +64,64 @@ struct AArgs {
 __device__ __forceinline__ const float* row_ptr(const AArgs& a, int b, int rho) {
   if (rho <= a.gamma) return a.tl + ((size_t)b * (a.gamma + 1) + rho) * a.V;
   return a.dl + ((size_t)b * a.gamma + (rho - a.gamma - 1)) * a.V;
+}
+
+// Grid-wide wait `p` (0 or 1): arrive, and (if `wait`) wait for every
+// workgroup's arrival.  Each wait has its own arrival counter, which its last
+// arrival returns to zero before it advances the generation word the others
+// poll (polling the counter itself would slow the arrivals down).  The
+// generation is never reset: every workgroup reads it at its start, before
+// its first arrival, so wait p releases at that value + p + 1.
+__device__ void grid_wait(const AArgs& a, int p, unsigned g0, bool wait) {
+  __builtin_amdgcn_s_waitcnt(0);  // this workgroup's published data is visible
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int* cnt = a.arrive + p * (int)(kSyncLine / sizeof(int));
+    const int old = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (old == (int)gridDim.x - 1) {
+      reset_counter(cnt);
+      __hip_atomic_store(a.gen, g0 + (unsigned)p + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else if (wait) {
+      grp_poll(a.gen, g0 + (unsigned)p + 1u, a.status);
+    }
+  }
+  __syncthreads();
+}
+
+// Exclusive scans of two doubles per thread over the workgroup (fixed order,
+// the same as block_scan_f64's), sharing the barriers.
+__device__ void block_scan2_f64(double v0, double v1, double* s_w, double& e0, double& e1, double& t0,
+                                double& t1) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  double x0 = v0, x1 = v1;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const double y0 = __shfl_up(x0, o, 64), y1 = __shfl_up(x1, o, 64);
+    if (lane >= o) {
+      x0 += y0;
+      x1 += y1;
+    }
+  }
+  if (lane == 63) {
+    s_w[w] = x0;
+    s_w[kAccWaves + w] = x1;
+  }
+  __syncthreads();
+  double b0 = 0.0, b1 = 0.0, a0 = 0.0, a1 = 0.0;
+#pragma unroll
+  for (int k = 0; k < kAccWaves; ++k) {
+    if (k == w) {
+      b0 = a0;
+      b1 = a1;
+    }
+    a0 += s_w[k];
+    a1 += s_w[kAccWaves + k];
+  }
+  t0 = a0;
+  t1 = a1;
+  e0 = b0 + (x0 - v0);
+  e1 = b1 + (x1 - v1);
+  __syncthreads();
 }
 
 // Exclusive scan of one double per thread over the workgroup (fixed order).
@@ -74,7 +136,8 @@ __device__ double block_scan_f64(double v, double* s_w, double* total) {
   if (lane == 63) s_w[w] = x;
   __syncthreads();
   double before = 0.0, tot = 0.0;
-  for (int k = 0; k < kAccThreads / 64; ++k) {
+#pragma unroll
+  for (int k = 0; k < kAccWaves; ++k) {
     if (k == w) before = tot;
     tot += s_w[k];
   }
@@ -83,12 +146,12 @@ __device__ double block_scan_f64(double v, double* s_w, double* total) {
   return before + (x - v);
 }
 
-// Workgroup-wide max with lowest-index tie-break (value, index), fixed order.
-__device__ void block_argmax(double& v, int& i, double* s_v, int* s_i) {
+// Workgroup-wide max with lowest-index tie-break (value, index).
+__device__ void block_argmax(float& v, int& i, float* s_v, int* s_i) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
-    const double v2 = __shfl_xor(v, o, 64);
+    const float v2 = __shfl_xor(v, o, 64);
     const int i2 = __shfl_xor(i, o, 64);
     if (v2 > v || (v2 == v && i2 < i)) {
       v = v2;
@@ -102,7 +165,8 @@ __device__ void block_argmax(double& v, int& i, double* s_v, int* s_i) {
   __syncthreads();
   v = s_v[0];
   i = s_i[0];
-  for (int k = 1; k < kAccThreads / 64; ++k)
+#pragma unroll
+  for (int k = 1; k < kAccWaves; ++k)
     if (s_v[k] > v || (s_v[k] == v && s_i[k] < i)) {
       v = s_v[k];
       i = s_i[k];
@@ -115,273 +179,360 @@ __device__ double block_sum(double x, double* s_v) {
   if ((threadIdx.x & 63) == 0) s_v[threadIdx.x >> 6] = x;
   __syncthreads();
   double t = 0.0;
-  for (int k = 0; k < kAccThreads / 64; ++k) t += s_v[k];
+#pragma unroll
+  for (int k = 0; k < kAccWaves; ++k) t += s_v[k];
   __syncthreads();
   return t;
 }
 
-__device__ __forceinline__ void finish(const AArgs& a, int* s_flag) {
-  if (wg_signal_last(a.bar + 1, gridDim.x, s_flag) && threadIdx.x == 0) {
-    reset_counter(a.bar);
-    reset_counter(a.bar + 1);
+// The kAccPer entries of chunk [y0, y1) this thread reads in phase 1 (coalesced:
+// entry 4 * (k * kAccThreads + tid) + e of the chunk), -inf past y1.
+template <bool VEC>
+__device__ __forceinline__ void load_strided(const float* z, int y0, int y1, float (&v)[kAccPer]) {
+#pragma unroll
+  for (int k = 0; k < kAccPer / 4; ++k) {
+    const int y = y0 + 4 * (k * kAccThreads + (int)threadIdx.x);
+    if constexpr (VEC) {
+      const float4 f = y < y1 ? *reinterpret_cast<const float4*>(z + y)
+                              : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+      v[4 * k] = f.x;
+      v[4 * k + 1] = f.y;
+      v[4 * k + 2] = f.z;
+      v[4 * k + 3] = f.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[4 * k + e] = y + e < y1 ? z[y + e] : -INFINITY;
+    }
   }
 }
+__device__ __forceinline__ int strided_index(int y0, int j) {
+  return y0 + 4 * ((j / 4) * kAccThreads + (int)threadIdx.x) + (j % 4);
+}
 
+// Per-batch state every draw workgroup derives after the first wait.
+struct Decision {
+  int acc, tie;
+  double pM, pZ, qM, qZ;
+};
+
+template <bool VEC>
 __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
-  __shared__ double s_v[kAccThreads / 64];
-  __shared__ int s_i[kAccThreads / 64];
-  __shared__ double s_M[65], s_Z[65], s_px[32], s_qx[32];
-  __shared__ int s_arg[65], s_xok[32];
-  __shared__ int s_a[kAccMaxB], s_tie[kAccMaxB];
-  __shared__ double s_pM[kAccMaxB], s_pZ[kAccMaxB], s_qM[kAccMaxB], s_qZ[kAccMaxB];
-  __shared__ double s_cr[kMaxChunks], s_cq[kMaxChunks];
-  __shared__ int s_win, s_flag;
+  __shared__ float s_fv[kAccWaves];
+  __shared__ int s_fi[kAccWaves];
+  __shared__ double s_d[2 * kAccWaves];
+  __shared__ double s_M[kMaxRows], s_Z[kMaxRows];
+  __shared__ int s_arg[kMaxRows], s_rej[32], s_tie[32];
+  __shared__ Decision s_dec;
+  __shared__ double s_pre;
+  __shared__ int s_win, s_cross, s_last;
   const int tid = threadIdx.x;
   const int RW = 2 * a.gamma + 1;
   const int W = gridDim.x;
-  const double tau = a.tau;
+  const double inv_tau = a.greedy ? 0.0 : 1.0 / a.tau;
+  const unsigned g0 = tid == 0 ? grp_read(a.gen) : 0u;
+  // the inputs of the decisions and the draw for this workgroup's first
+  // batch, loaded up front (drafted position t on thread kAccThreads - 32 + t)
+  const int nd_items = a.greedy ? 1 : a.B * a.ND;
+  const int pb = (int)blockIdx.x < nd_items ? (a.greedy ? 0 : (int)blockIdx.x / a.ND) : -1;
+  const int t_d = tid - (kAccThreads - 32);
+  const bool drafter = t_d >= 0 && t_d < a.gamma;
+  int pf_x = -1;
+  float pf_px = 0.f, pf_qx = 0.f;
+  double pf_ua = 0.0;
+  auto load_draft = [&](int b, int& x, float& px, float& qx, double& ua) {
+    const int xt = a.tok[(size_t)b * a.gamma + t_d];
+    x = xt >= 0 && xt < a.V ? xt : -1;
+    if (x >= 0 && !a.greedy) {
+      px = row_ptr(a, b, t_d)[x];
+      qx = row_ptr(a, b, a.gamma + 1 + t_d)[x];
+      ua = a.ua[(size_t)b * a.gamma + t_d];
+    }
+  };
+  if (pb >= 0 && drafter) load_draft(pb, pf_x, pf_px, pf_qx, pf_ua);
+  const double pf_us = pb >= 0 && !a.greedy ? a.us[pb] : 0.0;
 
-  // ---- phase 1: chunk max / argmax / exp-sum; the last chunk of a row
-  //      combines the row's totals
-  const int items1 = a.B * RW * a.NC;
+  // ---- phase 1: chunk max / argmax / exp-sum (greedy: target rows only)
+  const int rows1 = a.greedy ? a.gamma + 1 : RW;
+  const int items1 = a.B * rows1 * a.NC;
   for (int it = blockIdx.x; it < items1; it += W) {
-    const int c = it % a.NC, rho = (it / a.NC) % RW, b = it / (a.NC * RW);
-    if (a.greedy && rho > a.gamma) continue;
+    const int c = it % a.NC, rho = (it / a.NC) % rows1, b = it / (a.NC * rows1);
+    const size_t slot = ((size_t)b * RW + rho) * a.NC + c;
     const float* z = row_ptr(a, b, rho);
     const int y0 = c * kChunk, y1 = min(a.V, y0 + kChunk);
-    double mx = kNegInfD;
+    float v[kAccPer];
+    load_strided<VEC>(z, y0, y1, v);
+    float mx = -INFINITY;
     int am = 0x7fffffff;
-    for (int y = y0 + tid; y < y1; y += kAccThreads) {
-      const double v = z[y];
-      if (v > mx) {
-        mx = v;
-        am = y;
+#pragma unroll
+    for (int j = 0; j < kAccPer; ++j)
+      if (v[j] > mx) {  // ascending index order within the thread: first max kept
+        mx = v[j];
+        am = strided_index(y0, j);
       }
-    }
-    block_argmax(mx, am, s_v, s_i);
+    block_argmax(mx, am, s_fv, s_fi);
     double sum = 0.0;
-    if (!a.greedy && mx != kNegInfD)
-      for (int y = y0 + tid; y < y1; y += kAccThreads) sum += exp(((double)z[y] - mx) / tau);
-    sum = block_sum(sum, s_v);
-    if (tid == 0) {
-      st_agent(a.pm + it, mx);
-      st_agent(a.ps + it, sum);
-      st_agent(a.pi + it, am);
+    if (!a.greedy && mx != -INFINITY) {
+      // no branches around the exponentials (entries past the chunk are -inf
+      // and contribute exp(-inf) = 0), so their evaluations interleave
+      const double M = mx;
+      double e[kAccPer];
+#pragma unroll
+      for (int j = 0; j < kAccPer; ++j) e[j] = exp(((double)v[j] - M) * inv_tau);
+#pragma unroll
+      for (int j = 0; j < kAccPer; ++j) sum += e[j];
     }
-    const int r = b * RW + rho;
-    if (wg_signal_last(a.rowcnt + r, a.NC, &s_flag)) {
-      const size_t base = (size_t)r * a.NC;
-      double M = kNegInfD;
+    sum = block_sum(sum, s_d);
+    if (tid == 0) {
+      st_agent(a.pm + slot, mx == -INFINITY ? kNegInfD : (double)mx);
+      st_agent(a.ps + slot, sum);
+      st_agent(a.pi + slot, am);
+    }
+  }
+  const int items3 = a.B * a.ND;
+  const bool draws = !a.greedy && (int)blockIdx.x < items3;
+  const bool greedy_out = a.greedy && blockIdx.x == 0;
+  grid_wait(a, 0, g0, draws || greedy_out);
+
+  // every row's max, argmax and normaliser of batch b, the accept test of
+  // every drafted position (in parallel), and the first rejection, into
+  // s_dec (greedy: the outputs)
+  auto decide = [&](int b) {
+    const int rows = a.greedy ? a.gamma + 1 : RW;
+    // the drafted tokens and their logits (threads of the last wave), loaded
+    // up front for the first batch
+    const int t = t_d;
+    int x = pf_x;
+    float px = pf_px, qx = pf_qx;
+    double ua = pf_ua;
+    if (drafter && b != pb) load_draft(b, x, px, qx, ua);
+    // row r's NC chunk results are combined by an aligned group of NCp lanes
+    // (NCp = NC rounded up to a power of two, at most 64), lane k taking
+    // chunks k, k + NCp, ...; max and lowest argmax, then the normaliser, by
+    // butterflies within the group
+    const int NCp = a.NC <= 1 ? 1 : min(64, 1 << (32 - __clz(a.NC - 1)));
+    const int rpp = (kAccThreads - 64) / NCp;  // the last wave holds the drafted tokens
+    for (int r0 = 0; r0 < rows; r0 += rpp) {
+      const int r = r0 + tid / NCp, k0 = tid % NCp;
+      const bool act = r < rows && tid < rpp * NCp;
+      const size_t base = ((size_t)b * RW + r) * a.NC;
+      double M = kNegInfD, m0 = kNegInfD, s0 = 0.0;
       int A = 0x7fffffff;
-      for (int k = tid; k < a.NC; k += kAccThreads) {
-        const double m2 = ld_agent(a.pm + base + k);
-        const int i2 = ld_agent(a.pi + base + k);
+      if (act)
+        for (int k = k0; k < a.NC; k += NCp) {
+          const double m2 = ld_agent(a.pm + base + k);
+          const int i2 = ld_agent(a.pi + base + k);
+          if (k == k0) {
+            m0 = m2;
+            s0 = a.greedy ? 0.0 : ld_agent(a.ps + base + k);
+          }
+          if (m2 > M || (m2 == M && i2 < A)) {
+            M = m2;
+            A = i2;
+          }
+        }
+      for (int o = NCp / 2; o > 0; o >>= 1) {
+        const double m2 = __shfl_xor(M, o, 64);
+        const int i2 = __shfl_xor(A, o, 64);
         if (m2 > M || (m2 == M && i2 < A)) {
           M = m2;
           A = i2;
         }
       }
-      block_argmax(M, A, s_v, s_i);
       double Z = 0.0;
-      if (!a.greedy && M != kNegInfD)
-        for (int k = tid; k < a.NC; k += kAccThreads) {
-          const double m2 = ld_agent(a.pm + base + k);
-          if (m2 != kNegInfD) Z += ld_agent(a.ps + base + k) * exp((m2 - M) / tau);
+      if (act && !a.greedy && M != kNegInfD)
+        for (int k = k0; k < a.NC; k += NCp) {
+          const double m2 = k == k0 ? m0 : ld_agent(a.pm + base + k);
+          const double s2 = k == k0 ? s0 : ld_agent(a.ps + base + k);
+          if (m2 != kNegInfD) Z += s2 * exp((m2 - M) * inv_tau);
         }
-      Z = block_sum(Z, s_v);
-      if (tid == 0) {
-        st_agent(a.rowM + r, M);
-        st_agent(a.rowZ + r, Z);
-        st_agent(a.rowA + r, A);
-        reset_counter(a.rowcnt + r);
+      for (int o = NCp / 2; o > 0; o >>= 1) Z += __shfl_xor(Z, o, 64);
+      if (act && k0 == 0) {
+        s_M[r] = M;
+        s_Z[r] = Z;
+        s_arg[r] = A == 0x7fffffff ? 0 : A;
       }
     }
     __syncthreads();
-  }
-  wg_signal_wait(a.bar, W, a.status, true);
-
-  // ---- phase 2: the sequential accept decisions (every workgroup with later
-  //      work replays them from the row totals)
-  const bool has_late = a.greedy ? blockIdx.x == 0 : blockIdx.x < a.B * a.NC;
-  if (has_late) {
-    for (int b = 0; b < a.B; ++b) {
-      if (tid < RW && (!a.greedy || tid <= a.gamma)) {
-        s_M[tid] = ld_agent(a.rowM + b * RW + tid);
-        s_Z[tid] = ld_agent(a.rowZ + b * RW + tid);
-        s_arg[tid] = ld_agent(a.rowA + b * RW + tid);
+    if (drafter) {
+      int rej, tie = 0;
+      if (x < 0) {
+        rej = 2;  // invalid drafted token
+      } else if (a.greedy) {
+        rej = x != s_arg[t];
+      } else {
+        const int qr = a.gamma + 1 + t;
+        const double p = exp((px - s_M[t]) * inv_tau) / s_Z[t];
+        const double q = exp((qx - s_M[qr]) * inv_tau) / s_Z[qr];
+        const double lhs = ua * q;
+        tie = fabs(lhs - p) <= kNearTie * fmax(lhs, p);
+        rej = !(lhs < p);
       }
-      if (tid >= 64 && tid < 64 + a.gamma) {
-        const int t = tid - 64;
-        const int x = a.tok[(size_t)b * a.gamma + t];
-        const int ok = x >= 0 && x < a.V;
-        s_xok[t] = ok ? x : -1;
-        if (ok && !a.greedy) {
-          s_px[t] = row_ptr(a, b, t)[x];
-          s_qx[t] = row_ptr(a, b, a.gamma + 1 + t)[x];
-        }
-      }
-      __syncthreads();
-      if (tid == 0) {
-        int acc = a.gamma, tie = 0;
-        for (int t = 0; t < a.gamma; ++t) {
-          const int x = s_xok[t];
-          if (x < 0) {
-            dev_flag(a.status, PVLM_DEV_RANGE);
-            acc = t;
-            break;
-          }
-          bool ok;
-          if (a.greedy) {
-            ok = x == s_arg[t];
-          } else {
-            const int qr = a.gamma + 1 + t;
-            const double p = exp((s_px[t] - s_M[t]) / tau) / s_Z[t];
-            const double q = exp((s_qx[t] - s_M[qr]) / tau) / s_Z[qr];
-            const double lhs = a.ua[(size_t)b * a.gamma + t] * q;
-            if (fabs(lhs - p) <= kNearTie * fmax(lhs, p)) tie = 1;
-            ok = lhs < p;
-          }
-          if (!ok) {
-            acc = t;
-            break;
-          }
-        }
-        s_a[b] = acc;
-        s_tie[b] = tie;
-        s_pM[b] = s_M[acc];
-        s_pZ[b] = s_Z[acc];
-        if (acc < a.gamma) {
-          s_qM[b] = s_M[a.gamma + 1 + acc];
-          s_qZ[b] = s_Z[a.gamma + 1 + acc];
-        }
-        if (a.greedy) {
-          a.nacc[b] = acc;
-          a.next[b] = s_arg[acc];
-          if (a.near) a.near[b] = 0;
-        }
-      }
-      __syncthreads();
+      s_rej[t] = rej;
+      s_tie[t] = tie;
     }
-  }
-  if (a.greedy) {
-    finish(a, &s_flag);
-    return;
-  }
-
-  // r(y) of the draw distribution of batch b; also p(y)
-  auto draw_mass = [&](int b, int y, double& p_out) -> double {
-    const int acc = s_a[b];
-    const double p = exp(((double)row_ptr(a, b, acc)[y] - s_pM[b]) / tau) / s_pZ[b];
-    p_out = p;
-    if (acc == a.gamma) return p;
-    const double q = exp(((double)row_ptr(a, b, a.gamma + 1 + acc)[y] - s_qM[b]) / tau) / s_qZ[b];
-    return p > q ? p - q : 0.0;
+    __syncthreads();
+    if (tid == 0) {
+      int acc = a.gamma, tie = 0;
+      for (int u = 0; u < a.gamma; ++u) {
+        tie |= s_tie[u];
+        if (s_rej[u]) {
+          if (s_rej[u] == 2) dev_flag(a.status, PVLM_DEV_RANGE);
+          acc = u;
+          break;
+        }
+      }
+      Decision d;
+      d.acc = acc;
+      d.tie = tie;
+      d.pM = s_M[acc];
+      d.pZ = s_Z[acc];
+      d.qM = acc < a.gamma ? s_M[a.gamma + 1 + acc] : 0.0;
+      d.qZ = acc < a.gamma ? s_Z[a.gamma + 1 + acc] : 1.0;
+      s_dec = d;
+      if (a.greedy) {
+        a.nacc[b] = acc;
+        a.next[b] = s_arg[acc];
+        if (a.near) a.near[b] = 0;
+      }
+    }
+    __syncthreads();
   };
 
-  // ---- phase 3: chunk masses of the draw distribution; the last chunk of a
-  //      batch row locates the crossing chunk
-  const int items3 = a.B * a.NC;
-  for (int it = blockIdx.x; it < items3; it += W) {
-    const int b = it / a.NC, c = it % a.NC;
-    const int y0 = c * kChunk + tid * kAccPer;
-    double sr = 0.0, sp = 0.0;
-    for (int e = 0; e < kAccPer; ++e) {
-      const int y = y0 + e;
-      if (y < a.V) {
-        double p;
-        sr += draw_mass(b, y, p);
-        sp += p;
-      }
+  if (greedy_out)
+    for (int b = 0; b < a.B; ++b) decide(b);
+  if (a.greedy) return;
+
+  // Entries y = c * kDrawChunk + kDrawPer * tid + j of draw chunk c: r(y) of
+  // the draw distribution (the residual max(0, p - q), or p for the bonus)
+  // or, with want_p, p(y); returns this thread's sum of p(y) as well.
+  auto draw_values = [&](int b, int c, bool want_p, double (&r)[kDrawPer]) -> double {
+    const Decision d = s_dec;
+    const bool resid = !want_p && d.acc < a.gamma;
+    const double ipz = 1.0 / d.pZ, iqz = 1.0 / d.qZ;
+    const float* zpr = row_ptr(a, b, d.acc);
+    const float* zqr = row_ptr(a, b, a.gamma + 1 + min(d.acc, a.gamma - 1));
+    const int y = c * kDrawChunk + kDrawPer * tid;
+    float zp[kDrawPer], zq[kDrawPer];
+#pragma unroll
+    for (int j = 0; j < kDrawPer; ++j) {
+      zp[j] = y + j < a.V ? zpr[y + j] : -INFINITY;  // past V: p = 0
+      zq[j] = y + j < a.V && resid ? zqr[y + j] : -INFINITY;
     }
-    double tr, tp;
-    block_scan_f64(sr, s_v, &tr);
-    block_scan_f64(sp, s_v, &tp);
+    double psum = 0.0;
+#pragma unroll
+    for (int j = 0; j < kDrawPer; ++j) {
+      const double p = exp(((double)zp[j] - d.pM) * inv_tau) * ipz;
+      const double q = exp(((double)zq[j] - d.qM) * inv_tau) * iqz;
+      psum += p;
+      r[j] = !resid ? p : (p > q ? p - q : 0.0);
+    }
+    return psum;
+  };
+
+  // ---- phase 2: masses of the draw chunks (the values of the workgroup's
+  //      last item are kept)
+  double rr[kDrawPer];
+  double rr_excl = 0.0;  // exclusive prefix of the kept values' thread sums (residual)
+  int kept = -1, dec_b = -1;
+  for (int it = blockIdx.x; it < items3; it += W) {
+    const int b = it / a.ND, c = it % a.ND;
+    if (b != dec_b) {
+      decide(b);
+      dec_b = b;
+    }
+    const double sp = draw_values(b, c, false, rr);
+    kept = it;
+    double sr = 0.0;
+#pragma unroll
+    for (int j = 0; j < kDrawPer; ++j) sr += rr[j];
+    double tr, tp, ep;
+    block_scan2_f64(sr, sp, s_d, rr_excl, ep, tr, tp);
     if (tid == 0) {
       st_agent(a.rs + it, tr);
       st_agent(a.qs + it, tp);
     }
-    if (wg_signal_last(a.bcnt + b, a.NC, &s_flag)) {
-      for (int k = tid; k < a.NC; k += kAccThreads) {
-        s_cr[k] = ld_agent(a.rs + (size_t)b * a.NC + k);
-        s_cq[k] = ld_agent(a.qs + (size_t)b * a.NC + k);
-      }
-      __syncthreads();
-      if (tid == 0) {
-        double Zr = 0.0, Zp = 0.0;
-        for (int k = 0; k < a.NC; ++k) {
-          Zr += s_cr[k];
-          Zp += s_cq[k];
-        }
-        const bool use_r = Zr > 0.0;
-        const double* sums = use_r ? s_cr : s_cq;
-        const double Z = use_r ? Zr : Zp;
-        const double thr = a.us[b] * Z;
-        double run = 0.0, pre = 0.0, pre_last = 0.0;
-        int cross = -1, last_pos = -1;
-        for (int k = 0; k < a.NC; ++k) {
-          const double sk = sums[k];
-          if (sk > 0.0) {
-            last_pos = k;
-            pre_last = run;
-          }
-          if (cross < 0 && run + sk > thr) {
-            cross = k;
-            pre = run;
-          }
-          run += sk;
-        }
-        int mode = use_r ? 1 : 0;
-        if (cross < 0) {
-          mode |= 2;
-          cross = last_pos < 0 ? 0 : last_pos;
-          pre = pre_last;
-        }
-        st_agent(a.bZ + b, Z);
-        st_agent(a.bPre + b, pre);
-        st_agent(a.bCross + b, cross);
-        st_agent(a.bMode + b, mode);
-        reset_counter(a.bcnt + b);
-      }
+  }
+  grid_wait(a, 1, g0, draws);
+  if (!draws) return;
+
+  // ---- phase 3: the chunk where the cumulative mass first exceeds u' * Z
+  //      scans its values and writes the outputs
+  for (int it = blockIdx.x; it < items3; it += W) {
+    const int b = it / a.ND, c = it % a.ND;
+    // chunk sums of batch b in order: thread t owns chunks kSumPer * t + i
+    double cr[kSumPer], cq[kSumPer];
+    double own_r = 0.0, own_q = 0.0;
+#pragma unroll
+    for (int i = 0; i < kSumPer; ++i) {
+      const int k = kSumPer * tid + i;
+      cr[i] = k < a.ND ? ld_agent(a.rs + (size_t)b * a.ND + k) : 0.0;
+      cq[i] = k < a.ND ? ld_agent(a.qs + (size_t)b * a.ND + k) : 0.0;
+      own_r += cr[i];
+      own_q += cq[i];
+    }
+    double Zr, Zq, ex_r, ex_q;
+    block_scan2_f64(own_r, own_q, s_d, ex_r, ex_q, Zr, Zq);
+    const bool use_r = Zr > 0.0;  // else the residual is empty: draw from p
+    const double Z = use_r ? Zr : Zq;
+    const double thr = (b == pb ? pf_us : a.us[b]) * Z;
+    if (tid == 0) {
+      s_cross = 0x7fffffff;
+      s_last = -1;
     }
     __syncthreads();
-  }
-  wg_signal_wait(a.bar, 2 * W, a.status, true);
-
-  // ---- phase 4: the crossing chunk scans its elements and writes the outputs
-  for (int it = blockIdx.x; it < items3; it += W) {
-    const int b = it / a.NC, c = it % a.NC;
-    if (c != ld_agent(a.bCross + b)) continue;  // uniform across the workgroup
-    const int mode = ld_agent(a.bMode + b);
-    const bool use_r = mode & 1, fallback = mode & 2;
-    const double Z = ld_agent(a.bZ + b), pre = ld_agent(a.bPre + b);
-    const double thr = a.us[b] * Z;
-    const int y0 = c * kChunk + tid * kAccPer;
-    double r[kAccPer];
-    double own = 0.0;
-    for (int e = 0; e < kAccPer; ++e) {
-      const int y = y0 + e;
-      r[e] = 0.0;
-      if (y < a.V) {
-        double p;
-        const double rv = draw_mass(b, y, p);
-        r[e] = use_r ? rv : p;
+    double run = use_r ? ex_r : ex_q;
+    double pre_of[kSumPer];
+#pragma unroll
+    for (int i = 0; i < kSumPer; ++i) {
+      const int k = kSumPer * tid + i;
+      const double sk = use_r ? cr[i] : cq[i];
+      pre_of[i] = run;
+      if (k < a.ND) {
+        if (run + sk > thr) atomicMin(&s_cross, k);
+        if (sk > 0.0) atomicMax(&s_last, k);
       }
-      own += r[e];
+      run += sk;
     }
-    double tot;
-    const double excl = block_scan_f64(own, s_v, &tot);
+    __syncthreads();
+    const bool fallback = s_cross == 0x7fffffff;  // rounding: no chunk passes u' * Z
+    const int cross = fallback ? max(s_last, 0) : s_cross;
+#pragma unroll
+    for (int i = 0; i < kSumPer; ++i)
+      if (kSumPer * tid + i == cross) s_pre = s_last < 0 ? 0.0 : pre_of[i];
+    __syncthreads();
+    const double pre = s_pre;
+    __syncthreads();
+    if (cross != c) continue;  // uniform across the workgroup
+    if (b != dec_b) {
+      decide(b);
+      dec_b = b;
+    }
+    // the kept values, unless they belong to another item or the draw
+    // falls back to p
+    double excl = rr_excl;
+    if (it != kept || !use_r) {
+      draw_values(b, c, !use_r, rr);
+      kept = use_r ? it : -1;
+      double own = 0.0;
+#pragma unroll
+      for (int j = 0; j < kDrawPer; ++j) own += rr[j];
+      double tot;
+      excl = block_scan_f64(own, s_d, &tot);
+    }
     if (tid == 0) s_win = fallback ? -1 : 0x7fffffff;
     __syncthreads();
+    const int ybase = c * kDrawChunk + kDrawPer * tid;
     double cum = pre + excl;
     int mine = -1;
     double below = cum, at = cum;
-    for (int e = 0; e < kAccPer; ++e) {
+#pragma unroll
+    for (int j = 0; j < kDrawPer; ++j) {
       const double prev = cum;
-      cum += r[e];
+      cum += rr[j];
       if (fallback) {
-        if (r[e] > 0.0) mine = y0 + e;
+        if (rr[j] > 0.0) mine = ybase + j;
       } else if (mine < 0 && cum > thr) {
-        mine = y0 + e;
+        mine = ybase + j;
         below = prev;
         at = cum;
       }
@@ -400,59 +551,52 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
       if (tid == 0) s_win = -1;
       __syncthreads();
       mine = -1;
-      for (int e = 0; e < kAccPer; ++e)
-        if (r[e] > 0.0) mine = y0 + e;
+#pragma unroll
+      for (int j = 0; j < kDrawPer; ++j)
+        if (rr[j] > 0.0) mine = ybase + j;
       if (mine >= 0) atomicMax(&s_win, mine);
       __syncthreads();
       win = s_win;
       edge = true;
     }
+    const Decision d = s_dec;
     if (win < 0 && tid == 0) {  // no positive mass anywhere: degenerate input
       dev_flag(a.status, PVLM_DEV_RANGE);
-      a.nacc[b] = s_a[b];
+      a.nacc[b] = d.acc;
       a.next[b] = 0;
       if (a.near) a.near[b] = 1;
     }
     if (mine == win && win >= 0) {
-      int tie = s_tie[b];
+      int tie = d.tie;
       if (!edge) {
         if (fabs(at - thr) <= kNearTie * Z) tie = 1;
         if (win > 0 && fabs(below - thr) <= kNearTie * Z) tie = 1;
       } else {
         tie = 1;
       }
-      a.nacc[b] = s_a[b];
+      a.nacc[b] = d.acc;
       a.next[b] = win;
       if (a.near) a.near[b] = tie;
     }
     __syncthreads();
   }
-  finish(a, &s_flag);
 }
 
 struct APlan {
-  int NC;
-  size_t off_bar, off_pm, off_ps, off_pi, off_rowM, off_rowZ, off_rowA, off_rowcnt, off_rs, off_qs,
-      off_bcnt, off_bZ, off_bPre, off_bCross, off_bMode, bytes;
+  int NC, ND;
+  size_t off_arrive, off_gen, off_pm, off_ps, off_pi, off_rs, off_qs, bytes;
 };
 
 pvlm_status plan_accept(int B, int gamma, int V, APlan* p) {
   if (B < 1 || gamma < 1 || V < 1) return PVLM_ERR_SHAPE;
-  if (B > kAccMaxB || gamma > 32 || V > kMaxChunks * kChunk) return PVLM_ERR_UNSUPPORTED;
+  if (B > kAccMaxB || gamma > 32 || V > kMaxDraw * kDrawChunk) return PVLM_ERR_UNSUPPORTED;
   p->NC = (V + kChunk - 1) / kChunk;
+  p->ND = (V + kDrawChunk - 1) / kDrawChunk;
   const size_t rows = (size_t)B * (2 * gamma + 1);
   const size_t parts = rows * p->NC;
-  // counters first (inside the fixed synchronisation region), data after it
-  size_t sync = 0;
-  auto take_sync = [&](size_t bytes) {
-    const size_t at = sync;
-    sync += bytes;
-    return at;
-  };
-  p->off_bar = take_sync(2 * sizeof(int));
-  p->off_rowcnt = take_sync(rows * sizeof(int));
-  p->off_bcnt = take_sync(B * sizeof(int));
-  if (sync > kSyncMonoOff) return PVLM_ERR_UNSUPPORTED;
+  // counters inside the fixed synchronisation region, data after it
+  p->off_arrive = 0;
+  p->off_gen = kSyncAcceptOff;
   size_t off = kSyncRegion;
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -462,15 +606,8 @@ pvlm_status plan_accept(int B, int gamma, int V, APlan* p) {
   p->off_pm = take(parts * sizeof(double));
   p->off_ps = take(parts * sizeof(double));
   p->off_pi = take(parts * sizeof(int));
-  p->off_rowM = take(rows * sizeof(double));
-  p->off_rowZ = take(rows * sizeof(double));
-  p->off_rowA = take(rows * sizeof(int));
-  p->off_rs = take((size_t)B * p->NC * sizeof(double));
-  p->off_qs = take((size_t)B * p->NC * sizeof(double));
-  p->off_bZ = take(B * sizeof(double));
-  p->off_bPre = take(B * sizeof(double));
-  p->off_bCross = take(B * sizeof(int));
-  p->off_bMode = take(B * sizeof(int));
+  p->off_rs = take((size_t)B * p->ND * sizeof(double));
+  p->off_qs = take((size_t)B * p->ND * sizeof(double));
   p->bytes = off;
   return PVLM_OK;
 }
@@ -517,32 +654,29 @@ extern "C" pvlm_status pvlm_spec_accept(int B, int gamma, int V, float temperatu
   a.pm = reinterpret_cast<double*>(wsb + p.off_pm);
   a.ps = reinterpret_cast<double*>(wsb + p.off_ps);
   a.pi = reinterpret_cast<int*>(wsb + p.off_pi);
-  a.rowM = reinterpret_cast<double*>(wsb + p.off_rowM);
-  a.rowZ = reinterpret_cast<double*>(wsb + p.off_rowZ);
-  a.rowA = reinterpret_cast<int*>(wsb + p.off_rowA);
-  a.rowcnt = reinterpret_cast<int*>(wsb + p.off_rowcnt);
   a.rs = reinterpret_cast<double*>(wsb + p.off_rs);
   a.qs = reinterpret_cast<double*>(wsb + p.off_qs);
-  a.bcnt = reinterpret_cast<int*>(wsb + p.off_bcnt);
-  a.bZ = reinterpret_cast<double*>(wsb + p.off_bZ);
-  a.bPre = reinterpret_cast<double*>(wsb + p.off_bPre);
-  a.bCross = reinterpret_cast<int*>(wsb + p.off_bCross);
-  a.bMode = reinterpret_cast<int*>(wsb + p.off_bMode);
-  a.bar = reinterpret_cast<int*>(wsb + p.off_bar);
+  a.arrive = reinterpret_cast<int*>(wsb + p.off_arrive);
+  a.gen = reinterpret_cast<unsigned*>(wsb + p.off_gen);
   a.B = B;
   a.gamma = gamma;
   a.V = V;
   a.NC = p.NC;
+  a.ND = p.ND;
   a.tau = (double)temperature;
   a.greedy = temperature == 0.f;
-  const int items = B * (2 * gamma + 1) * p.NC;
+  const int items = max(B * (a.greedy ? gamma + 1 : 2 * gamma + 1) * p.NC, a.greedy ? 1 : B * p.ND);
   // a multiple of 8 workgroups (the XCD count) keeps the cooperative queue's
   // round-robin XCD placement aligned for the launches that follow
   int grid = (items + 7) / 8 * 8;
   if (grid > di.cus) grid = di.cus;
   if (grid < 1) grid = 1;
+  // float4 loads when every row starts on a 16-byte boundary
+  const bool vec = V % 4 == 0 && reinterpret_cast<uintptr_t>(draft_logits) % 16 == 0 &&
+                   reinterpret_cast<uintptr_t>(target_logits) % 16 == 0;
   void* args[] = {&a};
-  PVLM_HIP(launch_coresident(reinterpret_cast<const void*>(accept_kernel), dim3(grid),
-                             dim3(kAccThreads), args, 0, stream));
+  PVLM_HIP(launch_coresident(vec ? reinterpret_cast<const void*>(accept_kernel<true>)
+                                 : reinterpret_cast<const void*>(accept_kernel<false>),
+                             dim3(grid), dim3(kAccThreads), args, 0, stream));
   return PVLM_OK;
 }

@@ -40,10 +40,11 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // their counters never do.  Calls whose counters return to zero use the low
 // part of the region; monotonic counters (each call leaves them consistent,
 // never resets them) use the rest: verify's from kSyncMonoOff, top-k's from
-// kSyncTopkOff.
+// kSyncTopkOff (one line per batch row), accept's at kSyncAcceptOff.
 constexpr size_t kSyncRegion = 1024 * 1024;
 constexpr size_t kSyncMonoOff = 256 * 1024;
 constexpr size_t kSyncTopkOff = 768 * 1024;
+constexpr size_t kSyncAcceptOff = 896 * 1024;
 // Counters that many workgroups update or poll get a 128-byte line each, so
 // the memory-side atomics and polls of different counters never contend.
 constexpr size_t kSyncLine = 128;

@@ -317,7 +317,7 @@ pvlm_status plan_topk(int B, int64_t m_cap, TPlan* p) {
   p->slice = (int)((m_cap + nw - 1) / nw);
   // counters: arrivals return to zero (low part), generations are monotonic
   // (their own part of the monotonic region)
-  if (kSyncLine * (size_t)B > kSyncRegion - kSyncTopkOff) return PVLM_ERR_UNSUPPORTED;
+  if (kSyncLine * (size_t)B > kSyncAcceptOff - kSyncTopkOff) return PVLM_ERR_UNSUPPORTED;
   p->off_arrive = 0;
   p->off_gen = kSyncTopkOff;
   size_t off = kSyncRegion;
