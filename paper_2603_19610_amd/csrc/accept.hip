@@ -30,9 +30,11 @@ constexpr int kAccWaves = kAccThreads / 64;
 constexpr int kAccPer = 24;
 constexpr int kChunk = kAccThreads * kAccPer;  // vocabulary entries per item
 constexpr int kAccMaxB = 256;
-constexpr int kDrawPer = 2;                      // entries per thread in the draw phases
-constexpr int kDrawChunk = kAccThreads * kDrawPer;
-constexpr int kMaxDraw = 1024;                   // draw chunks per batch row: V <= kMaxDraw * kDrawChunk
+// Entries per thread in the draw phases: 2, or 8 when the batch would
+// otherwise have more draw chunks than the grid has workgroups.
+constexpr int kDrawPerMin = 2;
+constexpr int kDrawPerMax = 8;
+constexpr int kMaxDraw = 1024;  // draw chunks per batch row: V <= kMaxDraw * kAccThreads * kDrawPerMin
 constexpr int kSumPer = kMaxDraw / kAccThreads;  // draw-chunk sums per thread in the crossing search
 constexpr int kMaxRows = 65;                    // 2 * gamma + 1, gamma <= 32
 constexpr double kNearTie = 1e-9;
@@ -174,6 +176,31 @@ __device__ void block_argmax(float& v, int& i, float* s_v, int* s_i) {
   __syncthreads();
 }
 
+// Workgroup-wide minimum of lo and maximum of hi (butterflies within each
+// wave, then the waves' results through LDS; no atomics, whose per-lane
+// serialisation is slow when many lanes take part).
+__device__ void block_minmax(int& lo, int& hi, int* s_w) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    lo = min(lo, __shfl_xor(lo, o, 64));
+    hi = max(hi, __shfl_xor(hi, o, 64));
+  }
+  if (lane == 0) {
+    s_w[w] = lo;
+    s_w[kAccWaves + w] = hi;
+  }
+  __syncthreads();
+  lo = s_w[0];
+  hi = s_w[kAccWaves];
+#pragma unroll
+  for (int k = 1; k < kAccWaves; ++k) {
+    lo = min(lo, s_w[k]);
+    hi = max(hi, s_w[kAccWaves + k]);
+  }
+  __syncthreads();
+}
+
 __device__ double block_sum(double x, double* s_v) {
   x = warp_sum(x);
   if ((threadIdx.x & 63) == 0) s_v[threadIdx.x >> 6] = x;
@@ -215,8 +242,9 @@ struct Decision {
   double pM, pZ, qM, qZ;
 };
 
-template <bool VEC>
+template <bool VEC, int kDrawPer>
 __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
+  constexpr int kDrawChunk = kAccThreads * kDrawPer;
   __shared__ float s_fv[kAccWaves];
   __shared__ int s_fi[kAccWaves];
   __shared__ double s_d[2 * kAccWaves];
@@ -224,7 +252,7 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
   __shared__ int s_arg[kMaxRows], s_rej[32], s_tie[32];
   __shared__ Decision s_dec;
   __shared__ double s_pre;
-  __shared__ int s_win, s_cross, s_last;
+  __shared__ int s_mm[2 * kAccWaves];
   const int tid = threadIdx.x;
   const int RW = 2 * a.gamma + 1;
   const int W = gridDim.x;
@@ -233,7 +261,7 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
   // the inputs of the decisions and the draw for this workgroup's first
   // batch, loaded up front (drafted position t on thread kAccThreads - 32 + t)
   const int nd_items = a.greedy ? 1 : a.B * a.ND;
-  const int pb = (int)blockIdx.x < nd_items ? (a.greedy ? 0 : (int)blockIdx.x / a.ND) : -1;
+  const int pb = (int)blockIdx.x < nd_items ? (a.greedy ? 0 : (int)blockIdx.x % a.B) : -1;
   const int t_d = tid - (kAccThreads - 32);
   const bool drafter = t_d >= 0 && t_d < a.gamma;
   int pf_x = -1;
@@ -435,7 +463,7 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
   double rr_excl = 0.0;  // exclusive prefix of the kept values' thread sums (residual)
   int kept = -1, dec_b = -1;
   for (int it = blockIdx.x; it < items3; it += W) {
-    const int b = it / a.ND, c = it % a.ND;
+    const int b = it % a.B, c = it / a.B;
     if (b != dec_b) {
       decide(b);
       dec_b = b;
@@ -448,8 +476,8 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
     double tr, tp, ep;
     block_scan2_f64(sr, sp, s_d, rr_excl, ep, tr, tp);
     if (tid == 0) {
-      st_agent(a.rs + it, tr);
-      st_agent(a.qs + it, tp);
+      st_agent(a.rs + (size_t)b * a.ND + c, tr);
+      st_agent(a.qs + (size_t)b * a.ND + c, tp);
     }
   }
   grid_wait(a, 1, g0, draws);
@@ -458,7 +486,7 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
   // ---- phase 3: the chunk where the cumulative mass first exceeds u' * Z
   //      scans its values and writes the outputs
   for (int it = blockIdx.x; it < items3; it += W) {
-    const int b = it / a.ND, c = it % a.ND;
+    const int b = it % a.B, c = it / a.B;
     // chunk sums of batch b in order: thread t owns chunks kSumPer * t + i
     double cr[kSumPer], cq[kSumPer];
     double own_r = 0.0, own_q = 0.0;
@@ -475,30 +503,28 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
     const bool use_r = Zr > 0.0;  // else the residual is empty: draw from p
     const double Z = use_r ? Zr : Zq;
     const double thr = (b == pb ? pf_us : a.us[b]) * Z;
-    if (tid == 0) {
-      s_cross = 0x7fffffff;
-      s_last = -1;
-    }
-    __syncthreads();
+    // the first chunk whose cumulative mass passes u' * Z, and the last
+    // chunk with positive mass
     double run = use_r ? ex_r : ex_q;
     double pre_of[kSumPer];
+    int first = 0x7fffffff, last = -1;
 #pragma unroll
     for (int i = 0; i < kSumPer; ++i) {
       const int k = kSumPer * tid + i;
       const double sk = use_r ? cr[i] : cq[i];
       pre_of[i] = run;
       if (k < a.ND) {
-        if (run + sk > thr) atomicMin(&s_cross, k);
-        if (sk > 0.0) atomicMax(&s_last, k);
+        if (first == 0x7fffffff && run + sk > thr) first = k;
+        if (sk > 0.0) last = k;
       }
       run += sk;
     }
-    __syncthreads();
-    const bool fallback = s_cross == 0x7fffffff;  // rounding: no chunk passes u' * Z
-    const int cross = fallback ? max(s_last, 0) : s_cross;
+    block_minmax(first, last, s_mm);
+    const bool fallback = first == 0x7fffffff;  // rounding: no chunk passes u' * Z
+    const int cross = fallback ? max(last, 0) : first;
 #pragma unroll
     for (int i = 0; i < kSumPer; ++i)
-      if (kSumPer * tid + i == cross) s_pre = s_last < 0 ? 0.0 : pre_of[i];
+      if (kSumPer * tid + i == cross) s_pre = last < 0 ? 0.0 : pre_of[i];
     __syncthreads();
     const double pre = s_pre;
     __syncthreads();
@@ -519,46 +545,29 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
       double tot;
       excl = block_scan_f64(own, s_d, &tot);
     }
-    if (tid == 0) s_win = fallback ? -1 : 0x7fffffff;
-    __syncthreads();
+    // this thread's first entry passing u' * Z and last positive entry; the
+    // workgroup's first crossing wins, else (rounding, or the fallback
+    // chunk) its last positive entry
     const int ybase = c * kDrawChunk + kDrawPer * tid;
     double cum = pre + excl;
-    int mine = -1;
+    int cross_y = 0x7fffffff, last_y = -1;
     double below = cum, at = cum;
 #pragma unroll
     for (int j = 0; j < kDrawPer; ++j) {
       const double prev = cum;
       cum += rr[j];
-      if (fallback) {
-        if (rr[j] > 0.0) mine = ybase + j;
-      } else if (mine < 0 && cum > thr) {
-        mine = ybase + j;
+      if (!fallback && cross_y == 0x7fffffff && cum > thr) {
+        cross_y = ybase + j;
         below = prev;
         at = cum;
       }
+      if (rr[j] > 0.0) last_y = ybase + j;
     }
-    if (mine >= 0) {
-      if (fallback)
-        atomicMax(&s_win, mine);
-      else
-        atomicMin(&s_win, mine);
-    }
-    __syncthreads();
-    int win = s_win;
-    bool edge = fallback;
-    if (!fallback && win == 0x7fffffff) {  // rounding left no crossing: last positive
-      __syncthreads();
-      if (tid == 0) s_win = -1;
-      __syncthreads();
-      mine = -1;
-#pragma unroll
-      for (int j = 0; j < kDrawPer; ++j)
-        if (rr[j] > 0.0) mine = ybase + j;
-      if (mine >= 0) atomicMax(&s_win, mine);
-      __syncthreads();
-      win = s_win;
-      edge = true;
-    }
+    int lo = cross_y, hi = last_y;
+    block_minmax(lo, hi, s_mm);
+    const bool edge = fallback || lo == 0x7fffffff;
+    const int win = edge ? hi : lo;
+    const int mine = edge ? last_y : cross_y;
     const Decision d = s_dec;
     if (win < 0 && tid == 0) {  // no positive mass anywhere: degenerate input
       dev_flag(a.status, PVLM_DEV_RANGE);
@@ -589,9 +598,10 @@ struct APlan {
 
 pvlm_status plan_accept(int B, int gamma, int V, APlan* p) {
   if (B < 1 || gamma < 1 || V < 1) return PVLM_ERR_SHAPE;
-  if (B > kAccMaxB || gamma > 32 || V > kMaxDraw * kDrawChunk) return PVLM_ERR_UNSUPPORTED;
+  if (B > kAccMaxB || gamma > 32 || V > kMaxDraw * kAccThreads * kDrawPerMin)
+    return PVLM_ERR_UNSUPPORTED;
   p->NC = (V + kChunk - 1) / kChunk;
-  p->ND = (V + kDrawChunk - 1) / kDrawChunk;
+  p->ND = (V + kAccThreads * kDrawPerMin - 1) / (kAccThreads * kDrawPerMin);  // at most
   const size_t rows = (size_t)B * (2 * gamma + 1);
   const size_t parts = rows * p->NC;
   // counters inside the fixed synchronisation region, data after it
@@ -662,10 +672,12 @@ extern "C" pvlm_status pvlm_spec_accept(int B, int gamma, int V, float temperatu
   a.gamma = gamma;
   a.V = V;
   a.NC = p.NC;
-  a.ND = p.ND;
+  // draw chunks: 2 entries per thread unless that gives more items than CUs
+  const int dp = B * p.ND <= di.cus ? kDrawPerMin : kDrawPerMax;
+  a.ND = (V + kAccThreads * dp - 1) / (kAccThreads * dp);
   a.tau = (double)temperature;
   a.greedy = temperature == 0.f;
-  const int items = max(B * (a.greedy ? gamma + 1 : 2 * gamma + 1) * p.NC, a.greedy ? 1 : B * p.ND);
+  const int items = max(B * (a.greedy ? gamma + 1 : 2 * gamma + 1) * p.NC, a.greedy ? 1 : B * a.ND);
   // a multiple of 8 workgroups (the XCD count) keeps the cooperative queue's
   // round-robin XCD placement aligned for the launches that follow
   int grid = (items + 7) / 8 * 8;
@@ -675,8 +687,12 @@ extern "C" pvlm_status pvlm_spec_accept(int B, int gamma, int V, float temperatu
   const bool vec = V % 4 == 0 && reinterpret_cast<uintptr_t>(draft_logits) % 16 == 0 &&
                    reinterpret_cast<uintptr_t>(target_logits) % 16 == 0;
   void* args[] = {&a};
-  PVLM_HIP(launch_coresident(vec ? reinterpret_cast<const void*>(accept_kernel<true>)
-                                 : reinterpret_cast<const void*>(accept_kernel<false>),
+  const void* kern =
+      vec ? (dp == kDrawPerMin ? reinterpret_cast<const void*>(accept_kernel<true, kDrawPerMin>)
+                               : reinterpret_cast<const void*>(accept_kernel<true, kDrawPerMax>))
+          : (dp == kDrawPerMin ? reinterpret_cast<const void*>(accept_kernel<false, kDrawPerMin>)
+                               : reinterpret_cast<const void*>(accept_kernel<false, kDrawPerMax>));
+  PVLM_HIP(launch_coresident(kern,
                              dim3(grid), dim3(kAccThreads), args, 0, stream));
   return PVLM_OK;
 }
