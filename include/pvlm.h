@@ -166,10 +166,13 @@ pvlm_status pvlm_uvprune_criterion_cossim(int B, int64_t m_cap, const int32_t* m
  * are written in ascending order to idx[b, 0..k[b]) and idx[b, k[b]..k_cap)
  * is set to -1.  k[b] = 0 is legal (alpha = 1).
  *   score [B][m_cap] fp32; m, k: [B] int32 device; idx [B][k_cap] int32.
- * Each row is split over several workgroups of one co-resident launch that
- * exchange digit histograms and counts through `ws` (pvlm_topk_workspace_size
- * bytes, zero-filled before first use, reusable by later calls on the stream);
- * B may not exceed the device's compute units (PVLM_ERR_UNSUPPORTED).
+ * Rows of up to 16384 scores (m_cap <= 16384) are selected by one workgroup
+ * each and need no workspace (pvlm_topk_workspace_size returns 0, ws may be
+ * NULL).  Longer rows are split over several workgroups of one co-resident
+ * launch that exchange digit histograms and counts through `ws`
+ * (pvlm_topk_workspace_size bytes, zero-filled before first use, reusable by
+ * later calls on the stream); then B may not exceed the device's compute
+ * units (PVLM_ERR_UNSUPPORTED).
  * ---------------------------------------------------------------------- */
 size_t pvlm_topk_workspace_size(int B, int64_t m_cap);
 pvlm_status pvlm_topk_select(int B, int64_t m_cap, const int32_t* m, const int32_t* k,

@@ -9,7 +9,9 @@
 // the threshold plus the lowest-indexed ones equal to it.  The whole
 // selection is integer work, so the result is bit-exact.
 //
-// Each batch row is split over NW workgroups (one launch, grid co-resident):
+// Rows of up to 16384 scores take one 1024-thread workgroup each, the keys in
+// registers.  Longer rows are split over NW workgroups (one launch, grid
+// co-resident):
 // per digit, every workgroup histograms its slice in LDS and publishes it;
 // the last to arrive sums the NW histograms, picks the digit and publishes
 // it; the others wait for it.  The emission step exchanges per-slice counts
@@ -33,8 +35,9 @@ __device__ __forceinline__ uint32_t rank_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Exclusive prefix sum over the workgroup; returns the exclusive prefix of
-// this thread and writes the total to *total.
+// Exclusive prefix sum over a workgroup of WAVES waves; returns the exclusive
+// prefix of this thread and writes the total to *total.
+template <int WAVES = kTopkWaves>
 __device__ __forceinline__ int block_exclusive_scan(int v, int* s_warp, int* total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int x = v;
@@ -47,13 +50,46 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* s_warp, int* tot
   __syncthreads();
   int before = 0;
 #pragma unroll
-  for (int ww = 0; ww < kTopkWaves; ++ww) before += ww < w ? s_warp[ww] : 0;
+  for (int ww = 0; ww < WAVES; ++ww) before += ww < w ? s_warp[ww] : 0;
   int tot = 0;
 #pragma unroll
-  for (int ww = 0; ww < kTopkWaves; ++ww) tot += s_warp[ww];
+  for (int ww = 0; ww < WAVES; ++ww) tot += s_warp[ww];
   *total = tot;
   __syncthreads();
   return before + x - v;
+}
+
+// One wave (lanes 0-63): the digit of a 256-bin histogram (counts of the
+// keys in the current prefix range, by next digit) that holds the need-th
+// largest key, scanning digits from the top.  Lane l owns digits 255 - 4l ..
+// 252 - 4l.  The lane that finds it calls found(digit, keys above the digit).
+template <typename F>
+__device__ __forceinline__ void find_digit(const int* hist, int need, F found) {
+  const int lane = threadIdx.x & 63;
+  int c[4], own = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    c[q] = hist[255 - 4 * lane - q];
+    own += c[q];
+  }
+  int incl = own;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += y;
+  }
+  const int excl = incl - own;
+  if (excl < need && need <= incl) {
+    int acc = excl;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (acc + c[q] >= need) {
+        found(255 - 4 * lane - q, acc);
+        break;
+      }
+      acc += c[q];
+    }
+  }
 }
 
 struct TArgs {
@@ -182,35 +218,11 @@ __global__ void __launch_bounds__(kTopkThreads) topk_kernel(TArgs a) {
       }
       hist[tid] = t;
       __syncthreads();
-      if (tid < 64) {
-        // lane l owns digits 255-4l .. 252-4l (descending)
-        int c[4], own = 0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          c[q] = hist[255 - 4 * tid - q];
-          own += c[q];
-        }
-        int incl = own;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const int y = __shfl_up(incl, o, 64);
-          if (tid >= o) incl += y;
-        }
-        const int excl = incl - own;
-        const int need = kb - above;
-        if (excl < need && need <= incl) {
-          int acc = excl;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            if (acc + c[q] >= need) {
-              st_agent(a.res + b * 4, 255 - 4 * tid - q);
-              st_agent(a.res + b * 4 + 1, above + acc);
-              break;
-            }
-            acc += c[q];
-          }
-        }
-      }
+      if (tid < 64)
+        find_digit(hist, kb - above, [&](int digit, int acc) {
+          st_agent(a.res + b * 4, digit);
+          st_agent(a.res + b * 4 + 1, above + acc);
+        });
     });
     if (tid == 0) {
       s_res[0] = ld_agent(a.res + b * 4);
@@ -298,6 +310,161 @@ __global__ void __launch_bounds__(kTopkThreads) topk_kernel(TArgs a) {
   }
 }
 
+// Rows of at most kSmallMax scores: one 1024-thread workgroup per row, no
+// inter-workgroup exchange.  Thread t holds the keys of entries e * 1024 + t
+// (coalesced loads) in registers.  The radix select takes three digits of
+// 12, 10 and 10 bits: float keys of real data share few values of their top
+// 8 bits (sign and exponent), and a first digit that wide spreads them over
+// enough histogram bins that the LDS atomics rarely collide.  The ordered
+// emission computes every selected entry's output position directly from
+// per-(entry round, wave) counts, so no thread needs a contiguous range.
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallWaves = kSmallThreads / 64;
+constexpr int kSmallMaxPer = 16;  // beyond 16384 scores, several workgroups per row are faster
+constexpr int kSmallMax = kSmallThreads * kSmallMaxPer;
+constexpr int kSmallBins = 4096;
+
+template <int PER>
+__global__ void __launch_bounds__(kSmallThreads) topk_small_kernel(TArgs a) {
+  __shared__ int hist[kSmallBins];
+  __shared__ int s_warp[kSmallWaves];
+  __shared__ int s_res[2];
+  __shared__ int s_cnt[2][PER][kSmallWaves];  // per (round e, wave): keys above tau, equal to tau
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  const float* sc = a.score + (size_t)b * a.m_cap;
+  int32_t* out = a.idx + (size_t)b * a.k_cap;
+  int mb = a.m[b], kb = a.k[b];
+  bool bad = false;
+  if (mb < 0 || mb > a.m_cap) {
+    bad = true;
+    mb = mb < 0 ? 0 : (int)a.m_cap;
+  }
+  const int kmax = mb < a.k_cap ? mb : a.k_cap;
+  if (kb < 0 || kb > kmax) {
+    bad = true;
+    kb = kb < 0 ? 0 : kmax;
+  }
+  if (bad && tid == 0) dev_flag(a.status, PVLM_DEV_RANGE);
+  for (int r = kb + tid; r < a.k_cap; r += kSmallThreads) out[r] = -1;
+  if (kb == 0) return;  // uniform across the workgroup
+  uint32_t kr[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int i = e * kSmallThreads + tid;
+    kr[e] = i < mb ? rank_key(sc[i]) : 0u;
+  }
+
+  // ---- radix select of the kb-th largest key: digits [31:20], [19:10], [9:0]
+  uint32_t prefix = 0, mask = 0;
+  int above = 0;
+#pragma unroll 1
+  for (int pass = 0; pass < 3; ++pass) {
+    const int shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
+    const int nb = pass == 0 ? 4096 : 1024;
+    for (int i = tid; i < nb; i += kSmallThreads) hist[i] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < PER; ++e)
+      if (e * kSmallThreads + tid < mb && (kr[e] & mask) == prefix)
+        atomicAdd(&hist[(kr[e] >> shift) & (uint32_t)(nb - 1)], 1);
+    __syncthreads();
+    // bins in descending order: thread t owns q = nb / 1024 consecutive ones
+    const int q = nb / kSmallThreads;
+    const int top = nb - 1 - tid * q;
+    int own = 0;
+    for (int j = 0; j < q; ++j) own += hist[top - j];
+    int tot;
+    const int excl = block_exclusive_scan<kSmallWaves>(own, s_warp, &tot);
+    const int need = kb - above;
+    if (excl < need && need <= excl + own) {
+      int acc = excl;
+      for (int j = 0; j < q; ++j) {
+        const int c = hist[top - j];
+        if (acc + c >= need) {
+          s_res[0] = top - j;
+          s_res[1] = above + acc;
+          break;
+        }
+        acc += c;
+      }
+    }
+    __syncthreads();
+    prefix |= (uint32_t)s_res[0] << shift;
+    mask |= (uint32_t)(nb - 1) << shift;
+    above = s_res[1];
+  }
+  const uint32_t tau = prefix;
+  const int need_eq = kb - above;  // keys equal to tau to keep, lowest indices first
+
+  // ---- emission: output position of entry (e, w, lane) = keys above tau
+  //      before it + min(keys equal to tau before it, need_eq)
+  uint64_t bg[PER], be[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const bool valid = e * kSmallThreads + tid < mb;
+    bg[e] = __ballot(valid && kr[e] > tau);
+    be[e] = __ballot(valid && kr[e] == tau);
+    if (lane == 0) {
+      s_cnt[0][e][w] = __popcll(bg[e]);
+      s_cnt[1][e][w] = __popcll(be[e]);
+    }
+  }
+  __syncthreads();
+  // exclusive prefix over (e, w) in that order, by one wave: lane l takes
+  // PER * kSmallWaves / 64 consecutive slots
+  if (w == 0) {
+    constexpr int kSlots = PER * kSmallWaves;
+    constexpr int kPerLane = (kSlots + 63) / 64;
+    int* cg = &s_cnt[0][0][0];
+    int* ce = &s_cnt[1][0][0];
+    int sg = 0, se = 0;
+#pragma unroll
+    for (int j = 0; j < kPerLane; ++j) {
+      const int sl = lane * kPerLane + j;
+      if (sl < kSlots) {
+        sg += cg[sl];
+        se += ce[sl];
+      }
+    }
+    int ig = sg, ie = se;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int yg = __shfl_up(ig, o, 64), ye = __shfl_up(ie, o, 64);
+      if (lane >= o) {
+        ig += yg;
+        ie += ye;
+      }
+    }
+    int rg = ig - sg, re = ie - se;
+#pragma unroll
+    for (int j = 0; j < kPerLane; ++j) {
+      const int sl = lane * kPerLane + j;
+      if (sl < kSlots) {
+        const int g = cg[sl], q = ce[sl];
+        cg[sl] = rg;
+        ce[sl] = re;
+        rg += g;
+        re += q;
+      }
+    }
+  }
+  __syncthreads();
+  const uint64_t below = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const bool gt = (bg[e] >> lane) & 1ull, eq = (be[e] >> lane) & 1ull;
+    if (gt || eq) {
+      const int gt_before = s_cnt[0][e][w] + __popcll(bg[e] & below);
+      const int eq_before = s_cnt[1][e][w] + __popcll(be[e] & below);
+      if (gt || eq_before < need_eq) {
+        const int pos = gt_before + min(eq_before, need_eq);
+        if (pos < kb) out[pos] = e * kSmallThreads + tid;
+      }
+    }
+  }
+}
+
 struct TPlan {
   int NW, slice;
   size_t off_arrive, off_gen, off_hist, off_res, off_cnt, bytes;
@@ -305,6 +472,12 @@ struct TPlan {
 
 pvlm_status plan_topk(int B, int64_t m_cap, TPlan* p) {
   if (B < 1 || m_cap < 1 || m_cap > ((int64_t)1 << 30)) return PVLM_ERR_SHAPE;
+  if (m_cap <= kSmallMax) {  // one workgroup per row, no workspace
+    p->NW = 1;
+    p->slice = (int)m_cap;
+    p->bytes = 0;
+    return PVLM_OK;
+  }
   DeviceInfo di;
   pvlm_status st = device_info(&di);
   if (st != PVLM_OK) return st;
@@ -351,28 +524,34 @@ extern "C" pvlm_status pvlm_topk_select(int B, int64_t m_cap, const int32_t* m, 
   TPlan p;
   pvlm_status st = plan_topk(B, m_cap, &p);
   if (st != PVLM_OK) return st;
-  if (!ws || ws_bytes < p.bytes) return PVLM_ERR_WORKSPACE;
-  char* wsb = static_cast<char*>(ws);
-  TArgs a;
+  if (p.bytes > 0 && (!ws || ws_bytes < p.bytes)) return PVLM_ERR_WORKSPACE;
+  TArgs a = {};
   a.score = score;
   a.m = m;
   a.k = k;
   a.idx = idx;
   a.status = status;
-  a.hist = reinterpret_cast<int*>(wsb + p.off_hist);
-  a.res = reinterpret_cast<int*>(wsb + p.off_res);
-  a.cnt = reinterpret_cast<int*>(wsb + p.off_cnt);
-  a.arrive = reinterpret_cast<int*>(wsb + p.off_arrive);
-  a.gen = reinterpret_cast<unsigned*>(wsb + p.off_gen);
   a.m_cap = m_cap;
   a.k_cap = k_cap;
   a.NW = p.NW;
   a.slice = p.slice;
   void* args[] = {&a};
+  if (m_cap <= kSmallMax) {
+    const void* kern = m_cap <= kSmallThreads * 4   ? reinterpret_cast<const void*>(topk_small_kernel<4>)
+                       : m_cap <= kSmallThreads * 8 ? reinterpret_cast<const void*>(topk_small_kernel<8>)
+                                                    : reinterpret_cast<const void*>(topk_small_kernel<kSmallMaxPer>);
+    PVLM_HIP(hipLaunchKernel(kern, dim3(B), dim3(kSmallThreads), args, 0, stream));
+    return PVLM_OK;
+  }
+  char* wsb = static_cast<char*>(ws);
+  a.hist = reinterpret_cast<int*>(wsb + p.off_hist);
+  a.res = reinterpret_cast<int*>(wsb + p.off_res);
+  a.cnt = reinterpret_cast<int*>(wsb + p.off_cnt);
+  a.arrive = reinterpret_cast<int*>(wsb + p.off_arrive);
+  a.gen = reinterpret_cast<unsigned*>(wsb + p.off_gen);
   const void* kern = p.slice <= kTopkThreads * kPerThread
                          ? reinterpret_cast<const void*>(topk_kernel<true>)
                          : reinterpret_cast<const void*>(topk_kernel<false>);
-  PVLM_HIP(launch_coresident(kern, dim3(B * p.NW),
-                             dim3(kTopkThreads), args, 0, stream));
+  PVLM_HIP(launch_coresident(kern, dim3(B * p.NW), dim3(kTopkThreads), args, 0, stream));
   return PVLM_OK;
 }

@@ -13,7 +13,7 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("kind", ["normal", "ties", "zeros", "special"])
-@pytest.mark.parametrize("m_cap", [1, 1000, 12544, 40000, 131072])
+@pytest.mark.parametrize("m_cap", [1, 1000, 5000, 12544, 16384, 16385, 40000, 131072])
 def test_topk_bit_exact(kind, m_cap):
     B = 3
     s = W.make_scores(B, m_cap, kind, seed=m_cap)
