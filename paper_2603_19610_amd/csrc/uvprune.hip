@@ -88,6 +88,7 @@ __global__ void __launch_bounds__(256) txt_norm_kernel(const T* ht, int64_t off0
   if (j < nb) {
     const T* row = ht + (slot ? off1 : off0) + ((size_t)b * n_cap + j) * Dh;
     float ss = 0.f;
+#pragma unroll 8  // the row's loads in flight together
     for (int d = lane * 8; d < Dh; d += 512) {
       float f[8];
       HS<T>::load8(row + d, f);
@@ -100,31 +101,48 @@ __global__ void __launch_bounds__(256) txt_norm_kernel(const T* ht, int64_t off0
   if (lane == 0) inv_norm[wid] = inv;
 }
 
-// u[slot][b][d] = sum_{j<n[b]} ht[layer][b][j][d] * inv_norm[slot][b][j];
-// each thread owns 8 consecutive d.
+// u[slot][b][d] = sum_{j<n[b]} ht[layer][b][j][d] * inv_norm[slot][b][j], in
+// two steps so that many workgroups share the rows: partial sums over chunks
+// of kTxtChunk text rows (one wave per 512 columns and chunk, each lane 8
+// columns), then the chunks' sums in chunk order.
+constexpr int kTxtChunk = 32;
+
 template <typename T>
-__global__ void __launch_bounds__(256) txt_dir_kernel(const T* ht, int64_t off0, int64_t off1,
-                                                      const int32_t* n_txt,
-                                                      int B, int64_t n_cap, int Dh,
-                                                      const float* inv_norm, float* u) {
-  const int slot = blockIdx.z, b = blockIdx.y;
-  const int d = (blockIdx.x * blockDim.x + threadIdx.x) * 8;
+__global__ void __launch_bounds__(64) txt_dir_part_kernel(const T* ht, int64_t off0, int64_t off1,
+                                                          const int32_t* n_txt, int B,
+                                                          int64_t n_cap, int Dh, int nchunk,
+                                                          const float* inv_norm, float* part) {
+  const int c = blockIdx.y, sb = blockIdx.z, slot = sb / B, b = sb % B;
+  const int d = (blockIdx.x * 64 + threadIdx.x) * 8;
   if (d >= Dh) return;
   int nb = n_txt[b];
   nb = nb < 0 ? 0 : (nb > n_cap ? (int)n_cap : nb);
+  const int j0 = c * kTxtChunk, j1 = min(nb, j0 + kTxtChunk);
   const T* base = ht + (slot ? off1 : off0) + (size_t)b * n_cap * Dh + d;
   const float* inv = inv_norm + ((size_t)slot * B + b) * n_cap;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int j = 0; j < nb; ++j) {
-    const float w = inv[j];
+#pragma unroll 8  // rows' loads in flight together
+  for (int j = j0; j < j1; ++j) {
+    const float wj = inv[j];
     float f[8];
     HS<T>::load8(base + (size_t)j * Dh, f);
 #pragma unroll
-    for (int k = 0; k < 8; ++k) acc[k] = fmaf(f[k], w, acc[k]);
+    for (int k = 0; k < 8; ++k) acc[k] = fmaf(f[k], wj, acc[k]);
   }
-  float* up = u + ((size_t)slot * B + b) * Dh + d;
-#pragma unroll
-  for (int k = 0; k < 8; ++k) up[k] = acc[k];
+  float* pp = part + ((size_t)sb * nchunk + c) * Dh + d;
+  *reinterpret_cast<float4*>(pp) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+  *reinterpret_cast<float4*>(pp + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
+}
+
+__global__ void __launch_bounds__(256) txt_dir_sum_kernel(const float* part, int Dh, int nchunk,
+                                                          float* u) {
+  const int sb = blockIdx.y;
+  const int d = blockIdx.x * 256 + threadIdx.x;
+  if (d >= Dh) return;
+  const float* p = part + (size_t)sb * nchunk * Dh + d;
+  float acc = 0.f;
+  for (int c = 0; c < nchunk; ++c) acc += p[(size_t)c * Dh];
+  u[(size_t)sb * Dh + d] = acc;
 }
 
 // One wave per visual row: c_slot = <hv, u_slot> / |hv| (0 for zero norm).
@@ -170,9 +188,13 @@ __global__ void __launch_bounds__(256) vis_kernel(const T* hv, int64_t off0, int
   if (lane == 0) out[wid] = res;
 }
 
+int txt_chunks(int64_t n_cap) { return (int)((n_cap + kTxtChunk - 1) / kTxtChunk); }
+
+// inverse norms [2][B][n_cap], u [2][B][Dh], chunk partials [2][B][chunks][Dh]
 size_t cossim_ws(int B, int Dh, int64_t n_cap) {
   size_t off = align_up(sizeof(float) * 2 * (size_t)B * n_cap, 256);
   off = align_up(off + sizeof(float) * 2 * (size_t)B * Dh, 256);
+  off = align_up(off + sizeof(float) * 2 * (size_t)B * txt_chunks(n_cap) * Dh, 256);
   return off;
 }
 
@@ -180,13 +202,17 @@ template <typename T>
 pvlm_status launch_cossim(int nslots, int64_t voff0, int64_t voff1, int64_t toff0, int64_t toff1,
                           int B, int64_t m_cap, const int32_t* m, int Dh, int64_t n_cap,
                           const int32_t* n_txt, const T* hv, const T* ht, float* outp, float* inv,
-                          float* u, int32_t* status, hipStream_t stream) {
+                          float* u, float* part, int32_t* status, hipStream_t stream) {
   const int64_t nw = (int64_t)nslots * B * n_cap;
   hipLaunchKernelGGL(txt_norm_kernel<T>, dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream, ht,
                      toff0, toff1, n_txt, nslots, B, n_cap, Dh, inv, status);
   PVLM_LAUNCHED();
-  hipLaunchKernelGGL(txt_dir_kernel<T>, dim3((Dh / 8 + 255) / 256, B, nslots), dim3(256), 0, stream,
-                     ht, toff0, toff1, n_txt, B, n_cap, Dh, inv, u);
+  const int nchunk = txt_chunks(n_cap);
+  hipLaunchKernelGGL(txt_dir_part_kernel<T>, dim3((Dh / 8 + 63) / 64, nchunk, nslots * B), dim3(64), 0,
+                     stream, ht, toff0, toff1, n_txt, B, n_cap, Dh, nchunk, inv, part);
+  PVLM_LAUNCHED();
+  hipLaunchKernelGGL(txt_dir_sum_kernel, dim3((Dh + 255) / 256, nslots * B), dim3(256), 0, stream, part,
+                     Dh, nchunk, u);
   PVLM_LAUNCHED();
   const int64_t vw = (int64_t)B * m_cap;
   hipLaunchKernelGGL(vis_kernel<T>, dim3((unsigned)((vw + 3) / 4)), dim3(256), 0, stream, hv, voff0,
@@ -211,16 +237,19 @@ pvlm_status run_cossim(int nslots, int L, int B, int64_t m_cap, const int32_t* m
   char* w = static_cast<char*>(ws);
   float* inv = reinterpret_cast<float*>(w);
   float* u = reinterpret_cast<float*>(w + align_up(sizeof(float) * 2 * (size_t)B * n_cap, 256));
+  float* part = reinterpret_cast<float*>(
+      w + align_up(align_up(sizeof(float) * 2 * (size_t)B * n_cap, 256) + sizeof(float) * 2 * (size_t)B * Dh,
+                   256));
   const int64_t vls = (int64_t)B * m_cap * Dh, tls = (int64_t)B * n_cap * Dh;
   const int64_t l1 = nslots == 2 ? L : 0;
   if (hdt == PVLM_BF16)
     return launch_cossim<uint16_t>(nslots, 0, l1 * vls, 0, l1 * tls, B, m_cap, m, Dh, n_cap, n_txt,
                                    static_cast<const uint16_t*>(hs_vis),
-                                   static_cast<const uint16_t*>(hs_txt), outp, inv, u, status,
+                                   static_cast<const uint16_t*>(hs_txt), outp, inv, u, part, status,
                                    stream);
   return launch_cossim<float>(nslots, 0, l1 * vls, 0, l1 * tls, B, m_cap, m, Dh, n_cap, n_txt,
                               static_cast<const float*>(hs_vis), static_cast<const float*>(hs_txt),
-                              outp, inv, u, status, stream);
+                              outp, inv, u, part, status, stream);
 }
 
 }  // namespace
