@@ -29,6 +29,22 @@ def test_topk_bit_exact(kind, m_cap):
     assert np.array_equal(idx.cpu().numpy(), ref)
 
 
+def test_topk_many_long_rows():
+    """More rows x slices than compute units: the 256-thread slice path."""
+    B, m_cap = 40, 100000
+    s = W.make_scores(B, m_cap, "normal", seed=5)
+    rng = np.random.default_rng(5)
+    m = rng.integers(m_cap // 2, m_cap + 1, size=B).astype(np.int32)
+    k = (m // 20).astype(np.int32)
+    k_cap = int(k.max())
+    note(f"topk many long rows B={B} m_cap={m_cap}")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    idx = pv.topk_select(to_dev(s), to_dev(m), to_dev(k), k_cap, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    assert np.array_equal(idx.cpu().numpy(), oracle.topk_select(s, m, k, k_cap))
+
+
 def test_topk_keep_counts_of_workloads():
     for name in ("tiny", "llava7b", "llava72b", "qwen32b"):
         w = W.WORKLOADS[name]
