@@ -45,6 +45,8 @@ SHAPES = [
     (1, 3, 8, 8, 128, [20000], "bf16"),            # chunks > 512 tokens: stream variant
     (2, 3, 12, 4, 64, [77, 129], "f32"),           # fp32 path, D = 64, 3 row tiles
     (1, 4, 8, 1, 128, [333], "f32"),               # fp32 path, D = 128
+    (1, 32, 16, 2, 128, [700], "bf16"),            # T = 32 (the maximum): 256 rows, 4 row groups
+    (4, 9, 28, 4, 128, [100, 900, 3, 1500], "bf16"),  # batch 4 ragged, 7B head layout
 ]
 
 
