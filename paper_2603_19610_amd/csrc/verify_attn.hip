@@ -32,9 +32,11 @@
 //  * The mass is summed over KV heads and row groups by whichever workgroup
 //    of a chunk arrives last.  Every sum runs in a fixed order, so results
 //    are bit-reproducible.
-//  * Workgroups exchange data only through device-coherent stores and loads
-//    followed by a relaxed counter increment and a polling wait (no cache
-//    flush).
+//  * Workgroups exchange data through stores the writer waits for, a relaxed
+//    counter increment and a polling wait (no cache flush).  Within a group
+//    the stores and loads are plain when every workgroup of the group runs
+//    on one XCD (one L2; each address is written once per launch), else
+//    device-coherent; across groups (the mass sum) always device-coherent.
 //  * fp32 inputs take a VALU path with the two-wait structure.
 #include "common.h"
 
