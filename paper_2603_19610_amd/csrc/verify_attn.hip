@@ -19,13 +19,15 @@
 //  * "Resident" variant (chunks up to 512 tokens): every wave puts its K
 //    blocks in flight straight into MFMA operand registers, waves 1-3 stream
 //    the chunk's V into LDS behind them (global_load_lds), and the scores stay
-//    in registers.  P.V then runs against the workgroup's own row maxima, the
-//    four waves' O fragments are reduce-scattered through LDS, and the chunk
-//    partial (bf16) and the row statistics are published.  One wait on the
-//    group counter follows; after it each workgroup forms every row's global
-//    log-sum-exp, the exact normalised mass of its own tokens from the
-//    resident scores, and one slice of O as the factor-weighted sum of the
-//    chunk partials.
+//    in registers as probabilities relative to the workgroup's row maxima.
+//    The row statistics are published and, by the time V has landed, the
+//    group's other chunks have published theirs: one wait, then every row's
+//    global log-sum-exp makes the resident probabilities exact (one multiply
+//    per score), and P.V runs fused with the mass of the chunk's tokens, so
+//    the scores die block by block.  The four waves' O fragments are
+//    reduce-scattered through LDS and the normalised chunk partial (bf16) is
+//    published; after a second wait each workgroup writes one slice of O as
+//    the plain sum of the group's chunk partials.
 //  * "Stream" variant (longer chunks): statistics are exchanged after pass 1,
 //    pass 2 recomputes the scores from K (K is read twice) with the exact
 //    global log-sum-exp, and a second wait precedes the O sum.
@@ -54,11 +56,24 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kNegInf = -__builtin_huge_valf();
 
+// Field order matters for the kernels' scalar registers: the argument loads
+// merge adjacent fields into wide scalar loads whose registers are then
+// allocated (and, under pressure, spilled and restored) as one unit.  The
+// inputs read at the start, the sizes used throughout, and the workspace and
+// output pointers used late therefore sit in three separate runs.
 struct VArgs {
   const void* q;
   const void* k;
   const void* v;
   const int32_t* ctx_len;
+  int64_t n_cap;
+  int B, T, Hq, Hkv, G, R, RG, RT, D;
+  int max_ctx;
+  int splits, chunk, grp_base, ngrp, grid;
+  int xmap;         // workgroup i runs on XCD i % xmap (1: no XCD-aware mapping)
+  int local;        // every group's workgroups share one XCD
+  float sl2;        // scale * log2(e)
+  int f32;
   float* stats;     // [groups][splits] records of ROWS + 1 float2 (padded to 128 B):
                     // (log2-domain max, exp-sum) per row, then the launch tag
   float* opart;     // [groups][splits][ROWS][D] (bf16 pairs, or fp32)
@@ -71,14 +86,6 @@ struct VArgs {
   float* lse;
   float* mass;
   int32_t* status;
-  int64_t n_cap;
-  int B, T, Hq, Hkv, G, R, RG, RT, D;
-  int max_ctx;
-  int splits, chunk, grp_base, ngrp, grid;
-  int xmap;         // workgroup i runs on XCD i % xmap (1: no XCD-aware mapping)
-  int local;        // every group's workgroups share one XCD
-  float sl2;        // scale * log2(e)
-  int f32;
 };
 
 struct Unit {
@@ -196,19 +203,17 @@ __device__ __forceinline__ void o_finish(const VArgs& a, const Unit& u, unsigned
 // Every row's statistics over the group's nsp chunks, combined in parallel
 // (P thread sets per row): leaves the row's log2-sum-exp in s_lse (+inf for
 // padding rows, whose probabilities are then 0), its global max in s_pm[0]
-// and 1/sum in s_pz[0] (0 for padding rows) and, if s_fac is given, each
-// chunk's row max in s_fac[chunk * ROWS + row].
+// and 1/sum in s_pz[0] (0 for padding rows).
 template <int ROWS, bool LOCAL>
-__device__ void stats_combine(const VArgs& a, const Unit& u, int nsp, float* s_lse, float* s_fac,
+__device__ void stats_combine(const VArgs& a, const Unit& u, int nsp, float* s_lse,
                               float (*s_pm)[ROWS], float (*s_pz)[ROWS], unsigned base) {
   constexpr int kU = 16;
   constexpr int P = kThreads / ROWS < kWaves ? kThreads / ROWS : kWaves;
   const int tid = threadIdx.x;
   const float2* st0 = stats_rec<ROWS>(a, u, 0);
-  for (int sp = tid; sp < nsp; sp += kThreads) {  // every chunk's record is from this launch
-    const float2 h = x_load<LOCAL>(st0 + (size_t)sp * rec_stride<ROWS>() + ROWS);
-    if (__float_as_uint(h.x) != base + 1u) dev_flag(a.status, PVLM_DEV_PLACEMENT);
-  }
+  // every chunk's record is from this launch (its tag word); the first
+  // kThreads tags load together with the statistics and are checked after
+  const float2 tag = x_load<LOCAL>(st0 + (size_t)min(tid, nsp - 1) * rec_stride<ROWS>() + ROWS);
   if (tid < P * ROWS) {
     const int r = tid % ROWS, part = tid / ROWS;
     float M = kNegInf, Z = 0.f;
@@ -217,17 +222,27 @@ __device__ void stats_combine(const VArgs& a, const Unit& u, int nsp, float* s_l
 #pragma unroll
       for (int j = 0; j < kU; ++j)  // unconditional (clamped) loads: fine-grained waits
         v[j] = x_load<LOCAL>(st0 + (size_t)min(s0 + j * P, nsp - 1) * rec_stride<ROWS>() + r);
+      // the batch's maximum (exact in any order), then its exp-sum relative
+      // to it: independent exp2s instead of a chain of pairwise combines
+      float bm = kNegInf;
 #pragma unroll
-      for (int j = 0; j < kU; ++j) {
-        const int sp = s0 + j * P;
-        if (sp < nsp) {
-          if (s_fac) s_fac[sp * ROWS + r] = v[j].x;
-          lse_combine(M, Z, v[j].x, v[j].y);
-        }
+      for (int j = 0; j < kU; ++j)
+        if (s0 + j * P < nsp) bm = fmaxf(bm, v[j].x);
+      float bz = 0.f;
+      if (bm != kNegInf) {
+#pragma unroll
+        for (int j = 0; j < kU; ++j)
+          if (s0 + j * P < nsp) bz += v[j].y * fast_exp2(v[j].x - bm);
       }
+      lse_combine(M, Z, bm, bz);
     }
     s_pm[part][r] = M;
     s_pz[part][r] = Z;
+  }
+  if (__float_as_uint(tag.x) != base + 1u) dev_flag(a.status, PVLM_DEV_PLACEMENT);
+  for (int sp = tid + kThreads; sp < nsp; sp += kThreads) {
+    const float2 h = x_load<LOCAL>(st0 + (size_t)sp * rec_stride<ROWS>() + ROWS);
+    if (__float_as_uint(h.x) != base + 1u) dev_flag(a.status, PVLM_DEV_PLACEMENT);
   }
   lds_sync();
   if (tid < ROWS) {
@@ -259,40 +274,44 @@ __device__ void exchange_stats(const VArgs& a, const Unit& u, const float* s_m, 
   }
   __syncthreads();
   if (wait)
-    stats_combine<ROWS, LOCAL>(a, u, (u.N + a.chunk - 1) / a.chunk, s_lse, nullptr, s_pm, s_pz, base);
+    stats_combine<ROWS, LOCAL>(a, u, (u.N + a.chunk - 1) / a.chunk, s_lse, s_pm, s_pz, base);
 }
 
 // Per-token mass summed over the KV heads and row groups by the last
 // workgroup of each chunk to arrive (the chunk's workgroups sit on different
 // XCDs, so these exchanges are device-coherent).
-__device__ void mass_combine(const VArgs& a, const Unit& u, int* s_flag) {
+__device__ __forceinline__ int* mass_counter(const VArgs& a, const Unit& u) {
+  return a.mcnt + ((size_t)u.b * a.splits + u.split) * (kSyncLine / sizeof(int));
+}
+// The chunk's mass sum, by its last arrival (every partial is published).
+__device__ void mass_sum(const VArgs& a, const Unit& u) {
   const int tid = threadIdx.x;
-  if (!a.mass) return;
   const int P = a.Hkv * a.RG;
-  int* mc = a.mcnt + ((size_t)u.b * a.splits + u.split) * (kSyncLine / sizeof(int));
-  if (wg_signal_last(mc, P, s_flag)) {
-    const int64_t lo = u.c0;
-    const int64_t hi_sum = u.c1 > u.c0 ? u.c1 : u.c0;
-    const int64_t chunk_end = (int64_t)u.c0 + a.chunk;
-    const int64_t hi = u.split == a.splits - 1 ? a.n_cap : (chunk_end < a.n_cap ? chunk_end : a.n_cap);
-    const float* mp = a.mpart + (size_t)u.b * P * a.n_cap;
-    float* ms = a.mass + (size_t)u.b * a.n_cap;
-    for (int64_t i = lo + tid; i < hi; i += kThreads) {
-      float acc = 0.f;
-      if (i < hi_sum) {
-        for (int p0 = 0; p0 < P; p0 += 8) {
-          float v[8];
+  const int64_t lo = u.c0;
+  const int64_t hi_sum = u.c1 > u.c0 ? u.c1 : u.c0;
+  const int64_t chunk_end = (int64_t)u.c0 + a.chunk;
+  const int64_t hi = u.split == a.splits - 1 ? a.n_cap : (chunk_end < a.n_cap ? chunk_end : a.n_cap);
+  const float* mp = a.mpart + (size_t)u.b * P * a.n_cap;
+  float* ms = a.mass + (size_t)u.b * a.n_cap;
+  for (int64_t i = lo + tid; i < hi; i += kThreads) {
+    float acc = 0.f;
+    if (i < hi_sum) {
+      for (int p0 = 0; p0 < P; p0 += 8) {
+        float v[8];
 #pragma unroll
-          for (int j = 0; j < 8; ++j)
-            v[j] = p0 + j < P ? ld_agent(mp + (size_t)(p0 + j) * a.n_cap + i) : 0.f;
+        for (int j = 0; j < 8; ++j)
+          v[j] = p0 + j < P ? ld_agent(mp + (size_t)(p0 + j) * a.n_cap + i) : 0.f;
 #pragma unroll
-          for (int j = 0; j < 8; ++j) acc += v[j];
-        }
+        for (int j = 0; j < 8; ++j) acc += v[j];
       }
-      ms[i] = acc;
     }
-    if (tid == 0) reset_counter(mc);
+    ms[i] = acc;
   }
+  if (tid == 0) reset_counter(mass_counter(a, u));
+}
+__device__ void mass_combine(const VArgs& a, const Unit& u, int* s_flag) {
+  if (!a.mass) return;
+  if (wg_signal_last(mass_counter(a, u), a.Hkv * a.RG, s_flag)) mass_sum(a, u);
 }
 
 // End of the two-pass variants: the O partials are published (every wave's
@@ -726,18 +745,32 @@ __device__ __forceinline__ void block_probs(floatx4 (&S)[2][RT], const int (&vis
   }
 }
 
-// O += P.V of one block (P resident, converted to bf16 for the MFMA).
+// One resident block with the global statistics known: exact probabilities
+// p = P * c (P relative to the workgroup's row maximum ref, c = exp2(ref -
+// lse) per row), their sum over the block's rows (the workgroup's share of
+// each token's mass, written to mp when mp is set) and O += p.V on MFMA (p
+// converted to bf16).
 template <int D, int RT>
-__device__ __forceinline__ void pv_resident(const floatx4 (&P)[2][RT], const typename VVec<D>::T (&Vr)[8],
-                                            floatx4 (&O)[RT][D / 16]) {
+__device__ __forceinline__ void pv_exact_resident(const floatx4 (&P)[2][RT], const float (&c)[RT],
+                                                  const typename VVec<D>::T (&Vr)[8],
+                                                  floatx4 (&O)[RT][D / 16], float* mp, int tb, int c1,
+                                                  int n, int gq) {
   constexpr int DPL = D / 16;
+  float pm[8];
+#pragma unroll
+  for (int v = 0; v < 8; ++v) pm[v] = 0.f;
   bf16x8 Pa[RT];
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) Pa[rt][4 * tt + i] = static_cast<__bf16>(P[tt][rt][i]);
+      for (int i = 0; i < 4; ++i) {
+        const float p = P[tt][rt][i] * c[rt];
+        pm[4 * tt + i] += p;
+        Pa[rt][4 * tt + i] = static_cast<__bf16>(p);
+      }
+  if (mp) mass_reduce_store(pm, mp, tb, c1, n, gq);
 #pragma unroll
   for (int jd = 0; jd < DPL; ++jd) {
     const bf16x8 vb = pack_v(Vr, jd);
@@ -746,28 +779,6 @@ __device__ __forceinline__ void pv_resident(const floatx4 (&P)[2][RT], const typ
       O[rt][jd] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Pa[rt], vb, O[rt][jd], 0, 0, 0);
   }
 }
-
-// Exact probabilities of one block summed over its rows (the workgroup's
-// share of the per-token mass), written to mp: the resident P relative to
-// the workgroup's row maximum times c = exp2(ref - lse) per row.
-template <int RT>
-__device__ __forceinline__ void mass_block_resident(const floatx4 (&P)[2][RT], const float (&c)[RT],
-                                                    float* mp, int tb, int c1, int n, int gq) {
-  float pm[8];
-#pragma unroll
-  for (int v = 0; v < 8; ++v) pm[v] = 0.f;
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) pm[4 * tt + i] = fmaf(P[tt][rt][i], c[rt], pm[4 * tt + i]);
-  mass_reduce_store(pm, mp, tb, c1, n, gq);
-}
-
-// Exact probabilities exp2(S - lse2) of one block summed over its rows: the
-// workgroup's share of the per-token attention mass, written to mp.
-
 
 // P = exp2(S - lse2): per-token mass (sum over the block's rows, written to
 // mp) and O += P.V on MFMA.
@@ -873,38 +884,32 @@ __device__ __forceinline__ void write_opart(const VArgs& a, const Unit& u, float
   }
 }
 
-// Resident variant, after the chunk partial of O (relative to the
-// workgroup's own row maxima) is published and the workgroup has arrived at
-// cnt_o (thread 0 holds the value the arrival returned): wait for the group's
-// statistics (published right after pass 1, so normally complete), form each
-// row's global log2-sum-exp and the per-chunk rescale factors, wait for the O
-// partials and put the loads of this workgroup's O slice in flight, compute
-// the exact per-token mass from the resident scores meanwhile, then the
-// factor-weighted O sum, lse, and the mass sum over KV heads.
+// Resident variant, after the chunk partial of O (already normalised by the
+// rows' global statistics) and the mass partials are published and the
+// workgroup has arrived at cnt_o (thread 0 holds the value the arrival
+// returned): arrive at the chunk's mass counter (the chunk's last arrival
+// sums the mass over KV heads while its group's O partials land), wait for
+// the group's O partials, and write this workgroup's slice of O (the plain
+// sum over chunks) and the lse.
 template <int D, int RT, bool LOCAL>
-__device__ void verify_epilogue_local(const VArgs& a, const Unit& u, const floatx4 (&P)[kNB][2][RT],
-                                      const float (&ref)[RT],
-                                      float* s_lse, float* s_fac, float (*s_pm)[RT * 16],
-                                      float (*s_pz)[RT * 16], int* s_flag, int n, int gq, int w,
-                                      unsigned base, unsigned old) {
+__device__ void verify_epilogue_resident(const VArgs& a, const Unit& u, const float* s_lse, float* s_acc,
+                                         int* s_flag, unsigned base, unsigned old) {
   constexpr int ROWS = RT * 16;
   constexpr int kU = 16;
   const int tid = threadIdx.x;
   const int nsp = (u.N + a.chunk - 1) / a.chunk;
-  if (tid == 0) grp_poll(cnt_s(a, u), base + (unsigned)a.splits, a.status);
-  __syncthreads();
-  stats_combine<ROWS, LOCAL>(a, u, nsp, s_lse, s_fac, s_pm, s_pz, base);
-  // rescale factor of every chunk partial: exp2(m_chunk - M) / Z
-  for (int e = tid; e < nsp * ROWS; e += kThreads) {
-    const int r = e % ROWS;
-    const float m = s_fac[e], invZ = s_pz[0][r];
-    s_fac[e] = invZ != 0.f && m != kNegInf ? fast_exp2(m - s_pm[0][r]) * invZ : 0.f;
+  if (tid == 0) {
+    const int mold =
+        a.mass ? __hip_atomic_fetch_add(mass_counter(a, u), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+    *s_flag = a.mass && mold == a.Hkv * a.RG - 1;
   }
+  __syncthreads();
+  if (*s_flag) mass_sum(a, u);
   if (tid == 0) o_finish(a, u, base, old, true);
   __syncthreads();
-  // This workgroup's slice of O is the factor-weighted sum over chunks of the
-  // partials.  With few elements per workgroup the chunks are split over Q
-  // thread sets whose sums meet in LDS.
+  // This workgroup's slice of O is the sum over chunks of the partials.  With
+  // few elements per workgroup the chunks are split over Q thread sets whose
+  // sums meet in LDS.
   const int row0 = u.rg * a.RT * 16;
   const int rows = min(ROWS, a.R - row0);
   const int E4 = rows * D / 4;
@@ -915,20 +920,17 @@ __device__ void verify_epilogue_local(const VArgs& a, const Unit& u, const float
   const int q = cnt <= 0 ? 0 : tid / cnt, el = cnt <= 0 ? 0 : tid % cnt;
   const bool act = cnt > 0 && q < Q;  // first element e0 + el (Q = 1: el = tid)
   const uint64_t* op = reinterpret_cast<const uint64_t*>(a.opart) + (size_t)u.grp * a.splits * ROWS * D / 4;
-  auto load_parts = [&](int e, int s0, int Qs, uint64_t (&v)[kU]) {
+  auto sum_parts = [&](int e, int s0, int Qs, float (&acc)[4]) {
     // unconditional (clamped) loads keep the wait counts fine-grained
+    uint64_t v[kU];
 #pragma unroll
     for (int j = 0; j < kU; ++j)
       v[j] = x_load<LOCAL>(op + (size_t)min(s0 + j * Qs, nsp - 1) * ROWS * D / 4 + e);
-  };
-  auto fma_parts = [&](int e, int s0, int Qs, const uint64_t (&v)[kU], float (&acc)[4]) {
-    const int r = (4 * e) / D;
 #pragma unroll
     for (int j = 0; j < kU; ++j) {
-      const int sp = s0 + j * Qs;
-      const float f = sp < nsp ? s_fac[sp * ROWS + r] : 0.f;
+      const float f = s0 + j * Qs < nsp ? 1.f : 0.f;
 #pragma unroll
-      for (int h = 0; h < 4; ++h) acc[h] += f * bf16_to_f32((uint16_t)(v[j] >> (16 * h)));
+      for (int h = 0; h < 4; ++h) acc[h] = fmaf(f, bf16_to_f32((uint16_t)(v[j] >> (16 * h))), acc[h]);
     }
   };
   auto emit = [&](int e, const float (&acc)[4]) {
@@ -939,55 +941,27 @@ __device__ void verify_epilogue_local(const VArgs& a, const Unit& u, const float
     *reinterpret_cast<uint64_t*>(static_cast<uint16_t*>(a.out) + oi) =
         pack_bf16x4(acc[0], acc[1], acc[2], acc[3]);
   };
-  const int e_first = act ? e0 + el : 0;
-  uint64_t pre[kU];
-  load_parts(e_first, q, Q, pre);
-  __builtin_amdgcn_sched_barrier(0);
-  // exact per-token mass of this chunk's tokens: resident P times
-  // exp2(ref - lse) per row (0 for padding rows, whose lse is +inf)
-  float c[RT];
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) c[rt] = fast_exp2(ref[rt] - s_lse[rt * 16 + n]);
-  float* mp = a.mpart + ((size_t)u.b * a.Hkv * a.RG + u.g * a.RG + u.rg) * a.n_cap;
-  if (a.mass) {
-#pragma unroll
-    for (int j = 0; j < kNB; ++j) {
-      const int tb = u.c0 + 32 * (w + kWaves * j);
-      if (tb < u.c1) mass_block_resident<RT>(P[j], c, mp, tb, u.c1, n, gq);
-    }
-  }
-  // O slice
   if (act) {
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
-    fma_parts(e_first, q, Q, pre, acc);
-    for (int s0 = q + Q * kU; s0 < nsp; s0 += Q * kU) {
-      uint64_t v[kU];
-      load_parts(e_first, s0, Q, v);
-      fma_parts(e_first, s0, Q, v, acc);
-    }
+    for (int s0 = q; s0 < nsp; s0 += Q * kU) sum_parts(e0 + el, s0, Q, acc);
     if (Q == 1)
-      emit(e_first, acc);
+      emit(e0 + el, acc);
     else
-      reinterpret_cast<float4*>(s_fac + ((nsp * ROWS + 3) & ~3))[q * cnt + el] =
-          make_float4(acc[0], acc[1], acc[2], acc[3]);
+      reinterpret_cast<float4*>(s_acc)[q * cnt + el] = make_float4(acc[0], acc[1], acc[2], acc[3]);
   }
   if (Q == 1) {
     for (int e = e0 + tid + kThreads; e < e1; e += kThreads) {
       float acc[4] = {0.f, 0.f, 0.f, 0.f};
-      for (int s0 = 0; s0 < nsp; s0 += kU) {
-        uint64_t v[kU];
-        load_parts(e, s0, 1, v);
-        fma_parts(e, s0, 1, v, acc);
-      }
+      for (int s0 = 0; s0 < nsp; s0 += kU) sum_parts(e, s0, 1, acc);
       emit(e, acc);
     }
   } else {
     lds_sync();
     if (tid < cnt) {
-      const float4* s_acc = reinterpret_cast<const float4*>(s_fac + ((nsp * ROWS + 3) & ~3));
+      const float4* sa = reinterpret_cast<const float4*>(s_acc);
       float acc[4] = {0.f, 0.f, 0.f, 0.f};
       for (int qq = 0; qq < Q; ++qq) {
-        const float4 v = s_acc[qq * cnt + tid];
+        const float4 v = sa[qq * cnt + tid];
         acc[0] += v.x;
         acc[1] += v.y;
         acc[2] += v.z;
@@ -1002,7 +976,6 @@ __device__ void verify_epilogue_local(const VArgs& a, const Unit& u, const float
       a.lse[((size_t)u.b * a.Hq + h) * a.T + t] = s_lse[r] * kLn2;
     }
   }
-  mass_combine(a, u, s_flag);
 }
 
 // A chunk past this sequence's end: publish empty statistics, arrive at both
@@ -1123,12 +1096,28 @@ verify_mfma_kernel(VArgs a) {
       if (tb < u.c1) block_probs<RT>(S[j], vis, tb, gq, a.sl2, ref, z);
     }
     reduce_rows<RT, false>(z, n, gq, w, s_wz, s_z, 1.f);
-    // publish the statistics (wave 0); the arrival follows at the V wait
+    // publish the statistics (wave 0, which loads no V) and arrive as soon
+    // as they are stored
     stats_store<ROWS, LOCAL>(a, u, s_m, s_z, base);
-    // ---- pass 2 (no wait on other workgroups): P.V on MFMA
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's V loads (wave 0: its statistics stores) are done
+    if (__builtin_amdgcn_readfirstlane(w) == 0) {
+      __builtin_amdgcn_s_waitcnt(0);
+      if (lane == 0) grp_arrive(cnt_s(a, u));
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's V loads are done
     __syncthreads();                // ... and every other wave's
-    if (threadIdx.x == 0) grp_arrive(cnt_s(a, u));
+    // ---- the group's statistics (published right after each workgroup's
+    //      pass 1): every row's global log2-sum-exp, so P becomes exact
+    if (threadIdx.x == 0) grp_poll(cnt_s(a, u), base + (unsigned)a.splits, a.status);
+    __syncthreads();
+    stats_combine<ROWS, LOCAL>(a, u, (u.N + a.chunk - 1) / a.chunk, s_lse, s_wm, s_wz, base);
+    float c[RT];  // exp2(ref - lse): 0 for padding rows and rows with no visible token here
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const float mm = s_m[rt * 16 + n];
+      c[rt] = mm == kNegInf ? 0.f : fast_exp2(ref[rt] - s_lse[rt * 16 + n]);
+    }
+    // ---- pass 2: exact P, the mass partials and P.V on MFMA
+    float* mp = a.mass ? a.mpart + ((size_t)u.b * a.Hkv * a.RG + u.g * a.RG + u.rg) * a.n_cap : nullptr;
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -1140,17 +1129,16 @@ verify_mfma_kernel(VArgs a) {
       if (tb < u.c1) {
         VT Vr[8];
         read_v_lds<D>(s_v + blk * 32 * D, n, gq, Vr);
-        pv_resident<D, RT>(S[j], Vr, O);
+        pv_exact_resident<D, RT>(S[j], c, Vr, O, mp, tb, u.c1, n, gq);
       }
     }
     __syncthreads();  // V region of LDS is reused below
     write_opart<D, RT, LOCAL>(a, u, O, s_o, lane, w, n, gq);
-    __builtin_amdgcn_s_waitcnt(0);  // every wave's partial stores are complete
-    __syncthreads();                // (s_o is reused as the factor table)
+    __builtin_amdgcn_s_waitcnt(0);  // every wave's O and mass partial stores are complete
+    __syncthreads();                // (s_o is reused for the O-slice sums)
     unsigned old = 0;
     if (threadIdx.x == 0) old = grp_arrive(cnt_o(a, u));
-    verify_epilogue_local<D, RT, LOCAL>(a, u, S, ref, s_lse, s_o, s_wm, s_wz, &s_flag, n, gq, w, base,
-                                        old);
+    verify_epilogue_resident<D, RT, LOCAL>(a, u, s_lse, s_o, &s_flag, base, old);
     return;
   } else {
     // the Q tile in LDS (the region is reused for the O partials at the end)
