@@ -40,12 +40,19 @@ constexpr int kMaxRows = 65;                    // 2 * gamma + 1, gamma <= 32
 constexpr double kNearTie = 1e-9;
 constexpr double kNegInfD = -__builtin_huge_val();
 
+// Inputs, then sizes, then outputs and workspace: the argument loads merge
+// adjacent fields into wide scalar loads allocated (and spilled) as one
+// unit, so fields used at different times sit in separate runs.
 struct AArgs {
   const float* dl;
   const float* tl;
   const int32_t* tok;
   const double* ua;
   const double* us;
+  int B, gamma, V, NC;  // NC: phase-1 chunks per row
+  int ND;               // draw chunks per batch row
+  double tau;
+  int greedy;
   int32_t* nacc;
   int32_t* next;
   int32_t* near;
@@ -57,10 +64,6 @@ struct AArgs {
   double* qs;       // [B][ND] p mass of each draw chunk (used when the residual is empty)
   int* arrive;      // [2] arrivals at the two waits (128 bytes apart), zero at rest
   unsigned* gen;    // generation word, advanced once per wait
-  int B, gamma, V, NC;  // NC: phase-1 chunks per row
-  int ND;               // draw chunks per batch row
-  double tau;
-  int greedy;
 };
 
 __device__ __forceinline__ const float* row_ptr(const AArgs& a, int b, int rho) {
