@@ -293,19 +293,35 @@ __device__ void mass_sum(const VArgs& a, const Unit& u) {
   const int64_t hi = u.split == a.splits - 1 ? a.n_cap : (chunk_end < a.n_cap ? chunk_end : a.n_cap);
   const float* mp = a.mpart + (size_t)u.b * P * a.n_cap;
   float* ms = a.mass + (size_t)u.b * a.n_cap;
-  for (int64_t i = lo + tid; i < hi; i += kThreads) {
-    float acc = 0.f;
-    if (i < hi_sum) {
+  // two tokens per thread and pass, all their loads in flight together
+  // (clamped indices; the sums run over p in order, so results do not depend
+  // on the batching)
+  for (int64_t i0 = lo + tid; i0 < hi; i0 += 2 * kThreads) {
+    const int64_t i1 = i0 + kThreads;
+    float acc0 = 0.f, acc1 = 0.f;
+    if (hi_sum > lo) {
+      const int64_t t0 = i0 < hi_sum ? i0 : hi_sum - 1, t1 = i1 < hi_sum ? i1 : hi_sum - 1;
       for (int p0 = 0; p0 < P; p0 += 8) {
-        float v[8];
+        float v0[8], v1[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          v[j] = p0 + j < P ? ld_agent(mp + (size_t)(p0 + j) * a.n_cap + i) : 0.f;
+        for (int j = 0; j < 8; ++j) {
+          const float* row = mp + (size_t)min(p0 + j, P - 1) * a.n_cap;
+          v0[j] = ld_agent(row + t0);
+          v1[j] = ld_agent(row + t1);
+        }
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc += v[j];
+        for (int j = 0; j < 8; ++j) {
+          if (p0 + j < P) {
+            acc0 += v0[j];
+            acc1 += v1[j];
+          }
+        }
       }
+      if (i0 >= hi_sum) acc0 = 0.f;
+      if (i1 >= hi_sum) acc1 = 0.f;
     }
-    ms[i] = acc;
+    ms[i0] = acc0;
+    if (i1 < hi) ms[i1] = acc1;
   }
   if (tid == 0) reset_counter(mass_counter(a, u));
 }
