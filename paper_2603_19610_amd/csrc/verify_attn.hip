@@ -223,17 +223,16 @@ __device__ void stats_combine(const VArgs& a, const Unit& u, int nsp, float* s_l
       for (int j = 0; j < kU; ++j)  // unconditional (clamped) loads: fine-grained waits
         v[j] = x_load<LOCAL>(st0 + (size_t)min(s0 + j * P, nsp - 1) * rec_stride<ROWS>() + r);
       // the batch's maximum (exact in any order), then its exp-sum relative
-      // to it: independent exp2s instead of a chain of pairwise combines
+      // to it: independent exp2s instead of a chain of pairwise combines.
+      // Branch-free, so both halves of every record load together (a record
+      // with no visible token is (-inf, 0) and adds 0).
       float bm = kNegInf;
 #pragma unroll
-      for (int j = 0; j < kU; ++j)
-        if (s0 + j * P < nsp) bm = fmaxf(bm, v[j].x);
+      for (int j = 0; j < kU; ++j) bm = fmaxf(bm, s0 + j * P < nsp ? v[j].x : kNegInf);
+      const float bref = bm == kNegInf ? 0.f : bm;
       float bz = 0.f;
-      if (bm != kNegInf) {
 #pragma unroll
-        for (int j = 0; j < kU; ++j)
-          if (s0 + j * P < nsp) bz += v[j].y * fast_exp2(v[j].x - bm);
-      }
+      for (int j = 0; j < kU; ++j) bz += s0 + j * P < nsp ? v[j].y * fast_exp2(v[j].x - bref) : 0.f;
       lse_combine(M, Z, bm, bz);
     }
     s_pm[part][r] = M;
