@@ -1383,14 +1383,13 @@ VKernel pick_kernel(int dt, int D, int RT, bool resident, bool local) {
   return nullptr;
 }
 
-int lds_bytes(int dt, int D, int RT, bool resident, int splits) {
+int lds_bytes(int dt, int D, int RT, bool resident) {
   if (dt == PVLM_F32) return (RT * 16 * D + kF32Tile * D + RT * 16 * kF32Tile) * 4;
   int b = 3 * RT * 16 * D * 4;                                   // O partial reduce-scatter
   if (resident) {
     const int vq = kResTokens * D * 2 + RT * 16 * D * 2;          // the chunk's V, then Q (bf16)
     b = b > vq ? b : vq;
-    // rescale factors, then the O-sum partials (at most 256 float4)
-    const int f = (splits * RT * 16 + 3) / 4 * 16 + kThreads * 16;
+    const int f = kThreads * 16;  // the O-slice sums of the thread sets (at most 256 float4)
     b = b > f ? b : f;
   }
   return b;
@@ -1429,7 +1428,7 @@ pvlm_status plan_verify(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int
   p->splits = (int)((p->n_plan + chunk - 1) / chunk);
   p->resident = p->mfma && chunk <= kResTokens;
   p->grid = (p->per_launch * p->splits + 7) / 8 * 8;
-  p->lds_dyn = lds_bytes(dt, D, p->RT, p->resident, p->splits);
+  p->lds_dyn = lds_bytes(dt, D, p->RT, p->resident);
   const int ROWS = p->RT * 16;
   // Monotonic group counters sit at fixed per-group slots (cnt_s, cnt_o, base
   // of group g on lines 3g..3g+2 of the monotonic part), so calls of any shape
