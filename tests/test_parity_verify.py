@@ -103,6 +103,36 @@ def test_long_video_131k():
     _check(inp, w.hq, w.T, "long")
 
 
+@pytest.mark.parametrize("shape", [(1, 9, 64, 8, 128, [1111]), (4, 9, 28, 4, 128, [100, 900, 3, 1500]),
+                                   (1, 3, 8, 8, 128, [20000])],
+                         ids=["resident-72B-heads", "resident-ragged-empty-chunks", "stream"])
+def test_without_mass_or_lse(shape):
+    """Output alone (no mass, no lse): bit-identical to the full call's output
+    (the mass and lse are by-products of the same arithmetic) and within the
+    bar against the oracle, after a run in which the later calls' waits would
+    hang or time out if an arrival were skipped."""
+    B, T, Hq, Hkv, D, ctx = shape
+    inp = W.random_verify_inputs(B, T, Hq, Hkv, D, ctx, "bf16", seed=sum(ctx) + 7)
+    note(f"verify without mass/lse q{inp.q.shape} k{inp.k.shape} ctx={ctx}")
+    q, k, v, c = (to_dev(inp.q), to_dev(inp.k), to_dev(inp.v), to_dev(inp.ctx_len))
+    ws = pv.Workspace(torch.device("cuda", 0))
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    full, _, _ = pv.verify_attn(q, k, v, c, scale=inp.scale, ws=ws, status=status)
+    outs = []
+    for want_mass, want_lse in ((False, False), (True, False), (False, True), (False, False)):
+        o, m, l = pv.verify_attn(q, k, v, c, scale=inp.scale, ws=ws, status=status,
+                                 want_mass=want_mass, want_lse=want_lse)
+        assert (m is None) == (not want_mass) and (l is None) == (not want_lse)
+        outs.append(o)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    for o in outs:
+        assert torch.equal(o, full)
+    ro, _, _ = oracle.verify_attn(f64(inp.q, "bf16"), f64(inp.k, "bf16"), f64(inp.v, "bf16"),
+                                  inp.ctx_len, inp.scale)
+    assert_out(to_host_f64(outs[0]), ro)
+
+
 def test_deterministic_and_reusable_workspace():
     w = W.WORKLOADS["llava72b"]
     inp = W.make_verify_inputs(w, layer=1)
