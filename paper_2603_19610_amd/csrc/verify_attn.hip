@@ -502,6 +502,66 @@ __device__ __forceinline__ void read_v_lds(const uint16_t* lds_blk, int n, int g
   }
 }
 
+// Stream one 32-token block of K into LDS in the Q tile's layout (16-byte
+// chunks XOR-swizzled by row, so the MFMA operand reads hit distinct banks),
+// through untracked global->LDS loads like issue_v_lds.  Rows past the chunk
+// re-read its last row.
+template <int D>
+__device__ __forceinline__ void issue_k_lds(const uint16_t* kg, int tb, int c1, uint16_t* lds_blk,
+                                            int lane) {
+  constexpr int CH = D / 8;
+  constexpr int NI = 32 * CH / 64;
+#pragma unroll
+  for (int ins = 0; ins < NI; ++ins) {
+    const int slot = ins * 64 + lane, r = slot / CH, c = (slot % CH) ^ (r % CH);
+    const uint16_t* src = kg + (size_t)min(tb + r, c1 - 1) * D + 8 * c;
+    const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
+        reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint16_t*)(lds_blk + ins * 64 * 8))));
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(lds), "v"(src)
+                 : "memory", "m0");
+  }
+}
+
+// K operand of one block from its swizzled LDS copy: the registers
+// load_k_block would fill.
+template <int D>
+__device__ __forceinline__ void read_k_lds(const uint16_t* lds_blk, int n, int gq, uint4 (&Kr)[2][D / 32]) {
+  constexpr int CH = D / 8;
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt) {
+    const int r = 16 * tt + n;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      const int c = 4 * ks + gq;
+      Kr[tt][ks] = *reinterpret_cast<const uint4*>(lds_blk + (r * CH + (c ^ (r % CH))) * 8);
+    }
+  }
+}
+
+// Global->LDS loads of one 32-token block of K and V (issue_k_lds, issue_v_lds).
+template <int D>
+constexpr int kBlockDma = 32 * (D / 8) / 64 + 32 / (64 / (D / 8));
+
+// Wait until at most `younger` vector memory operations are outstanding, for
+// younger in {0, 1, kBlockDma, kBlockDma + 1} (wave-uniform): every older
+// one, in particular an untracked global->LDS load, has then completed.  The
+// asm's memory clobber keeps the LDS reads that follow after it.
+template <int D>
+__device__ __forceinline__ void wait_vm_younger(int younger) {
+  constexpr int N = kBlockDma<D>;
+  static_assert(N + 1 < 64, "vmcnt holds 6 bits");
+  if (younger == 0)
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else if (younger == 1)
+    asm volatile("s_waitcnt vmcnt(1)" ::: "memory");
+  else if (younger == N)
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+  else
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N + 1) : "memory");
+}
+
 // Scores of one block in the log2 domain, masked to -inf outside the chunk,
 // past the causal limit of each verify row, and on padding rows.
 template <int D, int RT>
@@ -1197,9 +1257,9 @@ verify_mfma_kernel(VArgs a) {
     float lse[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) lse[rt] = s_lse[rt * 16 + n];
-    // ---- pass 2: recompute scores from K, then P, mass and P.V.  Up to 3
-    //      row tiles the next block's K and V load during this one; with more
-    //      the O accumulators leave no registers for a second block.
+    // ---- pass 2: recompute scores from K, then P, mass and P.V, the next
+    //      block's K and V loading during this one (in registers up to 3 row
+    //      tiles; with more, in LDS).
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -1226,11 +1286,32 @@ verify_mfma_kernel(VArgs a) {
         step(Kb, Vb, b2);
       }
     } else {
-      for (int blk = w; blk < nblk; blk += kWaves) {
+      // No registers for a second block: each wave double-buffers its K and
+      // V blocks in LDS (after the Q tile) through untracked global->LDS
+      // loads, the next block's in flight while this one is computed.  The
+      // waits are counted by hand: younger than a block's loads are the
+      // previous block's mass store (one per block, always issued: lane 0
+      // holds the block's first token) and the next block's loads.
+      uint16_t* kv = s_q + RT * 16 * D + w * 4 * 32 * D;  // [2 buffers][K, V][32][D]
+      __builtin_amdgcn_s_waitcnt(0);                       // the counts below start from zero
+      if (w < nblk) {
+        issue_k_lds<D>(kg, u.c0 + 32 * w, u.c1, kv, lane);
+        issue_v_lds<D>(vg, u.c0 + 32 * w, u.c1, kv + 32 * D, lane);
+      }
+      int i = 0;
+      for (int blk = w; blk < nblk; blk += kWaves, ++i) {
+        uint16_t* cur = kv + (i & 1) * 2 * 32 * D;
+        const bool next = blk + kWaves < nblk;
+        if (next) {
+          uint16_t* nxt = kv + ((i + 1) & 1) * 2 * 32 * D;
+          issue_k_lds<D>(kg, u.c0 + 32 * (blk + kWaves), u.c1, nxt, lane);
+          issue_v_lds<D>(vg, u.c0 + 32 * (blk + kWaves), u.c1, nxt + 32 * D, lane);
+        }
+        wait_vm_younger<D>((i > 0 ? 1 : 0) + (next ? kBlockDma<D> : 0));
         uint4 Kr[2][KS];
-        load_k_block<D>(kg, u.c0 + 32 * blk, u.c1, n, gq, Kr);
+        read_k_lds<D>(cur, n, gq, Kr);
         VT Vr[8];
-        load_v_block<D>(vg, u.c0 + 32 * blk, u.c1, n, gq, Vr);
+        read_v_lds<D>(cur + 32 * D, n, gq, Vr);
         step(Kr, Vr, blk);
       }
     }
@@ -1386,6 +1467,10 @@ VKernel pick_kernel(int dt, int D, int RT, bool resident, bool local) {
 int lds_bytes(int dt, int D, int RT, bool resident) {
   if (dt == PVLM_F32) return (RT * 16 * D + kF32Tile * D + RT * 16 * kF32Tile) * 4;
   int b = 3 * RT * 16 * D * 4;                                   // O partial reduce-scatter
+  if (!resident && RT > 3) {
+    const int kv = RT * 16 * D * 2 + kWaves * 4 * 32 * D * 2;     // Q, then two K+V blocks per wave
+    b = b > kv ? b : kv;
+  }
   if (resident) {
     const int vq = kResTokens * D * 2 + RT * 16 * D * 2;          // the chunk's V, then Q (bf16)
     b = b > vq ? b : vq;

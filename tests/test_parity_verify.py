@@ -47,6 +47,9 @@ SHAPES = [
     (1, 4, 8, 1, 128, [333], "f32"),               # fp32 path, D = 128
     (1, 32, 16, 2, 128, [700], "bf16"),            # T = 32 (the maximum): 256 rows, 4 row groups
     (4, 9, 28, 4, 128, [100, 900, 3, 1500], "bf16"),  # batch 4 ragged, 7B head layout
+    (1, 9, 64, 8, 128, [40000], "bf16"),          # stream variant, 5 row tiles: K/V blocks through LDS
+    (1, 8, 64, 8, 128, [30000], "bf16"),          # stream variant, 4 row tiles
+    (2, 10, 16, 2, 64, [40000, 25000], "bf16"),   # stream variant, D = 64, 5 row tiles, ragged
 ]
 
 
