@@ -323,10 +323,17 @@ constexpr int kSmallWaves = kSmallThreads / 64;
 constexpr int kSmallMaxPer = 16;  // beyond 16384 scores, several workgroups per row are faster
 constexpr int kSmallMax = kSmallThreads * kSmallMaxPer;
 constexpr int kSmallBins = 4096;
+// Every histogram bin has kHistCopies counters, lane l adding to copy l % 8:
+// scores concentrate in few top digits (the UV-Prune scores of a 72B layer
+// fill 29 of the 4096 first-pass bins), and LDS atomics of one instruction to
+// one address serialise.
+constexpr int kHistCopies = 8;
+constexpr int kSmallLds = kSmallBins * (kHistCopies + 1) * 4;  // the copies, then the bin totals
 
 template <int PER>
 __global__ void __launch_bounds__(kSmallThreads) topk_small_kernel(TArgs a) {
-  __shared__ int hist[kSmallBins];
+  extern __shared__ __align__(16) int hist[];  // [kSmallBins][kHistCopies], then [kSmallBins] totals
+  int* bins = hist + kSmallBins * kHistCopies;
   __shared__ int s_warp[kSmallWaves];
   __shared__ int s_res[2];
   __shared__ int s_cnt[2][PER][kSmallWaves];  // per (round e, wave): keys above tau, equal to tau
@@ -362,31 +369,47 @@ __global__ void __launch_bounds__(kSmallThreads) topk_small_kernel(TArgs a) {
   for (int pass = 0; pass < 3; ++pass) {
     const int shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
     const int nb = pass == 0 ? 4096 : 1024;
-    for (int i = tid; i < nb; i += kSmallThreads) hist[i] = 0;
+    for (int i = tid; i < nb * kHistCopies / 4; i += kSmallThreads)
+      reinterpret_cast<int4*>(hist)[i] = make_int4(0, 0, 0, 0);
     __syncthreads();
+    const int copy = lane & (kHistCopies - 1);
 #pragma unroll
     for (int e = 0; e < PER; ++e)
       if (e * kSmallThreads + tid < mb && (kr[e] & mask) == prefix)
-        atomicAdd(&hist[(kr[e] >> shift) & (uint32_t)(nb - 1)], 1);
+        atomicAdd(&hist[((kr[e] >> shift) & (uint32_t)(nb - 1)) * kHistCopies + copy], 1);
+    __syncthreads();
+    // each bin's copies summed, consecutive threads on consecutive bins
+    for (int i = tid; i < nb; i += kSmallThreads) {
+      const int4* h = reinterpret_cast<const int4*>(hist + i * kHistCopies);
+      const int4 x = h[0], y = h[1];
+      bins[i] = x.x + x.y + x.z + x.w + y.x + y.y + y.z + y.w;
+    }
     __syncthreads();
     // bins in descending order: thread t owns q = nb / 1024 consecutive ones
     const int q = nb / kSmallThreads;
     const int top = nb - 1 - tid * q;
+    int cnt[kSmallBins / kSmallThreads];
     int own = 0;
-    for (int j = 0; j < q; ++j) own += hist[top - j];
+#pragma unroll
+    for (int j = 0; j < kSmallBins / kSmallThreads; ++j) {
+      cnt[j] = j < q ? bins[top - j] : 0;
+      own += cnt[j];
+    }
     int tot;
     const int excl = block_exclusive_scan<kSmallWaves>(own, s_warp, &tot);
     const int need = kb - above;
     if (excl < need && need <= excl + own) {
       int acc = excl;
-      for (int j = 0; j < q; ++j) {
-        const int c = hist[top - j];
-        if (acc + c >= need) {
-          s_res[0] = top - j;
-          s_res[1] = above + acc;
-          break;
+#pragma unroll
+      for (int j = 0; j < kSmallBins / kSmallThreads; ++j) {
+        if (j < q) {
+          if (acc + cnt[j] >= need) {
+            s_res[0] = top - j;
+            s_res[1] = above + acc;
+            break;
+          }
+          acc += cnt[j];
         }
-        acc += c;
       }
     }
     __syncthreads();
@@ -540,7 +563,8 @@ extern "C" pvlm_status pvlm_topk_select(int B, int64_t m_cap, const int32_t* m, 
     const void* kern = m_cap <= kSmallThreads * 4   ? reinterpret_cast<const void*>(topk_small_kernel<4>)
                        : m_cap <= kSmallThreads * 8 ? reinterpret_cast<const void*>(topk_small_kernel<8>)
                                                     : reinterpret_cast<const void*>(topk_small_kernel<kSmallMaxPer>);
-    PVLM_HIP(hipLaunchKernel(kern, dim3(B), dim3(kSmallThreads), args, 0, stream));
+    PVLM_HIP(allow_dynamic_lds(kern, kSmallLds));
+    PVLM_HIP(hipLaunchKernel(kern, dim3(B), dim3(kSmallThreads), args, kSmallLds, stream));
     return PVLM_OK;
   }
   char* wsb = static_cast<char*>(ws);
