@@ -222,16 +222,21 @@ __device__ __forceinline__ void load_strided(const float* z, int y0, int y1, flo
 #pragma unroll
   for (int k = 0; k < kAccPer / 4; ++k) {
     const int y = y0 + 4 * (k * kAccThreads + (int)threadIdx.x);
+    // clamped loads, all in flight together (VEC: rows and chunk ends are
+    // multiples of 4, so y1 - 4 is an aligned entry of the chunk)
     if constexpr (VEC) {
-      const float4 f = y < y1 ? *reinterpret_cast<const float4*>(z + y)
-                              : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-      v[4 * k] = f.x;
-      v[4 * k + 1] = f.y;
-      v[4 * k + 2] = f.z;
-      v[4 * k + 3] = f.w;
+      const float4 f = *reinterpret_cast<const float4*>(z + (y < y1 ? y : y1 - 4));
+      const bool in = y < y1;
+      v[4 * k] = in ? f.x : -INFINITY;
+      v[4 * k + 1] = in ? f.y : -INFINITY;
+      v[4 * k + 2] = in ? f.z : -INFINITY;
+      v[4 * k + 3] = in ? f.w : -INFINITY;
     } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[4 * k + e] = y + e < y1 ? z[y + e] : -INFINITY;
+      for (int e = 0; e < 4; ++e) {
+        const float x = z[min(y + e, y1 - 1)];
+        v[4 * k + e] = y + e < y1 ? x : -INFINITY;
+      }
     }
   }
 }
@@ -273,9 +278,10 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
   auto load_draft = [&](int b, int& x, float& px, float& qx, double& ua) {
     const int xt = a.tok[(size_t)b * a.gamma + t_d];
     x = xt >= 0 && xt < a.V ? xt : -1;
-    if (x >= 0 && !a.greedy) {
-      px = row_ptr(a, b, t_d)[x];
-      qx = row_ptr(a, b, a.gamma + 1 + t_d)[x];
+    if (!a.greedy) {  // clamped loads, all in flight; the values count only when x >= 0
+      const int xc = x >= 0 ? x : 0;
+      px = row_ptr(a, b, t_d)[xc];
+      qx = row_ptr(a, b, a.gamma + 1 + t_d)[xc];
       ua = a.ua[(size_t)b * a.gamma + t_d];
     }
   };
@@ -348,19 +354,26 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
       const size_t base = ((size_t)b * RW + r) * a.NC;
       double M = kNegInfD, m0 = kNegInfD, s0 = 0.0;
       int A = 0x7fffffff;
-      if (act)
-        for (int k = k0; k < a.NC; k += NCp) {
-          const double m2 = ld_agent(a.pm + base + k);
-          const int i2 = ld_agent(a.pi + base + k);
-          if (k == k0) {
-            m0 = m2;
-            s0 = a.greedy ? 0.0 : ld_agent(a.ps + base + k);
-          }
-          if (m2 > M || (m2 == M && i2 < A)) {
-            M = m2;
-            A = i2;
+      if (act) {
+        // the lane's first chunk: its three results loaded together (clamped)
+        const int kc = min(k0, a.NC - 1);
+        const double m2 = ld_agent(a.pm + base + kc);
+        const int i2 = ld_agent(a.pi + base + kc);
+        const double sv = a.greedy ? 0.0 : ld_agent(a.ps + base + kc);
+        if (k0 < a.NC) {
+          m0 = M = m2;
+          s0 = sv;
+          A = i2;
+        }
+        for (int k = k0 + NCp; k < a.NC; k += NCp) {
+          const double m3 = ld_agent(a.pm + base + k);
+          const int i3 = ld_agent(a.pi + base + k);
+          if (m3 > M || (m3 == M && i3 < A)) {
+            M = m3;
+            A = i3;
           }
         }
+      }
       for (int o = NCp / 2; o > 0; o >>= 1) {
         const double m2 = __shfl_xor(M, o, 64);
         const int i2 = __shfl_xor(A, o, 64);
@@ -446,8 +459,10 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
     float zp[kDrawPer], zq[kDrawPer];
 #pragma unroll
     for (int j = 0; j < kDrawPer; ++j) {
-      zp[j] = y + j < a.V ? zpr[y + j] : -INFINITY;  // past V: p = 0
-      zq[j] = y + j < a.V && resid ? zqr[y + j] : -INFINITY;
+      // clamped loads, all in flight together; past V: p = 0, q = 0
+      const float xp = zpr[min(y + j, a.V - 1)], xq = zqr[min(y + j, a.V - 1)];
+      zp[j] = y + j < a.V ? xp : -INFINITY;
+      zq[j] = y + j < a.V && resid ? xq : -INFINITY;
     }
     double psum = 0.0;
 #pragma unroll
@@ -496,8 +511,10 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
 #pragma unroll
     for (int i = 0; i < kSumPer; ++i) {
       const int k = kSumPer * tid + i;
-      cr[i] = k < a.ND ? ld_agent(a.rs + (size_t)b * a.ND + k) : 0.0;
-      cq[i] = k < a.ND ? ld_agent(a.qs + (size_t)b * a.ND + k) : 0.0;
+      const double xr = ld_agent(a.rs + (size_t)b * a.ND + min(k, a.ND - 1));  // clamped loads
+      const double xq = ld_agent(a.qs + (size_t)b * a.ND + min(k, a.ND - 1));
+      cr[i] = k < a.ND ? xr : 0.0;
+      cq[i] = k < a.ND ? xq : 0.0;
       own_r += cr[i];
       own_q += cq[i];
     }

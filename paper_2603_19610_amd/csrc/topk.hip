@@ -177,7 +177,10 @@ __global__ void __launch_bounds__(kTopkThreads) topk_kernel(TArgs a) {
   if constexpr (REG) {
     const int i0 = s0 + tid * kPerThread;
 #pragma unroll
-    for (int e = 0; e < kPerThread; ++e) kr[e] = i0 + e < s1 ? rank_key(sc[i0 + e]) : 0u;
+    for (int e = 0; e < kPerThread; ++e) {  // clamped loads, all in flight together
+      const float x = sc[min(i0 + e, s1 > 0 ? s1 - 1 : 0)];
+      kr[e] = i0 + e < s1 ? rank_key(x) : 0u;
+    }
   }
   // f(key) over this thread's scores of the slice
   auto visit = [&](auto f) {
@@ -212,7 +215,10 @@ __global__ void __launch_bounds__(kTopkThreads) topk_kernel(TArgs a) {
       for (int j0 = 0; j0 < a.NW; j0 += 8) {
         int v[8];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) v[q] = j0 + q < a.NW ? ld_agent(hrow + (j0 + q) * 256 + tid) : 0;
+        for (int q = 0; q < 8; ++q) {  // clamped loads, all in flight together
+          const int x = ld_agent(hrow + min(j0 + q, a.NW - 1) * 256 + tid);
+          v[q] = j0 + q < a.NW ? x : 0;
+        }
 #pragma unroll
         for (int q = 0; q < 8; ++q) t += v[q];
       }
@@ -284,7 +290,10 @@ __global__ void __launch_bounds__(kTopkThreads) topk_kernel(TArgs a) {
     for (int e = 0; e < kPerThread; ++e) {
       const bool valid = i0 + e < s1;
       if constexpr (REG) keys[e] = kr[e];
-      else keys[e] = valid ? rank_key(sc[i0 + e]) : 0u;
+      else {
+        const float x = sc[min(i0 + e, s1 - 1)];  // clamped load (s1 > base >= 0)
+        keys[e] = valid ? rank_key(x) : 0u;
+      }
       g += valid && keys[e] > tau;
       e_ += valid && keys[e] == tau;
     }
@@ -355,12 +364,14 @@ __global__ void __launch_bounds__(kSmallThreads) topk_small_kernel(TArgs a) {
   if (bad && tid == 0) dev_flag(a.status, PVLM_DEV_RANGE);
   for (int r = kb + tid; r < a.k_cap; r += kSmallThreads) out[r] = -1;
   if (kb == 0) return;  // uniform across the workgroup
+  // unconditional loads (indices clamped; kb > 0 implies mb > 0) so that all
+  // PER are in flight together, then the entries past the row are zeroed
+  float v[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) v[e] = sc[min(e * kSmallThreads + tid, mb - 1)];
   uint32_t kr[PER];
 #pragma unroll
-  for (int e = 0; e < PER; ++e) {
-    const int i = e * kSmallThreads + tid;
-    kr[e] = i < mb ? rank_key(sc[i]) : 0u;
-  }
+  for (int e = 0; e < PER; ++e) kr[e] = e * kSmallThreads + tid < mb ? rank_key(v[e]) : 0u;
 
   // ---- radix select of the kb-th largest key: digits [31:20], [19:10], [9:0]
   uint32_t prefix = 0, mask = 0;
