@@ -109,6 +109,18 @@ struct TArgs {
 
 constexpr int kLine = (int)(kSyncLine / sizeof(int));
 
+// A pair of ints exchanged between workgroups as one device-coherent 64-bit
+// access (8-byte aligned): one round trip for both, and a consistent pair.
+__device__ __forceinline__ void st_pair(int* p, int lo, int hi) {
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), (uint64_t)(uint32_t)lo | ((uint64_t)(uint32_t)hi << 32),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int2 ld_pair(const int* p) {
+  const uint64_t v =
+      __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_int2((int)(uint32_t)v, (int)(uint32_t)(v >> 32));
+}
+
 // Barrier `p` (0-based) of row b.  Thread 0 arrives; the launch's last arrival
 // runs `last` (with the whole workgroup) and then releases the others, which
 // wait for the generation word to reach g0 + p + 1.  Returns in every thread.
@@ -177,10 +189,9 @@ __global__ void __launch_bounds__(kTopkThreads) topk_kernel(TArgs a) {
   if constexpr (REG) {
     const int i0 = s0 + tid * kPerThread;
 #pragma unroll
-    for (int e = 0; e < kPerThread; ++e) {  // clamped loads, all in flight together
-      const float x = sc[min(i0 + e, s1 > 0 ? s1 - 1 : 0)];
-      kr[e] = i0 + e < s1 ? rank_key(x) : 0u;
-    }
+    for (int e = 0; e < kPerThread; ++e) kr[e] = __float_as_uint(sc[min(i0 + e, s1 > 0 ? s1 - 1 : 0)]);
+#pragma unroll  // (clamped loads, all in flight together, then the keys)
+    for (int e = 0; e < kPerThread; ++e) kr[e] = i0 + e < s1 ? rank_key(__uint_as_float(kr[e])) : 0u;
   }
   // f(key) over this thread's scores of the slice
   auto visit = [&](auto f) {
@@ -226,13 +237,13 @@ __global__ void __launch_bounds__(kTopkThreads) topk_kernel(TArgs a) {
       __syncthreads();
       if (tid < 64)
         find_digit(hist, kb - above, [&](int digit, int acc) {
-          st_agent(a.res + b * 4, digit);
-          st_agent(a.res + b * 4 + 1, above + acc);
+          st_pair(a.res + b * 4, digit, above + acc);
         });
     });
     if (tid == 0) {
-      s_res[0] = ld_agent(a.res + b * 4);
-      s_res[1] = ld_agent(a.res + b * 4 + 1);
+      const int2 r = ld_pair(a.res + b * 4);
+      s_res[0] = r.x;
+      s_res[1] = r.y;
     }
     __syncthreads();
     if (kb > 0) {
@@ -256,16 +267,16 @@ __global__ void __launch_bounds__(kTopkThreads) topk_kernel(TArgs a) {
   block_exclusive_scan(n_gt, s_warp, &slice_gt);
   block_exclusive_scan(n_eq, s_warp, &slice_eq);
   if (tid == 0) {
-    st_agent(a.cnt + ((size_t)b * a.NW + j) * 2, slice_gt);
-    st_agent(a.cnt + ((size_t)b * a.NW + j) * 2 + 1, slice_eq);
+    st_pair(a.cnt + ((size_t)b * a.NW + j) * 2, slice_gt, slice_eq);
   }
   row_barrier(a, b, 4, g0, &s_flag, []() {});
   if (kb == 0) return;
   if (tid < 64) {  // counts of the slices before this one
     int gt = 0, eq = 0;
     for (int q = tid; q < j; q += 64) {
-      gt += ld_agent(a.cnt + ((size_t)b * a.NW + q) * 2);
-      eq += ld_agent(a.cnt + ((size_t)b * a.NW + q) * 2 + 1);
+      const int2 c = ld_pair(a.cnt + ((size_t)b * a.NW + q) * 2);
+      gt += c.x;
+      eq += c.y;
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
