@@ -33,15 +33,13 @@ __global__ void __launch_bounds__(256) uv_mass_kernel(const float* crit, const i
   if (gid >= (int64_t)B * m_cap) return;
   const int b = gid / m_cap;
   const int64_t i = gid % m_cap;
+  // both criteria load together with the row's length (every gid < B * m_cap
+  // is inside the stack), which then decides whether the entry counts
+  const float cL = crit[(size_t)L * B * m_cap + gid], c0 = crit[gid];
   bool bad = false;
   const int mb = clampi(m[b], 0, (int)m_cap, bad);
   if (bad && i == 0) dev_flag(status, PVLM_DEV_RANGE);
-  float s = 0.f;
-  if (i < mb) {
-    const size_t layer = (size_t)B * m_cap;
-    s = crit[(size_t)L * layer + gid] - crit[gid];
-  }
-  score[gid] = s;
+  score[gid] = i < mb ? cL - c0 : 0.f;
 }
 
 template <typename T>
