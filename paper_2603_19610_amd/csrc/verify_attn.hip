@@ -1173,18 +1173,22 @@ verify_mfma_kernel(VArgs a) {
     reduce_rows<RT, false>(z, n, gq, w, s_wz, s_z, 1.f);
     // publish the statistics (wave 0, which loads no V) and arrive as soon
     // as they are stored
+    // ---- the group's statistics (published right after each workgroup's
+    //      pass 1): every row's global log2-sum-exp, so P becomes exact.
+    //      Thread 0 polls while waves 1-3 still wait for their V; their loads
+    //      of the records queue behind their V loads (in-order completion).
     stats_store<ROWS, LOCAL>(a, u, s_m, s_z, base);
     if (__builtin_amdgcn_readfirstlane(w) == 0) {
       __builtin_amdgcn_s_waitcnt(0);
-      if (lane == 0) grp_arrive(cnt_s(a, u));
+      if (lane == 0) {
+        grp_arrive(cnt_s(a, u));
+        grp_poll(cnt_s(a, u), base + (unsigned)a.splits, a.status);
+      }
     }
+    lds_sync();
+    stats_combine<ROWS, LOCAL>(a, u, (u.N + a.chunk - 1) / a.chunk, s_lse, s_wm, s_wz, base);
     __builtin_amdgcn_s_waitcnt(0);  // this wave's V loads are done
     __syncthreads();                // ... and every other wave's
-    // ---- the group's statistics (published right after each workgroup's
-    //      pass 1): every row's global log2-sum-exp, so P becomes exact
-    if (threadIdx.x == 0) grp_poll(cnt_s(a, u), base + (unsigned)a.splits, a.status);
-    __syncthreads();
-    stats_combine<ROWS, LOCAL>(a, u, (u.N + a.chunk - 1) / a.chunk, s_lse, s_wm, s_wz, base);
     float c[RT];  // exp2(ref - lse): 0 for padding rows and rows with no visible token here
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
