@@ -21,6 +21,9 @@ explicit loops over the indices the paper sums over, following the paper:
 * ``gather_kv``        -- the draft's compact cache [V*, X] (Sec. 4.2, Stage I).
 * ``spec_accept``      -- speculative-sampling accept/reject with residual
                           resampling (Sec. 2.2) and the bonus token (Suppl. B).
+* ``window``           -- draft window size, Eq. (Prefill), and the speedup
+                          model of Thm. (paravlm_speedup) and the supplement's
+                          theorems and Lemma 1.
 
 Parity status: every function here is pinned by the ``-m "not gpu"`` tests in
 ``tests/test_oracle_*.py`` against brute force, closed forms, library routines
@@ -31,6 +34,7 @@ from .uvprune import (cos_similarity, criterion_cossim, uvprune_score_cossim,
                       uvprune_score_mass)
 from .select import topk_keys, topk_select, gather_kv
 from .accept import spec_accept, softmax_t, NEAR_TIE_REL
+from . import window
 
 __all__ = [
     "verify_attn", "verify_attn_rows", "cos_similarity", "criterion_cossim",

@@ -70,3 +70,18 @@ def accept_fixture():
         else:
             out[key] = nums(rest.split())
     return out
+
+
+def window_fixture():
+    """The paper's printed speed ratios, integer windows and worked example."""
+    out = {"ratio": [], "gamma": [], "example": []}
+    for line in _lines("window_size.txt"):
+        key, *rest = line.split()
+        if key == "ratio" or key == "gamma":
+            pair, alpha, t_p, t_q, val = rest
+            out[key].append((pair, float(alpha), float(t_p), float(t_q), float(val)))
+        elif key == "example":
+            out["example"].append(tuple(float(v) for v in rest))
+        elif key == "window_gain":
+            out["window_gain"] = float(rest[0])
+    return out
