@@ -37,11 +37,14 @@ Readings where the paper is silent or loose:
   rollback speedup T_p / T_PSD_r at the (snapped) ratio, the smallest gamma
   on ties.  This is the criterion the supplement names for choosing between
   rounding down and up (the window size against the accepted length).  It
-  needs tau > 0.
+  needs tau > 0.  The comparison is exact (rational arithmetic on the binary
+  values of c and tau): at small tau the speedups of successive windows differ
+  by less than a float64 ulp, and a rounded comparison would call them tied.
 """
 from __future__ import annotations
 
 import math
+from fractions import Fraction
 
 SNAP_REL = 1e-9
 
@@ -104,6 +107,13 @@ def paravlm_speedup(tau_hat, c_star):
     return tau_hat * gamma * t_p / (gamma * t_q)
 
 
+def _rollback_speedup_exact(c, tau, gamma):
+    """T_p / T_PSD_r = c (1 + tau^gamma) E[X] / (2 max(gamma, c)), exactly."""
+    c, tau = Fraction(c), Fraction(tau)
+    ex = Fraction(gamma) if tau == 1 else tau * (1 - tau ** gamma) / (1 - tau)
+    return c * (1 + tau ** gamma) * ex / (2 * max(Fraction(gamma), c))
+
+
 def _snap(c):
     r = round(c)
     return float(r) if abs(c - r) <= SNAP_REL * abs(c) else c
@@ -122,9 +132,9 @@ def window_size(t_p, t_q, rounding="down", tau=None, gamma_max=64):
     elif rounding == "best":
         if tau is None or not 0.0 < tau <= 1.0:
             raise ValueError("best rounding needs 0 < tau <= 1")
-        best, g = -1.0, 1
+        best, g = Fraction(-1), 1
         for cand in range(1, gamma_max + 1):
-            v = speedup(cs, t_psd_rollback(cs, tau, cand))
+            v = _rollback_speedup_exact(cs, tau, cand)
             if v > best:
                 best, g = v, cand
         return g

@@ -160,5 +160,7 @@ def test_best_window_follows_the_supplement():
         for tau in (0.2, 0.5, 0.7, 0.9, 0.97, 1.0):
             g = W.window_size(t_p, t_q, "best", tau=tau)
             assert g in (math.floor(c), math.ceil(c)), (c, tau, g)
+    # below c the speedup still grows, even when by far less than an ulp
+    assert W.window_size(1000, 1, "best", tau=0.01, gamma_max=16) == 16
     with pytest.raises(ValueError):
         W.window_size(420, 78.3, "best", tau=0.0)
