@@ -13,6 +13,9 @@
  *   pvlm_gather_kv      the draft's compact cache [V*, X] (Sec. 4.2, Stage I)
  *   pvlm_spec_accept    speculative-sampling accept/reject (Sec. 2.2) with the
  *                       bonus token of Suppl. B
+ *   pvlm_window_size,   host-only: the draft window gamma = c* of Eq. (Prefill)
+ *   pvlm_speedup        and the speedup analysis (Thm. paravlm_speedup; the
+ *                       supplement's theorems and Lemma 1)
  *
  * Conventions shared by every call
  *   - Every tensor pointer is a caller-owned DEVICE pointer.  The library never
@@ -230,6 +233,61 @@ pvlm_status pvlm_spec_accept(int B, int gamma, int V, float temperature,
                              const double* u_sample, int32_t* n_accepted, int32_t* next_token,
                              int32_t* near_tie, void* ws, size_t ws_bytes, int32_t* status,
                              hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Window size and speedup model (host-only arithmetic: no device pointer, no
+ * stream, no GPU needed).  Times are per generated token in units of t, the
+ * draft's single forward time T_q; the target's verification forward is
+ * T_p = c t.  tau is the per-token acceptance rate.
+ *
+ * pvlm_speedup fills every quantity of the paper's speedup analysis for one
+ * (c, tau, gamma):
+ *   t_sd_ideal      (gamma + c) / (gamma + 1)          Suppl. Thm. Vanilla SD (Ideal)
+ *   t_psd_ideal     max(gamma, c) / gamma              Suppl. Thm. Parallel SD (Ideal)
+ *   t_sd            (gamma + c) / (tau gamma + 1)      Suppl. Thm. Vanilla SD (Practical)
+ *   t_psd           max(gamma, c) / (tau gamma)        Suppl. Thm. Parallel SD (Practical);
+ *                                                      at gamma = c its speedup is
+ *                                                      Thm. (paravlm_speedup), tau c*
+ *   expected_accepted  E[X] = tau (1 - tau^gamma) / (1 - tau), gamma at tau = 1
+ *                      (Suppl. Lemma 1; X is the accepted prefix of a window)
+ *   expected_total  (1 + tau^gamma) E[X], the tokens of the two rounds in the
+ *                   proof of Suppl. Thm. Parallel SD (with Rollback)
+ *   t_psd_rollback  2 max(gamma, c) / expected_total   (same theorem)
+ *   v_*             c / t_*: speedup against target-only decoding
+ * A per-token time that is unbounded (tau = 0 for the parallel forms) is
+ * HUGE_VAL and its speedup 0.
+ * Errors: PVLM_ERR_NULL if out is NULL; PVLM_ERR_SHAPE unless c is finite and
+ * > 0, 0 <= tau <= 1 and 1 <= gamma <= 2^20.
+ *
+ * pvlm_window_size: Eq. (Prefill), gamma = c* = T_p / T_q(alpha) as an
+ * integer in [1, gamma_max].  T_p, T_q: measured forward times (any one unit,
+ * finite, > 0).  The quotient is first taken as the integer it lies within
+ * 1e-9 (relative) of, if any.  Rounding (Suppl. "Window Size Selection"):
+ *   PVLM_ROUND_DOWN / PVLM_ROUND_UP / PVLM_ROUND_NEAREST (halves up);
+ *   PVLM_ROUND_BEST: the gamma of largest t_psd_rollback speedup at this
+ *   tau (0 < tau <= 1), the smaller gamma on ties; it is always the
+ *   rounded-down or rounded-up ratio.  tau is ignored by the other modes.
+ * *gamma receives the window, *c_out (nullable) the unrounded T_p / T_q.
+ * Errors: PVLM_ERR_NULL if gamma is NULL; PVLM_ERR_SHAPE for a time that is
+ * not finite and > 0, gamma_max outside [1, 2^20], an unknown rounding mode,
+ * or PVLM_ROUND_BEST with tau outside (0, 1].
+ * ---------------------------------------------------------------------- */
+typedef enum {
+  PVLM_ROUND_DOWN = 0,
+  PVLM_ROUND_UP = 1,
+  PVLM_ROUND_NEAREST = 2,
+  PVLM_ROUND_BEST = 3
+} pvlm_round;
+
+typedef struct {
+  double t_sd_ideal, t_psd_ideal, t_sd, t_psd, t_psd_rollback;
+  double v_sd_ideal, v_psd_ideal, v_sd, v_psd, v_psd_rollback;
+  double expected_accepted, expected_total;
+} pvlm_speedup_model;
+
+pvlm_status pvlm_speedup(double c, double tau, int gamma, pvlm_speedup_model* out);
+pvlm_status pvlm_window_size(double t_p, double t_q, pvlm_round rounding, double tau,
+                             int gamma_max, int* gamma, double* c_out);
 
 #ifdef __cplusplus
 }

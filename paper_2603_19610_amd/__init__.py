@@ -31,6 +31,7 @@ EXPORTS = (
     "pvlm_topk_workspace_size", "pvlm_topk_select",
     "pvlm_gather_kv",
     "pvlm_spec_accept_workspace_size", "pvlm_spec_accept",
+    "pvlm_speedup", "pvlm_window_size",
 )
 
 
@@ -52,6 +53,23 @@ _I = _c.c_int
 _I64 = _c.c_int64
 _SZ = _c.c_size_t
 _F = _c.c_float
+_D = _c.c_double
+
+PVLM_ROUND_DOWN, PVLM_ROUND_UP, PVLM_ROUND_NEAREST, PVLM_ROUND_BEST = 0, 1, 2, 3
+_ROUNDING = {"down": PVLM_ROUND_DOWN, "up": PVLM_ROUND_UP, "nearest": PVLM_ROUND_NEAREST,
+             "best": PVLM_ROUND_BEST}
+
+
+class SpeedupModel(_c.Structure):
+    """pvlm_speedup_model: per-token times (units of the draft forward t) and
+    speedups against target-only decoding."""
+    _fields_ = [(n, _c.c_double) for n in (
+        "t_sd_ideal", "t_psd_ideal", "t_sd", "t_psd", "t_psd_rollback",
+        "v_sd_ideal", "v_psd_ideal", "v_sd", "v_psd", "v_psd_rollback",
+        "expected_accepted", "expected_total")]
+
+    def as_dict(self):
+        return {n: getattr(self, n) for n, _ in self._fields_}
 
 _SIGS = {
     "pvlm_status_string": (_c.c_char_p, [_I]),
@@ -71,6 +89,8 @@ _SIGS = {
                             _P, _P]),
     "pvlm_spec_accept_workspace_size": (_SZ, [_I, _I, _I]),
     "pvlm_spec_accept": (_I, [_I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P]),
+    "pvlm_speedup": (_I, [_D, _D, _I, _c.POINTER(SpeedupModel)]),
+    "pvlm_window_size": (_I, [_D, _D, _I, _D, _I, _c.POINTER(_I), _c.POINTER(_D)]),
 }
 
 
@@ -356,3 +376,23 @@ __all__ = [
     "PVLM_F32", "PVLM_BF16", "PVLM_CRIT_MASS", "PVLM_CRIT_COSSIM", "PVLM_DEV_RANGE",
     "PVLM_DEV_TIMEOUT", "PVLM_DEV_PLACEMENT",
 ]
+
+
+def speedup(c: float, tau: float, gamma: int) -> dict:
+    """pvlm_speedup: the speedup analysis for speed ratio c, acceptance rate
+    tau and window gamma (host arithmetic, no GPU)."""
+    out = SpeedupModel()
+    _check(lib().pvlm_speedup(float(c), float(tau), int(gamma), _c.byref(out)), "speedup")
+    return out.as_dict()
+
+
+def window_size(t_p: float, t_q: float, rounding: str = "down", tau: float = 0.0,
+                gamma_max: int = 64):
+    """pvlm_window_size: the draft window gamma = T_p / T_q rounded as asked;
+    returns (gamma, c)."""
+    if rounding not in _ROUNDING:
+        raise ValueError(f"rounding must be one of {sorted(_ROUNDING)}")
+    g, c = _I(0), _D(0.0)
+    _check(lib().pvlm_window_size(float(t_p), float(t_q), _ROUNDING[rounding], float(tau),
+                                  int(gamma_max), _c.byref(g), _c.byref(c)), "window_size")
+    return g.value, c.value
