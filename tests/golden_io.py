@@ -85,3 +85,21 @@ def window_fixture():
         elif key == "window_gain":
             out["window_gain"] = float(rest[0])
     return out
+
+
+def pipeline_trace():
+    """The gamma = 3 pipeline example: startup tokens, scripted rounds and
+    the expected outcome."""
+    out = {"rounds": []}
+    for line in _lines("pipeline_trace.txt"):
+        key, rest = line.split(None, 1)
+        if key == "round":
+            drafted, outcome = rest.split("|")
+            drafted = [] if drafted.strip() == "-" else drafted.split()
+            acc, tok = outcome.split()
+            out["rounds"].append((drafted, int(acc), None if tok == "-" else tok))
+        elif key in ("startup", "output", "modes", "draft_keep"):
+            out[key] = rest.split()
+        else:
+            out[key] = float(rest)
+    return out
