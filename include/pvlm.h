@@ -16,6 +16,8 @@
  *   pvlm_window_size,   host-only: the draft window gamma = c* of Eq. (Prefill)
  *   pvlm_speedup        and the speedup analysis (Thm. paravlm_speedup; the
  *                       supplement's theorems and Lemma 1)
+ *   pvlm_pd_*           host-only: the parallel decoding scheduler (pre- and
+ *                       post-verify rounds, draft rollback; Suppl. B)
  *
  * Conventions shared by every call
  *   - Every tensor pointer is a caller-owned DEVICE pointer.  The library never
@@ -288,6 +290,85 @@ typedef struct {
 pvlm_status pvlm_speedup(double c, double tau, int gamma, pvlm_speedup_model* out);
 pvlm_status pvlm_window_size(double t_p, double t_q, pvlm_round rounding, double tau,
                              int gamma_max, int* gamma, double* c_out);
+
+/* ------------------------------------------------------------------------
+ * Parallel decoding scheduler (host-only: no device pointer, no stream).
+ * Suppl. "Parallel Pipeline Details", Alg. (speculative_decoding), with the
+ * startup window of Sec. 4.2, Stage I (iii) and the overlap of Stage II: the
+ * draft drafts the next window while the target verifies the previous one.
+ * The scheduler says what each round runs; the caller runs the draft and the
+ * target (e.g. on two HIP streams, the target's verdict from
+ * pvlm_spec_accept) and reports the outcome.  Positions count output tokens
+ * (the prompt excluded).  A pvlm_pd is owned by one caller thread.
+ *
+ *   startup round   after pvlm_pd_start(startup = d0, d1..d_gamma: the draft's
+ *                   first token and the window it drafted during prefill): the
+ *                   target's prefill output decides d0; no forward, cost 0.
+ *   PRE_VERIFY      nothing pending: the draft drafts gamma tokens from the
+ *                   committed prefix, the target verifies the first of them.
+ *   POST_VERIFY     the target verifies the pending window while the draft
+ *                   drafts gamma tokens after it.
+ * pvlm_pd_finish(drafted = the round's draft_count new tokens, n_accepted of
+ * the verify_count verified tokens, target_token = the target's token at the
+ * first rejection, ignored when all were accepted):
+ *   all accepted: they are committed; the rest stay pending; the next round
+ *   is POST_VERIFY, or PRE_VERIFY if nothing is pending (gamma = 1).
+ *   a rejection: the accepted prefix and target_token are committed, every
+ *   other draft is dropped, draft_keep becomes the committed count before
+ *   target_token (the draft truncates its cache to the prompt plus that many
+ *   output tokens and resumes from target_token), the next round is PRE_VERIFY.
+ * A round that runs forwards costs max(gamma, c) units of t (the draft's
+ * forward time); c = T_p / T_q.  Once max_len tokens are committed the plan's
+ * mode is PVLM_PD_DONE (the output may overrun max_len by the last round).
+ * max_draft_run is the longest run of committed draft tokens not interrupted
+ * by a target token (the adaptive draft length).
+ *
+ * Errors: PVLM_ERR_NULL for a NULL handle or required pointer; PVLM_ERR_SHAPE
+ * for gamma outside [1, 1024], c not finite and > 0, max_len outside
+ * [1, 2^26], start twice, plan/finish before start, finish when DONE, a
+ * drafted count other than the plan's draft_count or n_accepted outside
+ * [0, verify_count] (the state is then unchanged); PVLM_ERR_UNSUPPORTED if
+ * the handle cannot be allocated.  pvlm_pd_output / pvlm_pd_pending copy up
+ * to cap tokens to a host buffer and set *n to the full count; dst = NULL
+ * with cap = 0 only queries *n; a smaller cap copies a prefix and returns
+ * PVLM_ERR_SHAPE.
+ * ---------------------------------------------------------------------- */
+typedef enum {
+  PVLM_PD_PRE_VERIFY = 0,
+  PVLM_PD_POST_VERIFY = 1,
+  PVLM_PD_DONE = 2
+} pvlm_pd_mode;
+
+typedef struct {
+  int32_t mode;          /* pvlm_pd_mode */
+  int32_t verify_begin;  /* output position of the first token the target verifies */
+  int32_t verify_count;  /* tokens the target verifies */
+  int32_t draft_begin;   /* output position of the draft's first new token */
+  int32_t draft_count;   /* tokens the draft drafts this round */
+  double cost;           /* duration, units of t */
+} pvlm_pd_round;
+
+typedef struct {
+  int32_t mode;           /* mode of the next round */
+  int32_t committed;      /* committed output tokens */
+  int32_t pending;        /* drafted tokens awaiting verification */
+  int32_t target_rounds;  /* rounds that ran forwards */
+  int32_t max_draft_run;  /* adaptive draft length */
+  int32_t draft_keep;     /* rollback point of the last rejection (0 before any) */
+  double elapsed;         /* sum of round costs, units of t */
+} pvlm_pd_stats;
+
+typedef struct pvlm_pd pvlm_pd;
+
+pvlm_status pvlm_pd_create(int gamma, double c, int max_len, pvlm_pd** out);
+void pvlm_pd_destroy(pvlm_pd* pd);
+pvlm_status pvlm_pd_start(pvlm_pd* pd, const int32_t* startup);
+pvlm_status pvlm_pd_plan(const pvlm_pd* pd, pvlm_pd_round* round);
+pvlm_status pvlm_pd_finish(pvlm_pd* pd, const int32_t* drafted, int n_drafted, int n_accepted,
+                           int32_t target_token);
+pvlm_status pvlm_pd_output(const pvlm_pd* pd, int32_t* dst, int cap, int* n);
+pvlm_status pvlm_pd_pending(const pvlm_pd* pd, int32_t* dst, int cap, int* n);
+pvlm_status pvlm_pd_get_stats(const pvlm_pd* pd, pvlm_pd_stats* st);
 
 #ifdef __cplusplus
 }

@@ -32,6 +32,8 @@ EXPORTS = (
     "pvlm_gather_kv",
     "pvlm_spec_accept_workspace_size", "pvlm_spec_accept",
     "pvlm_speedup", "pvlm_window_size",
+    "pvlm_pd_create", "pvlm_pd_destroy", "pvlm_pd_start", "pvlm_pd_plan", "pvlm_pd_finish",
+    "pvlm_pd_output", "pvlm_pd_pending", "pvlm_pd_get_stats",
 )
 
 
@@ -71,6 +73,24 @@ class SpeedupModel(_c.Structure):
     def as_dict(self):
         return {n: getattr(self, n) for n, _ in self._fields_}
 
+
+PVLM_PD_PRE_VERIFY, PVLM_PD_POST_VERIFY, PVLM_PD_DONE = 0, 1, 2
+_PD_MODES = {PVLM_PD_PRE_VERIFY: "pre", PVLM_PD_POST_VERIFY: "post", PVLM_PD_DONE: "done"}
+
+
+class PdRound(_c.Structure):
+    """pvlm_pd_round: what one round of the parallel decoding pipeline runs."""
+    _fields_ = [("mode", _c.c_int32), ("verify_begin", _c.c_int32),
+                ("verify_count", _c.c_int32), ("draft_begin", _c.c_int32),
+                ("draft_count", _c.c_int32), ("cost", _c.c_double)]
+
+
+class PdStats(_c.Structure):
+    """pvlm_pd_stats: the scheduler's counters."""
+    _fields_ = [("mode", _c.c_int32), ("committed", _c.c_int32), ("pending", _c.c_int32),
+                ("target_rounds", _c.c_int32), ("max_draft_run", _c.c_int32),
+                ("draft_keep", _c.c_int32), ("elapsed", _c.c_double)]
+
 _SIGS = {
     "pvlm_status_string": (_c.c_char_p, [_I]),
     "pvlm_last_hip_error": (_c.c_char_p, []),
@@ -91,6 +111,14 @@ _SIGS = {
     "pvlm_spec_accept": (_I, [_I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P]),
     "pvlm_speedup": (_I, [_D, _D, _I, _c.POINTER(SpeedupModel)]),
     "pvlm_window_size": (_I, [_D, _D, _I, _D, _I, _c.POINTER(_I), _c.POINTER(_D)]),
+    "pvlm_pd_create": (_I, [_I, _D, _I, _c.POINTER(_P)]),
+    "pvlm_pd_destroy": (None, [_P]),
+    "pvlm_pd_start": (_I, [_P, _P]),
+    "pvlm_pd_plan": (_I, [_P, _c.POINTER(PdRound)]),
+    "pvlm_pd_finish": (_I, [_P, _P, _I, _I, _c.c_int32]),
+    "pvlm_pd_output": (_I, [_P, _P, _I, _c.POINTER(_I)]),
+    "pvlm_pd_pending": (_I, [_P, _P, _I, _c.POINTER(_I)]),
+    "pvlm_pd_get_stats": (_I, [_P, _c.POINTER(PdStats)]),
 }
 
 
@@ -396,3 +424,72 @@ def window_size(t_p: float, t_q: float, rounding: str = "down", tau: float = 0.0
     _check(lib().pvlm_window_size(float(t_p), float(t_q), _ROUNDING[rounding], float(tau),
                                   int(gamma_max), _c.byref(g), _c.byref(c)), "window_size")
     return g.value, c.value
+
+
+class Scheduler:
+    """The library's parallel decoding scheduler (pvlm_pd_*): host state only.
+
+    ``plan()`` says what the next round runs, ``finish()`` reports the
+    target's verdict; tokens are Python ints."""
+
+    def __init__(self, gamma: int, c: float, max_len: int):
+        h = _P()
+        _check(lib().pvlm_pd_create(int(gamma), float(c), int(max_len), _c.byref(h)),
+               "pd_create")
+        self._h = h
+        self.gamma = int(gamma)
+
+    def close(self):
+        if self._h is not None and self._h.value:
+            lib().pvlm_pd_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @staticmethod
+    def _arr(tokens):
+        tokens = list(tokens)
+        return (_c.c_int32 * max(len(tokens), 1))(*tokens), len(tokens)
+
+    def start(self, startup):
+        arr, n = self._arr(startup)
+        if n != self.gamma + 1:
+            raise ValueError(f"startup needs gamma + 1 = {self.gamma + 1} tokens")
+        _check(lib().pvlm_pd_start(self._h, arr), "pd_start")
+
+    def plan(self) -> dict:
+        r = PdRound()
+        _check(lib().pvlm_pd_plan(self._h, _c.byref(r)), "pd_plan")
+        d = {n: getattr(r, n) for n, _ in r._fields_}
+        d["mode"] = _PD_MODES[r.mode]
+        return d
+
+    def finish(self, drafted, n_accepted: int, target_token=None):
+        arr, n = self._arr(drafted)
+        tok = -1 if target_token is None else int(target_token)
+        _check(lib().pvlm_pd_finish(self._h, arr if n else None, n, int(n_accepted), tok),
+               "pd_finish")
+
+    def _tokens(self, fn):
+        n = _I(0)
+        _check(fn(self._h, None, 0, _c.byref(n)), "pd_tokens")
+        buf = (_c.c_int32 * max(n.value, 1))()
+        _check(fn(self._h, buf, n.value, _c.byref(n)), "pd_tokens")
+        return list(buf[:n.value])
+
+    def output(self):
+        return self._tokens(lib().pvlm_pd_output)
+
+    def pending(self):
+        return self._tokens(lib().pvlm_pd_pending)
+
+    def stats(self) -> dict:
+        st = PdStats()
+        _check(lib().pvlm_pd_get_stats(self._h, _c.byref(st)), "pd_stats")
+        d = {n: getattr(st, n) for n, _ in st._fields_}
+        d["mode"] = _PD_MODES[st.mode]
+        return d
