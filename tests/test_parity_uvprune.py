@@ -89,3 +89,32 @@ def test_cossim_72b_shape_sampled():
     r0 = oracle.criterion_cossim(hv0, ht0, mm, nn)
     rL = oracle.criterion_cossim(hvL, htL, mm, nn)
     _assert_score(got[0, rows], (rL - r0)[0], (np.abs(rL) + np.abs(r0))[0])
+
+
+@pytest.mark.parametrize("dtype,L", [("bf16", 5), ("f32", 2)])
+def test_cossim_streamed_over_layers(dtype, L):
+    """UV-Prune as the target's prefill would run it: one criterion launch as
+    layer 0's hidden states exist and one as layer L's, keeping only c^0 and
+    c^L (the layer sum telescopes); the score is their difference, taken by the
+    MASS operator over the two-row stack.  It must equal the literal
+    all-layer Eq. (average_similarity) of the oracle."""
+    w = W.WORKLOADS["tiny"]
+    w = W.Workload(**{**w.__dict__, "dtype": dtype, "batch": 2, "n_text": 33, "frames": 3,
+                      "tokens_per_frame": 101})
+    h = W.make_hidden_inputs(w, L, hidden=256)
+    m = np.array([303, 250], np.int32)
+    n = np.array([33, 20], np.int32)
+    note(f"uvprune streamed cossim {dtype} L={L}")
+    m_d, n_d = to_dev(m), to_dev(n)
+    stack = torch.zeros((2, 2, h.hv.shape[2]), dtype=torch.float32, device="cuda")
+    for l in range(L + 1):          # layers arrive one by one during prefill
+        if l in (0, L):
+            pv.uvprune_criterion_cossim(to_dev(h.hv[l]), to_dev(h.ht[l]), m_d, n_d,
+                                        out=stack[0 if l == 0 else 1])
+    s = pv.uvprune_score_mass(stack, m_d)
+    torch.cuda.synchronize()
+    hv64, ht64 = f64(h.hv, dtype), f64(h.ht, dtype)
+    ref = oracle.uvprune_score_cossim(hv64, ht64, m, n)
+    aL = _abs_cos_sum(hv64[L], ht64[L], m, n)
+    a0 = _abs_cos_sum(hv64[0], ht64[0], m, n)
+    _assert_score(to_host_f64(s), ref, aL + a0)
