@@ -24,6 +24,8 @@ explicit loops over the indices the paper sums over, following the paper:
 * ``window``           -- draft window size, Eq. (Prefill), and the speedup
                           model of Thm. (paravlm_speedup) and the supplement's
                           theorems and Lemma 1.
+* ``rope``             -- rotary position embedding (1-D or M-RoPE) of the
+                          verify rows and their append to the KV cache.
 * ``pipeline``         -- the parallel decoding pipeline's scheduling: pre- and
                           post-verify modes and draft rollback (Suppl.
                           "Parallel Pipeline Details").
@@ -37,7 +39,7 @@ from .uvprune import (cos_similarity, criterion_cossim, uvprune_score_cossim,
                       uvprune_score_mass)
 from .select import topk_keys, topk_select, gather_kv
 from .accept import spec_accept, softmax_t, NEAR_TIE_REL
-from . import pipeline, window
+from . import pipeline, rope, window
 
 __all__ = [
     "verify_attn", "verify_attn_rows", "cos_similarity", "criterion_cossim",
