@@ -4,6 +4,8 @@
  *
  * The five calls follow the paper's statement of the problem
  * (ParallelVLM, arXiv 2603.19610):
+ *   pvlm_rope_append    rotary embedding (1-D or M-RoPE) of the verify rows and
+ *                       their append to the KV cache
  *   pvlm_verify_attn    target verification forward over the video KV cache
  *                       (Sec. 2.2; Sec. 4.2 Parallel Decoding), fused with the
  *                       per-token verifier attention mass (Sec. 3, Challenge 2)
@@ -125,6 +127,41 @@ pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D
                              const void* q, const void* k_cache, const void* v_cache,
                              const int32_t* ctx_len, void* out, float* mass, float* lse,
                              void* ws, size_t ws_bytes, int32_t* status, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * pvlm_rope_append -- rotary embedding of the verify rows and their append to
+ * the cache.  The target verifies the T = gamma + 1 speculated positions in
+ * one forward (Sec. 2.2; Sec. 4.2, Parallel Decoding); pvlm_verify_attn reads
+ * post-rotation queries and a cache whose rows ctx_len[b] .. ctx_len[b]+T-1
+ * hold the verify rows.  This call produces both:
+ *   q_out[b,t,h]                 = rot(q_in[b,t,h],  positions of (b,t))
+ *   k_cache[b,g,ctx_len[b]+t]    = rot(k_in[b,t,g],  positions of (b,t))
+ *   v_cache[b,g,ctx_len[b]+t]    = v_in[b,t,g]       (bit copy)
+ * Every other cache row is left untouched.  rot pairs element i with
+ * i + D/2 (rotate-half): (x_i, x_{i+D/2}) turns by the angle
+ * p_i * base^(-2i/D), i < D/2.  1-D RoPE (LLaVA-OneVision's Qwen2 decoder):
+ * sections = NULL, pos [B][T], p_i = pos[b][t].  M-RoPE (Qwen2.5-VL's decoder,
+ * Qwen2-VL Sec. 2.1): sections = host int32[3] (s0, s1, s2) with
+ * s0 + s1 + s2 = D/2, e.g. (16, 24, 24) at D = 128; pos [3][B][T] holds the
+ * temporal, height and width components; pairs i < s0 take the temporal one,
+ * s0 <= i < s0 + s1 the height one and the rest the width one.  Angles and
+ * their sines and cosines are taken in float64; results are rounded once to
+ * the storage type.
+ *   q_in, q_out [B][T][Hq][D]; k_in, v_in [B][T][Hkv][D];
+ *   k_cache, v_cache [B][Hkv][n_cap][D]; pos, ctx_len int32 device.
+ * q_out may equal q_in (each element is read before it is written by the same
+ * thread); no other argument may alias another.  A ctx_len[b] outside
+ * [0, n_cap - T] is clamped into it and flagged PVLM_DEV_RANGE.
+ * Errors: PVLM_ERR_NULL for a NULL pointer (sections excepted);
+ * PVLM_ERR_SHAPE for a size < 1, Hq not a multiple of Hkv, D odd or > 1024,
+ * n_cap < T or > 2^30, base not finite and > 1, or sections that do not sum
+ * to D/2; PVLM_ERR_UNSUPPORTED for another dtype.
+ * ---------------------------------------------------------------------- */
+pvlm_status pvlm_rope_append(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int64_t n_cap,
+                             double base, const int32_t* sections, const int32_t* pos,
+                             const void* q_in, const void* k_in, const void* v_in,
+                             const int32_t* ctx_len, void* q_out, void* k_cache, void* v_cache,
+                             int32_t* status, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * pvlm_uvprune_score -- UV-Prune score, Eq. (average_similarity):

@@ -31,6 +31,7 @@ EXPORTS = (
     "pvlm_topk_workspace_size", "pvlm_topk_select",
     "pvlm_gather_kv",
     "pvlm_spec_accept_workspace_size", "pvlm_spec_accept",
+    "pvlm_rope_append",
     "pvlm_speedup", "pvlm_window_size",
     "pvlm_pd_create", "pvlm_pd_destroy", "pvlm_pd_start", "pvlm_pd_plan", "pvlm_pd_finish",
     "pvlm_pd_output", "pvlm_pd_pending", "pvlm_pd_get_stats",
@@ -111,6 +112,8 @@ _SIGS = {
     "pvlm_spec_accept": (_I, [_I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P]),
     "pvlm_speedup": (_I, [_D, _D, _I, _c.POINTER(SpeedupModel)]),
     "pvlm_window_size": (_I, [_D, _D, _I, _D, _I, _c.POINTER(_I), _c.POINTER(_D)]),
+    "pvlm_rope_append": (_I, [_I, _I, _I, _I, _I, _I, _I64, _D, _P, _P, _P, _P, _P, _P, _P, _P,
+                              _P, _P, _P]),
     "pvlm_pd_create": (_I, [_I, _D, _I, _c.POINTER(_P)]),
     "pvlm_pd_destroy": (None, [_P]),
     "pvlm_pd_start": (_I, [_P, _P]),
@@ -493,3 +496,40 @@ class Scheduler:
         d = {n: getattr(st, n) for n, _ in st._fields_}
         d["mode"] = _PD_MODES[st.mode]
         return d
+
+
+def rope_append(q, k_new, v_new, pos, ctx_len, k_cache, v_cache, *, base: float,
+                sections=None, q_out=None, status=None):
+    """pvlm_rope_append: rotate q and k_new by their positions (1-D RoPE, or
+    M-RoPE with ``sections`` = (s0, s1, s2)) and write k_new / v_new into the
+    caches at rows ctx_len[b] + t.  q [B][T][Hq][D]; k_new, v_new [B][T][Hkv][D];
+    pos [B][T] or [3][B][T] int32; caches [B][Hkv][n_cap][D].  Returns q_out."""
+    _need(q, "q")
+    dev = q.device
+    for t, name in ((k_new, "k_new"), (v_new, "v_new"), (k_cache, "k_cache"),
+                    (v_cache, "v_cache")):
+        _need(t, name, q.dtype, dev)
+    _need(pos, "pos", torch.int32, dev)
+    _need(ctx_len, "ctx_len", torch.int32, dev)
+    B, T, Hq, D = q.shape
+    Hkv = k_new.shape[2]
+    n_cap = k_cache.shape[2]
+    if tuple(k_new.shape) != (B, T, Hkv, D) or tuple(v_new.shape) != (B, T, Hkv, D):
+        raise ValueError("k_new and v_new must be [B][T][Hkv][D]")
+    if tuple(k_cache.shape) != (B, Hkv, n_cap, D) or tuple(v_cache.shape) != (B, Hkv, n_cap, D):
+        raise ValueError("caches must be [B][Hkv][n_cap][D]")
+    want = (B, T) if sections is None else (3, B, T)
+    if tuple(pos.shape) != want:
+        raise ValueError(f"pos must be {list(want)}")
+    if tuple(ctx_len.shape) != (B,):
+        raise ValueError("ctx_len must be [B]")
+    if q_out is None:
+        q_out = torch.empty_like(q)
+    else:
+        _need(q_out, "q_out", q.dtype, dev)
+    sec = None if sections is None else (_c.c_int32 * 3)(*[int(x) for x in sections])
+    st = lib().pvlm_rope_append(_dt(q), B, T, Hq, Hkv, D, n_cap, float(base), sec, _ptr(pos),
+                                _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(ctx_len), _ptr(q_out),
+                                _ptr(k_cache), _ptr(v_cache), _ptr(status), _stream())
+    _check(st, "pvlm_rope_append")
+    return q_out
