@@ -410,6 +410,43 @@ def cossim_record(torch, pv, W, dev):
     return rec
 
 
+def rope_record(torch, pv, W, dev):
+    """pvlm_rope_append at the 72B layer shape (T = 9 verify rows, 64 query and
+    8 KV heads, D = 128, bf16, M-RoPE sections 16/24/24), 80 launches per
+    graph replay.  Bytes: the rows read and written (q, k, v in; q, k, v out)."""
+    w = W.WORKLOADS["llava72b"]
+    B, T, Hq, Hkv, D = w.batch, w.T, w.hq, w.hkv, w.head_dim
+    n_cap = w.n_cap()
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2603)
+    q = torch.randn((B, T, Hq, D), device=dev, generator=gen).to(torch.bfloat16)
+    kn = torch.randn((B, T, Hkv, D), device=dev, generator=gen).to(torch.bfloat16)
+    vn = torch.randn((B, T, Hkv, D), device=dev, generator=gen).to(torch.bfloat16)
+    kc = torch.zeros((B, Hkv, n_cap, D), dtype=torch.bfloat16, device=dev)
+    vc = torch.zeros_like(kc)
+    ctx = torch.from_numpy(w.lengths().astype(np.int32)).to(dev)
+    p1 = ctx[:, None] + torch.arange(T, dtype=torch.int32, device=dev)[None, :]
+    pos = torch.stack([p1, p1, p1]).contiguous()
+    q_out = torch.empty_like(q)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    reps = 80
+
+    def fn():
+        for _ in range(reps):
+            pv.rope_append(q, kn, vn, pos, ctx, kc, vc, base=w.rope_base, sections=(16, 24, 24),
+                           q_out=q_out, status=status)
+
+    g = capture(torch, fn)
+    ms = time_replays(torch, g.replay, 10) / reps
+    nb = 2 * B * T * (Hq + 2 * Hkv) * D * 2 + 4 * (3 * B * T + B)
+    rec = {"workload": "llava72b verify rows: T 9, Hq 64, Hkv 8, D 128, bf16, M-RoPE 16/24/24",
+           "us": round(ms * 1e3, 2), "bytes": nb, "bound": "latency",
+           "device_status": int(status.item())}
+    del q, kn, vn, kc, vc, g
+    torch.cuda.empty_cache()
+    return rec
+
+
 def tiles(w):
     """16-row MFMA tiles per workgroup for the packed query rows of a KV head."""
     rtt = -(-w.group * w.T // 16)
@@ -564,7 +601,7 @@ def main():
     torch.cuda.empty_cache()
 
     others = None
-    cossim = None
+    cossim = rope = None
     if not args.no_extra and graph_used:
         others = {}
         for name in OTHER_CONFIGS:
@@ -574,6 +611,8 @@ def main():
                 f"({time.time() - t0:.1f} s)")
         cossim = cossim_record(torch, pv, W, dev)
         log(f"cossim: {cossim['us']} us")
+        rope = rope_record(torch, pv, W, dev)
+        log(f"rope_append: {rope['us']} us")
 
     rec = {
         "metric": METRIC,
@@ -614,6 +653,7 @@ def main():
         },
         "other_configs": others,
         "cossim": cossim,
+        "rope_append": rope,
         "cpu_baseline": cpu,
         "device_status": status,
     }
