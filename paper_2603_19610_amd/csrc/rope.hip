@@ -114,7 +114,8 @@ extern "C" pvlm_status pvlm_rope_append(pvlm_dtype dt, int B, int T, int Hq, int
   if (B < 1 || T < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || D < 2 || D % 2 != 0 || D > 1024 ||
       n_cap < T || n_cap > ((int64_t)1 << 30) || !(base > 1.0 && base < 1e300))
     return PVLM_ERR_SHAPE;
-  if ((int64_t)B * T * (Hq + 2 * Hkv) > ((int64_t)1 << 31)) return PVLM_ERR_SHAPE;
+  // one thread per rotation pair: keep the grid well inside its x-dimension limit
+  if ((int64_t)B * T * (Hq + 2 * Hkv) * (D / 2) > ((int64_t)1 << 38)) return PVLM_ERR_SHAPE;
   RArgs a;
   a.mrope = sections != nullptr;
   if (a.mrope) {
