@@ -155,7 +155,8 @@ pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D
  * Errors: PVLM_ERR_NULL for a NULL pointer (sections excepted);
  * PVLM_ERR_SHAPE for a size < 1, Hq not a multiple of Hkv, D odd or > 1024,
  * n_cap < T or > 2^30, base not finite and > 1, sections that do not sum
- * to D/2, or more than 2^38 rotation pairs (B*T*(Hq+2*Hkv)*D/2);
+ * to D/2, Hq + 2*Hkv > 65536, or more than 2^38 rotation pairs
+ * (B*T*(Hq+2*Hkv)*D/2);
  * PVLM_ERR_UNSUPPORTED for another dtype.
  * ---------------------------------------------------------------------- */
 pvlm_status pvlm_rope_append(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int64_t n_cap,

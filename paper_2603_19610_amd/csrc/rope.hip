@@ -115,7 +115,9 @@ extern "C" pvlm_status pvlm_rope_append(pvlm_dtype dt, int B, int T, int Hq, int
       n_cap < T || n_cap > ((int64_t)1 << 30) || !(base > 1.0 && base < 1e300))
     return PVLM_ERR_SHAPE;
   // one thread per rotation pair: keep the grid well inside its x-dimension limit
-  if ((int64_t)B * T * (Hq + 2 * Hkv) * (D / 2) > ((int64_t)1 << 38)) return PVLM_ERR_SHAPE;
+  const int64_t heads = (int64_t)Hq + 2 * (int64_t)Hkv;
+  if (heads > 65536 || (int64_t)B * T * heads * (D / 2) > ((int64_t)1 << 38))
+    return PVLM_ERR_SHAPE;
   RArgs a;
   a.mrope = sections != nullptr;
   if (a.mrope) {
@@ -143,7 +145,7 @@ extern "C" pvlm_status pvlm_rope_append(pvlm_dtype dt, int B, int T, int Hq, int
   a.Hq = Hq;
   a.Hkv = Hkv;
   a.D = D;
-  a.total = (int64_t)B * T * (Hq + 2 * Hkv) * (D / 2);
+  a.total = (int64_t)B * T * heads * (D / 2);
   const unsigned grid = (unsigned)((a.total + 255) / 256);
   if (dt == PVLM_F32)
     hipLaunchKernelGGL(rope_append_kernel<float>, dim3(grid), dim3(256), 0, stream, a);
