@@ -65,6 +65,8 @@ def parse():
                     help="verify launches per graph replay timed for the roofline")
     ap.add_argument("--verify-only", type=int, default=0,
                     help="profiling helper: run N verify launches and exit")
+    ap.add_argument("--gather-only", type=int, default=0,
+                    help="profiling helper: one eager step, then N 80-layer gathers, and exit")
     ap.add_argument("--copy-only", type=int, default=0,
                     help="profiling helper: N device copies of 512 MiB (counter calibration)")
     return ap.parse_args()
@@ -511,6 +513,15 @@ def main():
             st.verify(r % NL)
         torch.cuda.synchronize()
         print(json.dumps({"verify_only": args.verify_only, "status": int(st.status.item())}))
+        return
+
+    if args.gather_only:
+        st.step()  # the kept indices of this step
+        for _ in range(args.gather_only):
+            st.gather()
+        torch.cuda.synchronize()
+        print(json.dumps({"gather_only": args.gather_only, "bytes_per_gather": NL * gather_bytes(w),
+                          "status": int(st.status.item())}))
         return
 
     # eager warm-up (also sizes the workspaces before any capture)
