@@ -8,6 +8,8 @@
 // sum_j cos(V_i, X_j) = <V_i / |V_i|, sum_j X_j / |X_j|>, so the score needs
 // only layers 0 and L and one normalised mat-vec per layer: streaming work
 // bound by HBM bandwidth.  Zero-norm vectors contribute cosine 0.
+#include <algorithm>
+
 #include "common.h"
 
 namespace pvlm {
@@ -42,11 +44,11 @@ __global__ void __launch_bounds__(256) uv_mass_kernel(const float* crit, const i
   score[gid] = i < mb ? cL - c0 : 0.f;
 }
 
+// Hidden-state element loads: 8 consecutive elements, widened exactly.
 template <typename T>
 struct HS;
 template <>
 struct HS<uint16_t> {
-  // 8 bf16 -> 8 floats
   static __device__ __forceinline__ void load8(const uint16_t* p, float (&f)[8]) {
     const uint4 v = *reinterpret_cast<const uint4*>(p);
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
@@ -67,12 +69,24 @@ struct HS<float> {
   }
 };
 
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// The COSSIM criterion is a sum of n cosines that can cancel to far below
+// the size of its terms, so it is accumulated in float64: bf16 and fp32
+// inputs convert to float64 exactly, every norm, direction sum and dot
+// product is formed in float64, and only the final criterion (or the score
+// c^L - c^0) is rounded, once, to fp32.
+
 // One wave per text row: inv_norm[slot][b][j] = 1/|ht| (0 for zero norm or j >= n[b]).
 template <typename T>
 __global__ void __launch_bounds__(256) txt_norm_kernel(const T* ht, int64_t off0, int64_t off1,
                                                        const int32_t* n_txt,
                                                        int nslots, int B, int64_t n_cap, int Dh,
-                                                       float* inv_norm, int32_t* status) {
+                                                       double* inv_norm, int32_t* status) {
   const int64_t wid = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int lane = threadIdx.x & 63;
   if (wid >= (int64_t)nslots * B * n_cap) return;
@@ -82,19 +96,19 @@ __global__ void __launch_bounds__(256) txt_norm_kernel(const T* ht, int64_t off0
   bool bad = false;
   const int nb = clampi(n_txt[b], 0, (int)n_cap, bad);
   if (bad && j == 0 && slot == 0 && lane == 0) dev_flag(status, PVLM_DEV_RANGE);
-  float inv = 0.f;
+  double inv = 0.0;
   if (j < nb) {
     const T* row = ht + (slot ? off1 : off0) + ((size_t)b * n_cap + j) * Dh;
-    float ss = 0.f;
+    double ss = 0.0;
 #pragma unroll 8  // the row's loads in flight together
     for (int d = lane * 8; d < Dh; d += 512) {
       float f[8];
       HS<T>::load8(row + d, f);
 #pragma unroll
-      for (int k = 0; k < 8; ++k) ss = fmaf(f[k], f[k], ss);
+      for (int k = 0; k < 8; ++k) ss = fma((double)f[k], (double)f[k], ss);
     }
-    ss = warp_sum(ss);
-    inv = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;
+    ss = wave_sum_f64(ss);
+    inv = ss > 0.0 ? 1.0 / sqrt(ss) : 0.0;
   }
   if (lane == 0) inv_norm[wid] = inv;
 }
@@ -109,7 +123,7 @@ template <typename T>
 __global__ void __launch_bounds__(64) txt_dir_part_kernel(const T* ht, int64_t off0, int64_t off1,
                                                           const int32_t* n_txt, int B,
                                                           int64_t n_cap, int Dh, int nchunk,
-                                                          const float* inv_norm, float* part) {
+                                                          const double* inv_norm, double* part) {
   const int c = blockIdx.y, sb = blockIdx.z, slot = sb / B, b = sb % B;
   const int d = (blockIdx.x * 64 + threadIdx.x) * 8;
   if (d >= Dh) return;
@@ -117,90 +131,116 @@ __global__ void __launch_bounds__(64) txt_dir_part_kernel(const T* ht, int64_t o
   nb = nb < 0 ? 0 : (nb > n_cap ? (int)n_cap : nb);
   const int j0 = c * kTxtChunk, j1 = min(nb, j0 + kTxtChunk);
   const T* base = ht + (slot ? off1 : off0) + (size_t)b * n_cap * Dh + d;
-  const float* inv = inv_norm + ((size_t)slot * B + b) * n_cap;
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  const double* inv = inv_norm + ((size_t)slot * B + b) * n_cap;
+  double acc[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
 #pragma unroll 8  // rows' loads in flight together
   for (int j = j0; j < j1; ++j) {
-    const float wj = inv[j];
+    const double wj = inv[j];
     float f[8];
     HS<T>::load8(base + (size_t)j * Dh, f);
 #pragma unroll
-    for (int k = 0; k < 8; ++k) acc[k] = fmaf(f[k], wj, acc[k]);
+    for (int k = 0; k < 8; ++k) acc[k] = fma((double)f[k], wj, acc[k]);
   }
-  float* pp = part + ((size_t)sb * nchunk + c) * Dh + d;
-  *reinterpret_cast<float4*>(pp) = make_float4(acc[0], acc[1], acc[2], acc[3]);
-  *reinterpret_cast<float4*>(pp + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
+  double* pp = part + ((size_t)sb * nchunk + c) * Dh + d;
+#pragma unroll
+  for (int k = 0; k < 8; k += 2) *reinterpret_cast<double2*>(pp + k) = make_double2(acc[k], acc[k + 1]);
 }
 
-__global__ void __launch_bounds__(256) txt_dir_sum_kernel(const float* part, int Dh, int nchunk,
-                                                          float* u) {
+__global__ void __launch_bounds__(256) txt_dir_sum_kernel(const double* part, int Dh, int nchunk,
+                                                          double* u) {
   const int sb = blockIdx.y;
   const int d = blockIdx.x * 256 + threadIdx.x;
   if (d >= Dh) return;
-  const float* p = part + (size_t)sb * nchunk * Dh + d;
-  float acc = 0.f;
+  const double* p = part + (size_t)sb * nchunk * Dh + d;
+  double acc = 0.0;
   for (int c = 0; c < nchunk; ++c) acc += p[(size_t)c * Dh];
   u[(size_t)sb * Dh + d] = acc;
 }
 
-// One wave per visual row: c_slot = <hv, u_slot> / |hv| (0 for zero norm).
+// c_slot = <hv, u_slot> / |hv| (0 for zero norm), one wave per visual row.
+// A workgroup of 16 waves first stages the direction vectors of its batch
+// row (both slots, float64) in LDS, then its waves stream visual rows
+// against them (rows blockIdx.x * 16 + wave, stepping by the grid's waves).
+// Lane l handles elements 8 (l + 64 i) + k, k < 8, of a row (16-byte
+// loads); u is staged transposed, s_u[slot][k][d / 8], so the lanes of a
+// wave read consecutive words.  The dot product is float64 (it can cancel);
+// the squared norm sums positive terms only, so fp32 keeps its relative
+// error below 1e-5 (at most 134 roundings), far inside the criterion's gate.
 // nslots == 2: out = c_1 - c_0 (the score); nslots == 1: out = c_0.
+constexpr int kVisThreads = 1024;
 template <typename T>
-__global__ void __launch_bounds__(256) vis_kernel(const T* hv, int64_t off0, int64_t off1,
-                                                  const int32_t* m, int nslots,
-                                                  int B, int64_t m_cap, int Dh, const float* u,
-                                                  float* out, int32_t* status) {
-  const int64_t wid = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-  const int lane = threadIdx.x & 63;
-  if (wid >= (int64_t)B * m_cap) return;
-  const int b = wid / m_cap;
-  const int64_t i = wid % m_cap;
+__global__ void __launch_bounds__(kVisThreads) vis_kernel(const T* hv, int64_t off0, int64_t off1,
+                                                          const int32_t* m, int nslots,
+                                                          int B, int64_t m_cap, int Dh, const double* u,
+                                                          float* out, int32_t* status) {
+  extern __shared__ __align__(16) double s_u[];  // [nslots][8][Dh / 8]
+  const int b = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int D8 = Dh / 8;
+  for (int s = 0; s < nslots; ++s)
+    for (int d = threadIdx.x; d < Dh; d += kVisThreads)
+      s_u[(s * 8 + (d & 7)) * D8 + (d >> 3)] = u[((size_t)s * B + b) * Dh + d];
+  __syncthreads();
   bool bad = false;
   const int mb = clampi(m[b], 0, (int)m_cap, bad);
-  if (bad && i == 0 && lane == 0) dev_flag(status, PVLM_DEV_RANGE);
-  float res = 0.f;
-  if (i < mb) {
-    float c[2] = {0.f, 0.f};
-    for (int s = 0; s < nslots; ++s) {
-      const T* row = hv + (s ? off1 : off0) + ((size_t)b * m_cap + i) * Dh;
-      const float* us = u + ((size_t)s * B + b) * Dh;
-      float dot = 0.f, ss = 0.f;
-      for (int d = lane * 8; d < Dh; d += 512) {
-        float f[8];
-        HS<T>::load8(row + d, f);
-        const float4 u0 = *reinterpret_cast<const float4*>(us + d);
-        const float4 u1 = *reinterpret_cast<const float4*>(us + d + 4);
-        const float uu[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+  if (bad && blockIdx.x == 0 && threadIdx.x == 0) dev_flag(status, PVLM_DEV_RANGE);
+  const int64_t step = (int64_t)gridDim.x * (kVisThreads / 64);
+  for (int64_t i = (int64_t)blockIdx.x * (kVisThreads / 64) + wave; i < m_cap; i += step) {
+    double res = 0.0;
+    if (i < mb) {
+      double c[2] = {0.0, 0.0};
+      for (int s = 0; s < nslots; ++s) {
+        const T* row = hv + (s ? off1 : off0) + ((size_t)b * m_cap + i) * Dh;
+        const double* us = s_u + s * 8 * D8;
+        double dot = 0.0;
+        float ss = 0.f;
+#pragma unroll 8  // the row's loads in flight together
+        for (int j = lane; j < D8; j += 64) {
+          float f[8];
+          HS<T>::load8(row + 8 * j, f);
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          dot = fmaf(f[k], uu[k], dot);
-          ss = fmaf(f[k], f[k], ss);
+          for (int k = 0; k < 8; ++k) {
+            dot = fma((double)f[k], us[k * D8 + j], dot);
+            ss = fmaf(f[k], f[k], ss);
+          }
         }
+        dot = wave_sum_f64(dot);
+        ss = warp_sum(ss);
+        c[s] = ss > 0.f ? dot / sqrt((double)ss) : 0.0;
       }
-      dot = warp_sum(dot);
-      ss = warp_sum(ss);
-      c[s] = ss > 0.f ? dot / sqrtf(ss) : 0.f;
+      res = nslots == 2 ? c[1] - c[0] : c[0];
     }
-    res = nslots == 2 ? c[1] - c[0] : c[0];
+    if (lane == 0) out[(size_t)b * m_cap + i] = (float)res;
   }
-  if (lane == 0) out[wid] = res;
 }
 
 int txt_chunks(int64_t n_cap) { return (int)((n_cap + kTxtChunk - 1) / kTxtChunk); }
 
-// inverse norms [2][B][n_cap], u [2][B][Dh], chunk partials [2][B][chunks][Dh]
+// inverse norms [2][B][n_cap], u [2][B][Dh], chunk partials [2][B][chunks][Dh], all float64
 size_t cossim_ws(int B, int Dh, int64_t n_cap) {
-  size_t off = align_up(sizeof(float) * 2 * (size_t)B * n_cap, 256);
-  off = align_up(off + sizeof(float) * 2 * (size_t)B * Dh, 256);
-  off = align_up(off + sizeof(float) * 2 * (size_t)B * txt_chunks(n_cap) * Dh, 256);
+  size_t off = align_up(sizeof(double) * 2 * (size_t)B * n_cap, 256);
+  off = align_up(off + sizeof(double) * 2 * (size_t)B * Dh, 256);
+  off = align_up(off + sizeof(double) * 2 * (size_t)B * txt_chunks(n_cap) * Dh, 256);
   return off;
 }
+
+// Largest hidden size whose two float64 direction vectors fit the vis
+// kernel's LDS.
+constexpr int kMaxDh = 8192;
 
 template <typename T>
 pvlm_status launch_cossim(int nslots, int64_t voff0, int64_t voff1, int64_t toff0, int64_t toff1,
                           int B, int64_t m_cap, const int32_t* m, int Dh, int64_t n_cap,
-                          const int32_t* n_txt, const T* hv, const T* ht, float* outp, float* inv,
-                          float* u, float* part, int32_t* status, hipStream_t stream) {
+                          const int32_t* n_txt, const T* hv, const T* ht, float* outp, double* inv,
+                          double* u, double* part, int32_t* status, hipStream_t stream) {
+  const int lds = (int)(sizeof(double) * nslots * Dh);
+  PVLM_HIP(allow_dynamic_lds(reinterpret_cast<const void*>(vis_kernel<T>), 2 * kMaxDh * (int)sizeof(double)));
+  DeviceInfo di;
+  const pvlm_status st = device_info(&di);
+  if (st != PVLM_OK) return st;
+  // about one workgroup per compute unit over the batch rows
+  const int64_t per_b = (di.cus + B - 1) / B;
+  const int64_t vis_x = std::max<int64_t>(1, std::min<int64_t>(per_b, (m_cap + 15) / 16));
   const int64_t nw = (int64_t)nslots * B * n_cap;
   hipLaunchKernelGGL(txt_norm_kernel<T>, dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream, ht,
                      toff0, toff1, n_txt, nslots, B, n_cap, Dh, inv, status);
@@ -212,8 +252,7 @@ pvlm_status launch_cossim(int nslots, int64_t voff0, int64_t voff1, int64_t toff
   hipLaunchKernelGGL(txt_dir_sum_kernel, dim3((Dh + 255) / 256, nslots * B), dim3(256), 0, stream, part,
                      Dh, nchunk, u);
   PVLM_LAUNCHED();
-  const int64_t vw = (int64_t)B * m_cap;
-  hipLaunchKernelGGL(vis_kernel<T>, dim3((unsigned)((vw + 3) / 4)), dim3(256), 0, stream, hv, voff0,
+  hipLaunchKernelGGL(vis_kernel<T>, dim3((unsigned)vis_x, B), dim3(kVisThreads), lds, stream, hv, voff0,
                      voff1, m, nslots, B, m_cap, Dh, u, outp, status);
   PVLM_LAUNCHED();
   return PVLM_OK;
@@ -228,16 +267,21 @@ pvlm_status run_cossim(int nslots, int L, int B, int64_t m_cap, const int32_t* m
   if (!m || !n_txt || !hs_vis || !hs_txt || !outp) return PVLM_ERR_NULL;
   if (hdt != PVLM_F32 && hdt != PVLM_BF16) return PVLM_ERR_UNSUPPORTED;
   if (B < 1 || m_cap < 1 || n_cap < 1 || Dh < 8 || Dh % 8 != 0) return PVLM_ERR_SHAPE;
-  if (m_cap > ((int64_t)1 << 30) || n_cap > ((int64_t)1 << 30)) return PVLM_ERR_SHAPE;
+  if (Dh > kMaxDh) return PVLM_ERR_UNSUPPORTED;
+  // launch limits: grid y and z of at most 65535 (the text-direction
+  // partials run over 2 * B batch-slots and n_cap / 32 chunks), and one
+  // 64-lane wave per text row of both slots in a grid x below 2^31
+  if (m_cap > ((int64_t)1 << 30) || 2 * (int64_t)B > 65535 || txt_chunks(n_cap) > 65535 ||
+      ((int64_t)2 * B * n_cap + 3) / 4 >= ((int64_t)1 << 31))
+    return PVLM_ERR_SHAPE;
   if (nslots == 2 && L < 1) return PVLM_ERR_SHAPE;
   const size_t need = cossim_ws(B, Dh, n_cap);
   if (!ws || ws_bytes < need) return PVLM_ERR_WORKSPACE;
   char* w = static_cast<char*>(ws);
-  float* inv = reinterpret_cast<float*>(w);
-  float* u = reinterpret_cast<float*>(w + align_up(sizeof(float) * 2 * (size_t)B * n_cap, 256));
-  float* part = reinterpret_cast<float*>(
-      w + align_up(align_up(sizeof(float) * 2 * (size_t)B * n_cap, 256) + sizeof(float) * 2 * (size_t)B * Dh,
-                   256));
+  double* inv = reinterpret_cast<double*>(w);
+  const size_t off_u = align_up(sizeof(double) * 2 * (size_t)B * n_cap, 256);
+  double* u = reinterpret_cast<double*>(w + off_u);
+  double* part = reinterpret_cast<double*>(w + align_up(off_u + sizeof(double) * 2 * (size_t)B * Dh, 256));
   const int64_t vls = (int64_t)B * m_cap * Dh, tls = (int64_t)B * n_cap * Dh;
   const int64_t l1 = nslots == 2 ? L : 0;
   if (hdt == PVLM_BF16)

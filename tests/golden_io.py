@@ -58,9 +58,9 @@ def topk_fixture():
     return groups
 
 
-def accept_fixture():
+def accept_fixture(name="spec_accept.txt"):
     out = {"cases": []}
-    for line in _lines("spec_accept.txt"):
+    for line in _lines(name):
         key, rest = line.split(None, 1)
         if key == "case":
             u, e = rest.split("|")

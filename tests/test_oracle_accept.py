@@ -119,3 +119,83 @@ def test_near_tie_flag():
     _, _, tie = oracle.spec_accept(q[None, None], np.stack([p, p])[None],
                                    np.array([[1]], np.int32), np.array([[u]]), np.array([0.3]), 1.0)
     assert tie[0] == 1
+
+
+# ---- temperature (Sec. 2.2 rule with p and q at temperature tau) ----------
+def _tempered_fixture():
+    fx = accept_fixture("spec_accept_temperature.txt")
+    tau = float(fx["tau"][0])
+    dl = (tau * np.log(fx["q1"]))[None, None, :].astype(np.float32)
+    tl = np.stack([tau * np.log(fx["p1"]), tau * np.log(fx["p2"])])[None].astype(np.float32)
+    toks = np.array([[int(fx["x"][0])]], dtype=np.int32)
+    return fx, tau, dl, tl, toks
+
+
+def _fixture_mismatches(fn, fx, tau, dl, tl, toks):
+    bad = 0
+    for ua, us, na, nt in fx["cases"]:
+        n, y, _ = fn(dl, tl, toks, np.array([[ua]]), np.array([us]), tau)
+        bad += (int(n[0]), int(y[0])) != (na, nt)
+    return bad
+
+
+def test_golden_cases_at_temperature():
+    fx, tau, dl, tl, toks = _tempered_fixture()
+    for ua, us, na, nt in fx["cases"]:
+        n, y, tie = oracle.spec_accept(dl, tl, toks, np.array([[ua]]), np.array([us]), tau)
+        assert (int(n[0]), int(y[0])) == (na, nt), (ua, us)
+        assert tie[0] == 0
+
+
+def test_temperature_slips_fail_the_fixture(monkeypatch):
+    """Each plausible temperature slip, planted in the oracle, fails at least
+    one hand-derived case: the fixture pins the scaling, not just the rule."""
+    import oracle.accept as A
+    fx, tau, dl, tl, toks = _tempered_fixture()
+    assert _fixture_mismatches(oracle.spec_accept, fx, tau, dl, tl, toks) == 0
+    good = A.softmax_t
+
+    def times_tau(z, t):
+        return good(np.asarray(z, np.float64) * t * t, t)    # softmax(z * tau)
+
+    def untempered(z, t):
+        return good(np.asarray(z, np.float64) * t, t)        # softmax(z)
+
+    for slip in (times_tau, untempered):
+        monkeypatch.setattr(A, "softmax_t", slip)
+        assert _fixture_mismatches(A.spec_accept, fx, tau, dl, tl, toks) > 0, slip.__name__
+    monkeypatch.setattr(A, "softmax_t", good)
+    # only one of p and q tempered: the other's logits effectively unscaled
+    q_only = lambda d, t_, *r: A.spec_accept(d, (t_ * tau).astype(np.float32), *r)
+    p_only = lambda d, t_, *r: A.spec_accept((d * tau).astype(np.float32), t_, *r)
+    for slip in (q_only, p_only):
+        assert _fixture_mismatches(slip, fx, tau, dl, tl, toks) > 0
+
+
+def test_acceptance_rate_and_output_law_at_temperature():
+    """tau = 0.7: per-position acceptance probability sum_x min(p_tau, q_tau)
+    and the emitted-token law p_tau, with p_tau and q_tau from torch.softmax in
+    float64 (a library routine independent of the oracle's softmax)."""
+    import torch
+    tau = float(np.float32(0.7))   # the oracle takes the temperature as float32
+    V = 6
+    p_logits = np.array([1.2, -0.3, 0.5, 2.0, -1.0, 0.1], np.float32)
+    q_logits = np.array([0.2, 0.9, 0.4, 0.6, 0.5, -0.7], np.float32)
+    p = torch.softmax(torch.from_numpy(p_logits.astype(np.float64)) / tau, 0).numpy()
+    q = torch.softmax(torch.from_numpy(q_logits.astype(np.float64)) / tau, 0).numpy()
+    trials = 60000
+    rng = np.random.default_rng(7)
+    toks = rng.choice(V, size=trials, p=q).astype(np.int32)
+    dl = np.broadcast_to(q_logits, (trials, 1, V))
+    tl = np.broadcast_to(np.stack([p_logits, p_logits]), (trials, 2, V))
+    n, y, _ = oracle.spec_accept(dl, tl, toks[:, None], rng.random((trials, 1)), rng.random(trials), tau)
+    alpha = np.minimum(p, q).sum()
+    sigma = math.sqrt(alpha * (1 - alpha) / trials)
+    assert abs(n.mean() - alpha) < 4.5 * sigma
+    # the untempered rate differs by far more than the band: the test sees tau
+    p1, q1 = oracle.softmax_t(p_logits, 1.0), oracle.softmax_t(q_logits, 1.0)
+    assert abs(np.minimum(p1, q1).sum() - alpha) > 10 * sigma
+    first = np.where(n == 1, toks, y)
+    counts = np.bincount(first, minlength=V)
+    chi2 = ((counts - trials * p) ** 2 / (trials * p)).sum()
+    assert chi2 < 25.7                          # chi-square(5) at p = 1e-4

@@ -30,7 +30,11 @@ def _compare(a, label):
     rn, ry, rt = oracle.spec_accept(a.draft_logits, a.target_logits, a.draft_tokens,
                                     a.u_accept, a.u_sample, a.temperature)
     ok = (rt == 0) & (tie == 0)
-    assert ok.mean() >= 0.95, f"too many near ties: {ok.mean()}"
+    # near ties are excluded from bit-exactness and reported; the seeded
+    # inputs have none (a decision within 1e-9 relative of its boundary is
+    # rare), so any flagged row fails the test as well
+    print(f"[accept] {label}: {int((~ok).sum())} near-tie rows of {ok.size}", flush=True)
+    assert ok.all(), f"near ties flagged: oracle {int(rt.sum())}, GPU {int((tie != 0).sum())}"
     assert np.array_equal(n[ok], rn[ok]), (n, rn)
     assert np.array_equal(y[ok], ry[ok]), (y, ry)
     return n, rn

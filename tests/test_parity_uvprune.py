@@ -19,21 +19,6 @@ def _assert_score(got, ref, scale):
     assert not bad.any(), f"score: {bad.sum()} beyond tolerance, max err {err.max():.3g}"
 
 
-def _abs_cos_sum(hv, ht, m, n):
-    """sum_j |cos(V_i, X_j)| per (b, i): the scale of the criterion's rounding
-    error (a sum of n cosines, formed in fp32 as <V_i/|V_i|, sum_j X_j/|X_j|>,
-    can cancel to near zero; its error is bounded relative to this sum)."""
-    out = np.zeros(hv.shape[:2])
-    for b in range(hv.shape[0]):
-        v = hv[b, :m[b]]
-        x = ht[b, :n[b]]
-        vn = np.linalg.norm(v, axis=1)
-        xn = np.linalg.norm(x, axis=1)
-        c = (v @ x.T) / np.where(vn[:, None] * xn[None, :] > 0, vn[:, None] * xn[None, :], np.inf)
-        out[b, :m[b]] = np.abs(c).sum(axis=1)
-    return out
-
-
 def test_mass_criterion_stack():
     rng = np.random.default_rng(0)
     L, B, m_cap = 20, 3, 5000
@@ -66,10 +51,10 @@ def test_cossim_small_literal(dtype, L, Dh):
     ref = oracle.uvprune_score_cossim(hv64, ht64, m, n)
     cL = oracle.criterion_cossim(hv64[L], ht64[L], m, n)
     r0 = oracle.criterion_cossim(hv64[0], ht64[0], m, n)
-    aL = _abs_cos_sum(hv64[L], ht64[L], m, n)
-    a0 = _abs_cos_sum(hv64[0], ht64[0], m, n)
-    _assert_score(to_host_f64(s), ref, aL + a0)
-    _assert_score(to_host_f64(c0), r0, a0)
+    # the gate of the scope table: 1e-4 * max(|ref|, |c^L| + |c^0|), and the
+    # single-layer criterion within 1e-4 of itself
+    _assert_score(to_host_f64(s), ref, np.abs(cL) + np.abs(r0))
+    _assert_score(to_host_f64(c0), r0, np.abs(r0))
     assert np.all(to_host_f64(s)[1, 211:] == 0)
 
 
@@ -115,6 +100,6 @@ def test_cossim_streamed_over_layers(dtype, L):
     torch.cuda.synchronize()
     hv64, ht64 = f64(h.hv, dtype), f64(h.ht, dtype)
     ref = oracle.uvprune_score_cossim(hv64, ht64, m, n)
-    aL = _abs_cos_sum(hv64[L], ht64[L], m, n)
-    a0 = _abs_cos_sum(hv64[0], ht64[0], m, n)
-    _assert_score(to_host_f64(s), ref, aL + a0)
+    cL = oracle.criterion_cossim(hv64[L], ht64[L], m, n)
+    c0 = oracle.criterion_cossim(hv64[0], ht64[0], m, n)
+    _assert_score(to_host_f64(s), ref, np.abs(cL) + np.abs(c0))
