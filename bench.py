@@ -475,6 +475,20 @@ def verify_kernel_label(w, cus=256, xcds=8):
             f"{'same-XCD' if local else 'cross-XCD'}>")
 
 
+def teardown(torch, pv, *objs):
+    """Release graphs, tensors and the binding's default buffers and wait for
+    the device before the interpreter exits, so that nothing the GPU runtime
+    (or a profiler attached to it) tears down at process exit is still
+    referenced by live Python objects."""
+    for o in objs:
+        del o
+    import gc
+    gc.collect()
+    pv.release_workspaces()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -498,6 +512,8 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_only": args.copy_only, "bytes_read": COPY_BYTES,
                           "bytes_written": COPY_BYTES}))
+        del src, dst
+        teardown(torch, pv)
         return
 
     w = W.WORKLOADS[args.workload]
@@ -513,6 +529,8 @@ def main():
             st.verify(r % NL)
         torch.cuda.synchronize()
         print(json.dumps({"verify_only": args.verify_only, "status": int(st.status.item())}))
+        del st
+        teardown(torch, pv)
         return
 
     if args.gather_only:
@@ -522,6 +540,8 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"gather_only": args.gather_only, "bytes_per_gather": NL * gather_bytes(w),
                           "status": int(st.status.item())}))
+        del st
+        teardown(torch, pv)
         return
 
     # eager warm-up (also sizes the workspaces before any capture)
@@ -668,7 +688,8 @@ def main():
         "cpu_baseline": cpu,
         "device_status": status,
     }
-    print(json.dumps(rec))
+    print(json.dumps(rec), flush=True)
+    teardown(torch, pv)
 
 
 if __name__ == "__main__":

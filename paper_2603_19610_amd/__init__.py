@@ -187,29 +187,94 @@ class Workspace:
     """A zero-initialised device scratch buffer that grows on demand.
 
     The library leaves its synchronisation words consistent after every call,
-    so one buffer can serve successive calls on a stream (not concurrent ones).
+    so one buffer can serve successive calls on one stream (not concurrent
+    calls: give each stream its own workspace).  A buffer that is outgrown is
+    kept alive, not freed: a graph captured earlier, or a call still running,
+    may use it.
     """
 
     def __init__(self, device=None):
         self.device = torch.device("cuda", torch.cuda.current_device()) if device is None else device
         self.buf = torch.zeros(256, dtype=torch.uint8, device=self.device)
+        self._retired = []
 
     def get(self, nbytes: int) -> torch.Tensor:
         if nbytes > self.buf.numel():
+            self._retired.append(self.buf)
             self.buf = torch.zeros(max(nbytes, 2 * self.buf.numel()), dtype=torch.uint8,
                                    device=self.device)
         return self.buf
 
 
+# Default workspaces, one per (call kind, device, stream): calls on different
+# streams never share counters or data.
 _ws_cache = {}
+# Default status words, one per device (see synchronize()).
+_status_cache = {}
+
+
+def _no_capture(what: str):
+    if torch.cuda.is_current_stream_capturing():
+        raise PvlmError(4, "status", f"cannot {what} during graph capture: call "
+                        "default_status() once before capturing, or pass status=")
 
 
 def _default_ws(kind: str) -> Workspace:
-    key = (kind, torch.cuda.current_device())
+    key = (kind, torch.cuda.current_device(), torch.cuda.current_stream().cuda_stream)
     ws = _ws_cache.get(key)
     if ws is None:
+        # (under graph capture the buffer comes from the graph's pool and its
+        # zero fill replays with the graph, which leaves the counters consistent)
         ws = _ws_cache[key] = Workspace()
     return ws
+
+
+def _status(status):
+    """The caller's status word, or this device's default one."""
+    if status is not None:
+        return status
+    dev = torch.cuda.current_device()
+    st = _status_cache.get(dev)
+    if st is None:
+        _no_capture("allocate the default status word")
+        st = _status_cache[dev] = torch.zeros(1, dtype=torch.int32, device=torch.device("cuda", dev))
+    return st
+
+
+def default_status() -> torch.Tensor:
+    """The status word calls without an explicit ``status`` OR their device
+    flags (PVLM_DEV_*) into, on the current device."""
+    return _status(None)
+
+
+def synchronize(raise_on_status: bool = True) -> int:
+    """Wait for the current device, then read and clear its default status
+    word.  Raises PvlmError when a call flagged a device-side condition (an
+    out-of-range device size, a wait that gave up, a misplaced workgroup)
+    unless ``raise_on_status`` is False; returns the flags."""
+    torch.cuda.synchronize()
+    st = _status(None)
+    flags = int(st.item())
+    if flags:
+        st.zero_()
+        torch.cuda.synchronize()
+        if raise_on_status:
+            raise PvlmError(flags, "device status", _flag_text(flags))
+    return flags
+
+
+def _flag_text(flags: int) -> str:
+    names = [(PVLM_DEV_RANGE, "device size out of range"), (PVLM_DEV_TIMEOUT, "wait gave up"),
+             (PVLM_DEV_PLACEMENT, "workgroup placement")]
+    return ", ".join(n for bit, n in names if flags & bit)
+
+
+def release_workspaces():
+    """Drop the default workspaces and status words (every call using them must
+    have completed, and no live graph may reference them)."""
+    torch.cuda.synchronize()
+    _ws_cache.clear()
+    _status_cache.clear()
 
 
 # ------------------------------------------------------------------ calls --
@@ -252,7 +317,7 @@ def verify_attn(q, k_cache, v_cache, ctx_len, *, scale: Optional[float] = None,
     wsb = (ws or _default_ws("verify")).get(need)
     st = lib().pvlm_verify_attn(dt, B, T, Hq, Hkv, D, n_cap, max_ctx, float(scale), _ptr(q),
                                 _ptr(k_cache), _ptr(v_cache), _ptr(ctx_len), _ptr(out), _ptr(mass),
-                                _ptr(lse), _ptr(wsb), wsb.numel(), _ptr(status), _stream())
+                                _ptr(lse), _ptr(wsb), wsb.numel(), _ptr(_status(status)), _stream())
     _check(st, "pvlm_verify_attn")
     return out, mass, lse
 
@@ -268,7 +333,7 @@ def uvprune_score_mass(crit_stack, m, *, score=None, status=None):
     _need(score, "score", torch.float32, dev)
     st = lib().pvlm_uvprune_score(PVLM_CRIT_MASS, B, Lp1 - 1, m_cap, _ptr(m), _ptr(crit_stack),
                                   PVLM_F32, 0, 0, None, None, None, _ptr(score), None, 0,
-                                  _ptr(status), _stream())
+                                  _ptr(_status(status)), _stream())
     _check(st, "pvlm_uvprune_score")
     return score
 
@@ -291,7 +356,7 @@ def uvprune_score_cossim(hs_vis, hs_txt, m, n_txt, *, score=None, ws=None, statu
     wsb = (ws or _default_ws("uvprune")).get(need)
     st = lib().pvlm_uvprune_score(PVLM_CRIT_COSSIM, B, Lp1 - 1, m_cap, _ptr(m), None,
                                   _dt(hs_vis), Dh, n_cap, _ptr(n_txt), _ptr(hs_vis), _ptr(hs_txt),
-                                  _ptr(score), _ptr(wsb), wsb.numel(), _ptr(status), _stream())
+                                  _ptr(score), _ptr(wsb), wsb.numel(), _ptr(_status(status)), _stream())
     _check(st, "pvlm_uvprune_score")
     return score
 
@@ -312,7 +377,7 @@ def uvprune_criterion_cossim(hv, ht, m, n_txt, *, out=None, ws=None, status=None
     wsb = (ws or _default_ws("uvprune")).get(need)
     st = lib().pvlm_uvprune_criterion_cossim(B, m_cap, _ptr(m), _dt(hv), Dh, n_cap, _ptr(n_txt),
                                              _ptr(hv), _ptr(ht), _ptr(out), _ptr(wsb), wsb.numel(),
-                                             _ptr(status), _stream())
+                                             _ptr(_status(status)), _stream())
     _check(st, "pvlm_uvprune_criterion_cossim")
     return out
 
@@ -328,9 +393,10 @@ def topk_select(score, m, k, k_cap: int, *, idx=None, ws=None, status=None):
         idx = torch.empty((B, k_cap), dtype=torch.int32, device=dev)
     _need(idx, "idx", torch.int32, dev)
     need = int(lib().pvlm_topk_workspace_size(B, m_cap))
-    wsb = (ws or _default_ws("topk")).get(need)
+    wsb = (ws or _default_ws("topk")).get(need) if need else None
     st = lib().pvlm_topk_select(B, m_cap, _ptr(m), _ptr(k), int(k_cap), _ptr(score), _ptr(idx),
-                                _ptr(wsb), wsb.numel(), _ptr(status), _stream())
+                                _ptr(wsb), 0 if wsb is None else wsb.numel(), _ptr(_status(status)),
+                                _stream())
     _check(st, "pvlm_topk_select")
     return idx
 
@@ -365,8 +431,8 @@ def gather_kv(k_cache, v_cache, idx, k, tail_begin, tail_len, dst_cap: int, *, k
         raise ValueError("destination shape mismatch")
     st = lib().pvlm_gather_kv(_dt(k_cache), n_layers, B, Hkv, D, n_cap, _ptr(k_cache),
                               _ptr(v_cache), _ptr(idx), _ptr(k), idx.shape[1], _ptr(tail_begin),
-                              _ptr(tail_len), dst_cap, _ptr(k_dst), _ptr(v_dst), _ptr(status),
-                              _stream())
+                              _ptr(tail_len), dst_cap, _ptr(k_dst), _ptr(v_dst),
+                              _ptr(_status(status)), _stream())
     _check(st, "pvlm_gather_kv")
     return k_dst, v_dst
 
@@ -395,13 +461,14 @@ def spec_accept(draft_logits, target_logits, draft_tokens, u_accept, u_sample,
     st = lib().pvlm_spec_accept(B, gamma, V, float(temperature), _ptr(draft_logits),
                                 _ptr(target_logits), _ptr(draft_tokens), _ptr(u_accept),
                                 _ptr(u_sample), _ptr(n_accepted), _ptr(next_token), _ptr(near_tie),
-                                _ptr(wsb), wsb.numel(), _ptr(status), _stream())
+                                _ptr(wsb), wsb.numel(), _ptr(_status(status)), _stream())
     _check(st, "pvlm_spec_accept")
     return n_accepted, next_token, near_tie
 
 
 __all__ = [
-    "LIB_PATH", "EXPORTS", "PvlmError", "Workspace", "lib", "verify_attn",
+    "LIB_PATH", "EXPORTS", "PvlmError", "Workspace", "lib", "synchronize", "default_status",
+    "release_workspaces", "verify_attn",
     "verify_attn_workspace_size", "uvprune_score_mass", "uvprune_score_cossim",
     "uvprune_criterion_cossim", "topk_select", "gather_kv", "spec_accept",
     "PVLM_F32", "PVLM_BF16", "PVLM_CRIT_MASS", "PVLM_CRIT_COSSIM", "PVLM_DEV_RANGE",
@@ -530,6 +597,6 @@ def rope_append(q, k_new, v_new, pos, ctx_len, k_cache, v_cache, *, base: float,
     sec = None if sections is None else (_c.c_int32 * 3)(*[int(x) for x in sections])
     st = lib().pvlm_rope_append(_dt(q), B, T, Hq, Hkv, D, n_cap, float(base), sec, _ptr(pos),
                                 _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(ctx_len), _ptr(q_out),
-                                _ptr(k_cache), _ptr(v_cache), _ptr(status), _stream())
+                                _ptr(k_cache), _ptr(v_cache), _ptr(_status(status)), _stream())
     _check(st, "pvlm_rope_append")
     return q_out

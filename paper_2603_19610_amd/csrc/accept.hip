@@ -712,7 +712,10 @@ extern "C" pvlm_status pvlm_spec_accept(int B, int gamma, int V, float temperatu
                                : reinterpret_cast<const void*>(accept_kernel<true, kDrawPerMax>))
           : (dp == kDrawPerMin ? reinterpret_cast<const void*>(accept_kernel<false, kDrawPerMin>)
                                : reinterpret_cast<const void*>(accept_kernel<false, kDrawPerMax>));
-  PVLM_HIP(launch_coresident(kern,
-                             dim3(grid), dim3(kAccThreads), args, 0, stream));
+  {
+    const pvlm_status cs = check_coresident(kern, grid, kAccThreads, 0);
+    if (cs != PVLM_OK) return cs;
+  }
+  PVLM_HIP(launch_coresident(kern, dim3(grid), dim3(kAccThreads), args, 0, stream));
   return PVLM_OK;
 }

@@ -52,9 +52,17 @@ constexpr size_t kSyncLine = 128;
 // Raise a kernel's dynamic-LDS limit to `bytes` (done once per kernel and size).
 hipError_t allow_dynamic_lds(const void* kernel, int bytes);
 
+// PVLM_OK when `grid` workgroups of `kernel` (with `block` threads and `lds`
+// dynamic LDS bytes) fit on the current device at once: the occupancy the
+// runtime reports per compute unit times the compute units.  Every launch
+// whose workgroups wait on each other checks this before launching.
+pvlm_status check_coresident(const void* kernel, int grid, int block, int lds);
+
 // Launch a kernel whose workgroups wait on each other: cooperatively (the
 // runtime guarantees co-residency), or as an ordinary launch while the stream
-// is being captured into a graph.  Grids are at most one workgroup per CU.
+// is being captured into a graph (then co-residency rests on check_coresident
+// and on the device not being shared, see pvlm.h).  Grids are at most one
+// workgroup per CU.
 hipError_t launch_coresident(const void* kernel, dim3 grid, dim3 block, void** args, int lds,
                              hipStream_t stream);
 

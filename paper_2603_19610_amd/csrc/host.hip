@@ -1,6 +1,8 @@
 // Host-side helpers of the pvlm library: status strings, HIP error capture and
 // the per-device compute-unit count used to size launches.
+#include <map>
 #include <mutex>
+#include <tuple>
 #include <set>
 #include <string>
 #include <utility>
@@ -17,6 +19,8 @@ int g_cus[kMaxDevices] = {0};
 int g_xcds[kMaxDevices] = {0};
 std::mutex g_lds_mu;
 std::set<std::pair<const void*, int>> g_lds_done;
+std::mutex g_occ_mu;
+std::map<std::tuple<int, const void*, int, int>, int> g_occ;  // (device, kernel, block, lds) -> per CU
 }  // namespace
 
 hipError_t allow_dynamic_lds(const void* kernel, int bytes) {
@@ -25,6 +29,29 @@ hipError_t allow_dynamic_lds(const void* kernel, int bytes) {
   hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   if (e == hipSuccess) g_lds_done.insert({kernel, bytes});
   return e;
+}
+
+pvlm_status check_coresident(const void* kernel, int grid, int block, int lds) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_check(e);
+  const std::tuple<int, const void*, int, int> key{dev, kernel, block, lds};
+  int per_cu = 0;
+  {
+    std::lock_guard<std::mutex> lock(g_occ_mu);
+    auto it = g_occ.find(key);
+    if (it != g_occ.end()) per_cu = it->second;
+  }
+  if (per_cu == 0) {
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, block, (size_t)lds);
+    if (e != hipSuccess) return hip_check(e);
+    std::lock_guard<std::mutex> lock(g_occ_mu);
+    g_occ[key] = per_cu;
+  }
+  DeviceInfo di;
+  const pvlm_status st = device_info(&di);
+  if (st != PVLM_OK) return st;
+  return (int64_t)per_cu * di.cus >= grid ? PVLM_OK : PVLM_ERR_UNSUPPORTED;
 }
 
 hipError_t launch_coresident(const void* kernel, dim3 grid, dim3 block, void** args, int lds,

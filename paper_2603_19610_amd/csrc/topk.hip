@@ -598,6 +598,10 @@ extern "C" pvlm_status pvlm_topk_select(int B, int64_t m_cap, const int32_t* m, 
   const void* kern = p.slice <= kTopkThreads * kPerThread
                          ? reinterpret_cast<const void*>(topk_kernel<true>)
                          : reinterpret_cast<const void*>(topk_kernel<false>);
+  {
+    const pvlm_status cs = check_coresident(kern, B * p.NW, kTopkThreads, 0);
+    if (cs != PVLM_OK) return cs;
+  }
   PVLM_HIP(launch_coresident(kern, dim3(B * p.NW), dim3(kTopkThreads), args, 0, stream));
   return PVLM_OK;
 }

@@ -1596,6 +1596,14 @@ extern "C" pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int
   a.grid = p.grid;
   a.sl2 = scale * kLog2e;
   if (!pick_kernel(dt, D, p.RT, p.resident, false)) return PVLM_ERR_UNSUPPORTED;
+  // every launch's grid fits the device at once (the first launch's grid is
+  // the largest; both exchange variants use the same resources)
+  for (int local = 0; local < 2; ++local) {
+    const void* k = reinterpret_cast<const void*>(pick_kernel(dt, D, p.RT, p.resident, local != 0));
+    PVLM_HIP(allow_dynamic_lds(k, p.lds_dyn));
+    const pvlm_status cs = check_coresident(k, p.grid, kThreads, p.lds_dyn);
+    if (cs != PVLM_OK) return cs;
+  }
   for (int g0 = 0; g0 < p.groups; g0 += p.per_launch) {
     a.grp_base = g0;
     a.ngrp = p.groups - g0 < p.per_launch ? p.groups - g0 : p.per_launch;
