@@ -129,6 +129,33 @@ pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D
                              void* ws, size_t ws_bytes, int32_t* status, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * pvlm_verify_attn_noalloc -- pvlm_verify_attn without a workspace argument,
+ * for callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, and harnesses that forbid allocation.  It
+ * allocates nothing (no hipMalloc / hipFree, no allocating library call):
+ * its scratch is a fixed device array inside the library, one per GPU,
+ * held until the process ends.  The caller still provides q, the caches,
+ * ctx_len, out and the optional mass / lse / status, with the meaning,
+ * layout and error behaviour of pvlm_verify_attn.
+ *   - Limit: the call needs pvlm_verify_attn_workspace_size() bytes of that
+ *     scratch; a request beyond pvlm_verify_attn_noalloc_max_bytes()
+ *     (32 MiB, which covers batch 4 at 33K tokens and 131K-token caches at
+ *     Hkv = 8) returns PVLM_ERR_WORKSPACE and launches nothing.
+ *   - Every call on one GPU shares that GPU's scratch: calls that overlap
+ *     on one GPU (on different streams, or a replayed graph beside another
+ *     call) race and give invalid results; serialise them.
+ *   - The first call on a GPU also clears the scratch's synchronisation
+ *     words with a small fill kernel on `stream` (never a memset, so a
+ *     capturing caller records no memset node).
+ * ---------------------------------------------------------------------- */
+size_t pvlm_verify_attn_noalloc_max_bytes(void);
+pvlm_status pvlm_verify_attn_noalloc(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D,
+                                     int64_t n_cap, int64_t max_ctx, float scale, const void* q,
+                                     const void* k_cache, const void* v_cache,
+                                     const int32_t* ctx_len, void* out, float* mass, float* lse,
+                                     int32_t* status, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * pvlm_rope_append -- rotary embedding of the verify rows and their append to
  * the cache.  The target verifies the T = gamma + 1 speculated positions in
  * one forward (Sec. 2.2; Sec. 4.2, Parallel Decoding); pvlm_verify_attn reads

@@ -27,6 +27,7 @@ PVLM_DEV_RANGE, PVLM_DEV_TIMEOUT, PVLM_DEV_PLACEMENT = 1, 2, 4
 EXPORTS = (
     "pvlm_status_string", "pvlm_last_hip_error", "pvlm_version",
     "pvlm_verify_attn_workspace_size", "pvlm_verify_attn",
+    "pvlm_verify_attn_noalloc", "pvlm_verify_attn_noalloc_max_bytes",
     "pvlm_uvprune_workspace_size", "pvlm_uvprune_score", "pvlm_uvprune_criterion_cossim",
     "pvlm_topk_workspace_size", "pvlm_topk_select",
     "pvlm_gather_kv",
@@ -99,6 +100,9 @@ _SIGS = {
     "pvlm_verify_attn_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I64, _I64]),
     "pvlm_verify_attn": (_I, [_I, _I, _I, _I, _I, _I, _I64, _I64, _F, _P, _P, _P, _P, _P, _P, _P,
                               _P, _SZ, _P, _P]),
+    "pvlm_verify_attn_noalloc": (_I, [_I, _I, _I, _I, _I, _I, _I64, _I64, _F, _P, _P, _P, _P, _P,
+                                      _P, _P, _P, _P]),
+    "pvlm_verify_attn_noalloc_max_bytes": (_SZ, []),
     "pvlm_uvprune_workspace_size": (_SZ, [_I, _I, _I, _I64]),
     "pvlm_uvprune_score": (_I, [_I, _I, _I, _I64, _P, _P, _I, _I, _I64, _P, _P, _P, _P, _P, _SZ,
                                 _P, _P]),
@@ -319,6 +323,35 @@ def verify_attn(q, k_cache, v_cache, ctx_len, *, scale: Optional[float] = None,
                                 _ptr(k_cache), _ptr(v_cache), _ptr(ctx_len), _ptr(out), _ptr(mass),
                                 _ptr(lse), _ptr(wsb), wsb.numel(), _ptr(_status(status)), _stream())
     _check(st, "pvlm_verify_attn")
+    return out, mass, lse
+
+
+def verify_attn_noalloc(q, k_cache, v_cache, ctx_len, *, out, mass=None, lse=None,
+                        scale: Optional[float] = None, max_ctx: Optional[int] = None, status=None):
+    """pvlm_verify_attn_noalloc: verify attention + mass with the library's
+    fixed device scratch (no workspace, nothing allocated: ``out`` and the
+    optional ``mass`` / ``lse`` are the caller's).  Calls that overlap on one
+    GPU race on the shared scratch."""
+    _need(q, "q")
+    dev = q.device
+    _need(k_cache, "k_cache", q.dtype, dev)
+    _need(v_cache, "v_cache", q.dtype, dev)
+    _need(ctx_len, "ctx_len", torch.int32, dev)
+    _need(out, "out", q.dtype, dev)
+    B, T, Hq, D = q.shape
+    Bk, Hkv, n_cap, Dk = k_cache.shape
+    if Bk != B or Dk != D or tuple(v_cache.shape) != tuple(k_cache.shape) or ctx_len.numel() != B:
+        raise ValueError("inconsistent verify_attn shapes")
+    if mass is not None:
+        _need(mass, "mass", torch.float32, dev)
+    if lse is not None:
+        _need(lse, "lse", torch.float32, dev)
+    st = lib().pvlm_verify_attn_noalloc(_dt(q), B, T, Hq, Hkv, D, n_cap,
+                                        n_cap - T if max_ctx is None else max_ctx,
+                                        float(D ** -0.5 if scale is None else scale), _ptr(q),
+                                        _ptr(k_cache), _ptr(v_cache), _ptr(ctx_len), _ptr(out),
+                                        _ptr(mass), _ptr(lse), _ptr(status), _stream())
+    _check(st, "pvlm_verify_attn_noalloc")
     return out, mass, lse
 
 

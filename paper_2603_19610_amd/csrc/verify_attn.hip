@@ -40,6 +40,8 @@
 //    on one XCD (one L2; each address is written once per launch), else
 //    device-coherent; across groups (the mass sum) always device-coherent.
 //  * fp32 inputs take a VALU path with the two-wait structure.
+#include <mutex>
+
 #include "common.h"
 
 namespace pvlm {
@@ -1439,6 +1441,18 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
   verify_epilogue<ROWS, D, false>(a, u, s_lse, false, &s_flag, base);
 }
 
+// -------------------------------------------------- allocation-free entry --
+// The scratch buffer of pvlm_verify_attn_noalloc: a file-scope device array
+// that every call on a device shares (each device holds its own copy for the
+// life of the process).  Host code never uses this name as an address: the
+// device address comes from hipGetSymbolAddress, once per device.
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+__global__ void __launch_bounds__(256) zero_words_kernel(uint32_t* p, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) p[i] = 0u;
+}
+
 // ------------------------------------------------------------------ host --
 struct VPlan {
   int G, R, RTT, RG, RT;
@@ -1620,4 +1634,49 @@ extern "C" pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int
                                args, p.lds_dyn, stream));
   }
   return PVLM_OK;
+}
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch[64] = {nullptr};  // device address of `scratch` per device
+}  // namespace
+
+extern "C" size_t pvlm_verify_attn_noalloc_max_bytes(void) { return kScratchBytes; }
+
+extern "C" pvlm_status pvlm_verify_attn_noalloc(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D,
+                                                int64_t n_cap, int64_t max_ctx, float scale,
+                                                const void* q, const void* k_cache,
+                                                const void* v_cache, const int32_t* ctx_len,
+                                                void* out, float* mass, float* lse, int32_t* status,
+                                                hipStream_t stream) {
+  if (!q || !k_cache || !v_cache || !ctx_len || !out) return PVLM_ERR_NULL;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return PVLM_ERR_SHAPE;
+  VPlan p;
+  pvlm_status st = plan_verify(dt, B, T, Hq, Hkv, D, n_cap, max_ctx, &p);
+  if (st != PVLM_OK) return st;
+  if (p.bytes > kScratchBytes) return PVLM_ERR_WORKSPACE;  // beyond the fixed scratch
+  int dev = 0;
+  PVLM_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return PVLM_ERR_UNSUPPORTED;
+  void* ptr = nullptr;
+  bool first = false;
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+      void* a = nullptr;
+      PVLM_HIP(hipGetSymbolAddress(&a, HIP_SYMBOL(scratch)));
+      if (!a) return PVLM_ERR_HIP;
+      g_scratch[dev] = a;
+      first = true;
+    }
+    ptr = g_scratch[dev];
+  }
+  if (first) {  // the synchronisation region starts at zero (a fill kernel, so
+                // a capturing caller records no memset node)
+    hipLaunchKernelGGL(zero_words_kernel, dim3(256), dim3(256), 0, stream, static_cast<uint32_t*>(ptr),
+                       kSyncRegion / sizeof(uint32_t));
+    PVLM_LAUNCHED();
+  }
+  return pvlm_verify_attn(dt, B, T, Hq, Hkv, D, n_cap, max_ctx, scale, q, k_cache, v_cache, ctx_len,
+                          out, mass, lse, ptr, kScratchBytes, status, stream);
 }
