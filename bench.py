@@ -136,8 +136,53 @@ def kernel_code_digest():
 
 
 # ------------------------------------------------------------ CPU baseline --
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def oracle_single_layer_step(w, W, oracle, thread_limits):
+    """Seconds the float64 oracle takes for one single-layer step of workload
+    w on the host, once per entry of thread_limits (same inputs): verify of
+    layer 1, the UV-Prune score over the masses of layers 0 and 1 (layer 0's
+    mass exists before the step, as in the GPU step), top-k, the gather and
+    accept."""
+    import time as _t
+    from threadpoolctl import threadpool_limits
+    l0, l1 = W.make_verify_inputs(w, layer=0), W.make_verify_inputs(w, layer=1)
+    f = lambda i: (W.storage_to_f64(i.q, i.dtype), W.storage_to_f64(i.k, i.dtype),
+                   W.storage_to_f64(i.v, i.dtype))
+    q0, k0, v0 = f(l0)
+    mass0 = oracle.verify_attn(q0, k0, v0, l0.ctx_len, l0.scale)[2]
+    q1, k1, v1 = f(l1)
+    m = l1.m.astype(np.int32)
+    K = w.keep_count(m).astype(np.int32)
+    acc = W.make_accept_inputs(w)
+    out = []
+    for lim in thread_limits:
+        with threadpool_limits(limits=lim):
+            t0 = _t.perf_counter()
+            mass1 = oracle.verify_attn(q1, k1, v1, l1.ctx_len, l1.scale)[2]
+            mc = int(m.max())
+            score = oracle.uvprune_score_mass(np.stack([mass0[:, :mc], mass1[:, :mc]]), m)
+            idx = oracle.topk_select(score, m, K, max(1, int(K.max())))
+            oracle.gather_kv(l1.k, l1.v, idx, K, m, np.full(w.batch, w.n_text),
+                             max(1, int(K.max())) + w.n_text)
+            oracle.spec_accept(acc.draft_logits, acc.target_logits, acc.draft_tokens, acc.u_accept,
+                               acc.u_sample, acc.temperature)
+            out.append(_t.perf_counter() - t0)
+    return out
+
+
 def cpu_baseline(w, layers_host, crit_layers, per_layer_ok):
-    """Time the float64 oracle on host copies of the same inputs."""
+    """Time the float64 oracle on host copies of the same inputs: a sample of
+    the stacked step with every host core, and the single-layer steps of the
+    tiny, 7B and 72B workloads with every core and with one thread."""
     import oracle
     import workloads as W
     from threadpoolctl import threadpool_info, threadpool_limits
@@ -171,18 +216,15 @@ def cpu_baseline(w, layers_host, crit_layers, per_layer_ok):
         oracle.spec_accept(acc.draft_logits, acc.target_logits, acc.draft_tokens, acc.u_accept,
                            acc.u_sample, acc.temperature)
         t_acc = time.perf_counter() - t0
+    singles = {}
+    for name in ("tiny", "llava7b", "llava72b"):
+        t_all, t_one = oracle_single_layer_step(W.WORKLOADS[name], W, oracle, (cores, 1))
+        singles[name] = {"all_cores_ms": round(t_all * 1e3, 2), "one_thread_ms": round(t_one * 1e3, 2)}
     per_layer = np.mean(t_verify) + t_gather
     once = t_uv + t_topk + t_acc
     L = per_layer_ok
     us_per_layer = (per_layer + once / L) * 1e6
-    cpu_model = ""
-    try:
-        for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                cpu_model = line.split(":", 1)[1].strip()
-                break
-    except OSError:
-        pass
+    cpu = cpu_model()
     return {
         "value": round(us_per_layer, 1), "unit": "us/layer", "cores": int(threads),
         "kind": "oracle",
@@ -190,8 +232,14 @@ def cpu_baseline(w, layers_host, crit_layers, per_layer_ok):
                    f"(mean {np.mean(t_verify):.2f} s/layer), gather of one layer "
                    f"({t_gather:.3f} s), UV-Prune over {crit_layers + 1} masses ({t_uv:.3f} s), "
                    f"top-k ({t_topk:.3f} s) and accept ({t_acc:.3f} s); per layer = verify + "
-                   f"gather + (UV-Prune + top-k + accept) / {L}; host cores available {cores}; "
-                   f"cpu {cpu_model}"),
+                   f"gather + (UV-Prune + top-k + accept) / {L}; BLAS threads {threads} of "
+                   f"{cores} host cores in the process affinity; cpu {cpu}"),
+        "cpu_model": cpu,
+        "affinity_cores": cores,
+        "single_layer_steps": singles,
+        "single_layer_steps_note": ("the oracle's whole single-layer step (verify of one layer, "
+                                    "UV-Prune, top-k, gather, accept) per workload, with every "
+                                    "core and with one BLAS thread"),
     }
 
 
@@ -449,6 +497,59 @@ def rope_record(torch, pv, W, dev):
     return rec
 
 
+def paged_record(torch, pv, W, dev, reps=20):
+    """Verify attention on the batch-4 ragged layer (lengths in [16384, 33280],
+    Hq 40, Hkv 8, D 128, bf16) from a padded cache and from paged pools of 32-
+    and 256-row pages scattered over the pool; the same data and launch plan
+    (max_ctx), graph-timed over `reps` launches each."""
+    w = W.WORKLOADS["qwen32b"]
+    q, k, v = W.make_verify_layer_torch(w, 1, 3.0, dev)
+    lens = w.lengths()
+    ctx = torch.from_numpy(lens.astype(np.int32)).to(dev)
+    max_ctx = int(lens.max())
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    out = torch.empty_like(q)
+    mass = torch.empty((w.batch, w.n_cap()), dtype=torch.float32, device=dev)
+    lse = torch.empty((w.batch, w.hq, w.T), dtype=torch.float32, device=dev)
+    ws = pv.Workspace(dev)
+
+    def padded():
+        pv.verify_attn(q, k, v, ctx, max_ctx=max_ctx, out=out, mass=mass, lse=lse, ws=ws,
+                       status=status)
+
+    g = capture(torch, lambda: [padded() for _ in range(reps)])
+    us_pad = time_replays(torch, g.replay, 5) * 1e3 / reps
+    del g
+    ref = (out.clone(), mass.clone())
+    vb = verify_bytes(w)
+    rec = {"workload": "qwen32b verify, batch 4 ragged 16384..33280, Hq 40, Hkv 8, D 128, bf16",
+           "bytes": vb, "padded_us": round(us_pad, 2),
+           "padded_frac_of_peak": round(vb / (us_pad * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+           "paged": {}}
+    for P in (32, 256):
+        table, n_pages = W.page_table(lens + w.T, P, seed=P)
+        kp, vp = W.to_pages(k, table, n_pages, P), W.to_pages(v, table, n_pages, P)
+        tab = torch.from_numpy(table).to(dev)
+        pmass = torch.empty((w.batch, table.shape[1] * P), dtype=torch.float32, device=dev)
+
+        def paged():
+            pv.verify_attn_paged(q, kp, vp, tab, ctx, max_ctx=max_ctx, out=out, mass=pmass,
+                                 lse=lse, ws=ws, status=status)
+
+        g = capture(torch, lambda: [paged() for _ in range(reps)])
+        us = time_replays(torch, g.replay, 5) * 1e3 / reps
+        n = ref[1].shape[1]
+        same = bool(torch.equal(out, ref[0]) and torch.equal(pmass[:, :n], ref[1]))
+        rec["paged"][str(P)] = {"us": round(us, 2), "pool_pages": n_pages,
+                                "frac_of_peak": round(vb / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                                "bit_equal_to_padded": same}
+        del g, kp, vp
+    rec["device_status"] = int(status.item())
+    del q, k, v, ws
+    torch.cuda.empty_cache()
+    return rec
+
+
 def tiles(w):
     """16-row MFMA tiles per workgroup for the packed query rows of a KV head."""
     rtt = -(-w.group * w.T // 16)
@@ -560,17 +661,17 @@ def main():
         run()
     torch.cuda.synchronize()
     st.status.zero_()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     h0 = time.perf_counter()
-    e0.record()
-    for _ in range(args.steps):
+    evs[0].record()
+    for i in range(args.steps):
         run()
-    e1.record()
+        evs[i + 1].record()
     torch.cuda.synchronize()
     host_s = time.perf_counter() - h0
-    ms_step = e0.elapsed_time(e1) / args.steps
+    ms_step = evs[0].elapsed_time(evs[-1]) / args.steps
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
     status = int(st.status.item())
     if status:
         log(f"device status {status} during the timed steps")
@@ -632,7 +733,7 @@ def main():
     torch.cuda.empty_cache()
 
     others = None
-    cossim = rope = None
+    cossim = rope = paged = None
     if not args.no_extra and graph_used:
         others = {}
         for name in OTHER_CONFIGS:
@@ -644,6 +745,8 @@ def main():
         log(f"cossim: {cossim['us']} us")
         rope = rope_record(torch, pv, W, dev)
         log(f"rope_append: {rope['us']} us")
+        paged = paged_record(torch, pv, W, dev)
+        log(f"paged verify: padded {paged['padded_us']} us, paged {paged['paged']}")
 
     rec = {
         "metric": METRIC,
@@ -653,6 +756,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "ms_per_step_p10_p50_p90": [round(float(x), 4) for x in np.percentile(per_step, [10, 50, 90])],
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -685,6 +789,7 @@ def main():
         "other_configs": others,
         "cossim": cossim,
         "rope_append": rope,
+        "paged_kv": paged,
         "cpu_baseline": cpu,
         "device_status": status,
     }

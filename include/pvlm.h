@@ -129,6 +129,40 @@ pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D
                              void* ws, size_t ws_bytes, int32_t* status, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * pvlm_verify_attn_paged -- pvlm_verify_attn over a paged KV cache: the same
+ * operation (Sec. 2.2 verification forward; attention mass of Sec. 3,
+ * Challenge 2), with every cache row read through a page table instead of a
+ * padded [B][Hkv][n_cap][D] slab, so ragged sequences share one pool without
+ * padding.  Logical row i of sequence b lives in pool page
+ * page_table[b][i / page_size] at row i % page_size of that page.
+ *   dt          PVLM_BF16 only (PVLM_ERR_UNSUPPORTED otherwise).
+ *   page_size   rows per page: a power of two in [32, 2^20] (PVLM_ERR_SHAPE).
+ *   max_pages   page-table columns; the logical capacity is
+ *               n_cap = max_pages * page_size (<= 2^30).
+ *   n_pages     pool pages, 1 .. 2^31 - 1.
+ *   k_pool,
+ *   v_pool      [n_pages][Hkv][page_size][D] bf16 (one page holds page_size
+ *               consecutive rows of every KV head).
+ *   page_table  [B][max_pages] int32 device.  Only the entries of pages that
+ *               hold rows < ctx_len[b] + T are read; an entry outside
+ *               [0, n_pages) among them is clamped into the pool for the
+ *               read (so no access leaves it) and flagged PVLM_DEV_RANGE.
+ *   mass        [B][n_cap] fp32 or NULL, indexed by logical row.
+ *   ws          >= pvlm_verify_attn_workspace_size(dt, B, T, Hq, Hkv, D,
+ *               n_cap, max_ctx) bytes.
+ * Every other argument, limit and error is that of pvlm_verify_attn.  With
+ * equal max_ctx the call runs the padded call's launch plan and arithmetic,
+ * so its results equal the padded call's bit for bit.
+ * ---------------------------------------------------------------------- */
+pvlm_status pvlm_verify_attn_paged(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D,
+                                   int page_size, int max_pages, int64_t n_pages,
+                                   int64_t max_ctx, float scale, const void* q,
+                                   const void* k_pool, const void* v_pool,
+                                   const int32_t* page_table, const int32_t* ctx_len, void* out,
+                                   float* mass, float* lse, void* ws, size_t ws_bytes,
+                                   int32_t* status, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * pvlm_verify_attn_noalloc -- pvlm_verify_attn without a workspace argument,
  * for callers that cannot allocate device memory: code under HIP graph
  * capture, tight serving loops, and harnesses that forbid allocation.  It
@@ -182,8 +216,8 @@ pvlm_status pvlm_verify_attn_noalloc(pvlm_dtype dt, int B, int T, int Hq, int Hk
  * Errors: PVLM_ERR_NULL for a NULL pointer (sections excepted);
  * PVLM_ERR_SHAPE for a size < 1, Hq not a multiple of Hkv, D odd or > 1024,
  * n_cap < T or > 2^30, base not finite and > 1, sections that do not sum
- * to D/2, Hq + 2*Hkv > 65536, or more than 2^38 rotation pairs
- * (B*T*(Hq+2*Hkv)*D/2);
+ * to D/2, Hq + 2*Hkv > 65536, or more than 2^32 - 256 rotation pairs
+ * (B*T*(Hq+2*Hkv)*D/2: one launch, one work-item per pair);
  * PVLM_ERR_UNSUPPORTED for another dtype.
  * ---------------------------------------------------------------------- */
 pvlm_status pvlm_rope_append(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int64_t n_cap,
@@ -191,6 +225,24 @@ pvlm_status pvlm_rope_append(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D
                              const void* q_in, const void* k_in, const void* v_in,
                              const int32_t* ctx_len, void* q_out, void* k_cache, void* v_cache,
                              int32_t* status, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * pvlm_rope_append_paged -- pvlm_rope_append into a paged cache: k_pool /
+ * v_pool [n_pages][Hkv][page_size][D] and page_table [B][max_pages] as for
+ * pvlm_verify_attn_paged (logical capacity n_cap = max_pages * page_size).
+ * The row of verify position t of sequence b goes to page
+ * page_table[b][(ctx_len[b] + t) / page_size], row (ctx_len[b] + t) %
+ * page_size; a row whose page entry lies outside [0, n_pages) is not written
+ * and is flagged PVLM_DEV_RANGE.  Other arguments, limits and errors are
+ * those of pvlm_rope_append; page_size and the page counts follow
+ * pvlm_verify_attn_paged (PVLM_ERR_SHAPE otherwise).
+ * ---------------------------------------------------------------------- */
+pvlm_status pvlm_rope_append_paged(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D,
+                                   int page_size, int max_pages, int64_t n_pages, double base,
+                                   const int32_t* sections, const int32_t* pos, const void* q_in,
+                                   const void* k_in, const void* v_in, const int32_t* page_table,
+                                   const int32_t* ctx_len, void* q_out, void* k_pool,
+                                   void* v_pool, int32_t* status, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * pvlm_uvprune_score -- UV-Prune score, Eq. (average_similarity):
@@ -269,6 +321,28 @@ pvlm_status pvlm_gather_kv(pvlm_dtype dt, int n_layers, int B, int Hkv, int D, i
                            const int32_t* k, int32_t k_cap, const int32_t* tail_begin,
                            const int32_t* tail_len, int64_t dst_cap, void* k_dst, void* v_dst,
                            int32_t* status, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * pvlm_gather_kv_paged -- pvlm_gather_kv from a paged cache into the compact
+ * (padded) draft cache of Sec. 4.2, Stage I.  Source row src of sequence b,
+ * layer l, KV head g is k_pool[l][page_table[b][src / page_size]][g]
+ * [src % page_size] (likewise V); one page table serves every layer.
+ *   k_pool, v_pool [n_layers][n_pages][Hkv][page_size][D];
+ *   page_table [B][max_pages] int32 device, n_cap = max_pages * page_size
+ *   bounds idx and tail_begin + tail_len as in pvlm_gather_kv;
+ *   k_dst, v_dst [n_layers][B][Hkv][dst_cap][D].
+ * A row whose page entry lies outside [0, n_pages) is skipped and flagged
+ * PVLM_DEV_RANGE.  Other arguments, limits and errors are those of
+ * pvlm_gather_kv; page_size and the page counts follow
+ * pvlm_verify_attn_paged (PVLM_ERR_SHAPE otherwise).
+ * ---------------------------------------------------------------------- */
+pvlm_status pvlm_gather_kv_paged(pvlm_dtype dt, int n_layers, int B, int Hkv, int D,
+                                 int page_size, int max_pages, int64_t n_pages,
+                                 const void* k_pool, const void* v_pool,
+                                 const int32_t* page_table, const int32_t* idx, const int32_t* k,
+                                 int32_t k_cap, const int32_t* tail_begin,
+                                 const int32_t* tail_len, int64_t dst_cap, void* k_dst,
+                                 void* v_dst, int32_t* status, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * pvlm_spec_accept -- speculative-sampling accept/reject (Sec. 2.2) with the

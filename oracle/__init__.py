@@ -29,6 +29,9 @@ explicit loops over the indices the paper sums over, following the paper:
 * ``pipeline``         -- the parallel decoding pipeline's scheduling: pre- and
                           post-verify modes and draft rollback (Suppl.
                           "Parallel Pipeline Details").
+* ``paged``            -- verify attention, rope append and the compact-cache
+                          gather over a paged cache, every row read or
+                          written through the page table.
 
 Parity status: every function here is pinned by the ``-m "not gpu"`` tests in
 ``tests/test_oracle_*.py`` against brute force, closed forms, library routines
@@ -39,7 +42,7 @@ from .uvprune import (cos_similarity, criterion_cossim, uvprune_score_cossim,
                       uvprune_score_mass)
 from .select import topk_keys, topk_select, gather_kv
 from .accept import spec_accept, softmax_t, NEAR_TIE_REL
-from . import pipeline, rope, window
+from . import paged, pipeline, rope, window
 
 __all__ = [
     "verify_attn", "verify_attn_rows", "cos_similarity", "criterion_cossim",

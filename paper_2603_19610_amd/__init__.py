@@ -26,13 +26,13 @@ PVLM_DEV_RANGE, PVLM_DEV_TIMEOUT, PVLM_DEV_PLACEMENT = 1, 2, 4
 
 EXPORTS = (
     "pvlm_status_string", "pvlm_last_hip_error", "pvlm_version",
-    "pvlm_verify_attn_workspace_size", "pvlm_verify_attn",
+    "pvlm_verify_attn_workspace_size", "pvlm_verify_attn", "pvlm_verify_attn_paged",
     "pvlm_verify_attn_noalloc", "pvlm_verify_attn_noalloc_max_bytes",
     "pvlm_uvprune_workspace_size", "pvlm_uvprune_score", "pvlm_uvprune_criterion_cossim",
     "pvlm_topk_workspace_size", "pvlm_topk_select",
-    "pvlm_gather_kv",
+    "pvlm_gather_kv", "pvlm_gather_kv_paged",
     "pvlm_spec_accept_workspace_size", "pvlm_spec_accept",
-    "pvlm_rope_append",
+    "pvlm_rope_append", "pvlm_rope_append_paged",
     "pvlm_speedup", "pvlm_window_size",
     "pvlm_pd_create", "pvlm_pd_destroy", "pvlm_pd_start", "pvlm_pd_plan", "pvlm_pd_finish",
     "pvlm_pd_output", "pvlm_pd_pending", "pvlm_pd_get_stats",
@@ -100,6 +100,8 @@ _SIGS = {
     "pvlm_verify_attn_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I64, _I64]),
     "pvlm_verify_attn": (_I, [_I, _I, _I, _I, _I, _I, _I64, _I64, _F, _P, _P, _P, _P, _P, _P, _P,
                               _P, _SZ, _P, _P]),
+    "pvlm_verify_attn_paged": (_I, [_I, _I, _I, _I, _I, _I, _I, _I, _I64, _I64, _F, _P, _P, _P,
+                                    _P, _P, _P, _P, _P, _P, _SZ, _P, _P]),
     "pvlm_verify_attn_noalloc": (_I, [_I, _I, _I, _I, _I, _I, _I64, _I64, _F, _P, _P, _P, _P, _P,
                                       _P, _P, _P, _P]),
     "pvlm_verify_attn_noalloc_max_bytes": (_SZ, []),
@@ -112,12 +114,16 @@ _SIGS = {
     "pvlm_topk_select": (_I, [_I, _I64, _P, _P, _I, _P, _P, _P, _SZ, _P, _P]),
     "pvlm_gather_kv": (_I, [_I, _I, _I, _I, _I, _I64, _P, _P, _P, _P, _I, _P, _P, _I64, _P, _P,
                             _P, _P]),
+    "pvlm_gather_kv_paged": (_I, [_I, _I, _I, _I, _I, _I, _I, _I64, _P, _P, _P, _P, _P, _I, _P,
+                                  _P, _I64, _P, _P, _P, _P]),
     "pvlm_spec_accept_workspace_size": (_SZ, [_I, _I, _I]),
     "pvlm_spec_accept": (_I, [_I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P]),
     "pvlm_speedup": (_I, [_D, _D, _I, _c.POINTER(SpeedupModel)]),
     "pvlm_window_size": (_I, [_D, _D, _I, _D, _I, _c.POINTER(_I), _c.POINTER(_D)]),
     "pvlm_rope_append": (_I, [_I, _I, _I, _I, _I, _I, _I64, _D, _P, _P, _P, _P, _P, _P, _P, _P,
                               _P, _P, _P]),
+    "pvlm_rope_append_paged": (_I, [_I, _I, _I, _I, _I, _I, _I, _I, _I64, _D, _P, _P, _P, _P, _P,
+                                    _P, _P, _P, _P, _P, _P, _P]),
     "pvlm_pd_create": (_I, [_I, _D, _I, _c.POINTER(_P)]),
     "pvlm_pd_destroy": (None, [_P]),
     "pvlm_pd_start": (_I, [_P, _P]),
@@ -326,6 +332,61 @@ def verify_attn(q, k_cache, v_cache, ctx_len, *, scale: Optional[float] = None,
     return out, mass, lse
 
 
+def _pool_shape(k_pool, v_pool, page_table, dev, dtype, stacked=False):
+    _need(k_pool, "k_pool", dtype, dev)
+    _need(v_pool, "v_pool", dtype, dev)
+    _need(page_table, "page_table", torch.int32, dev)
+    want = 5 if stacked else 4
+    if k_pool.dim() != want or tuple(v_pool.shape) != tuple(k_pool.shape):
+        raise ValueError("pools must be [n_pages][Hkv][page][D]" if not stacked else
+                         "pools must be [n_pages][Hkv][page][D] or [L][n_pages][Hkv][page][D]")
+    if page_table.dim() != 2:
+        raise ValueError("page_table must be [B][max_pages]")
+    return tuple(k_pool.shape)
+
+
+def verify_attn_paged(q, k_pool, v_pool, page_table, ctx_len, *, scale: Optional[float] = None,
+                      max_ctx: Optional[int] = None, out=None, mass=None, lse=None,
+                      want_mass: bool = True, want_lse: bool = True,
+                      ws: Optional[Workspace] = None, status=None):
+    """pvlm_verify_attn_paged: verify attention + mass over a paged cache.
+    q [B][T][Hq][D] bf16; pools [n_pages][Hkv][page][D]; page_table
+    [B][max_pages] int32; mass is [B][max_pages * page] by logical row."""
+    _need(q, "q", torch.bfloat16)
+    dev = q.device
+    n_pages, Hkv, page, Dk = _pool_shape(k_pool, v_pool, page_table, dev, q.dtype)
+    _need(ctx_len, "ctx_len", torch.int32, dev)
+    B, T, Hq, D = q.shape
+    if Dk != D or page_table.shape[0] != B or ctx_len.numel() != B:
+        raise ValueError("inconsistent verify_attn_paged shapes")
+    max_pages = page_table.shape[1]
+    n_cap = max_pages * page
+    if scale is None:
+        scale = D ** -0.5
+    if max_ctx is None:
+        max_ctx = n_cap - T
+    if out is None:
+        out = torch.empty_like(q)
+    _need(out, "out", q.dtype, dev)
+    if mass is None and want_mass:
+        mass = torch.empty((B, n_cap), dtype=torch.float32, device=dev)
+    if mass is not None:
+        _need(mass, "mass", torch.float32, dev)
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq, T), dtype=torch.float32, device=dev)
+    if lse is not None:
+        _need(lse, "lse", torch.float32, dev)
+    need = verify_attn_workspace_size(PVLM_BF16, B, T, Hq, Hkv, D, n_cap, max_ctx)
+    wsb = (ws or _default_ws("verify")).get(need)
+    st = lib().pvlm_verify_attn_paged(PVLM_BF16, B, T, Hq, Hkv, D, page, max_pages, n_pages,
+                                      max_ctx, float(scale), _ptr(q), _ptr(k_pool), _ptr(v_pool),
+                                      _ptr(page_table), _ptr(ctx_len), _ptr(out), _ptr(mass),
+                                      _ptr(lse), _ptr(wsb), wsb.numel(), _ptr(_status(status)),
+                                      _stream())
+    _check(st, "pvlm_verify_attn_paged")
+    return out, mass, lse
+
+
 def verify_attn_noalloc(q, k_cache, v_cache, ctx_len, *, out, mass=None, lse=None,
                         scale: Optional[float] = None, max_ctx: Optional[int] = None, status=None):
     """pvlm_verify_attn_noalloc: verify attention + mass with the library's
@@ -470,6 +531,47 @@ def gather_kv(k_cache, v_cache, idx, k, tail_begin, tail_len, dst_cap: int, *, k
     return k_dst, v_dst
 
 
+def gather_kv_paged(k_pool, v_pool, page_table, idx, k, tail_begin, tail_len, dst_cap: int, *,
+                    k_dst=None, v_dst=None, status=None):
+    """pvlm_gather_kv_paged: compact cache from a paged pool.  Pools are
+    [n_pages][Hkv][page][D] (one layer) or [L][n_pages][Hkv][page][D]; one
+    page_table [B][max_pages] serves every layer; outputs [(L,) B, Hkv, dst_cap, D]."""
+    _need(k_pool, "k_pool")
+    dev = k_pool.device
+    if k_pool.dim() == 4:
+        n_layers, (n_pages, Hkv, page, D) = 1, k_pool.shape
+    elif k_pool.dim() == 5:
+        n_layers, n_pages, Hkv, page, D = k_pool.shape
+    else:
+        raise ValueError("pools must be [n_pages][Hkv][page][D] or [L][n_pages][Hkv][page][D]")
+    _need(v_pool, "v_pool", k_pool.dtype, dev)
+    _need(page_table, "page_table", torch.int32, dev)
+    _need(idx, "idx", torch.int32, dev)
+    for name, t in (("k", k), ("tail_begin", tail_begin), ("tail_len", tail_len)):
+        _need(t, name, torch.int32, dev)
+    if tuple(v_pool.shape) != tuple(k_pool.shape) or page_table.dim() != 2:
+        raise ValueError("inconsistent gather_kv_paged shapes")
+    B, max_pages = page_table.shape
+    if idx.shape[0] != B:
+        raise ValueError("idx must be [B][k_cap]")
+    dst_shape = ((n_layers,) if k_pool.dim() == 5 else ()) + (B, Hkv, dst_cap, D)
+    if k_dst is None:
+        k_dst = torch.zeros(dst_shape, dtype=k_pool.dtype, device=dev)
+    if v_dst is None:
+        v_dst = torch.zeros(dst_shape, dtype=k_pool.dtype, device=dev)
+    _need(k_dst, "k_dst", k_pool.dtype, dev)
+    _need(v_dst, "v_dst", k_pool.dtype, dev)
+    if tuple(k_dst.shape) != dst_shape or tuple(v_dst.shape) != dst_shape:
+        raise ValueError("destination shape mismatch")
+    st = lib().pvlm_gather_kv_paged(_dt(k_pool), n_layers, B, Hkv, D, page, max_pages, n_pages,
+                                    _ptr(k_pool), _ptr(v_pool), _ptr(page_table), _ptr(idx),
+                                    _ptr(k), idx.shape[1], _ptr(tail_begin), _ptr(tail_len),
+                                    dst_cap, _ptr(k_dst), _ptr(v_dst), _ptr(_status(status)),
+                                    _stream())
+    _check(st, "pvlm_gather_kv_paged")
+    return k_dst, v_dst
+
+
 def spec_accept(draft_logits, target_logits, draft_tokens, u_accept, u_sample,
                 temperature: float, *, n_accepted=None, next_token=None, near_tie=None,
                 ws: Optional[Workspace] = None, status=None):
@@ -501,7 +603,8 @@ def spec_accept(draft_logits, target_logits, draft_tokens, u_accept, u_sample,
 
 __all__ = [
     "LIB_PATH", "EXPORTS", "PvlmError", "Workspace", "lib", "synchronize", "default_status",
-    "release_workspaces", "verify_attn",
+    "release_workspaces", "verify_attn", "verify_attn_paged", "verify_attn_noalloc",
+    "gather_kv_paged", "rope_append", "rope_append_paged",
     "verify_attn_workspace_size", "uvprune_score_mass", "uvprune_score_cossim",
     "uvprune_criterion_cossim", "topk_select", "gather_kv", "spec_accept",
     "PVLM_F32", "PVLM_BF16", "PVLM_CRIT_MASS", "PVLM_CRIT_COSSIM", "PVLM_DEV_RANGE",
@@ -632,4 +735,37 @@ def rope_append(q, k_new, v_new, pos, ctx_len, k_cache, v_cache, *, base: float,
                                 _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(ctx_len), _ptr(q_out),
                                 _ptr(k_cache), _ptr(v_cache), _ptr(_status(status)), _stream())
     _check(st, "pvlm_rope_append")
+    return q_out
+
+
+def rope_append_paged(q, k_new, v_new, pos, ctx_len, k_pool, v_pool, page_table, *, base: float,
+                      sections=None, q_out=None, status=None):
+    """pvlm_rope_append_paged: as ``rope_append``, writing the new rows into
+    the pools [n_pages][Hkv][page][D] through page_table [B][max_pages]."""
+    _need(q, "q")
+    dev = q.device
+    for t, name in ((k_new, "k_new"), (v_new, "v_new")):
+        _need(t, name, q.dtype, dev)
+    n_pages, Hkv, page, Dp = _pool_shape(k_pool, v_pool, page_table, dev, q.dtype)
+    _need(pos, "pos", torch.int32, dev)
+    _need(ctx_len, "ctx_len", torch.int32, dev)
+    B, T, Hq, D = q.shape
+    if tuple(k_new.shape) != (B, T, Hkv, D) or tuple(v_new.shape) != (B, T, Hkv, D) or Dp != D:
+        raise ValueError("k_new and v_new must be [B][T][Hkv][D] matching the pools")
+    if page_table.shape[0] != B or tuple(ctx_len.shape) != (B,):
+        raise ValueError("page_table must be [B][max_pages] and ctx_len [B]")
+    want = (B, T) if sections is None else (3, B, T)
+    if tuple(pos.shape) != want:
+        raise ValueError(f"pos must be {list(want)}")
+    if q_out is None:
+        q_out = torch.empty_like(q)
+    else:
+        _need(q_out, "q_out", q.dtype, dev)
+    sec = None if sections is None else (_c.c_int32 * 3)(*[int(x) for x in sections])
+    st = lib().pvlm_rope_append_paged(_dt(q), B, T, Hq, Hkv, D, page, page_table.shape[1], n_pages,
+                                      float(base), sec, _ptr(pos), _ptr(q), _ptr(k_new),
+                                      _ptr(v_new), _ptr(page_table), _ptr(ctx_len), _ptr(q_out),
+                                      _ptr(k_pool), _ptr(v_pool), _ptr(_status(status)),
+                                      _stream())
+    _check(st, "pvlm_rope_append_paged")
     return q_out

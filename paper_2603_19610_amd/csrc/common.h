@@ -234,6 +234,55 @@ __device__ __forceinline__ uint64_t x_load(const uint64_t* p) {
   else return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// The cache rows of one (batch, KV head): contiguous (base = the head's row
+// 0, rows of D elements), or paged: pages of 2^shift rows (a multiple of the
+// 32-row block) in a pool [n_pages][Hkv][2^shift][D]; base = the pool plus
+// the head's offset inside a page, page_elems = elements of one page (all
+// heads), table = the sequence's page-table row (logical page -> pool page).
+// A kernel may stage the entries it will use in LDS (staged, from logical
+// page page0), which takes the table load off each block's address path.
+struct KvRows {
+  const uint16_t* base;
+  const int32_t* table;  // read only when paged
+  const int32_t* staged; // LDS copy of the entries from logical page page0 (used when in_lds)
+  int64_t page_elems;
+  int64_t n_pages;
+  int shift, page0;
+  bool paged, in_lds;
+};
+
+// LDS byte address of a generic pointer into LDS: the shared aperture starts
+// at a multiple of 2^32, so the address is the pointer's low 32 bits.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
+}
+
+// log2 of a page size that is a power of two in [32, 2^20], else -1.
+inline int page_shift_of(int page_size) {
+  if (page_size < 32 || page_size > (1 << 20) || (page_size & (page_size - 1))) return -1;
+  int s = 0;
+  while ((1 << s) < page_size) ++s;
+  return s;
+}
+
+// The address of row te, where te is the 32-row block start tb, or for a
+// block past the chunk end c1 the start of the block holding row c1 - 1;
+// rows te .. te + 31 are contiguous from it.  A page-table entry outside the
+// pool is clamped into it (the kernel flags it separately).
+template <int D>
+__device__ __forceinline__ const uint16_t* kv_block(const KvRows& kv, int tb, int c1, int& te) {
+  te = tb < c1 ? tb : ((c1 - 1) & ~31);
+  if (!kv.paged) return kv.base + (size_t)te * D;
+  int page;
+  if (kv.in_lds) {
+    page = kv.staged[(te >> kv.shift) - kv.page0];  // already clamped
+  } else {
+    page = kv.table[te >> kv.shift];
+    page = page < 0 ? 0 : (page >= kv.n_pages ? (int)(kv.n_pages - 1) : page);
+  }
+  return kv.base + (size_t)page * kv.page_elems + (size_t)(te & ((1 << kv.shift) - 1)) * D;
+}
+
 // Cross-lane exchanges that stay in the VALU (no LDS crossbar round trip):
 // DPP row operations and the gfx950 permlane swaps.
 template <int CTRL>

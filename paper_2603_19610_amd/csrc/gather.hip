@@ -19,6 +19,9 @@ struct GArgs {
   uint4* kd;
   uint4* vd;
   int32_t* status;
+  const int32_t* table;  // paged source: [B][max_pages] pool page per logical page; NULL: padded
+  int64_t n_pages;
+  int max_pages, shift;
   int64_t n_cap, dst_cap;
   int B, Hkv, k_cap, row_vec;  // row_vec = 16-byte vectors per cache row
 };
@@ -63,7 +66,19 @@ __global__ void __launch_bounds__(256) gather_kernel(GArgs a) {
     src = tb + (r - kb);
   }
   const size_t bg = lb * a.Hkv + g;
-  const size_t si = (bg * a.n_cap + src) * a.row_vec + c;
+  size_t si;
+  if (a.table) {  // pool [n_layers][n_pages][Hkv][page][D]; one table serves every layer
+    const int pg = a.table[(size_t)b * a.max_pages + (src >> a.shift)];
+    if (pg < 0 || pg >= a.n_pages) {
+      if (c == 0) dev_flag(a.status, PVLM_DEV_RANGE);
+      return;
+    }
+    const size_t l = lb / a.B;
+    si = ((((l * a.n_pages + pg) * a.Hkv + g) << a.shift) + (src & ((1 << a.shift) - 1))) *
+             a.row_vec + c;
+  } else {
+    si = (bg * a.n_cap + src) * a.row_vec + c;
+  }
   const size_t di = (bg * a.dst_cap + r) * a.row_vec + c;
   const uint4 kv = a.k[si];
   const uint4 vv = a.v[si];
@@ -76,13 +91,13 @@ __global__ void __launch_bounds__(256) gather_kernel(GArgs a) {
 
 using namespace pvlm;
 
-extern "C" pvlm_status pvlm_gather_kv(pvlm_dtype dt, int n_layers, int B, int Hkv, int D,
-                                      int64_t n_cap,
-                                      const void* k_cache, const void* v_cache,
-                                      const int32_t* idx, const int32_t* k, int32_t k_cap,
-                                      const int32_t* tail_begin, const int32_t* tail_len,
-                                      int64_t dst_cap, void* k_dst, void* v_dst, int32_t* status,
-                                      hipStream_t stream) {
+namespace {
+pvlm_status gather_run(pvlm_dtype dt, int n_layers, int B, int Hkv, int D, int64_t n_cap,
+                       const void* k_cache, const void* v_cache, const int32_t* table,
+                       int64_t n_pages, int max_pages, int shift, const int32_t* idx,
+                       const int32_t* k, int32_t k_cap, const int32_t* tail_begin,
+                       const int32_t* tail_len, int64_t dst_cap, void* k_dst, void* v_dst,
+                       int32_t* status, hipStream_t stream) {
   if (!k_cache || !v_cache || !k || !tail_begin || !tail_len || !k_dst || !v_dst)
     return PVLM_ERR_NULL;
   if (k_cap > 0 && !idx) return PVLM_ERR_NULL;
@@ -107,6 +122,10 @@ extern "C" pvlm_status pvlm_gather_kv(pvlm_dtype dt, int n_layers, int B, int Hk
   a.kd = static_cast<uint4*>(k_dst);
   a.vd = static_cast<uint4*>(v_dst);
   a.status = status;
+  a.table = table;
+  a.n_pages = n_pages;
+  a.max_pages = max_pages;
+  a.shift = shift;
   a.n_cap = n_cap;
   a.dst_cap = dst_cap;
   a.B = B;
@@ -118,4 +137,31 @@ extern "C" pvlm_status pvlm_gather_kv(pvlm_dtype dt, int n_layers, int B, int Hk
   hipLaunchKernelGGL(gather_kernel, dim3((unsigned)xb, Hkv, n_layers * B), dim3(256), 0, stream, a);
   PVLM_LAUNCHED();
   return PVLM_OK;
+}
+}  // namespace
+
+extern "C" pvlm_status pvlm_gather_kv(pvlm_dtype dt, int n_layers, int B, int Hkv, int D,
+                                      int64_t n_cap, const void* k_cache, const void* v_cache,
+                                      const int32_t* idx, const int32_t* k, int32_t k_cap,
+                                      const int32_t* tail_begin, const int32_t* tail_len,
+                                      int64_t dst_cap, void* k_dst, void* v_dst, int32_t* status,
+                                      hipStream_t stream) {
+  return gather_run(dt, n_layers, B, Hkv, D, n_cap, k_cache, v_cache, nullptr, 0, 0, 0, idx, k,
+                    k_cap, tail_begin, tail_len, dst_cap, k_dst, v_dst, status, stream);
+}
+
+extern "C" pvlm_status pvlm_gather_kv_paged(pvlm_dtype dt, int n_layers, int B, int Hkv, int D,
+                                            int page_size, int max_pages, int64_t n_pages,
+                                            const void* k_pool, const void* v_pool,
+                                            const int32_t* page_table, const int32_t* idx,
+                                            const int32_t* k, int32_t k_cap,
+                                            const int32_t* tail_begin, const int32_t* tail_len,
+                                            int64_t dst_cap, void* k_dst, void* v_dst,
+                                            int32_t* status, hipStream_t stream) {
+  if (!page_table) return PVLM_ERR_NULL;
+  const int shift = page_shift_of(page_size);
+  if (shift < 0 || max_pages < 1 || n_pages < 1 || n_pages > INT32_MAX) return PVLM_ERR_SHAPE;
+  return gather_run(dt, n_layers, B, Hkv, D, (int64_t)max_pages << shift, k_pool, v_pool,
+                    page_table, n_pages, max_pages, shift, idx, k, k_cap, tail_begin, tail_len,
+                    dst_cap, k_dst, v_dst, status, stream);
 }

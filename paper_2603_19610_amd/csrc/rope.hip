@@ -26,6 +26,9 @@ struct RArgs {
   void* k_cache;
   void* v_cache;
   int32_t* status;
+  const int32_t* table;  // paged caches: [B][max_pages] pool page per logical page; NULL: padded
+  int64_t n_pages;
+  int max_pages, shift;
   int64_t n_cap, total;
   double log2_base;
   int B, T, Hq, Hkv, D, s0, s01, mrope;
@@ -70,7 +73,17 @@ __global__ void __launch_bounds__(256) rope_append_kernel(RArgs a) {
   } else {
     const int g = h < a.Hq + a.Hkv ? h - a.Hq : h - a.Hq - a.Hkv;
     so = (size_t)((bt * a.Hkv + g) * a.D);
-    d_off = (size_t)((((int64_t)b * a.Hkv + g) * a.n_cap + ctx + t) * a.D);
+    const int64_t lr = (int64_t)ctx + t;  // logical cache row
+    if (a.table) {  // pool [n_pages][Hkv][page][D]
+      const int pg = a.table[(size_t)b * a.max_pages + (lr >> a.shift)];
+      if (pg < 0 || pg >= a.n_pages) {
+        if (i == 0) dev_flag(a.status, PVLM_DEV_RANGE);
+        return;
+      }
+      d_off = (size_t)(((((int64_t)pg * a.Hkv + g) << a.shift) + (lr & ((1 << a.shift) - 1))) * a.D);
+    } else {
+      d_off = (size_t)((((int64_t)b * a.Hkv + g) * a.n_cap + lr) * a.D);
+    }
     const bool is_k = h < a.Hq + a.Hkv;
     src = is_k ? a.k_in : a.v_in;
     dst = is_k ? a.k_cache : a.v_cache;
@@ -102,21 +115,21 @@ __global__ void __launch_bounds__(256) rope_append_kernel(RArgs a) {
 
 using namespace pvlm;
 
-extern "C" pvlm_status pvlm_rope_append(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D,
-                                        int64_t n_cap, double base, const int32_t* sections,
-                                        const int32_t* pos, const void* q_in, const void* k_in,
-                                        const void* v_in, const int32_t* ctx_len, void* q_out,
-                                        void* k_cache, void* v_cache, int32_t* status,
-                                        hipStream_t stream) {
+namespace {
+pvlm_status rope_run(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int64_t n_cap,
+                     double base, const int32_t* sections, const int32_t* pos, const void* q_in,
+                     const void* k_in, const void* v_in, const int32_t* ctx_len, void* q_out,
+                     void* k_cache, void* v_cache, const int32_t* table, int64_t n_pages,
+                     int max_pages, int shift, int32_t* status, hipStream_t stream) {
   if (!pos || !q_in || !k_in || !v_in || !ctx_len || !q_out || !k_cache || !v_cache)
     return PVLM_ERR_NULL;
   if (dt != PVLM_F32 && dt != PVLM_BF16) return PVLM_ERR_UNSUPPORTED;
   if (B < 1 || T < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || D < 2 || D % 2 != 0 || D > 1024 ||
       n_cap < T || n_cap > ((int64_t)1 << 30) || !(base > 1.0 && base < 1e300))
     return PVLM_ERR_SHAPE;
-  // one thread per rotation pair: keep the grid well inside its x-dimension limit
+  // one thread per rotation pair, in one launch of at most 2^32 - 256 work-items
   const int64_t heads = (int64_t)Hq + 2 * (int64_t)Hkv;
-  if (heads > 65536 || (int64_t)B * T * heads * (D / 2) > ((int64_t)1 << 38))
+  if (heads > 65536 || (int64_t)B * T * heads * (D / 2) > ((int64_t)1 << 32) - 256)
     return PVLM_ERR_SHAPE;
   RArgs a;
   a.mrope = sections != nullptr;
@@ -138,6 +151,10 @@ extern "C" pvlm_status pvlm_rope_append(pvlm_dtype dt, int B, int T, int Hq, int
   a.k_cache = k_cache;
   a.v_cache = v_cache;
   a.status = status;
+  a.table = table;
+  a.n_pages = n_pages;
+  a.max_pages = max_pages;
+  a.shift = shift;
   a.n_cap = n_cap;
   a.log2_base = std::log2(base);
   a.B = B;
@@ -153,4 +170,31 @@ extern "C" pvlm_status pvlm_rope_append(pvlm_dtype dt, int B, int T, int Hq, int
     hipLaunchKernelGGL(rope_append_kernel<uint16_t>, dim3(grid), dim3(256), 0, stream, a);
   PVLM_LAUNCHED();
   return PVLM_OK;
+}
+}  // namespace
+
+extern "C" pvlm_status pvlm_rope_append(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D,
+                                        int64_t n_cap, double base, const int32_t* sections,
+                                        const int32_t* pos, const void* q_in, const void* k_in,
+                                        const void* v_in, const int32_t* ctx_len, void* q_out,
+                                        void* k_cache, void* v_cache, int32_t* status,
+                                        hipStream_t stream) {
+  return rope_run(dt, B, T, Hq, Hkv, D, n_cap, base, sections, pos, q_in, k_in, v_in, ctx_len,
+                  q_out, k_cache, v_cache, nullptr, 0, 0, 0, status, stream);
+}
+
+extern "C" pvlm_status pvlm_rope_append_paged(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D,
+                                              int page_size, int max_pages, int64_t n_pages,
+                                              double base, const int32_t* sections,
+                                              const int32_t* pos, const void* q_in,
+                                              const void* k_in, const void* v_in,
+                                              const int32_t* page_table, const int32_t* ctx_len,
+                                              void* q_out, void* k_pool, void* v_pool,
+                                              int32_t* status, hipStream_t stream) {
+  if (!page_table) return PVLM_ERR_NULL;
+  const int shift = page_shift_of(page_size);
+  if (shift < 0 || max_pages < 1 || n_pages < 1 || n_pages > INT32_MAX) return PVLM_ERR_SHAPE;
+  return rope_run(dt, B, T, Hq, Hkv, D, (int64_t)max_pages << shift, base, sections, pos, q_in,
+                  k_in, v_in, ctx_len, q_out, k_pool, v_pool, page_table, n_pages, max_pages,
+                  shift, status, stream);
 }

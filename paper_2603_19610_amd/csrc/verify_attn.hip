@@ -50,6 +50,7 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kMaxRT = 5;        // 16-row tiles per workgroup
+constexpr int kPageSlots = 512;  // page-table entries a workgroup stages in LDS
 constexpr int kOSets = 8;        // max thread sets splitting the O-partial sum
 constexpr int kNB = 4;           // 32-token blocks per wave (resident variant)
 constexpr int kResTokens = kWaves * kNB * 32;
@@ -68,6 +69,9 @@ struct VArgs {
   const void* k;
   const void* v;
   const int32_t* ctx_len;
+  const int32_t* table;  // paged caches: [B][max_pages] pool page of each logical page; NULL: padded
+  int64_t n_pages;       // pool pages
+  int max_pages, page_shift;
   int64_t n_cap;
   int B, T, Hq, Hkv, G, R, RG, RT, D;
   int max_ctx;
@@ -438,12 +442,14 @@ __device__ __forceinline__ bf16x8 pack_v(const VT (&vr)[8], int jd) {
 // (their scores are masked), keeping the loads unconditional so the
 // compiler can wait for one block while the later ones stay in flight.
 template <int D>
-__device__ __forceinline__ void load_k_block(const uint16_t* kg, int tb, int c1, int n, int gq,
+__device__ __forceinline__ void load_k_block(const KvRows& kv, int tb, int c1, int n, int gq,
                                              uint4 (&Kr)[2][D / 32]) {
+  int te;
+  const uint16_t* r0 = kv_block<D>(kv, tb, c1, te);
 #pragma unroll
   for (int tt = 0; tt < 2; ++tt) {
     const int tok = min(tb + 16 * tt + n, c1 - 1);
-    const uint16_t* kp = kg + (size_t)tok * D + 8 * gq;
+    const uint16_t* kp = r0 + (size_t)(tok - te) * D + 8 * gq;
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks) Kr[tt][ks] = *reinterpret_cast<const uint4*>(kp + 32 * ks);
   }
@@ -453,14 +459,16 @@ __device__ __forceinline__ void load_k_block(const uint16_t* kg, int tb, int c1,
 // tb + {4gq..4gq+3, 16+4gq..16+4gq+3}, d in [DPL*n, DPL*n + DPL).  Tokens past
 // the chunk load its last row (their probabilities are 0).
 template <int D>
-__device__ __forceinline__ void load_v_block(const uint16_t* vg, int tb, int c1, int n, int gq,
+__device__ __forceinline__ void load_v_block(const KvRows& kv, int tb, int c1, int n, int gq,
                                              typename VVec<D>::T (&Vr)[8]) {
   typedef typename VVec<D>::T VT;
   constexpr int DPL = D / 16;
+  int te;
+  const uint16_t* r0 = kv_block<D>(kv, tb, c1, te);
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
     const int tok = min(tb + (s < 4 ? 4 * gq + s : 16 + 4 * gq + (s - 4)), c1 - 1);
-    Vr[s] = *reinterpret_cast<const VT*>(vg + (size_t)tok * D + DPL * n);
+    Vr[s] = *reinterpret_cast<const VT*>(r0 + (size_t)(tok - te) * D + DPL * n);
   }
 }
 
@@ -473,17 +481,18 @@ __device__ __forceinline__ void load_v_block(const uint16_t* vg, int tb, int c1,
 // access); untracked loads can only lengthen the compiler's own vmcnt waits.
 // The consumer waits explicitly (s_waitcnt vmcnt(0) + workgroup barrier).
 template <int D>
-__device__ __forceinline__ void issue_v_lds(const uint16_t* vg, int tb, int c1, uint16_t* lds_blk,
+__device__ __forceinline__ void issue_v_lds(const KvRows& kv, int tb, int c1, uint16_t* lds_blk,
                                             int lane) {
   constexpr int CPR = D / 8;    // 16-byte columns per row
   constexpr int RPI = 64 / CPR; // rows per instruction
+  int te;
+  const uint16_t* r0 = kv_block<D>(kv, tb, c1, te);
 #pragma unroll
   for (int k = 0; k < 32 / RPI; ++k) {
     const int row = k * RPI + lane / CPR;
     const int tok = min(tb + row, c1 - 1);
-    const uint16_t* src = vg + (size_t)tok * D + 8 * (lane % CPR);
-    const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
-        reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint16_t*)(lds_blk + k * RPI * D))));
+    const uint16_t* src = r0 + (size_t)(tok - te) * D + 8 * (lane % CPR);
+    const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_addr(lds_blk + k * RPI * D));
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
                  :
                  : "s"(lds), "v"(src)
@@ -509,16 +518,17 @@ __device__ __forceinline__ void read_v_lds(const uint16_t* lds_blk, int n, int g
 // through untracked global->LDS loads like issue_v_lds.  Rows past the chunk
 // re-read its last row.
 template <int D>
-__device__ __forceinline__ void issue_k_lds(const uint16_t* kg, int tb, int c1, uint16_t* lds_blk,
+__device__ __forceinline__ void issue_k_lds(const KvRows& kv, int tb, int c1, uint16_t* lds_blk,
                                             int lane) {
   constexpr int CH = D / 8;
   constexpr int NI = 32 * CH / 64;
+  int te;
+  const uint16_t* r0 = kv_block<D>(kv, tb, c1, te);
 #pragma unroll
   for (int ins = 0; ins < NI; ++ins) {
     const int slot = ins * 64 + lane, r = slot / CH, c = (slot % CH) ^ (r % CH);
-    const uint16_t* src = kg + (size_t)min(tb + r, c1 - 1) * D + 8 * c;
-    const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
-        reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint16_t*)(lds_blk + ins * 64 * 8))));
+    const uint16_t* src = r0 + (size_t)(min(tb + r, c1 - 1) - te) * D + 8 * c;
+    const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_addr(lds_blk + ins * 64 * 8));
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
                  :
                  : "s"(lds), "v"(src)
@@ -720,8 +730,7 @@ __device__ __forceinline__ void issue_q_lds(const VArgs& a, const Unit& u, uint1
       const int row = min(u.rg * a.RT * 16 + r, a.R - 1);
       const int t = row / a.G, h = u.g * a.G + row % a.G;
       const uint16_t* src = q + (((size_t)u.b * a.T + t) * a.Hq + h) * D + 8 * c;
-      const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
-          reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint16_t*)(s_q + ins * 64 * 8))));
+      const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_addr(s_q + ins * 64 * 8));
       asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
                    :
                    : "s"(lds), "v"(src)
@@ -1082,6 +1091,7 @@ verify_mfma_kernel(VArgs a) {
   __shared__ float s_wm[kWaves][ROWS], s_wz[kWaves][ROWS];
   __shared__ float s_m[ROWS], s_z[ROWS], s_lse[ROWS];
   __shared__ int s_flag;
+  __shared__ int32_t s_pages[kPageSlots];  // paged caches: the chunk's pool pages
   extern __shared__ __align__(256) float s_o[];  // 16-byte LDS accesses need 16-byte alignment
 
   Unit u;
@@ -1098,9 +1108,33 @@ verify_mfma_kernel(VArgs a) {
     empty_chunk<ROWS, LOCAL>(a, u, s_m, s_z, base, &s_flag);
     return;
   }
-  const size_t kv_off = ((size_t)u.b * a.Hkv + u.g) * a.n_cap * D;
-  const uint16_t* kg = static_cast<const uint16_t*>(a.k) + kv_off;
-  const uint16_t* vg = static_cast<const uint16_t*>(a.v) + kv_off;
+  KvRows kg, vg;  // this (batch, KV head)'s K and V rows
+  if (a.table) {
+    const size_t hoff = ((size_t)u.g << a.page_shift) * D;
+    const int32_t* tab = a.table + (size_t)u.b * a.max_pages;
+    const int64_t pe = ((int64_t)a.Hkv << a.page_shift) * D;
+    // The chunk's page entries, checked against the pool, clamped into it
+    // and staged in LDS when they fit.
+    const int p0 = u.c0 >> a.page_shift, p1 = (u.c1 - 1) >> a.page_shift;
+    const bool fit = p1 - p0 < kPageSlots;
+    for (int pg = p0 + threadIdx.x; pg <= p1; pg += kThreads) {
+      int e = tab[pg];
+      if (e < 0 || e >= a.n_pages) {
+        dev_flag(a.status, PVLM_DEV_RANGE);
+        e = e < 0 ? 0 : (int)(a.n_pages - 1);
+      }
+      if (fit) s_pages[pg - p0] = e;
+    }
+    __syncthreads();
+    kg = {static_cast<const uint16_t*>(a.k) + hoff, tab, s_pages, pe, a.n_pages, a.page_shift, p0,
+          true, fit};
+    vg = {static_cast<const uint16_t*>(a.v) + hoff, tab, s_pages, pe, a.n_pages, a.page_shift, p0,
+          true, fit};
+  } else {
+    const size_t kv_off = ((size_t)u.b * a.Hkv + u.g) * a.n_cap * D;
+    kg = {static_cast<const uint16_t*>(a.k) + kv_off, a.ctx_len, s_pages, 0, 1, 5, 0, false, false};
+    vg = {static_cast<const uint16_t*>(a.v) + kv_off, a.ctx_len, s_pages, 0, 1, 5, 0, false, false};
+  }
   float* mp = a.mpart + ((size_t)u.b * a.Hkv * a.RG + u.g * a.RG + u.rg) * a.n_cap;
 
   float m[RT], z[RT];
@@ -1565,12 +1599,14 @@ extern "C" size_t pvlm_verify_attn_workspace_size(pvlm_dtype dt, int B, int T, i
   return p.bytes;
 }
 
-extern "C" pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D,
-                                        int64_t n_cap, int64_t max_ctx, float scale, const void* q,
-                                        const void* k_cache, const void* v_cache,
-                                        const int32_t* ctx_len, void* out, float* mass, float* lse,
-                                        void* ws, size_t ws_bytes, int32_t* status,
-                                        hipStream_t stream) {
+namespace {
+// The cache rows come from a padded cache (table == NULL) or through a page
+// table into a page pool (logical capacity n_cap = max_pages << page_shift).
+pvlm_status verify_run(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int64_t n_cap,
+                       int64_t max_ctx, float scale, const void* q, const void* k_cache,
+                       const void* v_cache, const int32_t* table, int64_t n_pages, int max_pages,
+                       int page_shift, const int32_t* ctx_len, void* out, float* mass, float* lse,
+                       void* ws, size_t ws_bytes, int32_t* status, hipStream_t stream) {
   if (!q || !k_cache || !v_cache || !ctx_len || !out) return PVLM_ERR_NULL;
   if (!(scale > 0.f) || !std::isfinite(scale)) return PVLM_ERR_SHAPE;
   VPlan p;
@@ -1584,6 +1620,10 @@ extern "C" pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int
   a.k = k_cache;
   a.v = v_cache;
   a.ctx_len = ctx_len;
+  a.table = table;
+  a.n_pages = n_pages;
+  a.max_pages = max_pages;
+  a.page_shift = page_shift;
   a.stats = reinterpret_cast<float*>(wsb + p.off_stats);
   a.opart = reinterpret_cast<float*>(wsb + p.off_opart);
   a.mpart = reinterpret_cast<float*>(wsb + p.off_mpart);
@@ -1634,6 +1674,34 @@ extern "C" pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int
                                args, p.lds_dyn, stream));
   }
   return PVLM_OK;
+}
+}  // namespace
+
+extern "C" pvlm_status pvlm_verify_attn(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D,
+                                        int64_t n_cap, int64_t max_ctx, float scale, const void* q,
+                                        const void* k_cache, const void* v_cache,
+                                        const int32_t* ctx_len, void* out, float* mass, float* lse,
+                                        void* ws, size_t ws_bytes, int32_t* status,
+                                        hipStream_t stream) {
+  return verify_run(dt, B, T, Hq, Hkv, D, n_cap, max_ctx, scale, q, k_cache, v_cache, nullptr, 0, 0,
+                    0, ctx_len, out, mass, lse, ws, ws_bytes, status, stream);
+}
+
+extern "C" pvlm_status pvlm_verify_attn_paged(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D,
+                                              int page_size, int max_pages, int64_t n_pages,
+                                              int64_t max_ctx, float scale, const void* q,
+                                              const void* k_pool, const void* v_pool,
+                                              const int32_t* page_table, const int32_t* ctx_len,
+                                              void* out, float* mass, float* lse, void* ws,
+                                              size_t ws_bytes, int32_t* status,
+                                              hipStream_t stream) {
+  if (!page_table) return PVLM_ERR_NULL;
+  const int shift = page_shift_of(page_size);
+  if (shift < 0 || max_pages < 1 || n_pages < 1 || n_pages > INT32_MAX) return PVLM_ERR_SHAPE;
+  if (dt != PVLM_BF16) return PVLM_ERR_UNSUPPORTED;
+  return verify_run(dt, B, T, Hq, Hkv, D, (int64_t)max_pages << shift, max_ctx, scale, q, k_pool,
+                    v_pool, page_table, n_pages, max_pages, shift, ctx_len, out, mass, lse, ws,
+                    ws_bytes, status, stream);
 }
 
 namespace {

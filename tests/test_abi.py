@@ -94,3 +94,38 @@ def test_missing_library_fails_loudly(monkeypatch):
     monkeypatch.setattr(pv, "LIB_PATH", "/nonexistent/libpvlm.so")
     with pytest.raises(RuntimeError, match="not built"):
         pv.lib()
+
+
+def test_paged_calls_reject():
+    """Host-side argument checks of the paged entry points (nothing launched)."""
+    L = pv.lib()
+
+    def verify(dt=1, page=32, max_pages=4, n_pages=8, table=FAKE):
+        return L.pvlm_verify_attn_paged(dt, 1, 5, 8, 2, 128, page, max_pages, n_pages, 100, 0.088,
+                                        FAKE, FAKE, FAKE, table, FAKE, FAKE, None, None, FAKE,
+                                        1 << 30, None, None)
+    assert verify(table=None) == 1
+    for bad in (dict(page=48), dict(page=16), dict(page=1 << 21), dict(max_pages=0),
+                dict(n_pages=0), dict(n_pages=1 << 31)):
+        assert verify(**bad) == 2, bad
+    assert verify(dt=0) == 3                          # bf16 only
+    assert verify(max_pages=3) == 2                   # 96 logical rows < max_ctx + T
+
+    def gather(page=64, table=FAKE):
+        return L.pvlm_gather_kv_paged(1, 2, 1, 1, 128, page, 4, 8, FAKE, FAKE, table, FAKE, FAKE,
+                                      4, FAKE, FAKE, 8, FAKE, FAKE, None, None)
+    assert gather(table=None) == 1
+    assert gather(page=100) == 2
+
+    def rope(B=1, page=32, table=FAKE):
+        return L.pvlm_rope_append_paged(1, B, 4, 8, 2, 128, page, 4, 8, 1e6, None, FAKE, FAKE,
+                                        FAKE, FAKE, table, FAKE, FAKE, FAKE, FAKE, None, None)
+    assert rope(table=None) == 1
+    assert rope(page=24) == 2
+
+
+def test_rope_rejects_more_pairs_than_one_launch_holds():
+    L = pv.lib()
+    # B * T * (Hq + 2 Hkv) * D / 2 = 4096 * 32 * 80 * 512 > 2^32 - 256
+    assert L.pvlm_rope_append(1, 4096, 32, 64, 8, 1024, 64, 1e6, None, FAKE, FAKE, FAKE, FAKE,
+                              FAKE, FAKE, FAKE, FAKE, None, None) == 2

@@ -15,7 +15,8 @@ Recipe (all draws in float64, then rounded once to the storage dtype):
 
 * Seeds: ``PCG64(SeedSequence([260319610, config_id, layer, tensor_id]))``
   with tensor ids Q=0, K=1, V=2, salient=3, draft logits=4, target noise=5,
-  draft tokens=6, uniforms=7, visual hidden=8, text hidden=9, lengths=10.
+  draft tokens=6, uniforms=7, visual hidden=8, text hidden=9, lengths=10,
+  page assignment=11.
 * Q, K, V ~ N(0, 1).  A fraction of the visual keys is made salient:
   ``k += boost * u_g`` where ``u_g`` is the unit vector of the mean query of
   KV group g (over its query heads and all verify rows), added before RoPE.
@@ -26,6 +27,12 @@ Recipe (all draws in float64, then rounded once to the storage dtype):
   ``uint16`` bit patterns.
 * Cache rows: visual rows [0, m), text rows [m, m + n), then the T = gamma + 1
   verify-block rows [ctx_len, ctx_len + T); rows past that are zero.
+* Paged layout: a paged cache holds the same rows as the padded one, in pages
+  of P rows (a power of two >= 32) of a shared pool [n_pages][Hkv][P][D].
+  Each sequence takes ceil(rows / P) pages; pool pages are handed out in the
+  order of a seeded random permutation (so a sequence's pages are scattered
+  through the pool), a few spare pool pages stay unused, and page-table
+  entries past a sequence's last page are -1.
 * Logits: draft ~ N(0, s_d), target = draft + N(0, s_n), float32.  Draft
   tokens are ``argmax(z / temperature + Gumbel)`` per position (the argmax at
   temperature 0).  Uniforms are float64 in [0, 1).
@@ -40,7 +47,8 @@ import numpy as np
 
 SEED_ROOT = 260319610
 
-TID_Q, TID_K, TID_V, TID_SAL, TID_DL, TID_TL, TID_TOK, TID_U, TID_HV, TID_HT, TID_LEN = range(11)
+TID_Q, TID_K, TID_V, TID_SAL, TID_DL, TID_TL, TID_TOK, TID_U, TID_HV, TID_HT, TID_LEN, TID_PAGE = \
+    range(12)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -265,6 +273,60 @@ def random_verify_inputs(B: int, T: int, Hq: int, Hkv: int, D: int, ctx: List[in
     return VerifyInputs(q=round_storage(q64, dtype), k=k, v=v, ctx_len=ctx.astype(np.int32),
                         m=ctx.astype(np.int32), n_cap=n_cap, dtype=dtype,
                         scale=1.0 / math.sqrt(D))
+
+
+# ------------------------------------------------------------ paged layout --
+def page_table(rows, page: int, seed: int = 0, spare: int = 3,
+               max_pages: Optional[int] = None) -> Tuple[np.ndarray, int]:
+    """Page table for sequences of ``rows[b]`` cache rows in pages of ``page``
+    rows.  Returns (table [B][max_pages] int32, n_pages): sequence b's logical
+    page j is pool page table[b, j]; entries past its last page are -1."""
+    rows = np.asarray(rows, dtype=np.int64)
+    need = -(-rows // page)
+    mp = int(need.max() if max_pages is None else max_pages)
+    if mp < need.max():
+        raise ValueError("max_pages too small")
+    n_pages = int(need.sum()) + int(spare)
+    perm = stream(70, seed, TID_PAGE).permutation(n_pages)
+    table = np.full((len(rows), mp), -1, dtype=np.int32)
+    o = 0
+    for b, nb in enumerate(need):
+        table[b, :nb] = perm[o:o + nb]
+        o += nb
+    return table, n_pages
+
+
+def to_pages(cache, table: np.ndarray, n_pages: int, page: int):
+    """Scatter a padded cache [..., B, Hkv, n_cap, D] (numpy or torch; leading
+    layer axes allowed) into a pool [..., n_pages, Hkv, page, D] by ``table``.
+    Pool pages that no sequence uses are zero."""
+    B, Hkv, n_cap, D = cache.shape[-4:]
+    lead = tuple(cache.shape[:-4])
+    mp = table.shape[1]
+    if n_cap > mp * page:
+        raise ValueError("table too short for the cache")
+    flat = np.asarray(table).reshape(-1)
+    src_sel = np.nonzero(flat >= 0)[0]
+    dst_sel = flat[src_sel]
+    if isinstance(cache, np.ndarray):
+        pad = np.zeros(lead + (B, Hkv, mp * page, D), dtype=cache.dtype)
+        pad[..., :n_cap, :] = cache
+        pool = np.zeros(lead + (n_pages, Hkv, page, D), dtype=cache.dtype)
+    else:
+        import torch
+        pad = torch.zeros(lead + (B, Hkv, mp * page, D), dtype=cache.dtype, device=cache.device)
+        pad[..., :n_cap, :] = cache
+        pool = torch.zeros(lead + (n_pages, Hkv, page, D), dtype=cache.dtype,
+                           device=cache.device)
+        src_sel = torch.from_numpy(src_sel).to(cache.device)
+        dst_sel = torch.from_numpy(dst_sel.astype(np.int64)).to(cache.device)
+    nl = len(lead)
+    blocks = pad.reshape(lead + (B, Hkv, mp, page, D))
+    order = tuple(range(nl)) + (nl, nl + 2, nl + 1, nl + 3, nl + 4)
+    blocks = blocks.transpose(*order) if isinstance(cache, np.ndarray) else blocks.permute(*order)
+    blocks = blocks.reshape(lead + (B * mp, Hkv, page, D))
+    pool[..., dst_sel, :, :, :] = blocks[..., src_sel, :, :, :]
+    return pool
 
 
 def crit_boost(w: Workload, layer: int) -> float:
