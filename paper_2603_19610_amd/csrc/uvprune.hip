@@ -270,9 +270,10 @@ pvlm_status run_cossim(int nslots, int L, int B, int64_t m_cap, const int32_t* m
   if (Dh > kMaxDh) return PVLM_ERR_UNSUPPORTED;
   // launch limits: grid y and z of at most 65535 (the text-direction
   // partials run over 2 * B batch-slots and n_cap / 32 chunks), and one
-  // 64-lane wave per text row of both slots in a grid x below 2^31
+  // 64-lane wave per text row of both slots, in one launch of at most
+  // 2^32 - 256 work-items
   if (m_cap > ((int64_t)1 << 30) || 2 * (int64_t)B > 65535 || txt_chunks(n_cap) > 65535 ||
-      ((int64_t)2 * B * n_cap + 3) / 4 >= ((int64_t)1 << 31))
+      ((int64_t)2 * B * n_cap + 3) / 4 * 256 > ((int64_t)1 << 32) - 256)
     return PVLM_ERR_SHAPE;
   if (nslots == 2 && L < 1) return PVLM_ERR_SHAPE;
   const size_t need = cossim_ws(B, Dh, n_cap);
@@ -314,7 +315,8 @@ extern "C" pvlm_status pvlm_uvprune_score(pvlm_crit crit, int B, int L, int64_t 
   if (crit == PVLM_CRIT_MASS) {
     if (!m || !crit_stack || !score) return PVLM_ERR_NULL;
     if (B < 1 || L < 1 || m_cap < 1 || m_cap > ((int64_t)1 << 30)) return PVLM_ERR_SHAPE;
-    const int64_t total = (int64_t)B * m_cap;
+    const int64_t total = (int64_t)B * m_cap;  // one work-item per score, one launch
+    if ((total + 255) / 256 * 256 > ((int64_t)1 << 32) - 256) return PVLM_ERR_SHAPE;
     hipLaunchKernelGGL(uv_mass_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
                        crit_stack, m, B, L, m_cap, score, status);
     PVLM_LAUNCHED();

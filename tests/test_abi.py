@@ -129,3 +129,16 @@ def test_rope_rejects_more_pairs_than_one_launch_holds():
     # B * T * (Hq + 2 Hkv) * D / 2 = 4096 * 32 * 80 * 512 > 2^32 - 256
     assert L.pvlm_rope_append(1, 4096, 32, 64, 8, 1024, 64, 1e6, None, FAKE, FAKE, FAKE, FAKE,
                               FAKE, FAKE, FAKE, FAKE, None, None) == 2
+
+
+def test_uvprune_rejects_more_work_items_than_one_launch_holds():
+    L = pv.lib()
+    # MASS: B * m_cap = 8 * 2^30 scores > 2^32 - 256 work-items
+    assert L.pvlm_uvprune_score(0, 8, 1, 1 << 30, FAKE, FAKE, 0, 0, 0, None, None, None, FAKE,
+                                None, 0, None, None) == 2
+    # COSSIM: 64 lanes * 2 * B * n_cap = 64 * 2 * 17 * (2^21 - 32) > 2^32 - 256, while
+    # its n_cap / 32 = 65535 chunks and 2 * B stay within the grid's y and z
+    assert L.pvlm_uvprune_score(1, 17, 2, 10, FAKE, None, 1, 8, (1 << 21) - 32, FAKE, FAKE, FAKE,
+                                FAKE, FAKE, 1 << 40, None, None) == 2
+    assert L.pvlm_uvprune_score(1, 8, 2, 10, FAKE, None, 1, 8, (1 << 21) - 32, FAKE, FAKE, FAKE,
+                                FAKE, FAKE, 8, None, None) == 4   # within the limits: ws too small
