@@ -137,13 +137,25 @@ def kernel_code_digest():
 
 # ------------------------------------------------------------ CPU baseline --
 def cpu_model():
+    """The first processor's identification in /proc/cpuinfo: the model name
+    exactly as the host reports it (a virtual machine may give only the
+    family name), with vendor, family, model, stepping and clock."""
+    keys = ("model name", "vendor_id", "cpu family", "model", "stepping", "cpu MHz")
+    found = {}
     try:
         for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                return line.split(":", 1)[1].strip()
+            if not line.strip():
+                break
+            k, _, v = line.partition(":")
+            k = k.strip()
+            if k in keys and k not in found:
+                found[k] = v.strip()
     except OSError:
-        pass
-    return "unknown"
+        return "unknown"
+    if not found:
+        return "unknown"
+    rest = ", ".join(f"{k} {found[k]}" for k in keys[1:] if k in found)
+    return f"{found.get('model name', 'unknown')} ({rest})"
 
 
 def oracle_single_layer_step(w, W, oracle, thread_limits):
@@ -550,6 +562,96 @@ def paged_record(torch, pv, W, dev, reps=20):
     return rec
 
 
+def overlap_record(torch, pv, W, dev, gamma=5, reps=50):
+    """Stage II concurrency at the 7B attention shape (28 query / 4 KV heads,
+    D 128, bf16): the draft's gamma decode steps (rope-append + verify, T = 1)
+    over the compact cache [V*, X] (627 kept visual + 160 text rows) on a
+    32-CU stream, beside the target's round (rope-append + verify of T =
+    gamma + 1 rows over the 6,432-row cache, then accept over V = 152064) on a
+    224-CU stream.  Each side is one HIP graph; times are per round."""
+    w = W.WORKLOADS["llava7b"]
+    Hq, Hkv, D, T = w.hq, w.hkv, w.head_dim, gamma + 1
+    n_prompt = int(w.lengths()[0])
+    m = n_prompt - w.n_text
+    n_c = int(w.keep_count(np.array([m]))[0]) + w.n_text
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(5)
+    bf = torch.bfloat16
+    rnd = lambda *sh: torch.randn(sh, device=dev, generator=gen).to(bf)
+    kt, vt = rnd(1, Hkv, n_prompt + 64, D), rnd(1, Hkv, n_prompt + 64, D)
+    kd, vd = rnd(1, Hkv, n_c + 64, D), rnd(1, Hkv, n_c + 64, D)
+    qt, knt, vnt = rnd(1, T, Hq, D), rnd(1, T, Hkv, D), rnd(1, T, Hkv, D)
+    qd, knd, vnd = rnd(1, 1, Hq, D), rnd(1, 1, Hkv, D), rnd(1, 1, Hkv, D)
+    ctx_t = torch.tensor([n_prompt], dtype=torch.int32, device=dev)
+    pos_t = (n_prompt + torch.arange(T, dtype=torch.int32, device=dev))[None].contiguous()
+    ctx_d = [torch.tensor([n_c + i], dtype=torch.int32, device=dev) for i in range(gamma)]
+    pos_d = [torch.tensor([[n_prompt + i]], dtype=torch.int32, device=dev) for i in range(gamma)]
+    V = w.vocab
+    dl = torch.randn((1, gamma, V), device=dev, generator=gen)
+    tl = torch.randn((1, gamma + 1, V), device=dev, generator=gen)
+    tok = torch.randint(0, V, (1, gamma), device=dev, generator=gen).to(torch.int32)
+    ua = torch.rand((1, gamma), device=dev, generator=gen, dtype=torch.float64)
+    us = torch.rand((1,), device=dev, generator=gen, dtype=torch.float64)
+    s_t, s_d = torch.cuda.Stream(), torch.cuda.Stream()
+    pv.set_stream_cu_budget(s_t, 224)
+    pv.set_stream_cu_budget(s_d, 32)
+    ws_t, ws_d = pv.Workspace(dev), pv.Workspace(dev)
+    st = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def target_round():
+        q = pv.rope_append(qt, knt, vnt, pos_t, ctx_t, kt, vt, base=w.rope_base, status=st)
+        pv.verify_attn(q, kt, vt, ctx_t, want_lse=False, ws=ws_t, status=st)
+        pv.spec_accept(dl, tl, tok, ua, us, 1.0, ws=ws_t, status=st)
+
+    def draft_steps():
+        for i in range(gamma):
+            q = pv.rope_append(qd, knd, vnd, pos_d[i], ctx_d[i], kd, vd, base=w.rope_base, status=st)
+            pv.verify_attn(q, kd, vd, ctx_d[i], want_mass=False, want_lse=False, ws=ws_d, status=st)
+
+    graphs = {}
+    for name, fn, s in (("target", target_round, s_t), ("draft", draft_steps, s_d)):
+        with torch.cuda.stream(s):
+            fn()                                  # sizes the workspaces, loads kernels
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            fn()
+        torch.cuda.synchronize()
+        graphs[name] = (g, s)
+
+    def timed(names):
+        for _ in range(3):
+            for n in names:
+                g, s = graphs[n]
+                with torch.cuda.stream(s):
+                    g.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            for n in names:
+                g, s = graphs[n]
+                with torch.cuda.stream(s):
+                    g.replay()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e6 / reps
+
+    t_t = timed(["target"])
+    t_d = timed(["draft"])
+    t_both = timed(["target", "draft"])
+    rec = {"workload": f"llava7b heads, gamma {gamma}: draft {gamma} x (rope + verify T=1) over "
+                       f"{n_c} rows on 32 CUs beside target rope + verify T={T} over {n_prompt} rows "
+                       f"+ accept (V {V}) on 224 CUs",
+           "target_us": round(t_t, 2), "draft_us": round(t_d, 2), "both_us": round(t_both, 2),
+           "overlap_frac": round((t_t + t_d - t_both) / min(t_t, t_d), 3),
+           "timing": f"HIP graph per stream, {reps} rounds between host synchronisations",
+           "device_status": int(st.item())}
+    pv.set_stream_cu_budget(s_t, 0)
+    pv.set_stream_cu_budget(s_d, 0)
+    del graphs, ws_t, ws_d, kt, vt, kd, vd
+    torch.cuda.empty_cache()
+    return rec
+
+
 def tiles(w):
     """16-row MFMA tiles per workgroup for the packed query rows of a KV head."""
     rtt = -(-w.group * w.T // 16)
@@ -733,7 +835,7 @@ def main():
     torch.cuda.empty_cache()
 
     others = None
-    cossim = rope = paged = None
+    cossim = rope = paged = overlap = None
     if not args.no_extra and graph_used:
         others = {}
         for name in OTHER_CONFIGS:
@@ -747,6 +849,8 @@ def main():
         log(f"rope_append: {rope['us']} us")
         paged = paged_record(torch, pv, W, dev)
         log(f"paged verify: padded {paged['padded_us']} us, paged {paged['paged']}")
+        overlap = overlap_record(torch, pv, W, dev)
+        log(f"stage II overlap: {overlap}")
 
     rec = {
         "metric": METRIC,
@@ -790,6 +894,7 @@ def main():
         "cossim": cossim,
         "rope_append": rope,
         "paged_kv": paged,
+        "stage2_overlap": overlap,
         "cpu_baseline": cpu,
         "device_status": status,
     }

@@ -34,8 +34,34 @@
  *     clamps it into range (so memory is never touched out of bounds) and, if
  *     `status` is non-NULL, ORs PVLM_DEV_RANGE into *status.
  *   - Outputs must not alias inputs.  Optional outputs may be NULL.
- *   - No global mutable state: calls are re-entrant; a workspace buffer must
- *     not be shared by two calls in flight at the same time.
+ *   - Calls are re-entrant; a workspace buffer must not be shared by two calls
+ *     in flight at the same time.  The library's only mutable state is the
+ *     per-stream compute-unit budgets below and the fixed scratch of
+ *     pvlm_verify_attn_noalloc.
+ *   - Workgroups that wait on each other.  pvlm_verify_attn(_paged), top-k
+ *     rows longer than 16384 scores and pvlm_spec_accept split their work
+ *     over workgroups of one launch that exchange partial results and wait
+ *     for each other (bounded waits: a wait that gives up sets
+ *     PVLM_DEV_TIMEOUT, and the results are invalid).  Every workgroup must
+ *     therefore be resident at once.  Each call checks before launching that
+ *     its grid fits the device (the runtime's occupancy per compute unit
+ *     times the compute units it plans for; PVLM_ERR_UNSUPPORTED otherwise).
+ *     Eager launches on a stream without a budget are cooperative launches,
+ *     whose co-residency the runtime guarantees.  Launches captured into a
+ *     graph, and launches on a budgeted stream, are ordinary launches: then
+ *     the caller guarantees that no other work holds compute units the call
+ *     needs for longer than the call itself runs.  Without budgets that means
+ *     the device to itself while such a call runs: no two of these calls in
+ *     flight at once on different streams.  Kernels that never wait (rope,
+ *     UV-Prune, short top-k rows, gather) and finish on their own may run
+ *     beside them: they only delay them.
+ *   - Compute-unit budgets (pvlm_set_stream_cu_budget): calls of the waiting
+ *     kind on a stream with a budget of C compute units plan their grids for
+ *     at most C workgroups.  Streams whose budgets sum to at most the
+ *     device's compute units may then run such calls at the same time, since
+ *     every workgroup of all of them fits at once (one workgroup per compute
+ *     unit at most; budgets are multiples of the XCD count, so a grid spreads
+ *     evenly over the XCDs the device deals workgroups to in turn).
  *   - Workspaces: zero-fill a workspace once before its first use.  Its first
  *     1 MiB holds the counters of the waits between workgroups, and every
  *     call leaves them in a consistent state (zero again, or, for verify's
@@ -80,6 +106,16 @@ typedef enum {
                                zero-fill the workspace again before reusing it) */
 #define PVLM_DEV_PLACEMENT 4 /* a workgroup ran on another XCD than the launch
                                planned for (results may be invalid)          */
+
+/* Compute-unit budget of `stream` on the current device: cus = 0 removes it
+ * (calls then plan for the whole device), otherwise a multiple of the
+ * device's XCD count (8 on MI355X) up to its compute units (a budget of all
+ * of them is the same as none).  PVLM_ERR_SHAPE for another value.  Set it
+ * before the stream's first call and clear it before destroying the stream
+ * (budgets are keyed by the stream handle).  pvlm_stream_cu_budget returns
+ * the stream's budget, 0 for none. */
+pvlm_status pvlm_set_stream_cu_budget(hipStream_t stream, int cus);
+int pvlm_stream_cu_budget(hipStream_t stream);
 
 const char* pvlm_status_string(pvlm_status s);
 /* Text of the last HIP error seen by a pvlm call on this host thread. */

@@ -26,6 +26,7 @@ PVLM_DEV_RANGE, PVLM_DEV_TIMEOUT, PVLM_DEV_PLACEMENT = 1, 2, 4
 
 EXPORTS = (
     "pvlm_status_string", "pvlm_last_hip_error", "pvlm_version",
+    "pvlm_set_stream_cu_budget", "pvlm_stream_cu_budget",
     "pvlm_verify_attn_workspace_size", "pvlm_verify_attn", "pvlm_verify_attn_paged",
     "pvlm_verify_attn_noalloc", "pvlm_verify_attn_noalloc_max_bytes",
     "pvlm_uvprune_workspace_size", "pvlm_uvprune_score", "pvlm_uvprune_criterion_cossim",
@@ -97,6 +98,8 @@ _SIGS = {
     "pvlm_status_string": (_c.c_char_p, [_I]),
     "pvlm_last_hip_error": (_c.c_char_p, []),
     "pvlm_version": (_I, []),
+    "pvlm_set_stream_cu_budget": (_I, [_P, _I]),
+    "pvlm_stream_cu_budget": (_I, [_P]),
     "pvlm_verify_attn_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I64, _I64]),
     "pvlm_verify_attn": (_I, [_I, _I, _I, _I, _I, _I, _I64, _I64, _F, _P, _P, _P, _P, _P, _P, _P,
                               _P, _SZ, _P, _P]),
@@ -288,6 +291,20 @@ def release_workspaces():
 
 
 # ------------------------------------------------------------------ calls --
+def set_stream_cu_budget(stream, cus: int):
+    """Give ``stream`` (a torch.cuda.Stream) a compute-unit budget: its verify,
+    long-row top-k and accept calls then plan for at most ``cus`` workgroups
+    and launch as ordinary launches, so they may run beside calls on streams
+    whose budgets sum with it to at most the device's compute units.  0
+    removes the budget."""
+    _check(lib().pvlm_set_stream_cu_budget(_P(stream.cuda_stream), int(cus)),
+           "pvlm_set_stream_cu_budget")
+
+
+def stream_cu_budget(stream) -> int:
+    return int(lib().pvlm_stream_cu_budget(_P(stream.cuda_stream)))
+
+
 def verify_attn_workspace_size(dtype: int, B, T, Hq, Hkv, D, n_cap, max_ctx) -> int:
     return int(lib().pvlm_verify_attn_workspace_size(dtype, B, T, Hq, Hkv, D, n_cap, max_ctx))
 
@@ -603,7 +620,8 @@ def spec_accept(draft_logits, target_logits, draft_tokens, u_accept, u_sample,
 
 __all__ = [
     "LIB_PATH", "EXPORTS", "PvlmError", "Workspace", "lib", "synchronize", "default_status",
-    "release_workspaces", "verify_attn", "verify_attn_paged", "verify_attn_noalloc",
+    "release_workspaces", "set_stream_cu_budget", "stream_cu_budget",
+    "verify_attn", "verify_attn_paged", "verify_attn_noalloc",
     "gather_kv_paged", "rope_append", "rope_append_paged",
     "verify_attn_workspace_size", "uvprune_score_mass", "uvprune_score_cossim",
     "uvprune_criterion_cossim", "topk_select", "gather_kv", "spec_accept",

@@ -668,7 +668,7 @@ extern "C" pvlm_status pvlm_spec_accept(int B, int gamma, int V, float temperatu
   if (st != PVLM_OK) return st;
   if (!ws || ws_bytes < p.bytes) return PVLM_ERR_WORKSPACE;
   DeviceInfo di;
-  st = device_info(&di);
+  st = device_info(&di, stream);
   if (st != PVLM_OK) return st;
   char* wsb = static_cast<char*>(ws);
   AArgs a;
@@ -713,7 +713,7 @@ extern "C" pvlm_status pvlm_spec_accept(int B, int gamma, int V, float temperatu
           : (dp == kDrawPerMin ? reinterpret_cast<const void*>(accept_kernel<false, kDrawPerMin>)
                                : reinterpret_cast<const void*>(accept_kernel<false, kDrawPerMax>));
   {
-    const pvlm_status cs = check_coresident(kern, grid, kAccThreads, 0);
+    const pvlm_status cs = check_coresident(kern, grid, kAccThreads, 0, stream);
     if (cs != PVLM_OK) return cs;
   }
   PVLM_HIP(launch_coresident(kern, dim3(grid), dim3(kAccThreads), args, 0, stream));

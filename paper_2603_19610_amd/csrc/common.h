@@ -26,11 +26,14 @@ pvlm_status hip_check(hipError_t e);
   } while (0)
 
 struct DeviceInfo {
-  int cus = 0;
+  int cus = 0;   // compute units a call may plan for: the device's, or the stream's budget
   int xcds = 0;  // accelerator complex dies (workgroup i runs on die i % xcds); 0 = unknown
+  bool budgeted = false;  // the stream has a compute-unit budget (pvlm_set_stream_cu_budget)
 };
-// Compute-unit and XCD counts of the current device (queried once per device).
+// Compute-unit and XCD counts of the current device (queried once per
+// device); with a stream, its compute-unit budget when it has one.
 pvlm_status device_info(DeviceInfo* out);
+pvlm_status device_info(DeviceInfo* out, hipStream_t stream);
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -54,15 +57,18 @@ hipError_t allow_dynamic_lds(const void* kernel, int bytes);
 
 // PVLM_OK when `grid` workgroups of `kernel` (with `block` threads and `lds`
 // dynamic LDS bytes) fit on the current device at once: the occupancy the
-// runtime reports per compute unit times the compute units.  Every launch
-// whose workgroups wait on each other checks this before launching.
-pvlm_status check_coresident(const void* kernel, int grid, int block, int lds);
+// runtime reports per compute unit times the compute units (the stream's
+// budget when it has one).  Every launch whose workgroups wait on each other
+// checks this before launching.
+pvlm_status check_coresident(const void* kernel, int grid, int block, int lds,
+                             hipStream_t stream);
 
 // Launch a kernel whose workgroups wait on each other: cooperatively (the
 // runtime guarantees co-residency), or as an ordinary launch while the stream
-// is being captured into a graph (then co-residency rests on check_coresident
-// and on the device not being shared, see pvlm.h).  Grids are at most one
-// workgroup per CU.
+// is being captured into a graph or has a compute-unit budget (then
+// co-residency rests on check_coresident and on the caller's contract: the
+// device not shared, or the budgets of overlapping streams within its compute
+// units).  Grids are at most one workgroup per CU.
 hipError_t launch_coresident(const void* kernel, dim3 grid, dim3 block, void** args, int lds,
                              hipStream_t stream);
 

@@ -21,6 +21,8 @@ std::mutex g_lds_mu;
 std::set<std::pair<const void*, int>> g_lds_done;
 std::mutex g_occ_mu;
 std::map<std::tuple<int, const void*, int, int>, int> g_occ;  // (device, kernel, block, lds) -> per CU
+std::mutex g_budget_mu;
+std::map<std::pair<int, hipStream_t>, int> g_budget;  // (device, stream) -> compute units
 }  // namespace
 
 hipError_t allow_dynamic_lds(const void* kernel, int bytes) {
@@ -31,7 +33,8 @@ hipError_t allow_dynamic_lds(const void* kernel, int bytes) {
   return e;
 }
 
-pvlm_status check_coresident(const void* kernel, int grid, int block, int lds) {
+pvlm_status check_coresident(const void* kernel, int grid, int block, int lds,
+                             hipStream_t stream) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_check(e);
@@ -49,7 +52,7 @@ pvlm_status check_coresident(const void* kernel, int grid, int block, int lds) {
     g_occ[key] = per_cu;
   }
   DeviceInfo di;
-  const pvlm_status st = device_info(&di);
+  const pvlm_status st = device_info(&di, stream);
   if (st != PVLM_OK) return st;
   return (int64_t)per_cu * di.cus >= grid ? PVLM_OK : PVLM_ERR_UNSUPPORTED;
 }
@@ -59,8 +62,11 @@ hipError_t launch_coresident(const void* kernel, dim3 grid, dim3 block, void** a
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
   hipError_t e = hipStreamIsCapturing(stream, &cap);
   if (e != hipSuccess) return e;
-  if (cap == hipStreamCaptureStatusNone)
-    return hipLaunchCooperativeKernel(kernel, grid, block, args, lds, stream);
+  if (cap == hipStreamCaptureStatusNone) {
+    DeviceInfo di;
+    if (device_info(&di, stream) != PVLM_OK) return hipErrorInvalidDevice;
+    if (!di.budgeted) return hipLaunchCooperativeKernel(kernel, grid, block, args, lds, stream);
+  }
   return hipLaunchKernel(kernel, grid, block, args, lds, stream);
 }
 
@@ -94,6 +100,22 @@ pvlm_status device_info(DeviceInfo* out) {
   }
   out->cus = g_cus[dev];
   out->xcds = g_xcds[dev];
+  out->budgeted = false;
+  return PVLM_OK;
+}
+
+pvlm_status device_info(DeviceInfo* out, hipStream_t stream) {
+  const pvlm_status st = device_info(out);
+  if (st != PVLM_OK) return st;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_check(e);
+  std::lock_guard<std::mutex> lock(g_budget_mu);
+  auto it = g_budget.find({dev, stream});
+  if (it != g_budget.end() && it->second < out->cus) {
+    out->cus = it->second;
+    out->budgeted = true;
+  }
   return PVLM_OK;
 }
 
@@ -114,3 +136,23 @@ extern "C" const char* pvlm_status_string(pvlm_status s) {
 extern "C" const char* pvlm_last_hip_error(void) { return pvlm::g_last_hip_error.c_str(); }
 
 extern "C" int pvlm_version(void) { return 1; }
+
+extern "C" pvlm_status pvlm_set_stream_cu_budget(hipStream_t stream, int cus) {
+  pvlm::DeviceInfo di;
+  const pvlm_status st = pvlm::device_info(&di);
+  if (st != PVLM_OK) return st;
+  const int step = di.xcds > 0 ? di.xcds : 1;
+  if (cus != 0 && (cus < step || cus > di.cus || cus % step != 0)) return PVLM_ERR_SHAPE;
+  int dev = 0;
+  PVLM_HIP(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> lock(pvlm::g_budget_mu);
+  if (cus == 0 || cus == di.cus) pvlm::g_budget.erase({dev, stream});
+  else pvlm::g_budget[{dev, stream}] = cus;
+  return PVLM_OK;
+}
+
+extern "C" int pvlm_stream_cu_budget(hipStream_t stream) {
+  pvlm::DeviceInfo di;
+  if (pvlm::device_info(&di, stream) != PVLM_OK) return 0;
+  return di.budgeted ? di.cus : 0;
+}

@@ -515,7 +515,8 @@ struct TPlan {
   size_t off_arrive, off_gen, off_hist, off_res, off_cnt, bytes;
 };
 
-pvlm_status plan_topk(int B, int64_t m_cap, TPlan* p) {
+// stream / with_stream: as for verify's plan (the stream's compute-unit budget).
+pvlm_status plan_topk(int B, int64_t m_cap, TPlan* p, hipStream_t stream, bool with_stream) {
   if (B < 1 || m_cap < 1 || m_cap > ((int64_t)1 << 30)) return PVLM_ERR_SHAPE;
   if (m_cap <= kSmallMax) {  // one workgroup per row, no workspace
     p->NW = 1;
@@ -524,7 +525,7 @@ pvlm_status plan_topk(int B, int64_t m_cap, TPlan* p) {
     return PVLM_OK;
   }
   DeviceInfo di;
-  pvlm_status st = device_info(&di);
+  pvlm_status st = with_stream ? device_info(&di, stream) : device_info(&di);
   if (st != PVLM_OK) return st;
   if (B > di.cus) return PVLM_ERR_UNSUPPORTED;
   const int nw_max = di.cus / B;  // co-resident: at most one workgroup per CU
@@ -556,7 +557,7 @@ using namespace pvlm;
 
 extern "C" size_t pvlm_topk_workspace_size(int B, int64_t m_cap) {
   TPlan p;
-  if (plan_topk(B, m_cap, &p) != PVLM_OK) return 0;
+  if (plan_topk(B, m_cap, &p, nullptr, false) != PVLM_OK) return 0;
   return p.bytes;
 }
 
@@ -567,7 +568,7 @@ extern "C" pvlm_status pvlm_topk_select(int B, int64_t m_cap, const int32_t* m, 
   if (B < 1 || m_cap < 1 || k_cap < 0 || m_cap > ((int64_t)1 << 30)) return PVLM_ERR_SHAPE;
   if (k_cap == 0) return PVLM_OK;
   TPlan p;
-  pvlm_status st = plan_topk(B, m_cap, &p);
+  pvlm_status st = plan_topk(B, m_cap, &p, stream, true);
   if (st != PVLM_OK) return st;
   if (p.bytes > 0 && (!ws || ws_bytes < p.bytes)) return PVLM_ERR_WORKSPACE;
   TArgs a = {};
@@ -599,7 +600,7 @@ extern "C" pvlm_status pvlm_topk_select(int B, int64_t m_cap, const int32_t* m, 
                          ? reinterpret_cast<const void*>(topk_kernel<true>)
                          : reinterpret_cast<const void*>(topk_kernel<false>);
   {
-    const pvlm_status cs = check_coresident(kern, B * p.NW, kTopkThreads, 0);
+    const pvlm_status cs = check_coresident(kern, B * p.NW, kTopkThreads, 0, stream);
     if (cs != PVLM_OK) return cs;
   }
   PVLM_HIP(launch_coresident(kern, dim3(B * p.NW), dim3(kTopkThreads), args, 0, stream));

@@ -1495,6 +1495,7 @@ struct VPlan {
   bool resident, mfma;
   int lds_dyn;
   int xcds;
+  bool budgeted;  // planned for a stream's compute-unit budget
   size_t off_cnt_s, off_mcnt, off_stats, off_opart, off_mpart, bytes;
 };
 
@@ -1532,8 +1533,11 @@ int lds_bytes(int dt, int D, int RT, bool resident) {
   return b;
 }
 
+// stream: the launch's stream, whose compute-unit budget bounds the plan;
+// with_stream false plans for the whole device (workspace sizes, an upper
+// bound for every budget).
 pvlm_status plan_verify(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int64_t n_cap,
-                        int64_t max_ctx, VPlan* p) {
+                        int64_t max_ctx, VPlan* p, hipStream_t stream, bool with_stream) {
   if (dt != PVLM_F32 && dt != PVLM_BF16) return PVLM_ERR_UNSUPPORTED;
   if (B < 1 || T < 1 || Hq < 1 || Hkv < 1 || n_cap < 1) return PVLM_ERR_SHAPE;
   if (T > 32 || Hq % Hkv != 0 || (D != 64 && D != 128)) return PVLM_ERR_UNSUPPORTED;
@@ -1548,10 +1552,11 @@ pvlm_status plan_verify(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int
   p->mfma = dt == PVLM_BF16;
   p->groups = B * Hkv * p->RG;
   DeviceInfo di;
-  pvlm_status st = device_info(&di);
+  pvlm_status st = with_stream ? device_info(&di, stream) : device_info(&di);
   if (st != PVLM_OK) return st;
   const int W = di.cus;  // one workgroup per CU (registers / LDS bound)
   p->xcds = di.xcds;
+  p->budgeted = di.budgeted;
   p->per_launch = p->groups < W ? p->groups : W;
   int splits = W / p->per_launch;
   if (splits < 1) splits = 1;
@@ -1595,7 +1600,7 @@ using namespace pvlm;
 extern "C" size_t pvlm_verify_attn_workspace_size(pvlm_dtype dt, int B, int T, int Hq, int Hkv,
                                                   int D, int64_t n_cap, int64_t max_ctx) {
   VPlan p;
-  if (plan_verify(dt, B, T, Hq, Hkv, D, n_cap, max_ctx, &p) != PVLM_OK) return 0;
+  if (plan_verify(dt, B, T, Hq, Hkv, D, n_cap, max_ctx, &p, nullptr, false) != PVLM_OK) return 0;
   return p.bytes;
 }
 
@@ -1610,7 +1615,7 @@ pvlm_status verify_run(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int6
   if (!q || !k_cache || !v_cache || !ctx_len || !out) return PVLM_ERR_NULL;
   if (!(scale > 0.f) || !std::isfinite(scale)) return PVLM_ERR_SHAPE;
   VPlan p;
-  pvlm_status st = plan_verify(dt, B, T, Hq, Hkv, D, n_cap, max_ctx, &p);
+  pvlm_status st = plan_verify(dt, B, T, Hq, Hkv, D, n_cap, max_ctx, &p, stream, true);
   if (st != PVLM_OK) return st;
   if (!ws) return PVLM_ERR_WORKSPACE;
   if (ws_bytes < p.bytes) return PVLM_ERR_WORKSPACE;
@@ -1655,7 +1660,7 @@ pvlm_status verify_run(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int6
   for (int local = 0; local < 2; ++local) {
     const void* k = reinterpret_cast<const void*>(pick_kernel(dt, D, p.RT, p.resident, local != 0));
     PVLM_HIP(allow_dynamic_lds(k, p.lds_dyn));
-    const pvlm_status cs = check_coresident(k, p.grid, kThreads, p.lds_dyn);
+    const pvlm_status cs = check_coresident(k, p.grid, kThreads, p.lds_dyn, stream);
     if (cs != PVLM_OK) return cs;
   }
   for (int g0 = 0; g0 < p.groups; g0 += p.per_launch) {
@@ -1666,7 +1671,10 @@ pvlm_status verify_run(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int6
     // group's workgroups then share one XCD (and so one L2), the group's
     // exchanges use plain loads and stores (fp32 path: always device-coherent).
     a.xmap = p.xcds > 0 && a.grid % p.xcds == 0 ? p.xcds : 1;
-    a.local = p.mfma && p.xcds > 0 && a.xmap == p.xcds && (a.grid / a.xmap) % p.splits == 0;
+    // (not on a budgeted stream: another stream's calls then run beside this
+    // one, and the same-XCD mode is kept to a device this call has alone)
+    a.local = p.mfma && !p.budgeted && p.xcds > 0 && a.xmap == p.xcds &&
+              (a.grid / a.xmap) % p.splits == 0;
     VKernel kern = pick_kernel(dt, D, p.RT, p.resident, a.local != 0);
     PVLM_HIP(allow_dynamic_lds(reinterpret_cast<const void*>(kern), p.lds_dyn));
     void* args[] = {&a};
@@ -1720,7 +1728,7 @@ extern "C" pvlm_status pvlm_verify_attn_noalloc(pvlm_dtype dt, int B, int T, int
   if (!q || !k_cache || !v_cache || !ctx_len || !out) return PVLM_ERR_NULL;
   if (!(scale > 0.f) || !std::isfinite(scale)) return PVLM_ERR_SHAPE;
   VPlan p;
-  pvlm_status st = plan_verify(dt, B, T, Hq, Hkv, D, n_cap, max_ctx, &p);
+  pvlm_status st = plan_verify(dt, B, T, Hq, Hkv, D, n_cap, max_ctx, &p, stream, true);
   if (st != PVLM_OK) return st;
   if (p.bytes > kScratchBytes) return PVLM_ERR_WORKSPACE;  // beyond the fixed scratch
   int dev = 0;

@@ -85,3 +85,59 @@ def test_default_workspaces_are_per_stream():
     assert pv._ws_cache[key(s1)].buf.data_ptr() != pv._ws_cache[key(s2)].buf.data_ptr()
     for o in outs:
         assert torch.equal(o[0], ref[0]) and torch.equal(o[1], ref[1]) and torch.equal(o[2], ref[2])
+
+
+@pytest.mark.parametrize("budgets", [(224, 32), (128, 128)])
+def test_two_budgeted_streams_run_waiting_calls_together(budgets):
+    """Verify (72B layer) on one budgeted stream and verify + accept (7B
+    layer) on another, enqueued together and repeated: every result equals
+    the same call's result on a lone stream with the same budget, and no
+    wait gives up."""
+    dev = torch.device("cuda", 0)
+    w72, w7 = W.WORKLOADS["llava72b"], W.WORKLOADS["llava7b"]
+    a_in = W.make_verify_inputs(w72, layer=1)
+    b_in = W.make_verify_inputs(w7, layer=1)
+    A = [to_dev(x) for x in (a_in.q, a_in.k, a_in.v, a_in.ctx_len)]
+    Bt = [to_dev(x) for x in (b_in.q, b_in.k, b_in.v, b_in.ctx_len)]
+    rng = np.random.default_rng(3)
+    Vv, g = 152064, 5
+    dl = torch.from_numpy(rng.standard_normal((1, g, Vv)).astype(np.float32)).to(dev)
+    tl = torch.from_numpy(rng.standard_normal((1, g + 1, Vv)).astype(np.float32)).to(dev)
+    tok = torch.from_numpy(rng.integers(0, Vv, (1, g)).astype(np.int32)).to(dev)
+    ua = torch.from_numpy(rng.random((1, g))).to(dev)
+    us = torch.from_numpy(rng.random(1)).to(dev)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    pv.set_stream_cu_budget(s1, budgets[0])
+    pv.set_stream_cu_budget(s2, budgets[1])
+    ws1, ws2 = pv.Workspace(dev), pv.Workspace(dev)
+    st1 = torch.zeros(1, dtype=torch.int32, device=dev)
+    st2 = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def run1():
+        return pv.verify_attn(*A, ws=ws1, status=st1)
+
+    def run2():
+        o = pv.verify_attn(*Bt, ws=ws2, status=st2)
+        n, y, _ = pv.spec_accept(dl, tl, tok, ua, us, 1.0, ws=ws2, status=st2)
+        return o + (n, y)
+
+    note(f"budgets {budgets}: each stream alone")
+    with torch.cuda.stream(s1):
+        r1 = [t.clone() for t in run1()]
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s2):
+        r2 = [t.clone() for t in run2()]
+    torch.cuda.synchronize()
+    assert int(st1.item()) == 0 and int(st2.item()) == 0
+    for rep in range(5):
+        note(f"budgets {budgets}: both streams together, round {rep}")
+        with torch.cuda.stream(s1):
+            x1 = run1()
+        with torch.cuda.stream(s2):
+            x2 = run2()
+        torch.cuda.synchronize()
+        assert int(st1.item()) == 0 and int(st2.item()) == 0
+        assert all(torch.equal(a, b) for a, b in zip(x1, r1))
+        assert all(torch.equal(a, b) for a, b in zip(x2, r2))
+    pv.set_stream_cu_budget(s1, 0)
+    pv.set_stream_cu_budget(s2, 0)
