@@ -329,9 +329,9 @@ class Step:
                             lse=self.lse, ws=self.ws_v, status=self.status)
 
     def prune(self):
-        self.pv.uvprune_score_mass(self.crit, self.m_t, score=self.score, status=self.status)
-        self.pv.topk_select(self.score, self.m_t, self.k_t, self.k_cap, idx=self.idx,
-                            status=self.status)
+        # UV-Prune's MASS variation and top-k in one launch
+        self.pv.uvprune_topk_mass(self.crit, self.m_t, self.k_t, self.k_cap, score=self.score,
+                                  idx=self.idx, status=self.status)
 
     def gather(self):
         self.pv.gather_kv(self.Kc, self.Vc, self.idx, self.k_t, self.tail_b, self.tail_l,
@@ -728,11 +728,21 @@ def main():
         f"{time.time() - t0:.1f} s")
 
     if args.verify_only:
-        for r in range(args.verify_only):
-            st.verify(r % NL)
+        # the launches as the bench times them: one graph of N verify
+        # launches (one per layer, cycling), replayed once; captured without
+        # an eager run, so the process makes no cooperative launch
+        st.ws_v.get(pv.verify_attn_workspace_size(
+            pv.PVLM_BF16 if w.dtype == "bf16" else pv.PVLM_F32, w.batch, w.T, w.hq, w.hkv,
+            w.head_dim, w.n_cap(), st.max_ctx))
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=torch.cuda.Stream()):
+            for r in range(args.verify_only):
+                st.verify(r % NL)
+        g.replay()
         torch.cuda.synchronize()
         print(json.dumps({"verify_only": args.verify_only, "status": int(st.status.item())}))
-        del st
+        del g, st
         teardown(torch, pv)
         return
 

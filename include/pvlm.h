@@ -348,6 +348,26 @@ pvlm_status pvlm_topk_select(int B, int64_t m_cap, const int32_t* m, const int32
                              size_t ws_bytes, int32_t* status, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * pvlm_uvprune_topk_mass -- the MASS form of pvlm_uvprune_score followed by
+ * pvlm_topk_select, in one launch: Eq. (average_similarity) over a criterion
+ * stack, score[b,i] = crit_stack[L][b][i] - crit_stack[0][b][i] (one fp32
+ * subtraction, as pvlm_uvprune_score(MASS) rounds it), then Eq.
+ * (topk_selection) over those scores.  The kept indices equal those of the
+ * two calls bit for bit.
+ *   crit_stack [L+1][B][m_cap] fp32, L >= 1; m, k [B] int32 device;
+ *   score      [B][m_cap] fp32 output or NULL (written as pvlm_uvprune_score
+ *              writes it, 0 past m[b]);
+ *   idx        [B][k_cap] int32 output, as pvlm_topk_select (may be NULL
+ *              when k_cap = 0: then only the scores are written).
+ * Workspace, limits and errors are pvlm_topk_select's
+ * (pvlm_topk_workspace_size(B, m_cap)); PVLM_ERR_SHAPE also for L < 1.
+ * ---------------------------------------------------------------------- */
+pvlm_status pvlm_uvprune_topk_mass(int B, int L, int64_t m_cap, const int32_t* m,
+                                   const float* crit_stack, const int32_t* k, int32_t k_cap,
+                                   float* score, int32_t* idx, void* ws, size_t ws_bytes,
+                                   int32_t* status, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * pvlm_gather_kv -- compact draft cache (Sec. 4.2 Stage I: the draft holds
  * [V*, X]).  For every layer l, batch b and KV head g:
  *   dst[l,b,g,r]      = src[l,b,g,idx[b,r]]             r < k[b]

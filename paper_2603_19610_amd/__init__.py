@@ -30,7 +30,7 @@ EXPORTS = (
     "pvlm_verify_attn_workspace_size", "pvlm_verify_attn", "pvlm_verify_attn_paged",
     "pvlm_verify_attn_noalloc", "pvlm_verify_attn_noalloc_max_bytes",
     "pvlm_uvprune_workspace_size", "pvlm_uvprune_score", "pvlm_uvprune_criterion_cossim",
-    "pvlm_topk_workspace_size", "pvlm_topk_select",
+    "pvlm_topk_workspace_size", "pvlm_topk_select", "pvlm_uvprune_topk_mass",
     "pvlm_gather_kv", "pvlm_gather_kv_paged",
     "pvlm_spec_accept_workspace_size", "pvlm_spec_accept",
     "pvlm_rope_append", "pvlm_rope_append_paged",
@@ -115,6 +115,7 @@ _SIGS = {
                                            _P, _P]),
     "pvlm_topk_workspace_size": (_SZ, [_I, _I64]),
     "pvlm_topk_select": (_I, [_I, _I64, _P, _P, _I, _P, _P, _P, _SZ, _P, _P]),
+    "pvlm_uvprune_topk_mass": (_I, [_I, _I, _I64, _P, _P, _P, _I, _P, _P, _P, _SZ, _P, _P]),
     "pvlm_gather_kv": (_I, [_I, _I, _I, _I, _I, _I64, _P, _P, _P, _P, _I, _P, _P, _I64, _P, _P,
                             _P, _P]),
     "pvlm_gather_kv_paged": (_I, [_I, _I, _I, _I, _I, _I, _I, _I64, _P, _P, _P, _P, _P, _I, _P,
@@ -512,6 +513,33 @@ def topk_select(score, m, k, k_cap: int, *, idx=None, ws=None, status=None):
     return idx
 
 
+def uvprune_topk_mass(crit_stack, m, k, k_cap: int, *, score=None, want_score: bool = True,
+                      idx=None, ws=None, status=None):
+    """pvlm_uvprune_topk_mass: the MASS score crit_stack[L] - crit_stack[0]
+    ([L+1][B][m_cap] fp32) and its top-k in one launch.  Returns (score or
+    None, idx)."""
+    _need(crit_stack, "crit_stack", torch.float32)
+    dev = crit_stack.device
+    _need(m, "m", torch.int32, dev)
+    _need(k, "k", torch.int32, dev)
+    L1, B, m_cap = crit_stack.shape
+    if score is None and want_score:
+        score = torch.empty((B, m_cap), dtype=torch.float32, device=dev)
+    if score is not None:
+        _need(score, "score", torch.float32, dev)
+    if idx is None:
+        idx = torch.empty((B, k_cap), dtype=torch.int32, device=dev)
+    _need(idx, "idx", torch.int32, dev)
+    need = int(lib().pvlm_topk_workspace_size(B, m_cap))
+    wsb = (ws or _default_ws("topk")).get(need) if need else None
+    st = lib().pvlm_uvprune_topk_mass(B, L1 - 1, m_cap, _ptr(m), _ptr(crit_stack), _ptr(k),
+                                      int(k_cap), _ptr(score), _ptr(idx), _ptr(wsb),
+                                      0 if wsb is None else wsb.numel(), _ptr(_status(status)),
+                                      _stream())
+    _check(st, "pvlm_uvprune_topk_mass")
+    return score, idx
+
+
 def gather_kv(k_cache, v_cache, idx, k, tail_begin, tail_len, dst_cap: int, *, k_dst=None,
               v_dst=None, status=None):
     """Compact cache: kept rows then tail rows.  Caches are [B][Hkv][n_cap][D]
@@ -624,7 +652,7 @@ __all__ = [
     "verify_attn", "verify_attn_paged", "verify_attn_noalloc",
     "gather_kv_paged", "rope_append", "rope_append_paged",
     "verify_attn_workspace_size", "uvprune_score_mass", "uvprune_score_cossim",
-    "uvprune_criterion_cossim", "topk_select", "gather_kv", "spec_accept",
+    "uvprune_criterion_cossim", "topk_select", "uvprune_topk_mass", "gather_kv", "spec_accept",
     "PVLM_F32", "PVLM_BF16", "PVLM_CRIT_MASS", "PVLM_CRIT_COSSIM", "PVLM_DEV_RANGE",
     "PVLM_DEV_TIMEOUT", "PVLM_DEV_PLACEMENT",
 ]

@@ -93,7 +93,9 @@ __device__ __forceinline__ void find_digit(const int* hist, int need, F found) {
 }
 
 struct TArgs {
-  const float* score;
+  const float* score;    // scores, or (fused MASS form) crit^L
+  const float* sub;      // fused MASS form: crit^0, subtracted from crit^L; else NULL
+  float* score_out;      // fused MASS form: the scores written out (nullable)
   const int32_t* m;
   const int32_t* k;
   int32_t* idx;
@@ -108,6 +110,15 @@ struct TArgs {
 };
 
 constexpr int kLine = (int)(kSyncLine / sizeof(int));
+
+// Entry i of a row (row offset `off`): the score, or in the fused MASS form
+// the UV-Prune variation crit^L - crit^0 of Eq. (average_similarity),
+// rounded exactly as pvlm_uvprune_score(MASS) rounds it (one fp32 subtraction).
+template <bool FUSED>
+__device__ __forceinline__ float score_at(const TArgs& a, size_t off, int64_t i) {
+  if constexpr (FUSED) return a.score[off + i] - a.sub[off + i];
+  else return a.score[off + i];
+}
 
 // A pair of ints exchanged between workgroups as one device-coherent 64-bit
 // access (8-byte aligned): one round trip for both, and a consistent pair.
@@ -154,7 +165,7 @@ __device__ __forceinline__ void row_barrier(const TArgs& a, int b, int p, unsign
 // REG: the slice (at most kTopkThreads * kPerThread scores) is read once into
 // registers, thread t holding the scores s0 + kPerThread*t + e; otherwise it
 // is read again from memory for every pass, in chunks of that size.
-template <bool REG>
+template <bool REG, bool FUSED>
 __global__ void __launch_bounds__(kTopkThreads) topk_kernel(TArgs a) {
   constexpr int kChunk = kTopkThreads * kPerThread;
   __shared__ int hist[256];
@@ -162,7 +173,7 @@ __global__ void __launch_bounds__(kTopkThreads) topk_kernel(TArgs a) {
   __shared__ int s_flag, s_res[2];
   const int b = blockIdx.x / a.NW, j = blockIdx.x % a.NW;
   const int tid = threadIdx.x;
-  const float* sc = a.score + (size_t)b * a.m_cap;
+  const size_t roff = (size_t)b * a.m_cap;
   int32_t* out = a.idx + (size_t)b * a.k_cap;
   // the generation at launch start, read before this workgroup first arrives
   // (only thread 0 arrives and waits)
@@ -184,12 +195,30 @@ __global__ void __launch_bounds__(kTopkThreads) topk_kernel(TArgs a) {
     for (int r = kb + tid; r < a.k_cap; r += kTopkThreads) out[r] = -1;
   const int s0 = min(mb, j * a.slice), s1 = min(mb, s0 + a.slice);
   int* hrow = a.hist + (size_t)b * a.NW * 256;
+  if constexpr (FUSED) {  // the scores of this workgroup's share of the row (0 past m[b])
+    if (a.score_out && !REG) {
+      const int64_t e1 = min((int64_t)(j + 1) * a.slice, a.m_cap);
+      for (int64_t i = (int64_t)j * a.slice + tid; i < e1; i += kTopkThreads)
+        a.score_out[roff + i] = i < mb ? score_at<true>(a, roff, i) : 0.f;
+    } else if (a.score_out) {  // past m[b] only; the kept slice is written with its keys
+      const int64_t e0 = max((int64_t)j * a.slice, (int64_t)mb);
+      const int64_t e1 = min((int64_t)(j + 1) * a.slice, a.m_cap);
+      for (int64_t i = e0 + tid; i < e1; i += kTopkThreads) a.score_out[roff + i] = 0.f;
+    }
+  }
 
   uint32_t kr[kPerThread];
   if constexpr (REG) {
     const int i0 = s0 + tid * kPerThread;
 #pragma unroll
-    for (int e = 0; e < kPerThread; ++e) kr[e] = __float_as_uint(sc[min(i0 + e, s1 > 0 ? s1 - 1 : 0)]);
+    for (int e = 0; e < kPerThread; ++e)
+      kr[e] = __float_as_uint(score_at<FUSED>(a, roff, min(i0 + e, s1 > 0 ? s1 - 1 : 0)));
+    if constexpr (FUSED) {
+      if (a.score_out)
+#pragma unroll
+        for (int e = 0; e < kPerThread; ++e)
+          if (i0 + e < s1) a.score_out[roff + i0 + e] = __uint_as_float(kr[e]);
+    }
 #pragma unroll  // (clamped loads, all in flight together, then the keys)
     for (int e = 0; e < kPerThread; ++e) kr[e] = i0 + e < s1 ? rank_key(__uint_as_float(kr[e])) : 0u;
   }
@@ -201,7 +230,7 @@ __global__ void __launch_bounds__(kTopkThreads) topk_kernel(TArgs a) {
       for (int e = 0; e < kPerThread; ++e)
         if (e < nv) f(kr[e]);
     } else {
-      for (int i = s0 + tid; i < s1; i += kTopkThreads) f(rank_key(sc[i]));
+      for (int i = s0 + tid; i < s1; i += kTopkThreads) f(rank_key(score_at<FUSED>(a, roff, i)));
     }
   };
 
@@ -302,7 +331,7 @@ __global__ void __launch_bounds__(kTopkThreads) topk_kernel(TArgs a) {
       const bool valid = i0 + e < s1;
       if constexpr (REG) keys[e] = kr[e];
       else {
-        const float x = sc[min(i0 + e, s1 - 1)];  // clamped load (s1 > base >= 0)
+        const float x = score_at<FUSED>(a, roff, min(i0 + e, s1 - 1));  // clamped (s1 > base >= 0)
         keys[e] = valid ? rank_key(x) : 0u;
       }
       g += valid && keys[e] > tau;
@@ -350,7 +379,7 @@ constexpr int kSmallBins = 4096;
 constexpr int kHistCopies = 8;
 constexpr int kSmallLds = kSmallBins * (kHistCopies + 1) * 4;  // the copies, then the bin totals
 
-template <int PER>
+template <int PER, bool FUSED>
 __global__ void __launch_bounds__(kSmallThreads) topk_small_kernel(TArgs a) {
   extern __shared__ __align__(16) int hist[];  // [kSmallBins][kHistCopies], then [kSmallBins] totals
   int* bins = hist + kSmallBins * kHistCopies;
@@ -359,7 +388,7 @@ __global__ void __launch_bounds__(kSmallThreads) topk_small_kernel(TArgs a) {
   __shared__ int s_cnt[2][PER][kSmallWaves];  // per (round e, wave): keys above tau, equal to tau
   const int b = blockIdx.x, tid = threadIdx.x;
   const int lane = tid & 63, w = tid >> 6;
-  const float* sc = a.score + (size_t)b * a.m_cap;
+  const size_t roff = (size_t)b * a.m_cap;
   int32_t* out = a.idx + (size_t)b * a.k_cap;
   int mb = a.m[b], kb = a.k[b];
   bool bad = false;
@@ -374,12 +403,22 @@ __global__ void __launch_bounds__(kSmallThreads) topk_small_kernel(TArgs a) {
   }
   if (bad && tid == 0) dev_flag(a.status, PVLM_DEV_RANGE);
   for (int r = kb + tid; r < a.k_cap; r += kSmallThreads) out[r] = -1;
-  if (kb == 0) return;  // uniform across the workgroup
-  // unconditional loads (indices clamped; kb > 0 implies mb > 0) so that all
-  // PER are in flight together, then the entries past the row are zeroed
+  if (!FUSED && kb == 0) return;  // uniform across the workgroup
+  // unconditional loads (indices clamped into the row, or to entry 0 of an
+  // empty row) so that all PER are in flight together, then the entries past
+  // the row are zeroed
   float v[PER];
 #pragma unroll
-  for (int e = 0; e < PER; ++e) v[e] = sc[min(e * kSmallThreads + tid, mb - 1)];
+  for (int e = 0; e < PER; ++e) v[e] = score_at<FUSED>(a, roff, min(e * kSmallThreads + tid, max(mb - 1, 0)));
+  if constexpr (FUSED) {  // the scores written out (0 past m[b]), then the selection
+    if (a.score_out)
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        const int i = e * kSmallThreads + tid;
+        if (i < a.m_cap) a.score_out[roff + i] = i < mb ? v[e] : 0.f;
+      }
+    if (kb == 0) return;
+  }
   uint32_t kr[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) kr[e] = e * kSmallThreads + tid < mb ? rank_key(v[e]) : 0u;
@@ -561,18 +600,23 @@ extern "C" size_t pvlm_topk_workspace_size(int B, int64_t m_cap) {
   return p.bytes;
 }
 
-extern "C" pvlm_status pvlm_topk_select(int B, int64_t m_cap, const int32_t* m, const int32_t* k,
-                                        int32_t k_cap, const float* score, int32_t* idx, void* ws,
-                                        size_t ws_bytes, int32_t* status, hipStream_t stream) {
-  if (!m || !k || !score || !idx) return PVLM_ERR_NULL;
+namespace {
+// score: the scores, or with sub the fused MASS form (score = crit^L,
+// sub = crit^0, optional score_out).
+pvlm_status topk_run(int B, int64_t m_cap, const int32_t* m, const int32_t* k, int32_t k_cap,
+                     const float* score, const float* sub, float* score_out, int32_t* idx,
+                     void* ws, size_t ws_bytes, int32_t* status, hipStream_t stream) {
+  if (!m || !k || !score || (k_cap > 0 && !idx)) return PVLM_ERR_NULL;
   if (B < 1 || m_cap < 1 || k_cap < 0 || m_cap > ((int64_t)1 << 30)) return PVLM_ERR_SHAPE;
-  if (k_cap == 0) return PVLM_OK;
+  if (k_cap == 0 && !score_out) return PVLM_OK;
   TPlan p;
   pvlm_status st = plan_topk(B, m_cap, &p, stream, true);
   if (st != PVLM_OK) return st;
   if (p.bytes > 0 && (!ws || ws_bytes < p.bytes)) return PVLM_ERR_WORKSPACE;
   TArgs a = {};
   a.score = score;
+  a.sub = sub;
+  a.score_out = score_out;
   a.m = m;
   a.k = k;
   a.idx = idx;
@@ -582,10 +626,16 @@ extern "C" pvlm_status pvlm_topk_select(int B, int64_t m_cap, const int32_t* m, 
   a.NW = p.NW;
   a.slice = p.slice;
   void* args[] = {&a};
+  const bool fused = sub != nullptr;
   if (m_cap <= kSmallMax) {
-    const void* kern = m_cap <= kSmallThreads * 4   ? reinterpret_cast<const void*>(topk_small_kernel<4>)
-                       : m_cap <= kSmallThreads * 8 ? reinterpret_cast<const void*>(topk_small_kernel<8>)
-                                                    : reinterpret_cast<const void*>(topk_small_kernel<kSmallMaxPer>);
+    const int per = m_cap <= kSmallThreads * 4 ? 4 : (m_cap <= kSmallThreads * 8 ? 8 : kSmallMaxPer);
+    const void* kern =
+        per == 4 ? (fused ? reinterpret_cast<const void*>(topk_small_kernel<4, true>)
+                          : reinterpret_cast<const void*>(topk_small_kernel<4, false>))
+        : per == 8 ? (fused ? reinterpret_cast<const void*>(topk_small_kernel<8, true>)
+                            : reinterpret_cast<const void*>(topk_small_kernel<8, false>))
+                   : (fused ? reinterpret_cast<const void*>(topk_small_kernel<kSmallMaxPer, true>)
+                            : reinterpret_cast<const void*>(topk_small_kernel<kSmallMaxPer, false>));
     PVLM_HIP(allow_dynamic_lds(kern, kSmallLds));
     PVLM_HIP(hipLaunchKernel(kern, dim3(B), dim3(kSmallThreads), args, kSmallLds, stream));
     return PVLM_OK;
@@ -596,13 +646,34 @@ extern "C" pvlm_status pvlm_topk_select(int B, int64_t m_cap, const int32_t* m, 
   a.cnt = reinterpret_cast<int*>(wsb + p.off_cnt);
   a.arrive = reinterpret_cast<int*>(wsb + p.off_arrive);
   a.gen = reinterpret_cast<unsigned*>(wsb + p.off_gen);
-  const void* kern = p.slice <= kTopkThreads * kPerThread
-                         ? reinterpret_cast<const void*>(topk_kernel<true>)
-                         : reinterpret_cast<const void*>(topk_kernel<false>);
+  const bool reg = p.slice <= kTopkThreads * kPerThread;
+  const void* kern = reg ? (fused ? reinterpret_cast<const void*>(topk_kernel<true, true>)
+                                  : reinterpret_cast<const void*>(topk_kernel<true, false>))
+                         : (fused ? reinterpret_cast<const void*>(topk_kernel<false, true>)
+                                  : reinterpret_cast<const void*>(topk_kernel<false, false>));
   {
     const pvlm_status cs = check_coresident(kern, B * p.NW, kTopkThreads, 0, stream);
     if (cs != PVLM_OK) return cs;
   }
   PVLM_HIP(launch_coresident(kern, dim3(B * p.NW), dim3(kTopkThreads), args, 0, stream));
   return PVLM_OK;
+}
+}  // namespace
+
+extern "C" pvlm_status pvlm_topk_select(int B, int64_t m_cap, const int32_t* m, const int32_t* k,
+                                        int32_t k_cap, const float* score, int32_t* idx, void* ws,
+                                        size_t ws_bytes, int32_t* status, hipStream_t stream) {
+  return topk_run(B, m_cap, m, k, k_cap, score, nullptr, nullptr, idx, ws, ws_bytes, status,
+                  stream);
+}
+
+extern "C" pvlm_status pvlm_uvprune_topk_mass(int B, int L, int64_t m_cap, const int32_t* m,
+                                              const float* crit_stack, const int32_t* k,
+                                              int32_t k_cap, float* score, int32_t* idx, void* ws,
+                                              size_t ws_bytes, int32_t* status,
+                                              hipStream_t stream) {
+  if (!crit_stack) return PVLM_ERR_NULL;
+  if (B < 1 || L < 1 || m_cap < 1 || m_cap > ((int64_t)1 << 30)) return PVLM_ERR_SHAPE;
+  return topk_run(B, m_cap, m, k, k_cap, crit_stack + (size_t)L * B * m_cap, crit_stack, score, idx,
+                  ws, ws_bytes, status, stream);
 }

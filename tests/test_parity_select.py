@@ -113,3 +113,39 @@ def test_gather_rejects_out_of_range_index():
     got = kd.cpu().numpy()
     assert np.array_equal(got[0, :, 0], kc[0, :, 3]) and np.all(got[0, :, 1] == 0)
     assert np.array_equal(got[0, :, 3:7], kc[0, :, 60:64])
+
+
+@pytest.mark.parametrize("m_cap", [1, 1000, 12544, 16385, 40000, 400000])
+def test_uvprune_topk_mass_fused(m_cap):
+    """pvlm_uvprune_topk_mass equals pvlm_uvprune_score(MASS) followed by
+    pvlm_topk_select bit for bit (scores and indices), its scores are within
+    one fp32 rounding of the oracle's variation, and its indices are the
+    oracle's top-k of those scores.  400000 scores per row take the slice
+    path that re-reads the scores every pass."""
+    B, L = 3, 4
+    rng = np.random.default_rng(m_cap)
+    stack = rng.standard_normal((L + 1, B, m_cap)).astype(np.float32)
+    stack[:, :, ::7] = stack[:, :, :1]          # repeated values: ties in the scores
+    m = np.array([m_cap, max(1, m_cap - 17), max(1, m_cap // 3)], np.int32)
+    k = np.array([m[0] // 10, m[1], 0], np.int32)
+    k_cap = int(k.max()) + 5
+    note(f"uvprune_topk_mass m_cap={m_cap}")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    d_stack, d_m, d_k = to_dev(stack), to_dev(m), to_dev(k)
+    score, idx = pv.uvprune_topk_mass(d_stack, d_m, d_k, k_cap, status=status)
+    ref_score = pv.uvprune_score_mass(d_stack, d_m, status=status)
+    ref_idx = pv.topk_select(ref_score, d_m, d_k, k_cap, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    assert torch.equal(score.view(torch.int32), ref_score.view(torch.int32))
+    assert torch.equal(idx, ref_idx)
+    s_host = score.cpu().numpy()
+    o_score = oracle.uvprune_score_mass(stack.astype(np.float64), m)
+    assert np.all(np.abs(s_host - o_score) <= 6e-8 * np.abs(o_score) + 1e-45)
+    assert np.array_equal(idx.cpu().numpy(), oracle.topk_select(s_host, m, k, k_cap))
+    # without the score output, and with k_cap = 0 (scores only)
+    _, idx2 = pv.uvprune_topk_mass(d_stack, d_m, d_k, k_cap, want_score=False)
+    s3, _ = pv.uvprune_topk_mass(d_stack, d_m, torch.zeros_like(d_k), 0)
+    torch.cuda.synchronize()
+    assert torch.equal(idx2, ref_idx)
+    assert torch.equal(s3.view(torch.int32), ref_score.view(torch.int32))
