@@ -472,6 +472,52 @@ def cossim_record(torch, pv, W, dev):
     return rec
 
 
+def epilogue_record(torch, pv, W, dev):
+    """A prefill layer's epilogue at the 72B hidden shape (12,544 visual and
+    256 text rows, D_h 8192, bf16): the residual add with the layer's COSSIM
+    criterion fused in (pvlm_prefill_epilogue_cossim), against the add
+    followed by a separate criterion pass over the stored rows.  Bytes of the
+    fused call: prev and delta read, the sum written, once each."""
+    w = W.WORKLOADS["llava72b"]
+    B, m, n, Dh = w.batch, int(w.m_per_seq().max()), w.n_text, w.hidden
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(4242)
+    bf = torch.bfloat16
+    vp = torch.randn((B, m, Dh), device=dev, generator=gen).to(bf)
+    vd = torch.randn((B, m, Dh), device=dev, generator=gen).to(bf)
+    tp = torch.randn((B, n, Dh), device=dev, generator=gen).to(bf)
+    td = torch.randn((B, n, Dh), device=dev, generator=gen).to(bf)
+    vo, to = torch.empty_like(vp), torch.empty_like(tp)
+    crit = torch.empty((B, m), dtype=torch.float32, device=dev)
+    m_t = torch.full((B,), m, dtype=torch.int32, device=dev)
+    n_t = torch.full((B,), n, dtype=torch.int32, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    ws = pv.Workspace(dev)
+
+    def fused():
+        pv.prefill_epilogue_cossim(vp, vd, tp, td, m_t, n_t, vis_out=vo, txt_out=to, crit=crit,
+                                   ws=ws, status=status)
+
+    def separate():
+        torch.add(vp, vd, out=vo)
+        torch.add(tp, td, out=to)
+        pv.uvprune_criterion_cossim(vo, to, m_t, n_t, out=crit, ws=ws, status=status)
+
+    res = {}
+    for name, fn in (("fused", fused), ("separate", separate)):
+        g = capture(torch, lambda: [fn() for _ in range(5)])
+        res[name] = time_replays(torch, g.replay, 5) * 1e3 / 5
+        del g
+    nb = 3 * (m + n) * Dh * 2 * B
+    rec = {"workload": "llava72b hidden states: 12544 visual + 256 text rows, D_h 8192, bf16",
+           "fused_us": round(res["fused"], 2), "separate_us": round(res["separate"], 2),
+           "fused_bytes": nb, "fused_tbs": round(nb / (res["fused"] * 1e-6) / 1e12, 3),
+           "device_status": int(status.item())}
+    del vp, vd, tp, td, vo, to
+    torch.cuda.empty_cache()
+    return rec
+
+
 def rope_record(torch, pv, W, dev):
     """pvlm_rope_append at the 72B layer shape (T = 9 verify rows, 64 query and
     8 KV heads, D = 128, bf16, M-RoPE sections 16/24/24), 80 launches per
@@ -845,7 +891,7 @@ def main():
     torch.cuda.empty_cache()
 
     others = None
-    cossim = rope = paged = overlap = None
+    cossim = rope = paged = overlap = epi = None
     if not args.no_extra and graph_used:
         others = {}
         for name in OTHER_CONFIGS:
@@ -857,6 +903,8 @@ def main():
         log(f"cossim: {cossim['us']} us")
         rope = rope_record(torch, pv, W, dev)
         log(f"rope_append: {rope['us']} us")
+        epi = epilogue_record(torch, pv, W, dev)
+        log(f"prefill epilogue: {epi}")
         paged = paged_record(torch, pv, W, dev)
         log(f"paged verify: padded {paged['padded_us']} us, paged {paged['paged']}")
         overlap = overlap_record(torch, pv, W, dev)
@@ -903,6 +951,7 @@ def main():
         "other_configs": others,
         "cossim": cossim,
         "rope_append": rope,
+        "prefill_epilogue": epi,
         "paged_kv": paged,
         "stage2_overlap": overlap,
         "cpu_baseline": cpu,

@@ -327,6 +327,35 @@ pvlm_status pvlm_uvprune_criterion_cossim(int B, int64_t m_cap, const int32_t* m
                                           hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * pvlm_prefill_epilogue_cossim -- the UV-Prune criterion fused into a prefill
+ * layer's epilogue (Sec. 4.1 defines the criterion on the early layers'
+ * hidden states; Sec. 4.2 computes it while the target prefills).  The
+ * epilogue's residual add and the criterion of its result in one pass over
+ * the rows:
+ *   vis_out[b,i] = vis_prev[b,i] + vis_delta[b,i]   i < m[b]
+ *   txt_out[b,j] = txt_prev[b,j] + txt_delta[b,j]   j < n_txt[b]
+ * (the sum taken in fp32 and rounded once to hdt; rows past m[b] / n_txt[b]
+ * are not written), then, from those stored values,
+ *   crit_out[b,i] = sum_{j<n_txt[b]} cos(vis_out[b,i], txt_out[b,j]),
+ * 0 past m[b]: what pvlm_uvprune_criterion_cossim gives on the outputs, bit
+ * for bit, without reading them again.  Called at layers 0 and L, it yields
+ * the two criteria whose difference is the score (pvlm_uvprune_score, MASS,
+ * over the stack [c^0, c^L]).
+ *   vis_* [B][m_cap][Dh], txt_* [B][n_cap][Dh] in hdt; an output may be its
+ *   prev (in place); crit_out [B][m_cap] fp32; ws as for
+ *   pvlm_uvprune_criterion_cossim (pvlm_uvprune_workspace_size(COSSIM, B,
+ *   Dh, n_cap) bytes).  Sizes, limits and errors are those of
+ *   pvlm_uvprune_criterion_cossim.
+ * ---------------------------------------------------------------------- */
+pvlm_status pvlm_prefill_epilogue_cossim(int B, int64_t m_cap, const int32_t* m, int64_t n_cap,
+                                         const int32_t* n_txt, pvlm_dtype hdt, int Dh,
+                                         const void* vis_prev, const void* vis_delta,
+                                         void* vis_out, const void* txt_prev,
+                                         const void* txt_delta, void* txt_out, float* crit_out,
+                                         void* ws, size_t ws_bytes, int32_t* status,
+                                         hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * pvlm_topk_select -- Eq. (topk_selection).  For each b keep the k[b]
  * visual tokens of largest score[b, 0..m[b]) (k[b] = floor(m[b]*(1-alpha)),
  * Sec. 4.2), ranking larger scores first, the lower index first among equal

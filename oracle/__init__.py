@@ -15,6 +15,8 @@ explicit loops over the indices the paper sums over, following the paper:
                           (Sec. 3, Challenge 2).
 * ``cos_similarity``   -- Eq. (similarity).
 * ``criterion_cossim`` -- sum over text tokens of Eq. (similarity) for one layer.
+* ``prefill_epilogue`` -- a prefill layer's residual add with that criterion
+                          computed from the stored result (Sec. 4.1, 4.2).
 * ``uvprune_score_*``  -- Eq. (average_similarity): layer-to-layer variation
                           summed over text tokens and layers 1..L.
 * ``topk_select``      -- Eq. (topk_selection), keep ratio 1 - alpha (Sec. 4.2).
@@ -38,14 +40,14 @@ Parity status: every function here is pinned by the ``-m "not gpu"`` tests in
 or hand-computed fixtures; none is "parity unpinned".
 """
 from .attention import verify_attn, verify_attn_rows
-from .uvprune import (cos_similarity, criterion_cossim, uvprune_score_cossim,
+from .uvprune import (cos_similarity, criterion_cossim, prefill_epilogue, uvprune_score_cossim,
                       uvprune_score_mass)
 from .select import topk_keys, topk_select, gather_kv
 from .accept import spec_accept, softmax_t, NEAR_TIE_REL
 from . import paged, pipeline, rope, window
 
 __all__ = [
-    "verify_attn", "verify_attn_rows", "cos_similarity", "criterion_cossim",
+    "verify_attn", "verify_attn_rows", "cos_similarity", "criterion_cossim", "prefill_epilogue",
     "uvprune_score_cossim", "uvprune_score_mass", "topk_keys", "topk_select",
     "gather_kv", "spec_accept", "softmax_t", "NEAR_TIE_REL",
 ]

@@ -96,3 +96,39 @@ def uvprune_score_mass(crit, m):
             acc += crit[l, b, :mb] - crit[l - 1, b, :mb]
         score[b, :mb] = acc
     return score
+
+
+# ---- the prefill layer's epilogue (the UV-Prune criterion computed where
+#      the layer's hidden states are produced, Sec. 4.1 / 4.2) ---------------
+def round_to_storage(x64, dtype):
+    """Round float64 values to the storage type: fp32 (round to nearest,
+    ties to even), or bf16 through fp32 (round to nearest even on the low 16
+    bits of the fp32 pattern).  Returned as float64 values."""
+    f = np.asarray(x64, dtype=np.float64).astype(np.float32)
+    if dtype == "f32":
+        return f.astype(np.float64)
+    if dtype != "bf16":
+        raise ValueError(dtype)
+    u = f.view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    r = ((u + 0x7FFF + lsb) >> 16) << 16            # (finite values only)
+    return r.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def prefill_epilogue(vis_prev, vis_delta, txt_prev, txt_delta, m, n, dtype):
+    """The epilogue of a prefill layer with the UV-Prune criterion fused in:
+    the residual add h = prev + delta (the sum in fp32, rounded once to the
+    storage type) for visual rows i < m[b] and text rows j < n[b], then the
+    criterion of the layer, c[b, i] = sum_j cos(h_vis[b, i], h_txt[b, j]),
+    over those stored values.  Rows past m[b] / n[b] are left as prev (the
+    call does not write them).  Returns (vis_out, txt_out, c), float64."""
+    def add(prev, delta, count):
+        prev = np.asarray(prev, dtype=np.float64)
+        out = prev.copy()
+        for b in range(prev.shape[0]):
+            k = int(count[b])
+            out[b, :k] = round_to_storage(prev[b, :k] + np.asarray(delta, dtype=np.float64)[b, :k], dtype)
+        return out
+    hv = add(vis_prev, vis_delta, m)
+    ht = add(txt_prev, txt_delta, n)
+    return hv, ht, criterion_cossim(hv, ht, m, n)

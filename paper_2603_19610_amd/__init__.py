@@ -30,6 +30,7 @@ EXPORTS = (
     "pvlm_verify_attn_workspace_size", "pvlm_verify_attn", "pvlm_verify_attn_paged",
     "pvlm_verify_attn_noalloc", "pvlm_verify_attn_noalloc_max_bytes",
     "pvlm_uvprune_workspace_size", "pvlm_uvprune_score", "pvlm_uvprune_criterion_cossim",
+    "pvlm_prefill_epilogue_cossim",
     "pvlm_topk_workspace_size", "pvlm_topk_select", "pvlm_uvprune_topk_mass",
     "pvlm_gather_kv", "pvlm_gather_kv_paged",
     "pvlm_spec_accept_workspace_size", "pvlm_spec_accept",
@@ -113,6 +114,8 @@ _SIGS = {
                                 _P, _P]),
     "pvlm_uvprune_criterion_cossim": (_I, [_I, _I64, _P, _I, _I, _I64, _P, _P, _P, _P, _P, _SZ,
                                            _P, _P]),
+    "pvlm_prefill_epilogue_cossim": (_I, [_I, _I64, _P, _I64, _P, _I, _I, _P, _P, _P, _P, _P, _P,
+                                          _P, _P, _SZ, _P, _P]),
     "pvlm_topk_workspace_size": (_SZ, [_I, _I64]),
     "pvlm_topk_select": (_I, [_I, _I64, _P, _P, _I, _P, _P, _P, _SZ, _P, _P]),
     "pvlm_uvprune_topk_mass": (_I, [_I, _I, _I64, _P, _P, _P, _I, _P, _P, _P, _SZ, _P, _P]),
@@ -494,6 +497,45 @@ def uvprune_criterion_cossim(hv, ht, m, n_txt, *, out=None, ws=None, status=None
     return out
 
 
+def prefill_epilogue_cossim(vis_prev, vis_delta, txt_prev, txt_delta, m, n_txt, *, vis_out=None,
+                            txt_out=None, crit=None, ws=None, status=None):
+    """pvlm_prefill_epilogue_cossim: the residual add of a prefill layer's
+    visual [B][m_cap][Dh] and text [B][n_cap][Dh] rows with the layer's
+    COSSIM criterion of the result fused in.  Outputs default to new tensors
+    (pass vis_out=vis_prev for an in-place add).  Returns (vis_out, txt_out,
+    crit [B][m_cap])."""
+    _need(vis_prev, "vis_prev")
+    dev = vis_prev.device
+    dtp = vis_prev.dtype
+    for t, name in ((vis_delta, "vis_delta"), (txt_prev, "txt_prev"), (txt_delta, "txt_delta")):
+        _need(t, name, dtp, dev)
+    _need(m, "m", torch.int32, dev)
+    _need(n_txt, "n_txt", torch.int32, dev)
+    B, m_cap, Dh = vis_prev.shape
+    n_cap = txt_prev.shape[1]
+    if (tuple(vis_delta.shape) != (B, m_cap, Dh) or tuple(txt_prev.shape) != (B, n_cap, Dh)
+            or tuple(txt_delta.shape) != (B, n_cap, Dh)):
+        raise ValueError("inconsistent prefill_epilogue_cossim shapes")
+    if vis_out is None:
+        vis_out = torch.empty_like(vis_prev)
+    if txt_out is None:
+        txt_out = torch.empty_like(txt_prev)
+    _need(vis_out, "vis_out", dtp, dev)
+    _need(txt_out, "txt_out", dtp, dev)
+    if crit is None:
+        crit = torch.empty((B, m_cap), dtype=torch.float32, device=dev)
+    _need(crit, "crit", torch.float32, dev)
+    need = int(lib().pvlm_uvprune_workspace_size(PVLM_CRIT_COSSIM, B, Dh, n_cap))
+    wsb = (ws or _default_ws("uvprune")).get(need)
+    st = lib().pvlm_prefill_epilogue_cossim(B, m_cap, _ptr(m), n_cap, _ptr(n_txt), _dt(vis_prev), Dh,
+                                            _ptr(vis_prev), _ptr(vis_delta), _ptr(vis_out),
+                                            _ptr(txt_prev), _ptr(txt_delta), _ptr(txt_out),
+                                            _ptr(crit), _ptr(wsb), wsb.numel(), _ptr(_status(status)),
+                                            _stream())
+    _check(st, "pvlm_prefill_epilogue_cossim")
+    return vis_out, txt_out, crit
+
+
 def topk_select(score, m, k, k_cap: int, *, idx=None, ws=None, status=None):
     """Ascending kept indices [B][k_cap] (-1 padded)."""
     _need(score, "score", torch.float32)
@@ -652,7 +694,7 @@ __all__ = [
     "verify_attn", "verify_attn_paged", "verify_attn_noalloc",
     "gather_kv_paged", "rope_append", "rope_append_paged",
     "verify_attn_workspace_size", "uvprune_score_mass", "uvprune_score_cossim",
-    "uvprune_criterion_cossim", "topk_select", "uvprune_topk_mass", "gather_kv", "spec_accept",
+    "uvprune_criterion_cossim", "prefill_epilogue_cossim", "topk_select", "uvprune_topk_mass", "gather_kv", "spec_accept",
     "PVLM_F32", "PVLM_BF16", "PVLM_CRIT_MASS", "PVLM_CRIT_COSSIM", "PVLM_DEV_RANGE",
     "PVLM_DEV_TIMEOUT", "PVLM_DEV_PLACEMENT",
 ]

@@ -69,6 +69,39 @@ struct HS<float> {
   }
 };
 
+// The prefill epilogue's residual add: out = prev + delta, the sum taken in
+// fp32 and rounded once to the storage type; the rounded values are stored
+// and returned, so the criterion uses exactly the stored hidden state.
+__device__ __forceinline__ void add_round_store8(uint16_t* out, float (&f)[8], const float (&g)[8]) {
+  uint32_t w[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint16_t lo = f32_to_bf16(f[2 * k] + g[2 * k]), hi = f32_to_bf16(f[2 * k + 1] + g[2 * k + 1]);
+    w[k] = (uint32_t)lo | ((uint32_t)hi << 16);
+    f[2 * k] = bf16_to_f32(lo);
+    f[2 * k + 1] = bf16_to_f32(hi);
+  }
+  *reinterpret_cast<uint4*>(out) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+__device__ __forceinline__ void add_round_store8(float* out, float (&f)[8], const float (&g)[8]) {
+#pragma unroll
+  for (int k = 0; k < 8; ++k) f[k] += g[k];
+  *reinterpret_cast<float4*>(out) = make_float4(f[0], f[1], f[2], f[3]);
+  *reinterpret_cast<float4*>(out + 4) = make_float4(f[4], f[5], f[6], f[7]);
+}
+
+// 8 consecutive elements of a hidden-state row at element offset `off`: the
+// row itself, or (FUSED) the epilogue's prev + delta, written to `out`.
+template <typename T, bool FUSED>
+__device__ __forceinline__ void row8(const T* h, const T* delta, T* out, size_t off, float (&f)[8]) {
+  HS<T>::load8(h + off, f);
+  if constexpr (FUSED) {
+    float g[8];
+    HS<T>::load8(delta + off, g);
+    add_round_store8(out + off, f, g);
+  }
+}
+
 __device__ __forceinline__ double wave_sum_f64(double v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -82,11 +115,12 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 // c^L - c^0) is rounded, once, to fp32.
 
 // One wave per text row: inv_norm[slot][b][j] = 1/|ht| (0 for zero norm or j >= n[b]).
-template <typename T>
+template <typename T, bool FUSED>
 __global__ void __launch_bounds__(256) txt_norm_kernel(const T* ht, int64_t off0, int64_t off1,
                                                        const int32_t* n_txt,
                                                        int nslots, int B, int64_t n_cap, int Dh,
-                                                       double* inv_norm, int32_t* status) {
+                                                       double* inv_norm, int32_t* status,
+                                                       const T* dt, T* ot) {
   const int64_t wid = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int lane = threadIdx.x & 63;
   if (wid >= (int64_t)nslots * B * n_cap) return;
@@ -98,12 +132,12 @@ __global__ void __launch_bounds__(256) txt_norm_kernel(const T* ht, int64_t off0
   if (bad && j == 0 && slot == 0 && lane == 0) dev_flag(status, PVLM_DEV_RANGE);
   double inv = 0.0;
   if (j < nb) {
-    const T* row = ht + (slot ? off1 : off0) + ((size_t)b * n_cap + j) * Dh;
+    const size_t roff = (slot ? off1 : off0) + ((size_t)b * n_cap + j) * Dh;
     double ss = 0.0;
 #pragma unroll 8  // the row's loads in flight together
     for (int d = lane * 8; d < Dh; d += 512) {
       float f[8];
-      HS<T>::load8(row + d, f);
+      row8<T, FUSED>(ht, dt, ot, roff + d, f);
 #pragma unroll
       for (int k = 0; k < 8; ++k) ss = fma((double)f[k], (double)f[k], ss);
     }
@@ -168,11 +202,12 @@ __global__ void __launch_bounds__(256) txt_dir_sum_kernel(const double* part, in
 // error below 1e-5 (at most 134 roundings), far inside the criterion's gate.
 // nslots == 2: out = c_1 - c_0 (the score); nslots == 1: out = c_0.
 constexpr int kVisThreads = 1024;
-template <typename T>
+template <typename T, bool FUSED>
 __global__ void __launch_bounds__(kVisThreads) vis_kernel(const T* hv, int64_t off0, int64_t off1,
                                                           const int32_t* m, int nslots,
                                                           int B, int64_t m_cap, int Dh, const double* u,
-                                                          float* out, int32_t* status) {
+                                                          float* out, int32_t* status, const T* dv,
+                                                          T* ov) {
   extern __shared__ __align__(16) double s_u[];  // [nslots][8][Dh / 8]
   const int b = blockIdx.y;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -190,14 +225,14 @@ __global__ void __launch_bounds__(kVisThreads) vis_kernel(const T* hv, int64_t o
     if (i < mb) {
       double c[2] = {0.0, 0.0};
       for (int s = 0; s < nslots; ++s) {
-        const T* row = hv + (s ? off1 : off0) + ((size_t)b * m_cap + i) * Dh;
+        const size_t roff = (s ? off1 : off0) + ((size_t)b * m_cap + i) * Dh;
         const double* us = s_u + s * 8 * D8;
         double dot = 0.0;
         float ss = 0.f;
 #pragma unroll 8  // the row's loads in flight together
         for (int j = lane; j < D8; j += 64) {
           float f[8];
-          HS<T>::load8(row + 8 * j, f);
+          row8<T, FUSED>(hv, dv, ov, roff + 8 * j, f);
 #pragma unroll
           for (int k = 0; k < 8; ++k) {
             dot = fma((double)f[k], us[k * D8 + j], dot);
@@ -228,13 +263,19 @@ size_t cossim_ws(int B, int Dh, int64_t n_cap) {
 // kernel's LDS.
 constexpr int kMaxDh = 8192;
 
-template <typename T>
+// FUSED (the prefill epilogue, nslots == 1): the rows are prev + delta
+// (hv/ht the previous hidden states, dv/dt the deltas), written to ov/ot on
+// the first read; the text directions then read ot.
+template <typename T, bool FUSED = false>
 pvlm_status launch_cossim(int nslots, int64_t voff0, int64_t voff1, int64_t toff0, int64_t toff1,
                           int B, int64_t m_cap, const int32_t* m, int Dh, int64_t n_cap,
                           const int32_t* n_txt, const T* hv, const T* ht, float* outp, double* inv,
-                          double* u, double* part, int32_t* status, hipStream_t stream) {
+                          double* u, double* part, int32_t* status, hipStream_t stream,
+                          const T* dv = nullptr, T* ov = nullptr, const T* dt = nullptr,
+                          T* ot = nullptr) {
   const int lds = (int)(sizeof(double) * nslots * Dh);
-  PVLM_HIP(allow_dynamic_lds(reinterpret_cast<const void*>(vis_kernel<T>), 2 * kMaxDh * (int)sizeof(double)));
+  PVLM_HIP(allow_dynamic_lds(reinterpret_cast<const void*>(vis_kernel<T, FUSED>),
+                             2 * kMaxDh * (int)sizeof(double)));
   DeviceInfo di;
   const pvlm_status st = device_info(&di);
   if (st != PVLM_OK) return st;
@@ -242,28 +283,32 @@ pvlm_status launch_cossim(int nslots, int64_t voff0, int64_t voff1, int64_t toff
   const int64_t per_b = (di.cus + B - 1) / B;
   const int64_t vis_x = std::max<int64_t>(1, std::min<int64_t>(per_b, (m_cap + 15) / 16));
   const int64_t nw = (int64_t)nslots * B * n_cap;
-  hipLaunchKernelGGL(txt_norm_kernel<T>, dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream, ht,
-                     toff0, toff1, n_txt, nslots, B, n_cap, Dh, inv, status);
+  hipLaunchKernelGGL((txt_norm_kernel<T, FUSED>), dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream,
+                     ht, toff0, toff1, n_txt, nslots, B, n_cap, Dh, inv, status, dt, ot);
   PVLM_LAUNCHED();
   const int nchunk = txt_chunks(n_cap);
   hipLaunchKernelGGL(txt_dir_part_kernel<T>, dim3((Dh / 8 + 63) / 64, nchunk, nslots * B), dim3(64), 0,
-                     stream, ht, toff0, toff1, n_txt, B, n_cap, Dh, nchunk, inv, part);
+                     stream, FUSED ? static_cast<const T*>(ot) : ht, toff0, toff1, n_txt, B, n_cap, Dh,
+                     nchunk, inv, part);
   PVLM_LAUNCHED();
   hipLaunchKernelGGL(txt_dir_sum_kernel, dim3((Dh + 255) / 256, nslots * B), dim3(256), 0, stream, part,
                      Dh, nchunk, u);
   PVLM_LAUNCHED();
-  hipLaunchKernelGGL(vis_kernel<T>, dim3((unsigned)vis_x, B), dim3(kVisThreads), lds, stream, hv, voff0,
-                     voff1, m, nslots, B, m_cap, Dh, u, outp, status);
+  hipLaunchKernelGGL((vis_kernel<T, FUSED>), dim3((unsigned)vis_x, B), dim3(kVisThreads), lds, stream, hv,
+                     voff0, voff1, m, nslots, B, m_cap, Dh, u, outp, status, dv, ov);
   PVLM_LAUNCHED();
   return PVLM_OK;
 }
 
 // nslots == 2: score from layers 0 and L of [L+1]-layer stacks; nslots == 1:
 // the criterion of a single layer (L ignored, stacks hold one layer).
+// With the epilogue pointers (dv, ov, dt, ot non-NULL, nslots == 1): the
+// rows are hs + delta, stored to the outputs as they are read.
 pvlm_status run_cossim(int nslots, int L, int B, int64_t m_cap, const int32_t* m, pvlm_dtype hdt,
                        int Dh, int64_t n_cap, const int32_t* n_txt, const void* hs_vis,
                        const void* hs_txt, float* outp, void* ws, size_t ws_bytes,
-                       int32_t* status, hipStream_t stream) {
+                       int32_t* status, hipStream_t stream, const void* dv = nullptr,
+                       void* ov = nullptr, const void* dt = nullptr, void* ot = nullptr) {
   if (!m || !n_txt || !hs_vis || !hs_txt || !outp) return PVLM_ERR_NULL;
   if (hdt != PVLM_F32 && hdt != PVLM_BF16) return PVLM_ERR_UNSUPPORTED;
   if (B < 1 || m_cap < 1 || n_cap < 1 || Dh < 8 || Dh % 8 != 0) return PVLM_ERR_SHAPE;
@@ -285,6 +330,19 @@ pvlm_status run_cossim(int nslots, int L, int B, int64_t m_cap, const int32_t* m
   double* part = reinterpret_cast<double*>(w + align_up(off_u + sizeof(double) * 2 * (size_t)B * Dh, 256));
   const int64_t vls = (int64_t)B * m_cap * Dh, tls = (int64_t)B * n_cap * Dh;
   const int64_t l1 = nslots == 2 ? L : 0;
+  if (dv) {
+    typedef uint16_t H;
+    if (hdt == PVLM_BF16)
+      return launch_cossim<H, true>(1, 0, 0, 0, 0, B, m_cap, m, Dh, n_cap, n_txt,
+                                    static_cast<const H*>(hs_vis), static_cast<const H*>(hs_txt),
+                                    outp, inv, u, part, status, stream, static_cast<const H*>(dv),
+                                    static_cast<H*>(ov), static_cast<const H*>(dt), static_cast<H*>(ot));
+    return launch_cossim<float, true>(1, 0, 0, 0, 0, B, m_cap, m, Dh, n_cap, n_txt,
+                                      static_cast<const float*>(hs_vis),
+                                      static_cast<const float*>(hs_txt), outp, inv, u, part, status,
+                                      stream, static_cast<const float*>(dv), static_cast<float*>(ov),
+                                      static_cast<const float*>(dt), static_cast<float*>(ot));
+  }
   if (hdt == PVLM_BF16)
     return launch_cossim<uint16_t>(nslots, 0, l1 * vls, 0, l1 * tls, B, m_cap, m, Dh, n_cap, n_txt,
                                    static_cast<const uint16_t*>(hs_vis),
@@ -335,4 +393,17 @@ extern "C" pvlm_status pvlm_uvprune_criterion_cossim(int B, int64_t m_cap, const
                                                      hipStream_t stream) {
   return run_cossim(1, 0, B, m_cap, m, hdt, Dh, n_cap, n_txt, hs_vis, hs_txt, crit_out, ws,
                     ws_bytes, status, stream);
+}
+
+extern "C" pvlm_status pvlm_prefill_epilogue_cossim(int B, int64_t m_cap, const int32_t* m,
+                                                    int64_t n_cap, const int32_t* n_txt,
+                                                    pvlm_dtype hdt, int Dh, const void* vis_prev,
+                                                    const void* vis_delta, void* vis_out,
+                                                    const void* txt_prev, const void* txt_delta,
+                                                    void* txt_out, float* crit_out, void* ws,
+                                                    size_t ws_bytes, int32_t* status,
+                                                    hipStream_t stream) {
+  if (!vis_delta || !vis_out || !txt_delta || !txt_out) return PVLM_ERR_NULL;
+  return run_cossim(1, 0, B, m_cap, m, hdt, Dh, n_cap, n_txt, vis_prev, txt_prev, crit_out, ws,
+                    ws_bytes, status, stream, vis_delta, vis_out, txt_delta, txt_out);
 }

@@ -93,3 +93,45 @@ def test_mass_variation_properties():
     # explicit differences of a hand-made stack
     hand = np.array([[[1.0, 2.0]], [[4.0, 1.0]], [[2.0, 7.0]]])
     np.testing.assert_allclose(oracle.uvprune_score_mass(hand, [2])[0], [1.0, 5.0])
+
+
+# ---- the prefill epilogue (residual add + criterion of the stored result) --
+def test_round_to_storage_matches_torch_bf16():
+    """The oracle's bf16 rounding (round to nearest even, through fp32) equals
+    torch's conversion, a library routine, on random values, exact ties and
+    values near the fp32 limits."""
+    import torch
+    rng = np.random.default_rng(3)
+    x = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.integers(-30, 30, 20000),
+                        (np.arange(-300, 300) + 0.5) * 2.0 ** -7,      # exact bf16 ties
+                        [3.0e38, -3.0e38, 1e-38, -1e-40, 0.0, -0.0]])
+    mine = oracle.uvprune.round_to_storage(x, "bf16")
+    ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(mine, ref)
+    assert np.array_equal(oracle.uvprune.round_to_storage(x, "f32"), x.astype(np.float32).astype(np.float64))
+
+
+def test_prefill_epilogue_pins():
+    rng = np.random.default_rng(4)
+    B, m_cap, n_cap, D = 2, 9, 5, 16
+    m, n = np.array([9, 4]), np.array([5, 2])
+    bf = lambda a: oracle.uvprune.round_to_storage(a, "bf16")
+    vp, vd = bf(rng.standard_normal((B, m_cap, D))), bf(rng.standard_normal((B, m_cap, D)))
+    tp, td = bf(rng.standard_normal((B, n_cap, D))), bf(rng.standard_normal((B, n_cap, D)))
+    # a zero delta leaves the rows and gives the plain criterion of them
+    hv, ht, c = oracle.prefill_epilogue(vp, 0 * vd, tp, 0 * td, m, n, "bf16")
+    assert np.array_equal(hv, vp) and np.array_equal(ht, tp)
+    assert np.array_equal(c, oracle.criterion_cossim(vp, tp, m, n))
+    # small integers add exactly: the rounding is then the identity
+    ip = rng.integers(-50, 50, (B, m_cap, D)).astype(np.float64)
+    idl = rng.integers(-50, 50, (B, m_cap, D)).astype(np.float64)
+    hv, _, _ = oracle.prefill_epilogue(ip, idl, tp, td, m, n, "bf16")
+    assert np.array_equal(hv[0], ip[0] + idl[0]) and np.array_equal(hv[1, :4], ip[1, :4] + idl[1, :4])
+    # rows past m / n are not written
+    hv, ht, c = oracle.prefill_epilogue(vp, vd, tp, td, m, n, "bf16")
+    assert np.array_equal(hv[1, 4:], vp[1, 4:]) and np.array_equal(ht[1, 2:], tp[1, 2:])
+    assert not c[1, 4:].any()
+    # the criterion is that of the rounded sums, not of the exact ones
+    exact = oracle.criterion_cossim(vp + vd, tp + td, m, n)
+    assert np.array_equal(c, oracle.criterion_cossim(bf(vp + vd), ht, m, n))
+    assert not np.array_equal(c, exact)

@@ -103,3 +103,43 @@ def test_cossim_streamed_over_layers(dtype, L):
     cL = oracle.criterion_cossim(hv64[L], ht64[L], m, n)
     c0 = oracle.criterion_cossim(hv64[0], ht64[0], m, n)
     _assert_score(to_host_f64(s), ref, np.abs(cL) + np.abs(c0))
+
+
+@pytest.mark.parametrize("dtype,Dh", [("bf16", 512), ("f32", 256), ("bf16", 8192)])
+def test_prefill_epilogue_fused(dtype, Dh):
+    """pvlm_prefill_epilogue_cossim: the residual add bit-exact against the
+    oracle (sum in fp32, one rounding), rows past m / n untouched, and the
+    criterion of the stored rows within the gate of the oracle's and
+    bit-equal to pvlm_uvprune_criterion_cossim run on the outputs; in place
+    (out = prev) gives the same."""
+    rng = np.random.default_rng(Dh)
+    B, m_cap, n_cap = 2, 700 if Dh < 8192 else 300, 48
+    m = np.array([m_cap, m_cap - 123], np.int32)
+    n = np.array([n_cap, 17], np.int32)
+    st = np.float32 if dtype == "f32" else np.uint16
+    gen = lambda *sh: W.round_storage(rng.standard_normal(sh), dtype).astype(st)
+    vp, vd, tp, td = gen(B, m_cap, Dh), gen(B, m_cap, Dh), gen(B, n_cap, Dh), gen(B, n_cap, Dh)
+    vd[0, 5] = 0 if dtype == "f32" else np.uint16(0)
+    note(f"prefill epilogue {dtype} Dh={Dh}")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    d = [to_dev(x) for x in (vp, vd, tp, td)]
+    dm, dn = to_dev(m), to_dev(n)
+    vo, to, c = pv.prefill_epilogue_cossim(*d, dm, dn, status=status)
+    c_ref_gpu = pv.uvprune_criterion_cossim(vo, to, dm, dn, status=status)
+    # in place
+    vi, ti = d[0].clone(), d[2].clone()
+    _, _, c_in = pv.prefill_epilogue_cossim(vi, d[1], ti, d[3], dm, dn, vis_out=vi, txt_out=ti,
+                                            status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    hv, ht, cref = oracle.prefill_epilogue(f64(vp, dtype), f64(vd, dtype), f64(tp, dtype),
+                                           f64(td, dtype), m, n, dtype)
+    gv, gt = to_host_f64(vo), to_host_f64(to)
+    assert np.array_equal(gv[0], hv[0]) and np.array_equal(gv[1, :m[1]], hv[1, :m[1]])
+    assert np.array_equal(gt[0], ht[0]) and np.array_equal(gt[1, :n[1]], ht[1, :n[1]])
+    assert torch.equal(c.view(torch.int32), c_ref_gpu.view(torch.int32))
+    assert torch.equal(c.view(torch.int32), c_in.view(torch.int32))
+    assert torch.equal(vi[0], vo[0]) and torch.equal(vi[1, :m[1]], vo[1, :m[1]])
+    assert torch.equal(vi[1, m[1]:], d[0][1, m[1]:]) and torch.equal(ti[1, n[1]:], d[2][1, n[1]:])
+    _assert_score(to_host_f64(c), cref, np.abs(cref))
+    assert np.all(to_host_f64(c)[1, m[1]:] == 0)
