@@ -2,19 +2,27 @@
  * pvlm.h -- C ABI of the ParallelVLM verify + UV-Prune + accept hot path
  * on AMD Instinct MI355X (gfx950).
  *
- * The five calls follow the paper's statement of the problem
- * (ParallelVLM, arXiv 2603.19610):
+ * The calls follow the paper's statement of the problem (ParallelVLM,
+ * arXiv 2603.19610):
  *   pvlm_rope_append    rotary embedding (1-D or M-RoPE) of the verify rows and
  *                       their append to the KV cache
  *   pvlm_verify_attn    target verification forward over the video KV cache
  *                       (Sec. 2.2; Sec. 4.2 Parallel Decoding), fused with the
  *                       per-token verifier attention mass (Sec. 3, Challenge 2)
+ *   pvlm_*_paged        verify, rope-append and gather over a paged cache
+ *   pvlm_verify_attn_noalloc  verify with the library's fixed scratch
  *   pvlm_uvprune_score  UV-Prune variation score, Eq. (average_similarity),
- *                       over Eq. (similarity) or over a per-layer criterion
- *   pvlm_topk_select    Eq. (topk_selection): keep the top 1 - alpha fraction
+ *                       over Eq. (similarity) or over a per-layer criterion;
+ *                       pvlm_uvprune_criterion_cossim one layer of it, and
+ *                       pvlm_prefill_epilogue_cossim that layer's criterion
+ *                       fused into the prefill layer's residual add
+ *   pvlm_topk_select    Eq. (topk_selection): keep the top 1 - alpha fraction;
+ *                       pvlm_uvprune_topk_mass with the MASS score in one launch
  *   pvlm_gather_kv      the draft's compact cache [V*, X] (Sec. 4.2, Stage I)
  *   pvlm_spec_accept    speculative-sampling accept/reject (Sec. 2.2) with the
  *                       bonus token of Suppl. B
+ *   pvlm_set_stream_cu_budget  compute-unit budgets, so the draft's and the
+ *                       target's waiting kernels can run at once (Stage II)
  *   pvlm_window_size,   host-only: the draft window gamma = c* of Eq. (Prefill)
  *   pvlm_speedup        and the speedup analysis (Thm. paravlm_speedup; the
  *                       supplement's theorems and Lemma 1)
