@@ -43,7 +43,7 @@ PROFILES = os.path.join(ROOT, "profiles")
 VERIFY_SRCS = [os.path.join(ROOT, "paper_2603_19610_amd", "csrc", f)
                for f in ("verify_attn.hip", "common.h")]
 COPY_BYTES = 512 << 20
-OTHER_CONFIGS = ("llava7b", "llava72b", "qwen32b", "long")
+OTHER_CONFIGS = ("tiny", "llava7b", "llava72b", "qwen32b", "long")
 
 
 def log(msg):
@@ -73,16 +73,22 @@ def parse():
 
 
 # ------------------------------------------------------------ byte counts --
-def verify_bytes(w, esize=2):
+def esize_of(w):
+    return 4 if w.dtype == "f32" else 2
+
+
+def verify_bytes(w, esize=None):
     """Algorithmic HBM bytes of one verify launch: K and V of the N + T visible
     rows, Q, O, mass and lse, each moved once."""
+    esize = esize_of(w) if esize is None else esize
     N = int(w.lengths().sum()) + w.batch * w.T
     kv = 2 * N * w.hkv * w.head_dim * esize
     qo = 2 * w.batch * w.T * w.hq * w.head_dim * esize
     return kv + qo + 4 * w.batch * w.n_cap() + 4 * w.batch * w.hq * w.T
 
 
-def gather_bytes(w, esize=2):
+def gather_bytes(w, esize=None):
+    esize = esize_of(w) if esize is None else esize
     m = w.m_per_seq()
     rows = int((w.keep_count(m) + w.n_text).sum())
     return 2 * 2 * rows * w.hkv * w.head_dim * esize + 4 * int(w.keep_count(m).sum())
@@ -388,6 +394,23 @@ def time_replays(torch, run, n):
     return a.elapsed_time(b) / n
 
 
+def replay_percentiles(torch, run, n, per_call=1):
+    """(mean, p10, p50, p90) ms per call over n replays of run(), each
+    bracketed by HIP events on the current stream (per_call calls each)."""
+    run()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(n)]
+    for a, b in ev:
+        a.record()
+        run()
+        b.record()
+    torch.cuda.synchronize()
+    t = np.array([a.elapsed_time(b) for a, b in ev]) / per_call
+    p10, p50, p90 = np.percentile(t, [10, 50, 90])
+    return float(t.mean()), float(p10), float(p50), float(p90)
+
+
 def copy_bandwidth(torch, dev, nbytes, reps):
     """Device-to-device copy GB/s (bytes read + written) for copies moving
     nbytes each.  The copies cycle over enough distinct buffers (>= 2 GiB in
@@ -408,15 +431,22 @@ def copy_bandwidth(torch, dev, nbytes, reps):
     return nbytes / (ms * 1e-3) / 1e9
 
 
-def stage_times(torch, st, reps):
+def stage_times(torch, st, reps, pct=None):
     """Graph-timed mean us of each stage of the step (`reps` verify launches,
-    cycling over the layers, or 10 launches of another stage per graph)."""
+    cycling over the layers, or 10 launches of another stage per graph).
+    With a dict `pct`, also each stage's [p10, p50, p90] over 10 replays."""
     out = {}
     g = capture(torch, lambda: [st.verify((7 * r + 3) % st.NL) for r in range(reps)])
-    out["verify"] = time_replays(torch, g.replay, 5) * 1e3 / reps
+    graphs = [("verify", g, reps)]
     for name, fn in (("uvprune+topk", st.prune), ("gather", st.gather), ("accept", st.accept)):
-        g = capture(torch, lambda: [fn() for _ in range(10)])
-        out[name] = time_replays(torch, g.replay, 5) * 1e3 / 10
+        graphs.append((name, capture(torch, lambda: [fn() for _ in range(10)]), 10))
+    for name, g, k in graphs:
+        if pct is None:
+            out[name] = time_replays(torch, g.replay, 5) * 1e3 / k
+        else:
+            mean, p10, p50, p90 = replay_percentiles(torch, g.replay, 10, k)
+            out[name] = mean * 1e3
+            pct[name] = [round(p10 * 1e3, 2), round(p50 * 1e3, 2), round(p90 * 1e3, 2)]
     return out
 
 
@@ -424,11 +454,14 @@ def single_layer_record(torch, pv, W, name, dev, steps):
     w = W.WORKLOADS[name]
     st = Step(torch, pv, W, w, False, dev)
     g = capture(torch, st.step)
-    ms = time_replays(torch, g.replay, steps)
-    stg = stage_times(torch, st, 20)
+    ms, p10, p50, p90 = replay_percentiles(torch, g.replay, steps)
+    pct = {}
+    stg = stage_times(torch, st, 20, pct)
     vb = verify_bytes(w)
     rec = {
         "us_per_step": round(ms * 1e3, 2),
+        "us_per_step_p10_p50_p90": [round(p10 * 1e3, 2), round(p50 * 1e3, 2), round(p90 * 1e3, 2)],
+        "stages_us_p10_p50_p90": pct,
         "step_bytes": st.bytes(),
         "step_tbs": round(st.bytes() / (ms * 1e-3) / 1e12, 3),
         "stages_us": {k: round(v, 2) for k, v in stg.items()},

@@ -1367,10 +1367,13 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
   constexpr int ROWS = RT * 16;
   constexpr int TC = kF32Tile;
   constexpr int OPT = ROWS * D / kThreads;
+  // K/V tile rows padded by one word: the score loop's lanes take
+  // consecutive tokens, which would otherwise all read one LDS bank
+  constexpr int KVS = D + 1;
   extern __shared__ __align__(256) float sm[];
   float* sQ = sm;                // [ROWS][D]
-  float* sKV = sQ + ROWS * D;    // [TC][D]
-  float* sS = sKV + TC * D;      // [ROWS][TC]
+  float* sKV = sQ + ROWS * D;    // [TC][KVS]
+  float* sS = sKV + TC * KVS;    // [ROWS][TC]
   __shared__ float s_m[ROWS], s_z[ROWS], s_lse[ROWS];
   __shared__ float s_pm[kWaves][ROWS], s_pz[kWaves][ROWS];
   __shared__ int s_flag;
@@ -1406,8 +1409,8 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
 
   auto load_rows = [&](const float* src, int base, int nt) {
     for (int e = tid; e < TC * D; e += kThreads) {
-      const int tt = e / D;
-      sKV[e] = tt < nt ? src[(size_t)(base + tt) * D + e % D] : 0.f;
+      const int tt = e / D, d = e % D;
+      sKV[tt * KVS + d] = tt < nt ? src[(size_t)(base + tt) * D + d] : 0.f;
     }
   };
   auto scores = [&](int base, int nt) {  // sS = scaled, masked scores (log2 domain)
@@ -1416,7 +1419,7 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
       float s = kNegInf;
       if (tt < nt && row < a.R && tok <= u.ctx + row / a.G) {
         float acc = 0.f;
-        for (int d = 0; d < D; ++d) acc = fmaf(sQ[r * D + d], sKV[tt * D + d], acc);
+        for (int d = 0; d < D; ++d) acc = fmaf(sQ[r * D + d], sKV[tt * KVS + d], acc);
         s = acc * a.sl2;
       }
       sS[e] = s;
@@ -1465,7 +1468,7 @@ __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
     for (int k = 0; k < OPT; ++k) {
       const int e = tid + k * kThreads, r = e / D, d = e % D;
       float acc = O[k];
-      for (int tt = 0; tt < nt; ++tt) acc = fmaf(sS[r * TC + tt], sKV[tt * D + d], acc);
+      for (int tt = 0; tt < nt; ++tt) acc = fmaf(sS[r * TC + tt], sKV[tt * KVS + d], acc);
       O[k] = acc;
     }
   }
@@ -1518,7 +1521,7 @@ VKernel pick_kernel(int dt, int D, int RT, bool resident, bool local) {
 }
 
 int lds_bytes(int dt, int D, int RT, bool resident) {
-  if (dt == PVLM_F32) return (RT * 16 * D + kF32Tile * D + RT * 16 * kF32Tile) * 4;
+  if (dt == PVLM_F32) return (RT * 16 * D + kF32Tile * (D + 1) + RT * 16 * kF32Tile) * 4;
   int b = 3 * RT * 16 * D * 4;                                   // O partial reduce-scatter
   if (!resident && RT > 3) {
     const int kv = RT * 16 * D * 2 + kWaves * 4 * 32 * D * 2;     // Q, then two K+V blocks per wave
