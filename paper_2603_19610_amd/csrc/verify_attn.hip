@@ -798,37 +798,51 @@ __device__ __forceinline__ void scores_raw(const uint4 (&Kr)[2][D / 32], const u
   }
 }
 
-// Per-lane maximum of the visible raw scores of one block, per row tile.
+// Masks a block's raw scores in place: -inf past the chunk, past the causal
+// limit of each verify row, and on padding rows (vis = -1).  Only blocks
+// that some real row does not see whole need it; every other block skips it,
+// which keeps the per-score work of the maximum and the probabilities free of
+// compares.  Padding rows of unmasked blocks keep finite values, which only
+// reach their own statistics (their factor c is 0 wherever it is used).
 template <int RT>
-__device__ __forceinline__ void block_max_raw(const floatx4 (&S)[2][RT], const int (&vis)[RT], int tb,
-                                              int gq, float (&mx)[RT]) {
+__device__ __forceinline__ void mask_block(floatx4 (&S)[2][RT], const int (&vis)[RT], int tb, int gq) {
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
     const int off = vis[rt] - tb - 4 * gq;  // element (tt, i) visible iff 16 tt + i <= off
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) mx[rt] = fmaxf(mx[rt], 16 * tt + i <= off ? S[tt][rt][i] : kNegInf);
+      for (int i = 0; i < 4; ++i)
+        if (16 * tt + i > off) S[tt][rt][i] = kNegInf;
   }
 }
 
-// Raw scores -> probabilities relative to the workgroup's row maxima,
-// P = exp2(scale * s - ref) (0 where masked), in place; per-lane row sums.
+// Per-lane maximum of one block's (masked) raw scores, per row tile.
 template <int RT>
-__device__ __forceinline__ void block_probs(floatx4 (&S)[2][RT], const int (&vis)[RT], int tb, int gq,
-                                            float sl2, const float (&ref)[RT], float (&z)[RT]) {
+__device__ __forceinline__ void block_max_raw(const floatx4 (&S)[2][RT], float (&mx)[RT]) {
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    const int off = vis[rt] - tb - 4 * gq;
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+      mx[rt] = fmaxf(fmaxf(mx[rt], fmaxf(S[tt][rt][0], S[tt][rt][1])), fmaxf(S[tt][rt][2], S[tt][rt][3]));
+}
+
+// Raw scores -> probabilities relative to the workgroup's row maxima,
+// P = exp2(scale * s - ref), in place (masked scores are -inf and the scale
+// is positive, so they give 0); per-lane row sums.
+template <int RT>
+__device__ __forceinline__ void block_probs(floatx4 (&S)[2][RT], float sl2, const float (&ref)[RT],
+                                            float (&z)[RT]) {
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float p = 16 * tt + i <= off ? fast_exp2(fmaf(S[tt][rt][i], sl2, -ref[rt])) : 0.f;
+        const float p = fast_exp2(fmaf(S[tt][rt][i], sl2, -ref[rt]));
         S[tt][rt][i] = p;
         z[rt] += p;
       }
-  }
 }
 
 // One resident block with the global statistics known: exact probabilities
@@ -1184,12 +1198,15 @@ verify_mfma_kernel(VArgs a) {
     if (w > 0)
       for (int blk = w - 1; blk < nblk; blk += kWaves - 1)
         issue_v_lds<D>(vg, u.c0 + 32 * blk, u.c1, s_v + blk * 32 * D, lane);
+    // a block every real row sees whole needs no mask (row 0 sees the least)
+    const int vis_all = min(u.c1 - 1, u.ctx);
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
       const int tb = u.c0 + 32 * (w + kWaves * j);
       if (tb < u.c1) {
         scores_raw<D, RT>(Kr[j], s_q, n, gq, S[j]);
-        block_max_raw<RT>(S[j], vis, tb, gq, m);
+        if (tb + 31 > vis_all) mask_block<RT>(S[j], vis, tb, gq);
+        block_max_raw<RT>(S[j], m);
       }
     }
     // the workgroup's row maxima (log2 domain), then the resident scores
@@ -1204,7 +1221,7 @@ verify_mfma_kernel(VArgs a) {
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
       const int tb = u.c0 + 32 * (w + kWaves * j);
-      if (tb < u.c1) block_probs<RT>(S[j], vis, tb, gq, a.sl2, ref, z);
+      if (tb < u.c1) block_probs<RT>(S[j], a.sl2, ref, z);
     }
     reduce_rows<RT, false>(z, n, gq, w, s_wz, s_z, 1.f);
     // publish the statistics (wave 0, which loads no V) and arrive as soon
@@ -1229,7 +1246,7 @@ verify_mfma_kernel(VArgs a) {
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       const float mm = s_m[rt * 16 + n];
-      c[rt] = mm == kNegInf ? 0.f : fast_exp2(ref[rt] - s_lse[rt * 16 + n]);
+      c[rt] = vis[rt] < 0 || mm == kNegInf ? 0.f : fast_exp2(ref[rt] - s_lse[rt * 16 + n]);
     }
     // ---- pass 2: exact P, the mass partials and P.V on MFMA
     float* mp = a.mass ? a.mpart + ((size_t)u.b * a.Hkv * a.RG + u.g * a.RG + u.rg) * a.n_cap : nullptr;
