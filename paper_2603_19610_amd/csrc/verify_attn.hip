@@ -1567,13 +1567,20 @@ pvlm_status plan_verify(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int
   if (p->R > 640) return PVLM_ERR_UNSUPPORTED;
   p->RTT = (p->R + 15) / 16;
   p->RG = (p->RTT + kMaxRT - 1) / kMaxRT;
-  p->RT = (p->RTT + p->RG - 1) / p->RG;
   p->n_plan = max_ctx + T;
   p->mfma = dt == PVLM_BF16;
-  p->groups = B * Hkv * p->RG;
   DeviceInfo di;
   pvlm_status st = with_stream ? device_info(&di, stream) : device_info(&di);
   if (st != PVLM_OK) return st;
+  // Fewer (batch, KV head) groups than XCDs: split the rows into more groups
+  // (K/V are then read once per row group) so that every group's workgroups
+  // fit one XCD and exchange through its L2.
+  if (p->mfma && B * Hkv * p->RG < di.xcds && p->RTT > p->RG) {
+    const int want = (di.xcds + B * Hkv - 1) / (B * Hkv);
+    p->RG = want < p->RTT ? want : p->RTT;
+  }
+  p->RT = (p->RTT + p->RG - 1) / p->RG;
+  p->groups = B * Hkv * p->RG;
   const int W = di.cus;  // one workgroup per CU (registers / LDS bound)
   p->xcds = di.xcds;
   p->budgeted = di.budgeted;
