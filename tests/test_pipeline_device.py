@@ -18,9 +18,11 @@ waiting kernels may overlap.  The draft rolls back by truncating its device
 ctx_len to the longest prefix of its cache rows that is still valid.
 
 At temperature 0 the committed output must be the target's own greedy
-sequence (the lossless property of Sec. 2.2), computed here by target-only
-decoding one token per forward, and the scheduler must take the oracle's
-decisions given the kernel's verdicts.
+sequence (the lossless property of Sec. 2.2): target-only decoding, one token
+per forward and teacher-forced on the committed prefix, must rank every
+committed token first, up to the rounding of the bf16 attention output (the
+pipeline computes the same logits inside verify windows of other lengths).
+The scheduler must take the oracle's decisions given the kernel's verdicts.
 """
 import numpy as np
 import pytest
@@ -65,7 +67,8 @@ class Model:
         qr = pv.rope_append(q, kn, vn, pos, self.ctx, self.k, self.v, base=BASE, status=self.status)
         out, _, _ = pv.verify_attn(qr, self.k, self.v, self.ctx, want_mass=False, want_lse=False,
                                    ws=self.ws, status=self.status)
-        return out.float().reshape(T, Hq * D) @ self.wo.t()
+        self.last_out = out.float().reshape(T, Hq * D)
+        return self.last_out @ self.wo.t()
 
 
 def _setup(dev, seed, noise, cap_extra):
@@ -108,28 +111,42 @@ def _setup(dev, seed, noise, cap_extra):
     return target, draft, n_prompt, n_c
 
 
-def _greedy_reference(target, n_prompt, p_last, n, dev):
-    """Target-only decoding, one token (T = 1) per forward, on copies of the
-    cache; also the smallest top-2 logit gap seen."""
+def _check_greedy(target, n_prompt, p_last, out, dev):
+    """The committed tokens against target-only decoding, one token (T = 1)
+    per forward, teacher-forced on the committed prefix (on copies of the
+    cache).  Each committed token must be a greedy choice of the target's
+    logits up to rounding: the pipeline computes those logits inside verify
+    windows of other lengths, whose launch plans round the bf16 attention
+    output differently.  A logit then moves by at most
+    sum_j |dO_j| |wo[v, j]| with |dO_j| <= 2 ulp of bf16 (2^-7 |O_j|), so the
+    committed token's logit must be within that bound, taken for both
+    candidates, of the maximum.  Returns (positions where the committed token
+    is not the exact argmax, the smallest top-2 gap)."""
     k, v = target.k.clone(), target.v.clone()
     ref = Model((target.eq, target.ek, target.ev), target.wo, k, v, dev)
-    seq, gaps = [p_last], []
-    for i in range(n):
+    wabs = target.wo.abs()
+    prev, off, gaps = p_last, 0, []
+    for i, tok in enumerate(out):
         c = torch.tensor(n_prompt + i, dtype=torch.int32, device=dev)
-        lg = ref.forward(torch.tensor([seq[-1]], device=dev), c, c)[0]
+        lg = ref.forward(torch.tensor([prev], device=dev), c, c)[0]
+        o = ref.last_out.abs().reshape(-1)
+        best = int(torch.argmax(lg))
         top = torch.topk(lg, 2).values
         gaps.append(float(top[0] - top[1]))
-        seq.append(int(torch.argmax(lg)))
+        if tok != best:
+            bound = 2.0 ** -7 * float((wabs[best] @ o) + (wabs[tok] @ o))
+            assert float(lg[best] - lg[tok]) <= bound, (i, tok, best, float(lg[best] - lg[tok]), bound)
+            off += 1
+        prev = tok
     assert int(ref.status.item()) == 0
-    return seq[1:], min(gaps)
+    return off, min(gaps)
 
 
 def _run(gamma, c, max_len, noise, seed):
     dev = torch.device("cuda", 0)
     target, draft, n_prompt, n_c = _setup(dev, seed, noise, max_len + 4 * gamma + 8)
     p_last = 7
-    ref, gap = _greedy_reference(target, n_prompt, p_last, max_len + 2 * gamma + 2, dev)
-    note(f"pipeline on device gamma={gamma} c={c} noise={noise} min top-2 gap {gap:.3g}")
+    ref_k, ref_v = target.k.clone(), target.v.clone()  # the prompt cache, before the run appends
     s_t, s_d = torch.cuda.Stream(), torch.cuda.Stream()
     pv.set_stream_cu_budget(s_t, 224)
     pv.set_stream_cu_budget(s_d, 32)
@@ -223,7 +240,11 @@ def _run(gamma, c, max_len, noise, seed):
         assert sched.output() == pl.out and sched.pending() == pl.pending
     out = sched.output()
     assert int(target.status.item()) == 0 and int(draft.status.item()) == 0
-    assert out == ref[:len(out)], (out, ref[:len(out)])
+    target.k.copy_(ref_k)
+    target.v.copy_(ref_v)
+    off, gap = _check_greedy(target, n_prompt, p_last, out, dev)
+    note(f"pipeline on device gamma={gamma} c={c} noise={noise}: {len(out)} tokens, "
+         f"{off} within rounding of a tie, min top-2 gap {gap:.3g}")
     assert rejected > 0 and full > 0
     st = sched.stats()
     assert st["target_rounds"] == pl.rounds and st["elapsed"] == pl.clock
