@@ -410,6 +410,11 @@ __global__ void __launch_bounds__(kSmallThreads) topk_small_kernel(TArgs a) {
   float v[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) v[e] = score_at<FUSED>(a, roff, min(e * kSmallThreads + tid, max(mb - 1, 0)));
+  // the first digit's histogram (every copy) is cleared while the keys load
+  __builtin_amdgcn_sched_barrier(0);
+  for (int i = tid; i < kSmallBins * kHistCopies / 4; i += kSmallThreads)
+    reinterpret_cast<int4*>(hist)[i] = make_int4(0, 0, 0, 0);
+  __builtin_amdgcn_sched_barrier(0);
   if constexpr (FUSED) {  // the scores written out (0 past m[b]), then the selection
     if (a.score_out)
 #pragma unroll
@@ -423,29 +428,36 @@ __global__ void __launch_bounds__(kSmallThreads) topk_small_kernel(TArgs a) {
 #pragma unroll
   for (int e = 0; e < PER; ++e) kr[e] = e * kSmallThreads + tid < mb ? rank_key(v[e]) : 0u;
 
-  // ---- radix select of the kb-th largest key: digits [31:20], [19:10], [9:0]
+  // ---- radix select of the kb-th largest key: digits [31:20], [19:10], [9:0].
+  // The first digit's keys crowd into few bins (the sign and exponent of
+  // real scores), so its histogram has kHistCopies counters per bin; the later
+  // digits count only the keys left in the chosen bin, one counter per bin.
   uint32_t prefix = 0, mask = 0;
   int above = 0;
 #pragma unroll 1
   for (int pass = 0; pass < 3; ++pass) {
     const int shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
     const int nb = pass == 0 ? 4096 : 1024;
-    for (int i = tid; i < nb * kHistCopies / 4; i += kSmallThreads)
-      reinterpret_cast<int4*>(hist)[i] = make_int4(0, 0, 0, 0);
+    const int copies = pass == 0 ? kHistCopies : 1;
+    if (pass > 0)
+      for (int i = tid; i < nb / 4; i += kSmallThreads) reinterpret_cast<int4*>(hist)[i] = make_int4(0, 0, 0, 0);
     __syncthreads();
-    const int copy = lane & (kHistCopies - 1);
+    const int copy = pass == 0 ? (lane & (kHistCopies - 1)) : 0;
 #pragma unroll
     for (int e = 0; e < PER; ++e)
       if (e * kSmallThreads + tid < mb && (kr[e] & mask) == prefix)
-        atomicAdd(&hist[((kr[e] >> shift) & (uint32_t)(nb - 1)) * kHistCopies + copy], 1);
+        atomicAdd(&hist[((kr[e] >> shift) & (uint32_t)(nb - 1)) * copies + copy], 1);
     __syncthreads();
-    // each bin's copies summed, consecutive threads on consecutive bins
-    for (int i = tid; i < nb; i += kSmallThreads) {
-      const int4* h = reinterpret_cast<const int4*>(hist + i * kHistCopies);
-      const int4 x = h[0], y = h[1];
-      bins[i] = x.x + x.y + x.z + x.w + y.x + y.y + y.z + y.w;
+    if (pass == 0) {
+      // each bin's copies summed, consecutive threads on consecutive bins
+      for (int i = tid; i < nb; i += kSmallThreads) {
+        const int4* h = reinterpret_cast<const int4*>(hist + i * kHistCopies);
+        const int4 x = h[0], y = h[1];
+        bins[i] = x.x + x.y + x.z + x.w + y.x + y.y + y.z + y.w;
+      }
+      __syncthreads();
     }
-    __syncthreads();
+    const int* totals = pass == 0 ? bins : hist;
     // bins in descending order: thread t owns q = nb / 1024 consecutive ones
     const int q = nb / kSmallThreads;
     const int top = nb - 1 - tid * q;
@@ -453,7 +465,7 @@ __global__ void __launch_bounds__(kSmallThreads) topk_small_kernel(TArgs a) {
     int own = 0;
 #pragma unroll
     for (int j = 0; j < kSmallBins / kSmallThreads; ++j) {
-      cnt[j] = j < q ? bins[top - j] : 0;
+      cnt[j] = j < q ? totals[top - j] : 0;
       own += cnt[j];
     }
     int tot;
