@@ -579,7 +579,7 @@ __device__ __forceinline__ void wait_vm_younger(int younger) {
 template <int D, int RT>
 __device__ __forceinline__ void scores_block(const VArgs& a, const Unit& u, const uint4 (&Kr)[2][D / 32],
                                              const uint16_t* s_q, int tb, int n, int gq,
-                                             float (&S)[2][RT][4]);
+                                             const int (&lim)[RT], float (&S)[2][RT][4]);
 
 template <int RT>
 __device__ __forceinline__ void running_stats(const float (&S)[2][RT][4], float (&m)[RT], float (&z)[RT]) {
@@ -749,11 +749,15 @@ __device__ __forceinline__ bf16x8 q_operand(const uint16_t* s_q, int rt, int ks,
 
 // Scaled (log2 domain), masked scores of one block for the stream variant
 // (Q operands from the LDS tile): -inf past the chunk, past the causal limit
-// of each verify row, and on padding rows.
+// of each verify row (lim: the last token the lane's row of each tile sees,
+// -1 on padding rows), and on padding rows.  A block every real row sees
+// whole is only scaled: its padding rows keep finite scores, whose
+// log-sum-exp the statistics set to +inf, so their probabilities are 0.
 template <int D, int RT>
 __device__ __forceinline__ void scores_block(const VArgs& a, const Unit& u, const uint4 (&Kr)[2][D / 32],
                                              const uint16_t* s_q, int tb, int n, int gq,
-                                             float (&S)[2][RT][4]) {
+                                             const int (&lim)[RT], float (&S)[2][RT][4]) {
+  const bool full = tb + 31 <= min(u.c1 - 1, u.ctx);  // row 0 sees the least
 #pragma unroll
   for (int tt = 0; tt < 2; ++tt) {
     floatx4 acc[RT];
@@ -767,15 +771,19 @@ __device__ __forceinline__ void scores_block(const VArgs& a, const Unit& u, cons
         acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, q_operand<D, RT>(s_q, rt, ks, n, gq), acc[rt],
                                                           0, 0, 0);
     }
+    if (full) {
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      const int row = u.rg * a.RT * 16 + rt * 16 + n;
-      const int lim = row < a.R ? min(u.c1 - 1, u.ctx + row / a.G) : -1;  // last visible token
+      for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int tok = tb + 16 * tt + 4 * gq + i;
-        S[tt][rt][i] = tok <= lim ? acc[rt][i] * a.sl2 : kNegInf;
-      }
+        for (int i = 0; i < 4; ++i) S[tt][rt][i] = acc[rt][i] * a.sl2;
+    } else {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int tok = tb + 16 * tt + 4 * gq + i;
+          S[tt][rt][i] = tok <= lim[rt] ? acc[rt][i] * a.sl2 : kNegInf;
+        }
     }
   }
 }
@@ -1283,13 +1291,19 @@ verify_mfma_kernel(VArgs a) {
     //      current two are scored (loads past the chunk are clamped, their
     //      scores masked, so every load is unconditional).
     const int nblk = (u.c1 - u.c0 + 31) / 32;
+    int lim[RT];  // last token the lane's row of each tile sees (-1: padding row)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int row = u.rg * a.RT * 16 + rt * 16 + n;
+      lim[rt] = row < a.R ? min(u.c1 - 1, u.ctx + row / a.G) : -1;
+    }
     auto score_pair = [&](const uint4 (&K2)[2][2][KS], int blk0) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int blk = blk0 + h * kWaves;
         if (blk < nblk) {
           float S[2][RT][4];
-          scores_block<D, RT>(a, u, K2[h], s_q, u.c0 + 32 * blk, n, gq, S);
+          scores_block<D, RT>(a, u, K2[h], s_q, u.c0 + 32 * blk, n, gq, lim, S);
           running_stats<RT>(S, m, z);
         }
       }
@@ -1324,7 +1338,7 @@ verify_mfma_kernel(VArgs a) {
     auto step = [&](const uint4 (&Kr)[2][KS], const VT (&Vr)[8], int blk) {
       const int tb = u.c0 + 32 * blk;
       float S[2][RT][4];
-      scores_block<D, RT>(a, u, Kr, s_q, tb, n, gq, S);
+      scores_block<D, RT>(a, u, Kr, s_q, tb, n, gq, lim, S);
       pv_block<D, RT>(S, lse, Vr, O, mp, tb, u.c1, n, gq);
     };
     if constexpr (RT <= 3) {
