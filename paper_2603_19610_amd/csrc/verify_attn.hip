@@ -441,9 +441,12 @@ __device__ __forceinline__ bf16x8 pack_v(const VT (&vr)[8], int jd) {
 // d in [32*ks + 8*gq, +8).  Tokens past the chunk load the chunk's last row
 // (their scores are masked), keeping the loads unconditional so the
 // compiler can wait for one block while the later ones stay in flight.
-template <int D>
+// NT: non-temporal loads (cache rows read once, so they need not displace the
+// exchange data in L2).
+template <int D, bool NT = false>
 __device__ __forceinline__ void load_k_block(const KvRows& kv, int tb, int c1, int n, int gq,
                                              uint4 (&Kr)[2][D / 32]) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
   int te;
   const uint16_t* r0 = kv_block<D>(kv, tb, c1, te);
 #pragma unroll
@@ -451,7 +454,12 @@ __device__ __forceinline__ void load_k_block(const KvRows& kv, int tb, int c1, i
     const int tok = min(tb + 16 * tt + n, c1 - 1);
     const uint16_t* kp = r0 + (size_t)(tok - te) * D + 8 * gq;
 #pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) Kr[tt][ks] = *reinterpret_cast<const uint4*>(kp + 32 * ks);
+    for (int ks = 0; ks < D / 32; ++ks) {
+      if constexpr (NT)
+        Kr[tt][ks] = __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kp + 32 * ks)));
+      else
+        Kr[tt][ks] = *reinterpret_cast<const uint4*>(kp + 32 * ks);
+    }
   }
 }
 
@@ -480,7 +488,7 @@ __device__ __forceinline__ void load_v_block(const KvRows& kv, int tb, int c1, i
 // does not track them (it would otherwise wait for them before any later LDS
 // access); untracked loads can only lengthen the compiler's own vmcnt waits.
 // The consumer waits explicitly (s_waitcnt vmcnt(0) + workgroup barrier).
-template <int D>
+template <int D, bool NT = false>
 __device__ __forceinline__ void issue_v_lds(const KvRows& kv, int tb, int c1, uint16_t* lds_blk,
                                             int lane) {
   constexpr int CPR = D / 8;    // 16-byte columns per row
@@ -493,10 +501,16 @@ __device__ __forceinline__ void issue_v_lds(const KvRows& kv, int tb, int c1, ui
     const int tok = min(tb + row, c1 - 1);
     const uint16_t* src = r0 + (size_t)(tok - te) * D + 8 * (lane % CPR);
     const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_addr(lds_blk + k * RPI * D));
-    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
-                 :
-                 : "s"(lds), "v"(src)
-                 : "memory", "m0");
+    if constexpr (NT)
+      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off nt"
+                   :
+                   : "s"(lds), "v"(src)
+                   : "memory", "m0");
+    else
+      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+                   :
+                   : "s"(lds), "v"(src)
+                   : "memory", "m0");
   }
 }
 
@@ -1190,7 +1204,7 @@ verify_mfma_kernel(VArgs a) {
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
-      load_k_block<D>(kg, u.c0 + 32 * (w + kWaves * j), u.c1, n, gq, Kr[j]);
+      load_k_block<D, true>(kg, u.c0 + 32 * (w + kWaves * j), u.c1, n, gq, Kr[j]);
       __builtin_amdgcn_sched_barrier(0);
     }
     // this wave's Q chunks have landed once at most the 8 * KS K loads issued
@@ -1205,7 +1219,7 @@ verify_mfma_kernel(VArgs a) {
     const int nblk = (u.c1 - u.c0 + 31) / 32;
     if (w > 0)
       for (int blk = w - 1; blk < nblk; blk += kWaves - 1)
-        issue_v_lds<D>(vg, u.c0 + 32 * blk, u.c1, s_v + blk * 32 * D, lane);
+        issue_v_lds<D, true>(vg, u.c0 + 32 * blk, u.c1, s_v + blk * 32 * D, lane);
     // a block every real row sees whole needs no mask (row 0 sees the least)
     const int vis_all = min(u.c1 - 1, u.ctx);
 #pragma unroll
