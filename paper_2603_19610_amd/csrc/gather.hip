@@ -80,10 +80,13 @@ __global__ void __launch_bounds__(256) gather_kernel(GArgs a) {
     si = (bg * a.n_cap + src) * a.row_vec + c;
   }
   const size_t di = (bg * a.dst_cap + r) * a.row_vec + c;
-  const uint4 kv = a.k[si];
-  const uint4 vv = a.v[si];
-  a.kd[di] = kv;
-  a.vd[di] = vv;
+  // a pure stream: every source row is read once and every destination row
+  // written once, so both go through the non-temporal cache policy
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 kv = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a.k) + si);
+  const u32x4 vv = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a.v) + si);
+  __builtin_nontemporal_store(kv, reinterpret_cast<u32x4*>(a.kd) + di);
+  __builtin_nontemporal_store(vv, reinterpret_cast<u32x4*>(a.vd) + di);
 }
 
 }  // namespace
