@@ -44,13 +44,19 @@ __global__ void __launch_bounds__(256) uv_mass_kernel(const float* crit, const i
   score[gid] = i < mb ? cL - c0 : 0.f;
 }
 
-// Hidden-state element loads: 8 consecutive elements, widened exactly.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Hidden-state element loads: 8 consecutive elements, widened exactly.  NT:
+// through the non-temporal cache policy (rows streamed once).
 template <typename T>
 struct HS;
 template <>
 struct HS<uint16_t> {
+  template <bool NT = false>
   static __device__ __forceinline__ void load8(const uint16_t* p, float (&f)[8]) {
-    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    const u32x4 v = NT ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p))
+                       : *reinterpret_cast<const u32x4*>(p);
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -61,9 +67,12 @@ struct HS<uint16_t> {
 };
 template <>
 struct HS<float> {
+  template <bool NT = false>
   static __device__ __forceinline__ void load8(const float* p, float (&f)[8]) {
-    const float4 a = *reinterpret_cast<const float4*>(p);
-    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    const f32x4 a = NT ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p))
+                       : *reinterpret_cast<const f32x4*>(p);
+    const f32x4 b = NT ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + 4))
+                       : *reinterpret_cast<const f32x4*>(p + 4);
     f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
     f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
   }
@@ -72,6 +81,7 @@ struct HS<float> {
 // The prefill epilogue's residual add: out = prev + delta, the sum taken in
 // fp32 and rounded once to the storage type; the rounded values are stored
 // and returned, so the criterion uses exactly the stored hidden state.
+template <bool NT>
 __device__ __forceinline__ void add_round_store8(uint16_t* out, float (&f)[8], const float (&g)[8]) {
   uint32_t w[4];
 #pragma unroll
@@ -81,24 +91,36 @@ __device__ __forceinline__ void add_round_store8(uint16_t* out, float (&f)[8], c
     f[2 * k] = bf16_to_f32(lo);
     f[2 * k + 1] = bf16_to_f32(hi);
   }
-  *reinterpret_cast<uint4*>(out) = make_uint4(w[0], w[1], w[2], w[3]);
+  const u32x4 v = {w[0], w[1], w[2], w[3]};
+  if constexpr (NT) __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(out));
+  else *reinterpret_cast<u32x4*>(out) = v;
 }
+template <bool NT>
 __device__ __forceinline__ void add_round_store8(float* out, float (&f)[8], const float (&g)[8]) {
 #pragma unroll
   for (int k = 0; k < 8; ++k) f[k] += g[k];
-  *reinterpret_cast<float4*>(out) = make_float4(f[0], f[1], f[2], f[3]);
-  *reinterpret_cast<float4*>(out + 4) = make_float4(f[4], f[5], f[6], f[7]);
+  const f32x4 a = {f[0], f[1], f[2], f[3]}, b = {f[4], f[5], f[6], f[7]};
+  if constexpr (NT) {
+    __builtin_nontemporal_store(a, reinterpret_cast<f32x4*>(out));
+    __builtin_nontemporal_store(b, reinterpret_cast<f32x4*>(out + 4));
+  } else {
+    *reinterpret_cast<f32x4*>(out) = a;
+    *reinterpret_cast<f32x4*>(out + 4) = b;
+  }
 }
 
 // 8 consecutive elements of a hidden-state row at element offset `off`: the
 // row itself, or (FUSED) the epilogue's prev + delta, written to `out`.
-template <typename T, bool FUSED>
+// NT: the visual rows, streamed once, go through the non-temporal cache
+// policy; the text rows are read again by the direction sums and keep the
+// ordinary one.
+template <typename T, bool FUSED, bool NT = false>
 __device__ __forceinline__ void row8(const T* h, const T* delta, T* out, size_t off, float (&f)[8]) {
-  HS<T>::load8(h + off, f);
+  HS<T>::template load8<NT>(h + off, f);
   if constexpr (FUSED) {
     float g[8];
-    HS<T>::load8(delta + off, g);
-    add_round_store8(out + off, f, g);
+    HS<T>::template load8<NT>(delta + off, g);
+    add_round_store8<NT>(out + off, f, g);
   }
 }
 
@@ -232,7 +254,7 @@ __global__ void __launch_bounds__(kVisThreads) vis_kernel(const T* hv, int64_t o
 #pragma unroll 8  // the row's loads in flight together
         for (int j = lane; j < D8; j += 64) {
           float f[8];
-          row8<T, FUSED>(hv, dv, ov, roff + 8 * j, f);
+          row8<T, FUSED, true>(hv, dv, ov, roff + 8 * j, f);
 #pragma unroll
           for (int k = 0; k < 8; ++k) {
             dot = fma((double)f[k], us[k * D8 + j], dot);
