@@ -466,17 +466,22 @@ __device__ __forceinline__ void load_k_block(const KvRows& kv, int tb, int c1, i
 // V operand rows of one 32-token block: lane (n, gq) loads tokens
 // tb + {4gq..4gq+3, 16+4gq..16+4gq+3}, d in [DPL*n, DPL*n + DPL).  Tokens past
 // the chunk load its last row (their probabilities are 0).
-template <int D>
+template <int D, bool NT = false>
 __device__ __forceinline__ void load_v_block(const KvRows& kv, int tb, int c1, int n, int gq,
                                              typename VVec<D>::T (&Vr)[8]) {
   typedef typename VVec<D>::T VT;
+  typedef uint32_t vec_t __attribute__((ext_vector_type(sizeof(VT) / 4)));
   constexpr int DPL = D / 16;
   int te;
   const uint16_t* r0 = kv_block<D>(kv, tb, c1, te);
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
     const int tok = min(tb + (s < 4 ? 4 * gq + s : 16 + 4 * gq + (s - 4)), c1 - 1);
-    Vr[s] = *reinterpret_cast<const VT*>(r0 + (size_t)(tok - te) * D + DPL * n);
+    const uint16_t* p = r0 + (size_t)(tok - te) * D + DPL * n;
+    if constexpr (NT)
+      Vr[s] = __builtin_bit_cast(VT, __builtin_nontemporal_load(reinterpret_cast<const vec_t*>(p)));
+    else
+      Vr[s] = *reinterpret_cast<const VT*>(p);
   }
 }
 
@@ -531,7 +536,7 @@ __device__ __forceinline__ void read_v_lds(const uint16_t* lds_blk, int n, int g
 // chunks XOR-swizzled by row, so the MFMA operand reads hit distinct banks),
 // through untracked global->LDS loads like issue_v_lds.  Rows past the chunk
 // re-read its last row.
-template <int D>
+template <int D, bool NT = false>
 __device__ __forceinline__ void issue_k_lds(const KvRows& kv, int tb, int c1, uint16_t* lds_blk,
                                             int lane) {
   constexpr int CH = D / 8;
@@ -543,10 +548,16 @@ __device__ __forceinline__ void issue_k_lds(const KvRows& kv, int tb, int c1, ui
     const int slot = ins * 64 + lane, r = slot / CH, c = (slot % CH) ^ (r % CH);
     const uint16_t* src = r0 + (size_t)(min(tb + r, c1 - 1) - te) * D + 8 * c;
     const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_addr(lds_blk + ins * 64 * 8));
-    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
-                 :
-                 : "s"(lds), "v"(src)
-                 : "memory", "m0");
+    if constexpr (NT)
+      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off nt"
+                   :
+                   : "s"(lds), "v"(src)
+                   : "memory", "m0");
+    else
+      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+                   :
+                   : "s"(lds), "v"(src)
+                   : "memory", "m0");
   }
 }
 
@@ -1344,7 +1355,9 @@ verify_mfma_kernel(VArgs a) {
     for (int rt = 0; rt < RT; ++rt) lse[rt] = s_lse[rt * 16 + n];
     // ---- pass 2: recompute scores from K, then P, mass and P.V, the next
     //      block's K and V loading during this one (in registers up to 3 row
-    //      tiles; with more, in LDS).
+    //      tiles; with more, in LDS).  This is the rows' last read, so its
+    //      loads are non-temporal; pass 1's are not, because its K stays
+    //      cached for this re-read.
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -1358,16 +1371,16 @@ verify_mfma_kernel(VArgs a) {
     if constexpr (RT <= 3) {
       uint4 Ka[2][KS], Kb[2][KS];
       VT Va[8], Vb[8];
-      load_k_block<D>(kg, u.c0 + 32 * w, u.c1, n, gq, Ka);
-      load_v_block<D>(vg, u.c0 + 32 * w, u.c1, n, gq, Va);
+      load_k_block<D, true>(kg, u.c0 + 32 * w, u.c1, n, gq, Ka);
+      load_v_block<D, true>(vg, u.c0 + 32 * w, u.c1, n, gq, Va);
       for (int blk = w; blk < nblk; blk += 2 * kWaves) {
         const int b2 = blk + kWaves;
-        load_k_block<D>(kg, u.c0 + 32 * b2, u.c1, n, gq, Kb);
-        load_v_block<D>(vg, u.c0 + 32 * b2, u.c1, n, gq, Vb);
+        load_k_block<D, true>(kg, u.c0 + 32 * b2, u.c1, n, gq, Kb);
+        load_v_block<D, true>(vg, u.c0 + 32 * b2, u.c1, n, gq, Vb);
         step(Ka, Va, blk);
         if (b2 >= nblk) break;
-        load_k_block<D>(kg, u.c0 + 32 * (b2 + kWaves), u.c1, n, gq, Ka);
-        load_v_block<D>(vg, u.c0 + 32 * (b2 + kWaves), u.c1, n, gq, Va);
+        load_k_block<D, true>(kg, u.c0 + 32 * (b2 + kWaves), u.c1, n, gq, Ka);
+        load_v_block<D, true>(vg, u.c0 + 32 * (b2 + kWaves), u.c1, n, gq, Va);
         step(Kb, Vb, b2);
       }
     } else {
@@ -1380,8 +1393,8 @@ verify_mfma_kernel(VArgs a) {
       uint16_t* kv = s_q + RT * 16 * D + w * 4 * 32 * D;  // [2 buffers][K, V][32][D]
       __builtin_amdgcn_s_waitcnt(0);                       // the counts below start from zero
       if (w < nblk) {
-        issue_k_lds<D>(kg, u.c0 + 32 * w, u.c1, kv, lane);
-        issue_v_lds<D>(vg, u.c0 + 32 * w, u.c1, kv + 32 * D, lane);
+        issue_k_lds<D, true>(kg, u.c0 + 32 * w, u.c1, kv, lane);
+        issue_v_lds<D, true>(vg, u.c0 + 32 * w, u.c1, kv + 32 * D, lane);
       }
       int i = 0;
       for (int blk = w; blk < nblk; blk += kWaves, ++i) {
@@ -1389,8 +1402,8 @@ verify_mfma_kernel(VArgs a) {
         const bool next = blk + kWaves < nblk;
         if (next) {
           uint16_t* nxt = kv + ((i + 1) & 1) * 2 * 32 * D;
-          issue_k_lds<D>(kg, u.c0 + 32 * (blk + kWaves), u.c1, nxt, lane);
-          issue_v_lds<D>(vg, u.c0 + 32 * (blk + kWaves), u.c1, nxt + 32 * D, lane);
+          issue_k_lds<D, true>(kg, u.c0 + 32 * (blk + kWaves), u.c1, nxt, lane);
+          issue_v_lds<D, true>(vg, u.c0 + 32 * (blk + kWaves), u.c1, nxt + 32 * D, lane);
         }
         wait_vm_younger<D>((i > 0 ? 1 : 0) + (next ? kBlockDma<D> : 0));
         uint4 Kr[2][KS];
