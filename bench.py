@@ -731,30 +731,45 @@ def overlap_record(torch, pv, W, dev, gamma=5, reps=50):
     return rec
 
 
-def tiles(w):
-    """16-row MFMA tiles per workgroup for the packed query rows of a KV head."""
+def verify_plan(w, cus=256, xcds=8):
+    """The verify launch plan the library picks for this shape: (row tiles per
+    workgroup, row groups, splits, chunk tokens, resident, wide).  One
+    workgroup per CU; rows split into groups of at most 5 tiles, more groups
+    when the (batch, KV head) pairs are fewer than the XCDs; resident scores
+    for chunks of at most 512 tokens; one group of 9 tiles (wide variant, two
+    workgroups per CU) in place of two groups for streamed chunks."""
     rtt = -(-w.group * w.T // 16)
+    n = int(w.lengths().max()) + w.T
+
+    def layout(rg, slots=cus):
+        per_launch = min(w.batch * w.hkv * rg, slots)
+        splits = max(1, slots // per_launch)
+        chunk = -(-(-(-n // splits)) // 32) * 32
+        return per_launch, -(-n // chunk), chunk
+
     rg = -(-rtt // 5)
-    return -(-rtt // rg)
+    if w.batch * w.hkv * rg < xcds and rtt > rg:
+        rg = min(-(-xcds // (w.batch * w.hkv)), rtt)
+    rt = -(-rtt // rg)
+    per_launch, splits, chunk = layout(rg)
+    resident = chunk <= 512
+    wide = not resident and 5 < rtt <= 9 and w.batch * w.hkv >= xcds
+    if wide:  # two workgroups per CU
+        rg, rt = 1, 9
+        per_launch, splits, chunk = layout(rg, 2 * cus)
+    return rt, rg, per_launch, splits, chunk, resident, wide
 
 
 def verify_kernel_label(w, cus=256, xcds=8):
-    """The verify kernel variant the library's launch plan picks for this shape
-    (one workgroup per CU; resident scores for chunks of at most 512 tokens;
-    same-XCD exchange when every group's workgroups share an XCD)."""
-    rtt = -(-w.group * w.T // 16)
-    rg = -(-rtt // 5)
-    groups = w.batch * w.hkv * rg
-    per_launch = min(groups, cus)
-    splits = max(1, cus // per_launch)
-    n = int(w.lengths().max()) + w.T
-    chunk = -(-(-(-n // splits)) // 32) * 32
-    splits = -(-n // chunk)
+    """The verify kernel variant of the launch plan (same-XCD exchange when
+    every group's workgroups share an XCD)."""
+    rt, rg, per_launch, splits, chunk, resident, wide = verify_plan(w, cus, xcds)
     grid = -(-per_launch * splits // 8) * 8
-    resident = chunk <= 512
     local = grid % xcds == 0 and (grid // xcds) % splits == 0
-    return (f"verify_mfma_kernel<{w.head_dim},{tiles(w)},{'resident' if resident else 'stream'},"
-            f"{'same-XCD' if local else 'cross-XCD'}>")
+    where = "same-XCD" if local else "cross-XCD"
+    if wide:
+        return f"verify_wide_kernel<{w.head_dim},{where}>"
+    return f"verify_mfma_kernel<{w.head_dim},{rt},{'resident' if resident else 'stream'},{where}>"
 
 
 def teardown(torch, pv, *objs):

@@ -729,6 +729,30 @@ __device__ __forceinline__ void mass_reduce_store(const float (&pm)[8], float* m
   if (!(n & 1) && tok < c1) st_agent(mp + tok, a2);
 }
 
+// The same per-token sums of one block written to LDS (dst[token - tb] for
+// the block's 32 tokens).  Kept apart from mass_reduce_store: sharing one
+// helper changed the register allocation of the kernels that use that one.
+__device__ __forceinline__ void mass_reduce_lds(const float (&pm)[8], float* dst, int n, int gq) {
+  const bool h8 = n & 8, h4 = n & 4, h2 = n & 2;
+  float a8[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float send = h8 ? pm[k] : pm[4 + k];
+    a8[k] = (h8 ? pm[4 + k] : pm[k]) + lane_xor8(send);
+  }
+  float a4[2];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const float send = h4 ? a8[k] : a8[2 + k];
+    a4[k] = (h4 ? a8[2 + k] : a8[k]) + lane_mirror8(send);
+  }
+  const float send2 = h2 ? a4[0] : a4[1];
+  float a2 = (h2 ? a4[1] : a4[0]) + lane_xor2(send2);
+  a2 += lane_xor1(a2);
+  const int v = (h8 ? 4 : 0) + (h4 ? 2 : 0) + (h2 ? 1 : 0);
+  if (!(n & 1)) dst[16 * (v >> 2) + 4 * gq + (v & 3)] = a2;
+}
+
 // ---- resident variant: the raw score accumulators stay exactly as the MFMA
 // produced them (unscaled, unmasked), which lets the compiler keep them in
 // accumulation registers; the scale and the causal / chunk-end mask are
@@ -772,16 +796,18 @@ __device__ __forceinline__ bf16x8 q_operand(const uint16_t* s_q, int rt, int ks,
       bf16x8, *reinterpret_cast<const uint4*>(s_q + (r * CH + (c ^ (r % CH))) * 8));
 }
 
-// Scaled (log2 domain), masked scores of one block for the stream variant
-// (Q operands from the LDS tile): -inf past the chunk, past the causal limit
-// of each verify row (lim: the last token the lane's row of each tile sees,
-// -1 on padding rows), and on padding rows.  A block every real row sees
-// whole is only scaled: its padding rows keep finite scores, whose
-// log-sum-exp the statistics set to +inf, so their probabilities are 0.
-template <int D, int RT>
-__device__ __forceinline__ void scores_block(const VArgs& a, const Unit& u, const uint4 (&Kr)[2][D / 32],
-                                             const uint16_t* s_q, int tb, int n, int gq,
-                                             const int (&lim)[RT], float (&S)[2][RT][4]) {
+// Scaled (log2 domain), masked scores of one block for the two-pass variants
+// (qop(rt, ks): the Q operand of tile rt, k-step ks): -inf past the chunk,
+// past the causal limit of each verify row (lim: the last token the lane's
+// row of each tile sees, -1 on padding rows), and on padding rows.  A block
+// every real row sees whole is only scaled: its padding rows keep finite
+// scores, whose log-sum-exp the statistics set to +inf, so their
+// probabilities are 0.
+template <int D, int RT, bool SCALED = true, typename QOp>
+__device__ __forceinline__ void scores_from(const VArgs& a, const Unit& u, const uint4 (&Kr)[2][D / 32],
+                                            QOp qop, int tb, int gq, const int (&lim)[RT],
+                                            float (&S)[2][RT][4]) {
+  const float sc = SCALED ? a.sl2 : 1.f;
   const bool full = tb + 31 <= min(u.c1 - 1, u.ctx);  // row 0 sees the least
 #pragma unroll
   for (int tt = 0; tt < 2; ++tt) {
@@ -793,24 +819,32 @@ __device__ __forceinline__ void scores_block(const VArgs& a, const Unit& u, cons
       const bf16x8 kk = __builtin_bit_cast(bf16x8, Kr[tt][ks]);
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
-        acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, q_operand<D, RT>(s_q, rt, ks, n, gq), acc[rt],
-                                                          0, 0, 0);
+        acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qop(rt, ks), acc[rt], 0, 0, 0);
     }
     if (full) {
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) S[tt][rt][i] = acc[rt][i] * a.sl2;
+        for (int i = 0; i < 4; ++i) S[tt][rt][i] = SCALED ? acc[rt][i] * sc : acc[rt][i];
     } else {
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int tok = tb + 16 * tt + 4 * gq + i;
-          S[tt][rt][i] = tok <= lim[rt] ? acc[rt][i] * a.sl2 : kNegInf;
+          S[tt][rt][i] = tok <= lim[rt] ? (SCALED ? acc[rt][i] * sc : acc[rt][i]) : kNegInf;
         }
     }
   }
+}
+
+// ... with the Q operands read from the workgroup's LDS tile (stream variant).
+template <int D, int RT>
+__device__ __forceinline__ void scores_block(const VArgs& a, const Unit& u, const uint4 (&Kr)[2][D / 32],
+                                             const uint16_t* s_q, int tb, int n, int gq,
+                                             const int (&lim)[RT], float (&S)[2][RT][4]) {
+  scores_from<D, RT>(a, u, Kr, [&](int rt, int ks) { return q_operand<D, RT>(s_q, rt, ks, n, gq); }, tb,
+                     gq, lim, S);
 }
 
 template <int D, int RT>
@@ -913,17 +947,13 @@ __device__ __forceinline__ void pv_exact_resident(const floatx4 (&P)[2][RT], con
   }
 }
 
-// P = exp2(S - lse2): per-token mass (sum over the block's rows, written to
-// mp) and O += P.V on MFMA.
-template <int D, int RT>
-__device__ __forceinline__ void pv_block(const float (&S)[2][RT][4], const float (&lse)[RT],
-                                         const typename VVec<D>::T (&Vr)[8], floatx4 (&O)[RT][D / 16],
-                                         float* mp, int tb, int c1, int n, int gq) {
-  constexpr int DPL = D / 16;
-  float pm[8];
+// P = exp2(S - lse2) of one block: the MFMA A operands (bf16) and each
+// lane's per-token sums over its rows.
+template <int RT>
+__device__ __forceinline__ void probs_block(const float (&S)[2][RT][4], const float (&lse)[RT],
+                                            bf16x8 (&Pa)[RT], float (&pm)[8]) {
 #pragma unroll
   for (int v = 0; v < 8; ++v) pm[v] = 0.f;
-  bf16x8 Pa[RT];
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
@@ -935,29 +965,13 @@ __device__ __forceinline__ void pv_block(const float (&S)[2][RT][4], const float
         Pa[rt][4 * tt + i] = static_cast<__bf16>(p);
       }
   }
-  // mass: sum the 8 token values over the 16 lanes of a lane group
-  // transpose-reduce: each step a lane keeps half of its values (chosen by
-  // one bit of n) and adds the partner's copy of that half; partners differ
-  // in that bit (n^8, then n^7 within each 8, n^2, n^1)
-  const bool h8 = n & 8, h4 = n & 4, h2 = n & 2;
-  float a8[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const float send = h8 ? pm[k] : pm[4 + k];
-    a8[k] = (h8 ? pm[4 + k] : pm[k]) + lane_xor8(send);
-  }
-  float a4[2];
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const float send = h4 ? a8[k] : a8[2 + k];
-    a4[k] = (h4 ? a8[2 + k] : a8[k]) + lane_mirror8(send);
-  }
-  const float send2 = h2 ? a4[0] : a4[1];
-  float a2 = (h2 ? a4[1] : a4[0]) + lane_xor2(send2);
-  a2 += lane_xor1(a2);
-  const int v = (h8 ? 4 : 0) + (h4 ? 2 : 0) + (h2 ? 1 : 0);
-  const int tok = tb + 16 * (v >> 2) + 4 * gq + (v & 3);
-  if (!(n & 1) && tok < c1) st_agent(mp + tok, a2);
+}
+
+// O += P.V of one block on MFMA.
+template <int D, int RT>
+__device__ __forceinline__ void pv_mfma(const bf16x8 (&Pa)[RT], const typename VVec<D>::T (&Vr)[8],
+                                        floatx4 (&O)[RT][D / 16]) {
+  constexpr int DPL = D / 16;
 #pragma unroll
   for (int jd = 0; jd < DPL; ++jd) {
     const bf16x8 vb = pack_v(Vr, jd);
@@ -965,6 +979,19 @@ __device__ __forceinline__ void pv_block(const float (&S)[2][RT][4], const float
     for (int rt = 0; rt < RT; ++rt)
       O[rt][jd] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Pa[rt], vb, O[rt][jd], 0, 0, 0);
   }
+}
+
+// P = exp2(S - lse2): per-token mass (sum over the block's rows, written to
+// mp) and O += P.V on MFMA.
+template <int D, int RT>
+__device__ __forceinline__ void pv_block(const float (&S)[2][RT][4], const float (&lse)[RT],
+                                         const typename VVec<D>::T (&Vr)[8], floatx4 (&O)[RT][D / 16],
+                                         float* mp, int tb, int c1, int n, int gq) {
+  bf16x8 Pa[RT];
+  float pm[8];
+  probs_block<RT>(S, lse, Pa, pm);
+  mass_reduce_store(pm, mp, tb, c1, n, gq);
+  pv_mfma<D, RT>(Pa, Vr, O);
 }
 
 // Sum the four waves' O fragments and write the chunk partial (row-major
@@ -1128,6 +1155,40 @@ __device__ void empty_chunk(const VArgs& a, const Unit& u, const float* s_m, con
   mass_combine(a, u, s_flag);
 }
 
+// This (batch, KV head)'s K and V rows: a padded cache's base, or the pool
+// through the page table, the chunk's page entries checked against the pool,
+// clamped into it and staged in LDS when they fit (every thread takes part).
+template <int D>
+__device__ __forceinline__ void kv_rows_setup(const VArgs& a, const Unit& u, int32_t* s_pages, KvRows& kg,
+                                              KvRows& vg) {
+  if (a.table) {
+    const size_t hoff = ((size_t)u.g << a.page_shift) * D;
+    const int32_t* tab = a.table + (size_t)u.b * a.max_pages;
+    const int64_t pe = ((int64_t)a.Hkv << a.page_shift) * D;
+    // The chunk's page entries, checked against the pool, clamped into it
+    // and staged in LDS when they fit.
+    const int p0 = u.c0 >> a.page_shift, p1 = (u.c1 - 1) >> a.page_shift;
+    const bool fit = p1 - p0 < kPageSlots;
+    for (int pg = p0 + threadIdx.x; pg <= p1; pg += kThreads) {
+      int e = tab[pg];
+      if (e < 0 || e >= a.n_pages) {
+        dev_flag(a.status, PVLM_DEV_RANGE);
+        e = e < 0 ? 0 : (int)(a.n_pages - 1);
+      }
+      if (fit) s_pages[pg - p0] = e;
+    }
+    __syncthreads();
+    kg = {static_cast<const uint16_t*>(a.k) + hoff, tab, s_pages, pe, a.n_pages, a.page_shift, p0,
+          true, fit};
+    vg = {static_cast<const uint16_t*>(a.v) + hoff, tab, s_pages, pe, a.n_pages, a.page_shift, p0,
+          true, fit};
+  } else {
+    const size_t kv_off = ((size_t)u.b * a.Hkv + u.g) * a.n_cap * D;
+    kg = {static_cast<const uint16_t*>(a.k) + kv_off, a.ctx_len, s_pages, 0, 1, 5, 0, false, false};
+    vg = {static_cast<const uint16_t*>(a.v) + kv_off, a.ctx_len, s_pages, 0, 1, 5, 0, false, false};
+  }
+}
+
 template <int D, int RT, bool RESIDENT, bool LOCAL>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 verify_mfma_kernel(VArgs a) {
@@ -1156,32 +1217,7 @@ verify_mfma_kernel(VArgs a) {
     return;
   }
   KvRows kg, vg;  // this (batch, KV head)'s K and V rows
-  if (a.table) {
-    const size_t hoff = ((size_t)u.g << a.page_shift) * D;
-    const int32_t* tab = a.table + (size_t)u.b * a.max_pages;
-    const int64_t pe = ((int64_t)a.Hkv << a.page_shift) * D;
-    // The chunk's page entries, checked against the pool, clamped into it
-    // and staged in LDS when they fit.
-    const int p0 = u.c0 >> a.page_shift, p1 = (u.c1 - 1) >> a.page_shift;
-    const bool fit = p1 - p0 < kPageSlots;
-    for (int pg = p0 + threadIdx.x; pg <= p1; pg += kThreads) {
-      int e = tab[pg];
-      if (e < 0 || e >= a.n_pages) {
-        dev_flag(a.status, PVLM_DEV_RANGE);
-        e = e < 0 ? 0 : (int)(a.n_pages - 1);
-      }
-      if (fit) s_pages[pg - p0] = e;
-    }
-    __syncthreads();
-    kg = {static_cast<const uint16_t*>(a.k) + hoff, tab, s_pages, pe, a.n_pages, a.page_shift, p0,
-          true, fit};
-    vg = {static_cast<const uint16_t*>(a.v) + hoff, tab, s_pages, pe, a.n_pages, a.page_shift, p0,
-          true, fit};
-  } else {
-    const size_t kv_off = ((size_t)u.b * a.Hkv + u.g) * a.n_cap * D;
-    kg = {static_cast<const uint16_t*>(a.k) + kv_off, a.ctx_len, s_pages, 0, 1, 5, 0, false, false};
-    vg = {static_cast<const uint16_t*>(a.v) + kv_off, a.ctx_len, s_pages, 0, 1, 5, 0, false, false};
-  }
+  kv_rows_setup<D>(a, u, s_pages, kg, vg);
   float* mp = a.mpart + ((size_t)u.b * a.Hkv * a.RG + u.g * a.RG + u.rg) * a.n_cap;
 
   float m[RT], z[RT];
@@ -1419,6 +1455,261 @@ verify_mfma_kernel(VArgs a) {
   verify_epilogue<ROWS, D, LOCAL>(a, u, s_lse, false, &s_flag, base);
 }
 
+// ------------------------------------------------------- wide variant --
+// Long chunks with more row tiles than one wave's accumulators hold (6 .. 9
+// tiles, e.g. 136 verify rows per KV head).  One workgroup holds every row,
+// so each cache row is read once per pass for all of them instead of once
+// per row group.  Waves 0-2 own three row tiles each (Q operands in
+// registers, O accumulators over the whole head dimension) and score every
+// token of the chunk; wave 3 streams the blocks into a ring of LDS slots that
+// the three read: K in pass 1, K and V in pass 2.  One workgroup barrier per
+// block hands a landed slot to the compute waves and the slot they finished
+// back to the loader.  The loader issues no other vector memory operation in
+// its loops, so its waits count its own global->LDS loads (which complete in
+// issue order).  Scores stay unscaled; the scale goes into the exponent
+// (one fused multiply-add per score).
+constexpr int kWideRT = 9;      // row tiles per workgroup
+constexpr int kWideTW = 3;      // row tiles per compute wave (waves 0 .. 2)
+constexpr int kWideSlots1 = 8;  // pass-1 ring: one K block per slot
+constexpr int kWideSlots2 = 4;  // pass-2 ring: a K and a V block per slot
+// Two workgroups per CU (registers and LDS allow it), so that on every SIMD
+// one workgroup's MFMA and exponentials overlap the other's barrier waits.
+constexpr int kWidePerCU = 2;
+static_assert(kWideRT == kWideTW * (kWaves - 1), "waves 0..2 compute, wave 3 loads");
+
+// Wait until at most `younger` groups of PER loads are outstanding (younger
+// in [0, K], wave-uniform; any other value waits for all).
+template <int PER, int K>
+__device__ __forceinline__ void wait_vm_groups(int younger) {
+  static_assert(K * PER < 64, "vmcnt holds 6 bits");
+  if constexpr (K == 0) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  } else {
+    if (younger == K)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(K * PER) : "memory");
+    else
+      wait_vm_groups<PER, K - 1>(younger);
+  }
+}
+
+// running_stats for unscaled scores: the row maximum in the scaled (log2)
+// domain, exp2(s * sl2 - M) as one fused multiply-add and an exponential.
+template <int RT>
+__device__ __forceinline__ void running_stats_raw(const float (&S)[2][RT][4], float sl2, float (&m)[RT],
+                                                  float (&z)[RT]) {
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    float mx = kNegInf;
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mx = fmaxf(mx, S[tt][rt][i]);
+    const float M = fmaxf(m[rt], mx * sl2);
+    if (M != kNegInf) {
+      float acc = z[rt] * fast_exp2(m[rt] - M);
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc += fast_exp2(fmaf(S[tt][rt][i], sl2, -M));
+      z[rt] = acc;
+      m[rt] = M;
+    }
+  }
+}
+
+// probs_block for unscaled scores: p = exp2(s * sl2 - lse2).
+template <int RT>
+__device__ __forceinline__ void probs_raw(const float (&S)[2][RT][4], float sl2, const float (&lse)[RT],
+                                          bf16x8 (&Pa)[RT], float (&pm)[8]) {
+#pragma unroll
+  for (int v = 0; v < 8; ++v) pm[v] = 0.f;
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = fast_exp2(fmaf(S[tt][rt][i], sl2, -lse[rt]));
+        pm[4 * tt + i] += p;
+        Pa[rt][4 * tt + i] = static_cast<__bf16>(p);
+      }
+}
+
+// A compute wave's chunk partial of O (its three row tiles, whole head
+// dimension; bf16, row-major [ROWS][D]): no reduction across waves.
+template <int D, bool LOCAL>
+__device__ __forceinline__ void write_opart_wide(const VArgs& a, const Unit& u,
+                                                 const floatx4 (&O)[kWideTW][D / 16], int t0, int n, int gq) {
+  constexpr int DPL = D / 16, ROWS = kWideRT * 16;
+  uint64_t* op = reinterpret_cast<uint64_t*>(a.opart) + ((size_t)u.grp * a.splits + u.split) * ROWS * D / 4;
+#pragma unroll
+  for (int t = 0; t < kWideTW; ++t)
+#pragma unroll
+    for (int h = 0; h < DPL / 4; ++h)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = (t0 + t) * 16 + 4 * gq + i;
+        x_store<LOCAL>(op + (row * D + DPL * n + 4 * h) / 4,
+                       pack_bf16x4(O[t][4 * h][i], O[t][4 * h + 1][i], O[t][4 * h + 2][i], O[t][4 * h + 3][i]));
+      }
+}
+
+template <int D, bool LOCAL>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kWidePerCU, kWidePerCU)))
+verify_wide_kernel(VArgs a) {
+  constexpr int RT = kWideRT, TW = kWideTW, ROWS = RT * 16, KS = D / 32, DPL = D / 16;
+  constexpr int BLK = 32 * D;              // bf16 elements of one 32-token K or V block
+  constexpr int KDMA = 32 * (D / 8) / 64;  // global->LDS loads per K (or V) block
+  constexpr int S1 = kWideSlots1, S2 = kWideSlots2;
+  typedef typename VVec<D>::T VT;
+  __shared__ float s_wm[kWaves][ROWS], s_wz[kWaves][ROWS];
+  __shared__ float s_m[ROWS], s_z[ROWS], s_lse[ROWS];
+  __shared__ float s_mass[2][TW][32];  // per-token sums of a block over each compute wave's rows
+  __shared__ int s_flag;
+  __shared__ int32_t s_pages[kPageSlots];
+  extern __shared__ __align__(256) float s_o[];
+
+  Unit u;
+  if (!decode_unit(a, u)) return;
+  const unsigned base = read_base(a, u);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n = lane & 15, gq = lane >> 4;
+  if (u.c0 >= u.N) {  // chunk past this sequence's end: empty statistics, no wait
+    for (int r = threadIdx.x; r < ROWS; r += kThreads) {
+      s_m[r] = kNegInf;
+      s_z[r] = 0.f;
+    }
+    __syncthreads();
+    empty_chunk<ROWS, LOCAL>(a, u, s_m, s_z, base, &s_flag);
+    return;
+  }
+  KvRows kg, vg;
+  kv_rows_setup<D>(a, u, s_pages, kg, vg);
+  float* mp = a.mpart + ((size_t)u.b * a.Hkv * a.RG + u.g * a.RG + u.rg) * a.n_cap;
+  uint16_t* ring = reinterpret_cast<uint16_t*>(s_o);
+  const bool loader = __builtin_amdgcn_readfirstlane(w) == kWaves - 1;
+  const int nblk = (u.c1 - u.c0 + 31) / 32;
+  const float sl2 = a.sl2;
+
+  // The Q tile through LDS into each compute wave's operand registers (the
+  // loader's copy is unused); the ring then reuses that LDS.
+  issue_q_lds<D, RT>(a, u, ring, w, lane);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  lds_sync();
+  const int t0 = loader ? 0 : w * TW;  // first row tile of this wave
+  bf16x8 Qr[TW][KS];
+  int lim[TW];  // last token the lane's row of each tile sees (-1: padding row)
+#pragma unroll
+  for (int t = 0; t < TW; ++t) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) Qr[t][ks] = q_operand<D, RT>(ring, t0 + t, ks, n, gq);
+    const int row = (t0 + t) * 16 + n;
+    lim[t] = row < a.R ? min(u.c1 - 1, u.ctx + row / a.G) : -1;
+  }
+  lds_sync();
+  auto qop = [&](int t, int ks) { return Qr[t][ks]; };
+
+  // ---- pass 1: running row statistics over the chunk
+  float m[TW], z[TW];
+#pragma unroll
+  for (int t = 0; t < TW; ++t) {
+    m[t] = kNegInf;
+    z[t] = 0.f;
+  }
+  if (loader) {
+    for (int s = 0; s < S1 && s < nblk; ++s) issue_k_lds<D>(kg, u.c0 + 32 * s, u.c1, ring + s * BLK, lane);
+    for (int j = 0; j < nblk; ++j) {
+      // blocks issued so far: the first S1, then one per barrier after the first
+      const int issued = min(nblk, S1 + max(j - 1, 0));
+      wait_vm_groups<KDMA, S1 - 1>(issued - j - 1);
+      lds_sync();  // block j landed; every compute wave is done with block j - 1
+      const int nb = j - 1 + S1;
+      if (j >= 1 && nb < nblk) issue_k_lds<D>(kg, u.c0 + 32 * nb, u.c1, ring + (nb % S1) * BLK, lane);
+    }
+  } else {
+    for (int j = 0; j < nblk; ++j) {
+      lds_sync();
+      uint4 Kr[2][KS];
+      read_k_lds<D>(ring + (j % S1) * BLK, n, gq, Kr);
+      float S[2][TW][4];
+      scores_from<D, TW, false>(a, u, Kr, qop, u.c0 + 32 * j, gq, lim, S);
+      running_stats_raw<TW>(S, sl2, m, z);
+    }
+  }
+  lds_sync();  // the ring is free
+  if (!loader) {
+#pragma unroll
+    for (int t = 0; t < TW; ++t) {
+#pragma unroll
+      for (int off = 16; off <= 32; off <<= 1) {
+        const float m2 = off == 16 ? lane_xor16(m[t]) : lane_xor32(m[t]);
+        const float z2 = off == 16 ? lane_xor16(z[t]) : lane_xor32(z[t]);
+        lse_combine(m[t], z[t], m2, z2);
+      }
+      if (gq == 0) {
+        s_m[(t0 + t) * 16 + n] = m[t];
+        s_z[(t0 + t) * 16 + n] = z[t];
+      }
+    }
+  }
+  exchange_stats<ROWS, LOCAL>(a, u, s_m, s_z, s_lse, s_wm, s_wz, base, true);
+  float lse[TW];
+#pragma unroll
+  for (int t = 0; t < TW; ++t) lse[t] = s_lse[(t0 + t) * 16 + n];
+
+  // ---- pass 2: scores again from K, exact probabilities, mass and P.V.
+  //      Each row's last read, so the loads are non-temporal.
+  floatx4 O[TW][DPL];
+#pragma unroll
+  for (int t = 0; t < TW; ++t)
+#pragma unroll
+    for (int jd = 0; jd < DPL; ++jd) O[t][jd] = floatx4{0.f, 0.f, 0.f, 0.f};
+  // wave 0 adds the three waves' per-token sums of block jj and stores them
+  auto store_mass = [&](int jj) {
+    const int tok = u.c0 + 32 * jj + lane;
+    if (lane < 32 && tok < u.c1)
+      st_agent(mp + tok, s_mass[jj & 1][0][lane] + s_mass[jj & 1][1][lane] + s_mass[jj & 1][2][lane]);
+  };
+  if (loader) {
+    for (int s = 0; s < S2 && s < nblk; ++s) {
+      issue_k_lds<D, true>(kg, u.c0 + 32 * s, u.c1, ring + s * 2 * BLK, lane);
+      issue_v_lds<D, true>(vg, u.c0 + 32 * s, u.c1, ring + s * 2 * BLK + BLK, lane);
+    }
+    for (int j = 0; j < nblk; ++j) {
+      const int issued = min(nblk, S2 + max(j - 1, 0));
+      wait_vm_groups<2 * KDMA, S2 - 1>(issued - j - 1);
+      lds_sync();
+      const int nb = j - 1 + S2;
+      if (j >= 1 && nb < nblk) {
+        issue_k_lds<D, true>(kg, u.c0 + 32 * nb, u.c1, ring + (nb % S2) * 2 * BLK, lane);
+        issue_v_lds<D, true>(vg, u.c0 + 32 * nb, u.c1, ring + (nb % S2) * 2 * BLK + BLK, lane);
+      }
+    }
+    lds_sync();
+  } else {
+    for (int j = 0; j < nblk; ++j) {
+      lds_sync();
+      if (w == 0 && j > 0) store_mass(j - 1);
+      const uint16_t* slot = ring + (j % S2) * 2 * BLK;
+      uint4 Kr[2][KS];
+      read_k_lds<D>(slot, n, gq, Kr);
+      VT Vr[8];
+      read_v_lds<D>(slot + BLK, n, gq, Vr);
+      float S[2][TW][4];
+      scores_from<D, TW, false>(a, u, Kr, qop, u.c0 + 32 * j, gq, lim, S);
+      bf16x8 Pa[TW];
+      float pm[8];
+      probs_raw<TW>(S, sl2, lse, Pa, pm);
+      mass_reduce_lds(pm, s_mass[j & 1][w], n, gq);
+      pv_mfma<D, TW>(Pa, Vr, O);
+    }
+    lds_sync();
+    if (w == 0) store_mass(nblk - 1);
+    write_opart_wide<D, LOCAL>(a, u, O, t0, n, gq);
+  }
+  verify_epilogue<ROWS, D, LOCAL>(a, u, s_lse, false, &s_flag, base);
+}
+
 // ------------------------------------------------------------ fp32 path --
 template <int D, int RT>
 __global__ void __launch_bounds__(kThreads) verify_f32_kernel(VArgs a) {
@@ -1554,6 +1845,7 @@ struct VPlan {
   int64_t n_plan;
   int splits, chunk, groups, per_launch, grid;
   bool resident, mfma;
+  bool wide;  // one group of kWideRT row tiles (wide variant)
   int lds_dyn;
   int xcds;
   bool budgeted;  // planned for a stream's compute-unit budget
@@ -1562,7 +1854,13 @@ struct VPlan {
 
 typedef void (*VKernel)(VArgs);
 
-VKernel pick_kernel(int dt, int D, int RT, bool resident, bool local) {
+VKernel pick_kernel(int dt, int D, int RT, bool resident, bool local, bool wide) {
+  if (wide) {
+    if (dt != PVLM_BF16 || RT != kWideRT) return nullptr;
+    if (D == 128) return local ? verify_wide_kernel<128, true> : verify_wide_kernel<128, false>;
+    if (D == 64) return local ? verify_wide_kernel<64, true> : verify_wide_kernel<64, false>;
+    return nullptr;
+  }
 #define PVLM_VK(DD, R_)                                                                  \
   if (D == DD && RT == R_) {                                                            \
     if (dt == PVLM_F32) return verify_f32_kernel<DD, R_>;                               \
@@ -1578,8 +1876,14 @@ VKernel pick_kernel(int dt, int D, int RT, bool resident, bool local) {
   return nullptr;
 }
 
-int lds_bytes(int dt, int D, int RT, bool resident) {
+int lds_bytes(int dt, int D, int RT, bool resident, bool wide) {
   if (dt == PVLM_F32) return (RT * 16 * D + kF32Tile * (D + 1) + RT * 16 * kF32Tile) * 4;
+  if (wide) {  // the Q tile, then the pass-1 and pass-2 rings (bf16)
+    int b = kWideRT * 16 * D * 2;
+    const int r1 = kWideSlots1 * 32 * D * 2, r2 = kWideSlots2 * 2 * 32 * D * 2;
+    b = b > r1 ? b : r1;
+    return b > r2 ? b : r2;
+  }
   int b = 3 * RT * 16 * D * 4;                                   // O partial reduce-scatter
   if (!resident && RT > 3) {
     const int kv = RT * 16 * D * 2 + kWaves * 4 * 32 * D * 2;     // Q, then two K+V blocks per wave
@@ -1621,24 +1925,38 @@ pvlm_status plan_verify(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int
     p->RG = want < p->RTT ? want : p->RTT;
   }
   p->RT = (p->RTT + p->RG - 1) / p->RG;
-  p->groups = B * Hkv * p->RG;
-  const int W = di.cus;  // one workgroup per CU (registers / LDS bound)
+  int W = di.cus;  // one workgroup per CU (registers / LDS bound)
   p->xcds = di.xcds;
   p->budgeted = di.budgeted;
-  p->per_launch = p->groups < W ? p->groups : W;
-  int splits = W / p->per_launch;
-  if (splits < 1) splits = 1;
-  if (!p->mfma) {
-    const int64_t want = (p->n_plan + kF32Tile - 1) / kF32Tile;
-    if (splits > want) splits = (int)want;
+  // groups, splits and chunk length for the row grouping in p->RG
+  auto layout = [&]() {
+    p->groups = B * Hkv * p->RG;
+    p->per_launch = p->groups < W ? p->groups : W;
+    int splits = W / p->per_launch;
+    if (splits < 1) splits = 1;
+    if (!p->mfma) {
+      const int64_t want = (p->n_plan + kF32Tile - 1) / kF32Tile;
+      if (splits > want) splits = (int)want;
+    }
+    int64_t chunk = (p->n_plan + splits - 1) / splits;
+    chunk = (chunk + 31) / 32 * 32;
+    p->chunk = (int)chunk;
+    p->splits = (int)((p->n_plan + chunk - 1) / chunk);
+    p->resident = p->mfma && chunk <= kResTokens;
+  };
+  layout();
+  // Rows that need two row groups, in streamed chunks: one group of the
+  // wide variant reads K and V once per pass for all of them instead.
+  p->wide = p->mfma && !p->resident && p->RTT > kMaxRT && p->RTT <= kWideRT && B * Hkv >= di.xcds;
+  if (p->wide) {
+    p->RG = 1;
+    p->RT = kWideRT;
+    W = kWidePerCU * di.cus;
+    layout();
+    p->resident = false;
   }
-  int64_t chunk = (p->n_plan + splits - 1) / splits;
-  chunk = (chunk + 31) / 32 * 32;
-  p->chunk = (int)chunk;
-  p->splits = (int)((p->n_plan + chunk - 1) / chunk);
-  p->resident = p->mfma && chunk <= kResTokens;
   p->grid = (p->per_launch * p->splits + 7) / 8 * 8;
-  p->lds_dyn = lds_bytes(dt, D, p->RT, p->resident);
+  p->lds_dyn = lds_bytes(dt, D, p->RT, p->resident, p->wide);
   const int ROWS = p->RT * 16;
   // Monotonic group counters sit at fixed per-group slots (cnt_s, cnt_o, base
   // of group g on lines 3g..3g+2 of the monotonic part), so calls of any shape
@@ -1722,11 +2040,11 @@ pvlm_status verify_run(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int6
   a.chunk = p.chunk;
   a.grid = p.grid;
   a.sl2 = scale * kLog2e;
-  if (!pick_kernel(dt, D, p.RT, p.resident, false)) return PVLM_ERR_UNSUPPORTED;
+  if (!pick_kernel(dt, D, p.RT, p.resident, false, p.wide)) return PVLM_ERR_UNSUPPORTED;
   // every launch's grid fits the device at once (the first launch's grid is
   // the largest; both exchange variants use the same resources)
   for (int local = 0; local < 2; ++local) {
-    const void* k = reinterpret_cast<const void*>(pick_kernel(dt, D, p.RT, p.resident, local != 0));
+    const void* k = reinterpret_cast<const void*>(pick_kernel(dt, D, p.RT, p.resident, local != 0, p.wide));
     PVLM_HIP(allow_dynamic_lds(k, p.lds_dyn));
     const pvlm_status cs = check_coresident(k, p.grid, kThreads, p.lds_dyn, stream);
     if (cs != PVLM_OK) return cs;
@@ -1743,7 +2061,7 @@ pvlm_status verify_run(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int6
     // one, and the same-XCD mode is kept to a device this call has alone)
     a.local = p.mfma && !p.budgeted && p.xcds > 0 && a.xmap == p.xcds &&
               (a.grid / a.xmap) % p.splits == 0;
-    VKernel kern = pick_kernel(dt, D, p.RT, p.resident, a.local != 0);
+    VKernel kern = pick_kernel(dt, D, p.RT, p.resident, a.local != 0, p.wide);
     PVLM_HIP(allow_dynamic_lds(reinterpret_cast<const void*>(kern), p.lds_dyn));
     void* args[] = {&a};
     PVLM_HIP(launch_coresident(reinterpret_cast<const void*>(kern), dim3(a.grid), dim3(kThreads),

@@ -75,6 +75,7 @@ SHAPES = [
     (1, 3, 8, 8, 128, [20000], 32),                # chunks > 512 tokens: stream variant
     (2, 9, 64, 8, 128, [40000, 25000], 128),       # stream variant, 5 row tiles, ragged
     (4, 9, 28, 4, 128, [100, 900, 3, 1500], 32),   # batch 4 ragged, empty chunks
+    (1, 17, 64, 8, 128, [20000], 32),              # wide variant (136 rows in one workgroup)
 ]
 
 

@@ -50,6 +50,9 @@ SHAPES = [
     (1, 9, 64, 8, 128, [40000], "bf16"),          # stream variant, 5 row tiles: K/V blocks through LDS
     (1, 8, 64, 8, 128, [30000], "bf16"),          # stream variant, 4 row tiles
     (2, 10, 16, 2, 64, [40000, 25000], "bf16"),   # stream variant, D = 64, 5 row tiles, ragged
+    (1, 17, 64, 8, 128, [20000], "bf16"),         # wide variant: 136 rows (9 tiles) in one workgroup
+    (1, 12, 64, 8, 128, [24000], "bf16"),         # wide variant, 6 row tiles (3 padding tiles)
+    (2, 16, 36, 4, 64, [30000, 9000], "bf16"),    # wide variant, D = 64, 144 rows, empty chunks
 ]
 
 
