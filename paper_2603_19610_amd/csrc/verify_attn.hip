@@ -1951,7 +1951,10 @@ pvlm_status plan_verify(pvlm_dtype dt, int B, int T, int Hq, int Hkv, int D, int
   if (p->wide) {
     p->RG = 1;
     p->RT = kWideRT;
-    W = kWidePerCU * di.cus;
+    // two workgroups per CU, except on a budgeted stream: there the grid
+    // keeps to one workgroup per budgeted CU, so that another stream's
+    // waiting calls still find whole CUs free
+    if (!di.budgeted) W = kWidePerCU * di.cus;
     layout();
     p->resident = false;
   }

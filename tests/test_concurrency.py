@@ -12,9 +12,10 @@ import numpy as np
 import pytest
 import torch
 
+import oracle
 import paper_2603_19610_amd as pv
 import workloads as W
-from gpu_util import note, to_dev
+from gpu_util import assert_mass, assert_out, f64, note, to_dev, to_host_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -87,15 +88,19 @@ def test_default_workspaces_are_per_stream():
         assert torch.equal(o[0], ref[0]) and torch.equal(o[1], ref[1]) and torch.equal(o[2], ref[2])
 
 
-@pytest.mark.parametrize("budgets", [(224, 32), (128, 128)])
-def test_two_budgeted_streams_run_waiting_calls_together(budgets):
-    """Verify (72B layer) on one budgeted stream and verify + accept (7B
-    layer) on another, enqueued together and repeated: every result equals
-    the same call's result on a lone stream with the same budget, and no
-    wait gives up."""
+@pytest.mark.parametrize("budgets,first", [((224, 32), "72b"), ((128, 128), "72b"), ((224, 32), "wide")])
+def test_two_budgeted_streams_run_waiting_calls_together(budgets, first):
+    """Verify (72B layer, or 136 rows per KV head over a 20K-token cache, the
+    wide variant) on one budgeted stream and verify + accept (7B layer) on
+    another, enqueued together and repeated: every result equals the same
+    call's result on a lone stream with the same budget, and no wait gives
+    up."""
     dev = torch.device("cuda", 0)
     w72, w7 = W.WORKLOADS["llava72b"], W.WORKLOADS["llava7b"]
-    a_in = W.make_verify_inputs(w72, layer=1)
+    if first == "wide":
+        a_in = W.random_verify_inputs(1, 17, 64, 8, 128, [20000], "bf16", seed=5)
+    else:
+        a_in = W.make_verify_inputs(w72, layer=1)
     b_in = W.make_verify_inputs(w7, layer=1)
     A = [to_dev(x) for x in (a_in.q, a_in.k, a_in.v, a_in.ctx_len)]
     Bt = [to_dev(x) for x in (b_in.q, b_in.k, b_in.v, b_in.ctx_len)]
@@ -129,6 +134,11 @@ def test_two_budgeted_streams_run_waiting_calls_together(budgets):
         r2 = [t.clone() for t in run2()]
     torch.cuda.synchronize()
     assert int(st1.item()) == 0 and int(st2.item()) == 0
+    if first == "wide":
+        ro, rl, rm = oracle.verify_attn(f64(a_in.q, "bf16"), f64(a_in.k, "bf16"), f64(a_in.v, "bf16"),
+                                        a_in.ctx_len, a_in.scale)
+        assert_out(to_host_f64(r1[0]), ro)
+        assert_mass(to_host_f64(r1[1]), rm, 64, 17)
     for rep in range(5):
         note(f"budgets {budgets}: both streams together, round {rep}")
         with torch.cuda.stream(s1):
