@@ -110,8 +110,8 @@ def test_long_video_131k():
 
 
 @pytest.mark.parametrize("shape", [(1, 9, 64, 8, 128, [1111]), (4, 9, 28, 4, 128, [100, 900, 3, 1500]),
-                                   (1, 3, 8, 8, 128, [20000])],
-                         ids=["resident-72B-heads", "resident-ragged-empty-chunks", "stream"])
+                                   (1, 3, 8, 8, 128, [20000]), (1, 17, 64, 8, 128, [20000])],
+                         ids=["resident-72B-heads", "resident-ragged-empty-chunks", "stream", "wide"])
 def test_without_mass_or_lse(shape):
     """Output alone (no mass, no lse): bit-identical to the full call's output
     (the mass and lse are by-products of the same arithmetic) and within the
@@ -152,8 +152,9 @@ def test_deterministic_and_reusable_workspace():
 
 def test_workspace_reused_across_shapes():
     ws = pv.Workspace(torch.device("cuda", 0))
-    shapes = [(2, 5, 8, 2, 128, [300, 517]), (1, 9, 64, 8, 128, [1111]),
-              (1, 3, 8, 8, 128, [3000]), (3, 4, 6, 3, 128, [0, 1, 31]), (1, 9, 16, 1, 128, [900])]
+    shapes = [(2, 5, 8, 2, 128, [300, 517]), (1, 9, 64, 8, 128, [1111]), (1, 17, 64, 8, 128, [20000]),
+              (1, 3, 8, 8, 128, [3000]), (3, 4, 6, 3, 128, [0, 1, 31]), (1, 17, 64, 8, 128, [20000]),
+              (1, 9, 16, 1, 128, [900])]
     for (B, T, Hq, Hkv, D, ctx) in shapes:
         inp = W.random_verify_inputs(B, T, Hq, Hkv, D, ctx, "bf16", seed=B + T + Hq)
         note(f"verify ws reuse {inp.q.shape} {inp.k.shape}")
