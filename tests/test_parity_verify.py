@@ -53,6 +53,7 @@ SHAPES = [
     (1, 17, 64, 8, 128, [20000], "bf16"),         # wide variant: 136 rows (9 tiles) in one workgroup
     (1, 12, 64, 8, 128, [24000], "bf16"),         # wide variant, 6 row tiles (3 padding tiles)
     (2, 16, 36, 4, 64, [30000, 9000], "bf16"),    # wide variant, D = 64, 144 rows, empty chunks
+    (3, 16, 36, 4, 128, [30000, 5000, 17000], "bf16"),  # wide variant, ragged batch 3: cross-XCD exchanges
 ]
 
 
