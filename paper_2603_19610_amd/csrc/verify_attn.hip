@@ -796,8 +796,9 @@ __device__ __forceinline__ bf16x8 q_operand(const uint16_t* s_q, int rt, int ks,
       bf16x8, *reinterpret_cast<const uint4*>(s_q + (r * CH + (c ^ (r % CH))) * 8));
 }
 
-// Scaled (log2 domain), masked scores of one block for the two-pass variants
-// (qop(rt, ks): the Q operand of tile rt, k-step ks): -inf past the chunk,
+// Scaled (log2 domain; unscaled with SCALED false), masked scores of one
+// block for the two-pass variants (qop(rt, ks): the Q operand of tile rt,
+// k-step ks): -inf past the chunk,
 // past the causal limit of each verify row (lim: the last token the lane's
 // row of each tile sees, -1 on padding rows), and on padding rows.  A block
 // every real row sees whole is only scaled: its padding rows keep finite
