@@ -62,8 +62,8 @@ struct AArgs {
   int* pi;          // [B][RW][NC] chunk argmax (lowest index)
   double* rs;       // [B][ND] residual mass of each draw chunk
   double* qs;       // [B][ND] p mass of each draw chunk (used when the residual is empty)
-  int* arrive;      // [2] arrivals at the two waits (128 bytes apart), zero at rest
-  unsigned* gen;    // generation word, advanced once per wait
+  int* arrive;      // [2][kArriveSets + 1] arrival counters of the two waits (128 bytes apart), zero at rest
+  unsigned* gen;    // [kArriveSets] generation words (128 bytes apart), advanced once per wait
 };
 
 __device__ __forceinline__ const float* row_ptr(const AArgs& a, int b, int rho) {
@@ -72,23 +72,41 @@ __device__ __forceinline__ const float* row_ptr(const AArgs& a, int b, int rho) 
 }
 
 // Grid-wide wait `p` (0 or 1): arrive, and (if `wait`) wait for every
-// workgroup's arrival.  Each wait has its own arrival counter, which its last
-// arrival returns to zero before it advances the generation word the others
-// poll (polling the counter itself would slow the arrivals down).  The
-// generation is never reset: every workgroup reads it at its start, before
+// workgroup's arrival.  The workgroups form eight sets (by index mod 8).
+// Arrivals go to their set's counter, so no counter line takes more than an
+// eighth of the grid's atomics (same-line atomics serialise); the last
+// arrival of each set counts it at a second counter, and the last of those
+// advances the generation word, one copy per set, which the set's others
+// poll (polling a counter itself would slow the arrivals down).  Every
+// counter returns to zero when its last arrival has seen it.  The generation
+// is never reset: every workgroup reads its set's copy at its start, before
 // its first arrival, so wait p releases at that value + p + 1.
+constexpr int kArriveSets = 8;
+__device__ __forceinline__ unsigned* gen_word(const AArgs& a) {
+  return a.gen + (blockIdx.x % kArriveSets) * (kSyncLine / sizeof(unsigned));
+}
 __device__ void grid_wait(const AArgs& a, int p, unsigned g0, bool wait) {
   __builtin_amdgcn_s_waitcnt(0);  // this workgroup's published data is visible
   __syncthreads();
   if (threadIdx.x == 0) {
-    int* cnt = a.arrive + p * (int)(kSyncLine / sizeof(int));
-    const int old = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (old == (int)gridDim.x - 1) {
-      reset_counter(cnt);
-      __hip_atomic_store(a.gen, g0 + (unsigned)p + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    } else if (wait) {
-      grp_poll(a.gen, g0 + (unsigned)p + 1u, a.status);
+    constexpr int kLineI = (int)(kSyncLine / sizeof(int));
+    int* base = a.arrive + p * (kArriveSets + 1) * kLineI;
+    const int set = (int)(blockIdx.x % kArriveSets);
+    const int members = ((int)gridDim.x - set + kArriveSets - 1) / kArriveSets;
+    const int sets = (int)gridDim.x < kArriveSets ? (int)gridDim.x : kArriveSets;
+    bool released = false;
+    int* c1 = base + set * kLineI;
+    if (__hip_atomic_fetch_add(c1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == members - 1) {
+      reset_counter(c1);
+      int* c2 = base + kArriveSets * kLineI;
+      if (__hip_atomic_fetch_add(c2, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == sets - 1) {
+        reset_counter(c2);
+        for (int k = 0; k < kArriveSets; ++k)
+          __hip_atomic_store(a.gen + k * kLineI, g0 + (unsigned)p + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        released = true;
+      }
     }
+    if (!released && wait) grp_poll(a.gen + set * kLineI, g0 + (unsigned)p + 1u, a.status);
   }
   __syncthreads();
 }
@@ -265,7 +283,7 @@ __global__ void __launch_bounds__(kAccThreads) accept_kernel(AArgs a) {
   const int RW = 2 * a.gamma + 1;
   const int W = gridDim.x;
   const double inv_tau = a.greedy ? 0.0 : 1.0 / a.tau;
-  const unsigned g0 = tid == 0 ? grp_read(a.gen) : 0u;
+  const unsigned g0 = tid == 0 ? grp_read(gen_word(a)) : 0u;
   // the inputs of the decisions and the draw for this workgroup's first
   // batch, loaded up front (drafted position t on thread kAccThreads - 32 + t)
   const int nd_items = a.greedy ? 1 : a.B * a.ND;
