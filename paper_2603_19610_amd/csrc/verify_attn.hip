@@ -171,6 +171,25 @@ __device__ __forceinline__ unsigned read_base(const VArgs& a, const Unit& u) {
   return grp_read(cnt_base(a, u));
 }
 
+// Release word of the statistics exchange, on the base's line: the last
+// arrival at cnt_s stores the count every workgroup waits for, and the others
+// poll that word instead of the counter, so that their polls do not contend
+// with the arrivals' atomics on the counter's line.  Like the counters it
+// only grows, and at rest it equals the base.  (The O exchange polls cnt_o
+// itself: there the release's extra hop after the last arrival cost more
+// than the contention it saves.)
+__device__ __forceinline__ unsigned* rel_s(const VArgs& a, const Unit& u) { return cnt_base(a, u) + 8; }
+
+// Thread 0: arrive at cnt_s (statistics published) and, if asked, wait for
+// the whole group.
+__device__ __forceinline__ void stats_arrive(const VArgs& a, const Unit& u, unsigned base, bool wait) {
+  const unsigned target = base + (unsigned)a.splits;
+  if (grp_arrive(cnt_s(a, u)) == target - 1u)
+    __hip_atomic_store(rel_s(a, u), target, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else if (wait)
+    grp_poll(rel_s(a, u), target, a.status);
+}
+
 // Each workgroup's statistics record holds ROWS (max, exp-sum) pairs and a
 // header stamped with the launch's tag (base + 1, different in every launch
 // of the group), which readers check: a record missing from this launch
@@ -273,10 +292,7 @@ __device__ void exchange_stats(const VArgs& a, const Unit& u, const float* s_m, 
   stats_store<ROWS, LOCAL>(a, u, s_m, s_z, base);
   // wave-uniform branch: only wave 0 wrote, only it waits for its stores
   if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) == 0) __builtin_amdgcn_s_waitcnt(0);
-  if (threadIdx.x == 0) {
-    grp_arrive(cnt_s(a, u));
-    if (wait) grp_poll(cnt_s(a, u), base + (unsigned)a.splits, a.status);
-  }
+  if (threadIdx.x == 0) stats_arrive(a, u, base, wait);
   __syncthreads();
   if (wait)
     stats_combine<ROWS, LOCAL>(a, u, (u.N + a.chunk - 1) / a.chunk, s_lse, s_pm, s_pz, base);
@@ -1148,7 +1164,7 @@ __device__ void empty_chunk(const VArgs& a, const Unit& u, const float* s_m, con
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0) {
-    grp_arrive(cnt_s(a, u));
+    stats_arrive(a, u, base, false);
     __builtin_amdgcn_s_waitcnt(0);  // the statistics arrival lands before the O arrival
     o_finish(a, u, base, grp_arrive(cnt_o(a, u)), false);
   }
@@ -1303,10 +1319,7 @@ verify_mfma_kernel(VArgs a) {
     stats_store<ROWS, LOCAL>(a, u, s_m, s_z, base);
     if (__builtin_amdgcn_readfirstlane(w) == 0) {
       __builtin_amdgcn_s_waitcnt(0);
-      if (lane == 0) {
-        grp_arrive(cnt_s(a, u));
-        grp_poll(cnt_s(a, u), base + (unsigned)a.splits, a.status);
-      }
+      if (lane == 0) stats_arrive(a, u, base, true);
     }
     lds_sync();
     stats_combine<ROWS, LOCAL>(a, u, (u.N + a.chunk - 1) / a.chunk, s_lse, s_wm, s_wz, base);
