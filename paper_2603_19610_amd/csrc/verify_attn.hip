@@ -1487,7 +1487,8 @@ constexpr int kWideTW = 3;      // row tiles per compute wave (waves 0 .. 2)
 constexpr int kWideSlots1 = 8;  // pass-1 ring: one K block per slot
 constexpr int kWideSlots2 = 4;  // pass-2 ring: a K and a V block per slot
 // Two workgroups per CU (registers and LDS allow it), so that on every SIMD
-// one workgroup's MFMA and exponentials overlap the other's barrier waits.
+// one workgroup's MFMA and exponentials overlap the other's barrier waits
+// (one per budgeted CU on a stream with a compute-unit budget).
 constexpr int kWidePerCU = 2;
 static_assert(kWideRT == kWideTW * (kWaves - 1), "waves 0..2 compute, wave 3 loads");
 
