@@ -9,6 +9,7 @@
 // only layers 0 and L and one normalised mat-vec per layer: streaming work
 // bound by HBM bandwidth.  Zero-norm vectors contribute cosine 0.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 
@@ -47,34 +48,88 @@ __global__ void __launch_bounds__(256) uv_mass_kernel(const float* crit, const i
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// Raw buffer resources (gfx9 descriptor word 3) bound a row segment's
+// accesses: loads past the resource's size return zeros and stores there are
+// dropped, so partial segments need no per-lane branches or address clamps.
+constexpr int kBufWord3 = 0x00020000;
+constexpr int kBufNT = 2;  // cache-policy bits: non-temporal (rows streamed once)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kBufWord3);
+}
+
 // Hidden-state element loads: 8 consecutive elements, widened exactly.  NT:
-// through the non-temporal cache policy (rows streamed once).
+// through the non-temporal cache policy (rows streamed once).  load() only
+// issues the load and unpack() widens, so a batch of loads can be in flight
+// before the first is used.
 template <typename T>
 struct HS;
 template <>
 struct HS<uint16_t> {
+  struct Raw {
+    u32x4 v;
+  };
   template <bool NT = false>
-  static __device__ __forceinline__ void load8(const uint16_t* p, float (&f)[8]) {
-    const u32x4 v = NT ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p))
-                       : *reinterpret_cast<const u32x4*>(p);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  static __device__ __forceinline__ Raw load(const uint16_t* p) {
+    return {NT ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p))
+               : *reinterpret_cast<const u32x4*>(p)};
+  }
+  static __device__ __forceinline__ void unpack(const Raw& r, float (&f)[8]) {
+    const uint32_t w[4] = {r.v.x, r.v.y, r.v.z, r.v.w};
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       f[2 * k] = __uint_as_float(w[k] << 16);
       f[2 * k + 1] = __uint_as_float(w[k] & 0xFFFF0000u);
     }
   }
+  template <bool NT = false>
+  static __device__ __forceinline__ void load8(const uint16_t* p, float (&f)[8]) {
+    unpack(load<NT>(p), f);
+  }
+  // through a buffer resource: bytes past its size read as zeros
+  template <int AUX = kBufNT>
+  static __device__ __forceinline__ Raw load_buf(__amdgpu_buffer_rsrc_t rs, int boff) {
+    return {__builtin_amdgcn_raw_buffer_load_b128(rs, boff, 0, AUX)};
+  }
+  // f holds bf16 values (widened exactly), so their high halves are the bf16 words
+  static __device__ __forceinline__ void store_buf(const float (&f)[8], __amdgpu_buffer_rsrc_t rs, int boff) {
+    uint32_t w[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      w[k] = (__float_as_uint(f[2 * k]) >> 16) | (__float_as_uint(f[2 * k + 1]) & 0xFFFF0000u);
+    const u32x4 v = {w[0], w[1], w[2], w[3]};
+    __builtin_amdgcn_raw_buffer_store_b128(v, rs, boff, 0, kBufNT);
+  }
 };
 template <>
 struct HS<float> {
+  struct Raw {
+    f32x4 a, b;
+  };
+  template <bool NT = false>
+  static __device__ __forceinline__ Raw load(const float* p) {
+    return {NT ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p))
+               : *reinterpret_cast<const f32x4*>(p),
+            NT ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + 4))
+               : *reinterpret_cast<const f32x4*>(p + 4)};
+  }
+  static __device__ __forceinline__ void unpack(const Raw& r, float (&f)[8]) {
+    f[0] = r.a.x; f[1] = r.a.y; f[2] = r.a.z; f[3] = r.a.w;
+    f[4] = r.b.x; f[5] = r.b.y; f[6] = r.b.z; f[7] = r.b.w;
+  }
   template <bool NT = false>
   static __device__ __forceinline__ void load8(const float* p, float (&f)[8]) {
-    const f32x4 a = NT ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p))
-                       : *reinterpret_cast<const f32x4*>(p);
-    const f32x4 b = NT ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + 4))
-                       : *reinterpret_cast<const f32x4*>(p + 4);
-    f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
-    f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+    unpack(load<NT>(p), f);
+  }
+  template <int AUX = kBufNT>
+  static __device__ __forceinline__ Raw load_buf(__amdgpu_buffer_rsrc_t rs, int boff) {
+    const u32x4 a = __builtin_amdgcn_raw_buffer_load_b128(rs, boff, 0, AUX);
+    const u32x4 b = __builtin_amdgcn_raw_buffer_load_b128(rs, boff + 16, 0, AUX);
+    return {__builtin_bit_cast(f32x4, a), __builtin_bit_cast(f32x4, b)};
+  }
+  static __device__ __forceinline__ void store_buf(const float (&f)[8], __amdgpu_buffer_rsrc_t rs, int boff) {
+    const f32x4 a = {f[0], f[1], f[2], f[3]}, b = {f[4], f[5], f[6], f[7]};
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, a), rs, boff, 0, kBufNT);
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, b), rs, boff + 16, 0, kBufNT);
   }
 };
 
@@ -109,6 +164,16 @@ __device__ __forceinline__ void add_round_store8(float* out, float (&f)[8], cons
   }
 }
 
+// The same add without the store: f becomes the stored values.
+__device__ __forceinline__ void add_round8(uint16_t, float (&f)[8], const float (&g)[8]) {
+#pragma unroll
+  for (int k = 0; k < 8; ++k) f[k] = bf16_to_f32(f32_to_bf16(f[k] + g[k]));
+}
+__device__ __forceinline__ void add_round8(float, float (&f)[8], const float (&g)[8]) {
+#pragma unroll
+  for (int k = 0; k < 8; ++k) f[k] += g[k];
+}
+
 // 8 consecutive elements of a hidden-state row at element offset `off`: the
 // row itself, or (FUSED) the epilogue's prev + delta, written to `out`.
 // NT: the visual rows, streamed once, go through the non-temporal cache
@@ -128,6 +193,41 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
+}
+
+// Wave totals through DPP lane moves: xor 1 and xor 2 inside each quad,
+// then the half-row and row mirrors give every lane its 16-lane row's sum;
+// the four row sums are read from lanes 0, 16, 32 and 48 and added in a
+// fixed order.  Every lane gets the same total.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), CTRL, 0xF, 0xF, true);
+  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, 0xF, 0xF, true);
+  return __hiloint2double(hi, lo);
+}
+__device__ __forceinline__ double lane_f64(double v, int l) {
+  return __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(v), l),
+                          __builtin_amdgcn_readlane(__double2loint(v), l));
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+__device__ __forceinline__ double wave_total_f64(double v) {
+  v += dpp_f64<kDppXor1>(v);
+  v += dpp_f64<kDppXor2>(v);
+  v += dpp_f64<kDppHalfMirror>(v);
+  v += dpp_f64<kDppMirror>(v);
+  return (lane_f64(v, 0) + lane_f64(v, 16)) + (lane_f64(v, 32) + lane_f64(v, 48));
+}
+__device__ __forceinline__ float wave_total_f32(float v) {
+  v += dpp_f32<kDppXor1>(v);
+  v += dpp_f32<kDppXor2>(v);
+  v += dpp_f32<kDppHalfMirror>(v);
+  v += dpp_f32<kDppMirror>(v);
+  auto at = [&](int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); };
+  return (at(0) + at(16)) + (at(32) + at(48));
 }
 
 // The COSSIM criterion is a sum of n cosines that can cancel to far below
@@ -180,22 +280,37 @@ __global__ void __launch_bounds__(64) txt_dir_part_kernel(const T* ht, int64_t o
                                                           const int32_t* n_txt, int B,
                                                           int64_t n_cap, int Dh, int nchunk,
                                                           const double* inv_norm, double* part) {
+  // the chunk's rows load in batches of RB, every load of a batch in flight
+  // together; rows past the chunk's end read as zeros through the buffer
+  // resource and get weight 0, so they add exact zeros
+  constexpr int RB = sizeof(T) == 2 ? kTxtChunk : kTxtChunk / 2;
   const int c = blockIdx.y, sb = blockIdx.z, slot = sb / B, b = sb % B;
   const int d = (blockIdx.x * 64 + threadIdx.x) * 8;
   if (d >= Dh) return;
   int nb = n_txt[b];
   nb = nb < 0 ? 0 : (nb > n_cap ? (int)n_cap : nb);
   const int j0 = c * kTxtChunk, j1 = min(nb, j0 + kTxtChunk);
-  const T* base = ht + (slot ? off1 : off0) + (size_t)b * n_cap * Dh + d;
+  const T* base = ht + (slot ? off1 : off0) + ((size_t)b * n_cap + j0) * Dh;
   const double* inv = inv_norm + ((size_t)slot * B + b) * n_cap;
+  const int rows = max(0, j1 - j0);
+  const auto rs = buf_rsrc(base, rows * Dh * (int)sizeof(T));
   double acc[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
-#pragma unroll 8  // rows' loads in flight together
-  for (int j = j0; j < j1; ++j) {
-    const double wj = inv[j];
-    float f[8];
-    HS<T>::load8(base + (size_t)j * Dh, f);
+  for (int jb = 0; jb < rows; jb += RB) {
+    typename HS<T>::Raw r[RB];
+    double w[RB];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) acc[k] = fma((double)f[k], wj, acc[k]);
+    for (int i = 0; i < RB; ++i) {
+      r[i] = HS<T>::template load_buf<0>(rs, ((jb + i) * Dh + d) * (int)sizeof(T));
+      const double wi = inv[j0 + min(jb + i, rows - 1)];
+      w[i] = jb + i < rows ? wi : 0.0;
+    }
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+      float f[8];
+      HS<T>::unpack(r[i], f);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc[k] = fma((double)f[k], w[i], acc[k]);
+    }
   }
   double* pp = part + ((size_t)sb * nchunk + c) * Dh + d;
 #pragma unroll
@@ -204,71 +319,231 @@ __global__ void __launch_bounds__(64) txt_dir_part_kernel(const T* ht, int64_t o
 
 __global__ void __launch_bounds__(256) txt_dir_sum_kernel(const double* part, int Dh, int nchunk,
                                                           double* u) {
+  // chunks in batches of CB, every load of a batch in flight together (past
+  // the last chunk the index is clamped and the value not added); the sum
+  // runs in chunk order
+  constexpr int CB = 8;
   const int sb = blockIdx.y;
   const int d = blockIdx.x * 256 + threadIdx.x;
   if (d >= Dh) return;
   const double* p = part + (size_t)sb * nchunk * Dh + d;
   double acc = 0.0;
-  for (int c = 0; c < nchunk; ++c) acc += p[(size_t)c * Dh];
+  for (int c0 = 0; c0 < nchunk; c0 += CB) {
+    double v[CB];
+#pragma unroll
+    for (int i = 0; i < CB; ++i) v[i] = p[(size_t)min(c0 + i, nchunk - 1) * Dh];
+#pragma unroll
+    for (int i = 0; i < CB; ++i)
+      if (c0 + i < nchunk) acc += v[i];
+  }
   u[(size_t)sb * Dh + d] = acc;
 }
 
-// c_slot = <hv, u_slot> / |hv| (0 for zero norm), one wave per visual row.
-// A workgroup of 16 waves first stages the direction vectors of its batch
-// row (both slots, float64) in LDS, then its waves stream visual rows
-// against them (rows blockIdx.x * 16 + wave, stepping by the grid's waves).
-// Lane l handles elements 8 (l + 64 i) + k, k < 8, of a row (16-byte
-// loads); u is staged transposed, s_u[slot][k][d / 8], so the lanes of a
-// wave read consecutive words.  The dot product is float64 (it can cancel);
-// the squared norm sums positive terms only, so fp32 keeps its relative
-// error below 1e-5 (at most 134 roundings), far inside the criterion's gate.
+// c_slot = <hv, u_slot> / |hv| (0 for zero norm) for the visual rows.  A
+// workgroup of 16 waves first stages the direction vectors of its batch row
+// (both slots, float64) in LDS.  It owns a contiguous run of rows, taken in
+// rounds of up to kVisRows, and splits each round into units (row, slot,
+// segment of 64 * kVisPieces 8-element pieces) that its waves take in turn,
+// so every wave carries nearly the same load.  Lane l of a unit handles
+// pieces segment * 64 * kVisPieces + l + 64 t, t < kVisPieces (16-byte
+// loads), kVisBatch of them in registers at a time: as it consumes a piece
+// it issues the next one (of this unit, then of its next unit) into the
+// same registers, so a unit's loads are in flight while the one before is
+// reduced.  A unit's dot product and squared norm (wave totals) go to LDS,
+// and one thread per row then sums the segments in order.  u is staged as
+// s_u[slot][k / 2][d / 8][k % 2]: a lane reads its 8 directions of a piece
+// as four 16-byte words, and the lanes of a wave read consecutive words.
+// The dot product is float64 (it can cancel); the squared norm sums positive
+// terms only, so fp32 keeps its relative error below 1e-5 (fewer than 80
+// roundings), far inside the criterion's gate.
 // nslots == 2: out = c_1 - c_0 (the score); nslots == 1: out = c_0.
+// Largest hidden size whose two float64 direction vectors fit the kernel's
+// LDS.
+constexpr int kMaxDh = 8192;
 constexpr int kVisThreads = 1024;
+constexpr int kVisWaves = kVisThreads / 64;
+constexpr int kVisRows = 128;
+// Pieces per lane and unit (the summation grouping, the same for the fused
+// and the plain kernel, so both give the same sums bit for bit), and pieces
+// in flight per lane (the register budget: the fused kernel also holds the
+// deltas).
+template <typename T>
+constexpr int kVisPieces = sizeof(T) == 2 ? 8 : 4;
+template <typename T, bool FUSED>
+constexpr int kVisBatch = FUSED ? kVisPieces<T> / 4 : kVisPieces<T>;
+
+// f(integral_constant<int, I>) for I = 0 .. N-1, unrolled at compile time.
+template <int N, int I = 0, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, I + 1>(f);
+  }
+}
+
+// One 8-element piece of a visual row against its directions (us points at
+// the slot's staged vector, j is the piece's index d / 8, clamped into the
+// row).  A piece past the row's end was read as zeros through the buffer
+// resource, so it adds exact zeros to both sums, and its store (FUSED, to
+// the output resource os) is dropped.
+template <typename T, bool FUSED>
+__device__ __forceinline__ void vis_piece(const typename HS<T>::Raw& r, const typename HS<T>::Raw& rd,
+                                          __amdgpu_buffer_rsrc_t os, int boff, const double* us, int D8,
+                                          int j, double& dot, float& ss) {
+  float f[8];
+  HS<T>::unpack(r, f);
+  if constexpr (FUSED) {
+    float g[8];
+    HS<T>::unpack(rd, g);
+    add_round8(T(), f, g);
+    HS<T>::store_buf(f, os, boff);
+  }
+  double2 w[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) w[p] = reinterpret_cast<const double2*>(us)[(size_t)p * D8 + j];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    dot = fma((double)f[2 * p], w[p].x, dot);
+    dot = fma((double)f[2 * p + 1], w[p].y, dot);
+  }
+#pragma unroll
+  for (int k = 0; k < 8; ++k) ss = fmaf(f[k], f[k], ss);
+}
+
 template <typename T, bool FUSED>
 __global__ void __launch_bounds__(kVisThreads) vis_kernel(const T* hv, int64_t off0, int64_t off1,
                                                           const int32_t* m, int nslots,
                                                           int B, int64_t m_cap, int Dh, const double* u,
                                                           float* out, int32_t* status, const T* dv,
                                                           T* ov) {
-  extern __shared__ __align__(16) double s_u[];  // [nslots][8][Dh / 8]
+  // [nslots][4][Dh / 8][2] directions, then the units' float64 dot products
+  // and fp32 squared norms, [kVisRows][nslots][nseg] each
+  extern __shared__ __align__(16) double s_u[];
+  constexpr int NP = kVisPieces<T>;
+  constexpr int NB = kVisBatch<T, FUSED>;
+  constexpr int SEG = 64 * NP;  // pieces per segment
   const int b = blockIdx.y;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: unit bookkeeping is scalar
   const int D8 = Dh / 8;
+  const int nseg = (D8 + SEG - 1) / SEG;
+  const int per_row = nslots * nseg;  // units per row
+  double* s_pd = s_u + (size_t)nslots * Dh;
+  float* s_ps = reinterpret_cast<float*>(s_pd + kVisRows * per_row);
   for (int s = 0; s < nslots; ++s)
     for (int d = threadIdx.x; d < Dh; d += kVisThreads)
-      s_u[(s * 8 + (d & 7)) * D8 + (d >> 3)] = u[((size_t)s * B + b) * Dh + d];
+      s_u[((size_t)(s * 4 + ((d & 7) >> 1)) * D8 + (d >> 3)) * 2 + (d & 1)] =
+          u[((size_t)s * B + b) * Dh + d];
   __syncthreads();
   bool bad = false;
   const int mb = clampi(m[b], 0, (int)m_cap, bad);
   if (bad && blockIdx.x == 0 && threadIdx.x == 0) dev_flag(status, PVLM_DEV_RANGE);
-  const int64_t step = (int64_t)gridDim.x * (kVisThreads / 64);
-  for (int64_t i = (int64_t)blockIdx.x * (kVisThreads / 64) + wave; i < m_cap; i += step) {
-    double res = 0.0;
-    if (i < mb) {
-      double c[2] = {0.0, 0.0};
-      for (int s = 0; s < nslots; ++s) {
-        const size_t roff = (s ? off1 : off0) + ((size_t)b * m_cap + i) * Dh;
-        const double* us = s_u + s * 8 * D8;
-        double dot = 0.0;
-        float ss = 0.f;
-#pragma unroll 8  // the row's loads in flight together
-        for (int j = lane; j < D8; j += 64) {
-          float f[8];
-          row8<T, FUSED, true>(hv, dv, ov, roff + 8 * j, f);
+  const int64_t per_wg = (m_cap + gridDim.x - 1) / gridDim.x;
+  const int64_t r_begin = (int64_t)blockIdx.x * per_wg;
+  const int64_t r_end = min(m_cap, r_begin + per_wg);
+  // element offset of unit q's segment start within the hidden-state stacks
+  auto unit = [&](int64_t r0, int q, int& seg) -> size_t {
+    const int row = q / per_row, rest = q % per_row, s = rest / nseg;
+    seg = rest % nseg;
+    return (s ? off1 : off0) + ((size_t)b * m_cap + r0 + row) * Dh + (size_t)8 * seg * SEG;
+  };
+  constexpr int PB = 8 * (int)sizeof(T);  // bytes per piece
+  // a resource over the rest of the row from a segment's start
+  auto rsrc = [&](const T* base, size_t off, int sg) { return buf_rsrc(base + off, (D8 - sg * SEG) * PB); };
+  for (int64_t r0 = r_begin; r0 < r_end; r0 += kVisRows) {
+    const int nr = (int)min((int64_t)kVisRows, r_end - r0);
+    const int nv = (int)max((int64_t)0, min((int64_t)nr, (int64_t)mb - r0));  // rows with data
+    const int U = nv * per_row;
+    // a ring of NB pieces in registers: piece t of a unit sits in slot
+    // t % NB; consuming it frees the slot for piece t + NB of the unit, or
+    // for the next unit's piece t + NB - NP
+    typename HS<T>::Raw r[NB], rd[NB];
+    int q = wave, seg = 0;
+    size_t off = 0;
+    if (q < U) {
+      off = unit(r0, q, seg);
+      const auto rs = rsrc(hv, off, seg);
+      const auto rsd = FUSED ? rsrc(dv, off, seg) : rs;
 #pragma unroll
-          for (int k = 0; k < 8; ++k) {
-            dot = fma((double)f[k], us[k * D8 + j], dot);
-            ss = fmaf(f[k], f[k], ss);
-          }
-        }
-        dot = wave_sum_f64(dot);
-        ss = warp_sum(ss);
-        c[s] = ss > 0.f ? dot / sqrt((double)ss) : 0.0;
+      for (int t = 0; t < NB; ++t) {
+        r[t] = HS<T>::load_buf(rs, (lane + 64 * t) * PB);
+        if constexpr (FUSED) rd[t] = HS<T>::load_buf(rsd, (lane + 64 * t) * PB);
       }
-      res = nslots == 2 ? c[1] - c[0] : c[0];
     }
-    if (lane == 0) out[(size_t)b * m_cap + i] = (float)res;
+    while (q < U) {
+      const int qn = q + kVisWaves;
+      const int s = (q % per_row) / nseg;
+      const double* us = s_u + (size_t)s * 8 * D8;
+      const auto rs = rsrc(hv, off, seg);
+      const auto rsd = FUSED ? rsrc(dv, off, seg) : rs;
+      const auto os = FUSED ? rsrc(ov, off, seg) : rs;
+      double dot = 0.0;
+      float ss = 0.f;
+      const bool more = qn < U;
+      int segn = seg;
+      size_t offn = off;
+      if (more) offn = unit(r0, qn, segn);
+      const auto rsn = rsrc(hv, offn, segn);
+      const auto rsdn = FUSED ? rsrc(dv, offn, segn) : rsn;
+      // consume piece t, then refill its slot; the unit's own pieces first
+      auto step = [&](auto tc, bool next) {
+        constexpr int t = decltype(tc)::value;
+        const int j = min(seg * SEG + lane + 64 * t, D8 - 1);
+        vis_piece<T, FUSED>(r[t % NB], rd[t % NB], os, (lane + 64 * t) * PB, us, D8, j, dot, ss);
+        if constexpr (t + NB < NP) {
+          r[t % NB] = HS<T>::load_buf(rs, (lane + 64 * (t + NB)) * PB);
+          if constexpr (FUSED) rd[t % NB] = HS<T>::load_buf(rsd, (lane + 64 * (t + NB)) * PB);
+        } else if (next) {
+          r[t % NB] = HS<T>::load_buf(rsn, (lane + 64 * (t + NB - NP)) * PB);
+          if constexpr (FUSED) rd[t % NB] = HS<T>::load_buf(rsdn, (lane + 64 * (t + NB - NP)) * PB);
+        }
+        // keep the order: a load hoisted above the pieces still to be
+        // consumed would hold a second set of registers
+        __builtin_amdgcn_sched_barrier(0);
+      };
+      if (more) {
+        static_for<NP>([&](auto tc) { step(tc, true); });
+      } else {
+        static_for<NP>([&](auto tc) { step(tc, false); });
+      }
+      seg = segn;
+      off = offn;
+      dot = wave_total_f64(dot);
+      ss = wave_total_f32(ss);
+      if (lane == 0) {
+        s_pd[q] = dot;
+        s_ps[q] = ss;
+      }
+      q = qn;
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < nr; k += kVisThreads) {
+      double res = 0.0;
+      if (k < nv) {
+        double c[2] = {0.0, 0.0};
+        for (int s = 0; s < nslots; ++s) {
+          double dot = 0.0;
+          float ss = 0.f;
+          for (int g = 0; g < nseg; ++g) {
+            dot += s_pd[k * per_row + s * nseg + g];
+            ss += s_ps[k * per_row + s * nseg + g];
+          }
+          c[s] = ss > 0.f ? dot / sqrt((double)ss) : 0.0;
+        }
+        res = nslots == 2 ? c[1] - c[0] : c[0];
+      }
+      out[(size_t)b * m_cap + r0 + k] = (float)res;
+    }
+    __syncthreads();  // the partials are reused by the next round
   }
+}
+
+// The visual kernel's LDS: the staged directions and one round's partials.
+template <typename T, bool FUSED>
+size_t vis_lds_bytes(int nslots, int Dh) {
+  const int seg = 64 * kVisPieces<T>;
+  const int nseg = (Dh / 8 + seg - 1) / seg;
+  return sizeof(double) * nslots * Dh + (sizeof(double) + sizeof(float)) * kVisRows * nslots * nseg;
 }
 
 int txt_chunks(int64_t n_cap) { return (int)((n_cap + kTxtChunk - 1) / kTxtChunk); }
@@ -281,10 +556,6 @@ size_t cossim_ws(int B, int Dh, int64_t n_cap) {
   return off;
 }
 
-// Largest hidden size whose two float64 direction vectors fit the vis
-// kernel's LDS.
-constexpr int kMaxDh = 8192;
-
 // FUSED (the prefill epilogue, nslots == 1): the rows are prev + delta
 // (hv/ht the previous hidden states, dv/dt the deltas), written to ov/ot on
 // the first read; the text directions then read ot.
@@ -295,9 +566,9 @@ pvlm_status launch_cossim(int nslots, int64_t voff0, int64_t voff1, int64_t toff
                           double* u, double* part, int32_t* status, hipStream_t stream,
                           const T* dv = nullptr, T* ov = nullptr, const T* dt = nullptr,
                           T* ot = nullptr) {
-  const int lds = (int)(sizeof(double) * nslots * Dh);
+  const int lds = (int)vis_lds_bytes<T, FUSED>(nslots, Dh);
   PVLM_HIP(allow_dynamic_lds(reinterpret_cast<const void*>(vis_kernel<T, FUSED>),
-                             2 * kMaxDh * (int)sizeof(double)));
+                             (int)vis_lds_bytes<T, FUSED>(2, kMaxDh)));
   DeviceInfo di;
   const pvlm_status st = device_info(&di);
   if (st != PVLM_OK) return st;
