@@ -58,6 +58,33 @@ def test_cossim_small_literal(dtype, L, Dh):
     assert np.all(to_host_f64(s)[1, 211:] == 0)
 
 
+@pytest.mark.parametrize("dtype,Dh,frames,tpf", [
+    ("bf16", 4896, 2, 150),    # a second segment of 100 pieces: whole and partial lanes
+    ("f32", 2368, 2, 150),     # the same for fp32 (segments of 256 pieces)
+    ("bf16", 5120, 2, 100),    # Qwen2.5-VL-32B hidden size
+    ("bf16", 3584, 2, 100),    # LLaVA-OV-7B hidden size: one segment, last piece past the row
+    ("bf16", 64, 200, 200),    # 40000 rows: more than one 128-row round per workgroup
+])
+def test_cossim_segments_and_rounds(dtype, Dh, frames, tpf):
+    """The visual kernel's units at segment and round boundaries: hidden
+    sizes whose last segment is partial, and rows enough that a workgroup
+    takes them in several rounds; every row against the oracle at the gate."""
+    w = W.WORKLOADS["tiny"]
+    w = W.Workload(**{**w.__dict__, "dtype": dtype, "batch": 1, "n_text": 24, "frames": frames,
+                      "tokens_per_frame": tpf})
+    h = W.make_hidden_inputs(w, 1, hidden=Dh)
+    m = h.m.astype(np.int32)
+    n = h.n.astype(np.int32)
+    note(f"uvprune cossim segments {dtype} Dh={Dh} m={int(m[0])}")
+    s = pv.uvprune_score_cossim(to_dev(h.hv), to_dev(h.ht), to_dev(m), to_dev(n))
+    torch.cuda.synchronize()
+    hv64, ht64 = f64(h.hv, dtype), f64(h.ht, dtype)
+    ref = oracle.uvprune_score_cossim(hv64, ht64, m, n)
+    cL = oracle.criterion_cossim(hv64[1], ht64[1], m, n)
+    c0 = oracle.criterion_cossim(hv64[0], ht64[0], m, n)
+    _assert_score(to_host_f64(s), ref, np.abs(cL) + np.abs(c0))
+
+
 def test_cossim_72b_shape_sampled():
     w = W.WORKLOADS["llava72b"]
     L = w.crit_layers
@@ -105,7 +132,8 @@ def test_cossim_streamed_over_layers(dtype, L):
     _assert_score(to_host_f64(s), ref, np.abs(cL) + np.abs(c0))
 
 
-@pytest.mark.parametrize("dtype,Dh", [("bf16", 512), ("f32", 256), ("bf16", 8192)])
+@pytest.mark.parametrize("dtype,Dh", [("bf16", 512), ("f32", 256), ("bf16", 8192), ("bf16", 4896),
+                                      ("f32", 2368)])
 def test_prefill_epilogue_fused(dtype, Dh):
     """pvlm_prefill_epilogue_cossim: the residual add bit-exact against the
     oracle (sum in fp32, one rounding), rows past m / n untouched, and the
