@@ -313,9 +313,9 @@ pvlm_status pvlm_rope_append_paged(pvlm_dtype dt, int B, int T, int Hq, int Hkv,
  * Limits, checked before any launch: m_cap <= 2^30 (PVLM_ERR_SHAPE); MASS:
  * B * m_cap rounded up to 256 <= 2^32 - 256 (one work-item per score in one
  * launch; PVLM_ERR_SHAPE); COSSIM: Dh <= 8192 (two float64 directions in the
- * visual kernel's LDS; PVLM_ERR_UNSUPPORTED), 2*B <= 65535,
- * ceil(n_cap / 32) <= 65535 and 64 * 2 * B * n_cap (one wave per text row of
- * both layers, rounded up to 256) <= 2^32 - 256 (PVLM_ERR_SHAPE).
+ * visual kernel's LDS; PVLM_ERR_UNSUPPORTED), 2*B <= 65535 and
+ * 64 * 2 * B * n_cap (one wave per text row of both layers, rounded up to
+ * 256) <= 2^32 - 256 (PVLM_ERR_SHAPE).
  * ---------------------------------------------------------------------- */
 size_t pvlm_uvprune_workspace_size(pvlm_crit crit, int B, int Dh, int64_t n_cap);
 pvlm_status pvlm_uvprune_score(pvlm_crit crit, int B, int L, int64_t m_cap, const int32_t* m,

@@ -269,74 +269,62 @@ __global__ void __launch_bounds__(256) txt_norm_kernel(const T* ht, int64_t off0
   if (lane == 0) inv_norm[wid] = inv;
 }
 
-// u[slot][b][d] = sum_{j<n[b]} ht[layer][b][j][d] * inv_norm[slot][b][j], in
-// two steps so that many workgroups share the rows: partial sums over chunks
-// of kTxtChunk text rows (one wave per 512 columns and chunk, each lane 8
-// columns), then the chunks' sums in chunk order.
-constexpr int kTxtChunk = 32;
-
+// u[slot][b][d] in one pass: one 1024-thread workgroup per (512 columns,
+// slot, batch row).  Wave w sums rows [w R, (w + 1) R), R = ceil(n / 16), for
+// its lanes' 8 columns each, loading kDirRows rows at a time through a buffer
+// resource over them; the waves' sums then meet in LDS and are added in wave
+// order.
+constexpr int kDirWaves = 16;
 template <typename T>
-__global__ void __launch_bounds__(64) txt_dir_part_kernel(const T* ht, int64_t off0, int64_t off1,
-                                                          const int32_t* n_txt, int B,
-                                                          int64_t n_cap, int Dh, int nchunk,
-                                                          const double* inv_norm, double* part) {
-  // the chunk's rows load in batches of RB, every load of a batch in flight
-  // together; rows past the chunk's end read as zeros through the buffer
-  // resource and get weight 0, so they add exact zeros
-  constexpr int RB = sizeof(T) == 2 ? kTxtChunk : kTxtChunk / 2;
-  const int c = blockIdx.y, sb = blockIdx.z, slot = sb / B, b = sb % B;
-  const int d = (blockIdx.x * 64 + threadIdx.x) * 8;
-  if (d >= Dh) return;
+__global__ void __launch_bounds__(64 * kDirWaves) txt_dir_kernel(const T* ht, int64_t off0, int64_t off1,
+                                                                 const int32_t* n_txt, int B, int64_t n_cap,
+                                                                 int Dh, const double* inv_norm, double* u) {
+  constexpr int RB = sizeof(T) == 2 ? 16 : 8;  // rows in flight per lane
+  __shared__ double s_acc[kDirWaves][512];
+  const int sb = blockIdx.y, slot = sb / B, b = sb % B;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: row weights are scalar
+  const int d = blockIdx.x * 512 + lane * 8;
   int nb = n_txt[b];
   nb = nb < 0 ? 0 : (nb > n_cap ? (int)n_cap : nb);
-  const int j0 = c * kTxtChunk, j1 = min(nb, j0 + kTxtChunk);
-  const T* base = ht + (slot ? off1 : off0) + ((size_t)b * n_cap + j0) * Dh;
-  const double* inv = inv_norm + ((size_t)slot * B + b) * n_cap;
-  const int rows = max(0, j1 - j0);
-  const auto rs = buf_rsrc(base, rows * Dh * (int)sizeof(T));
+  const int R = (nb + kDirWaves - 1) / kDirWaves;
+  const int j0 = min(nb, wave * R), rows = min(nb, j0 + R) - j0;
   double acc[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
-  for (int jb = 0; jb < rows; jb += RB) {
-    typename HS<T>::Raw r[RB];
-    double w[RB];
+  if (d < Dh) {
+    const T* base = ht + (slot ? off1 : off0) + ((size_t)b * n_cap + j0) * Dh;
+    const double* inv = inv_norm + ((size_t)slot * B + b) * n_cap + j0;
+    for (int jb = 0; jb < rows; jb += RB) {
+      const int nr = min(RB, rows - jb);  // rows past nr read as zeros and get weight 0
+      const auto rs = buf_rsrc(base + (size_t)jb * Dh, nr * Dh * (int)sizeof(T));
+      typename HS<T>::Raw r[RB];
+      double w[RB];
 #pragma unroll
-    for (int i = 0; i < RB; ++i) {
-      r[i] = HS<T>::template load_buf<0>(rs, ((jb + i) * Dh + d) * (int)sizeof(T));
-      const double wi = inv[j0 + min(jb + i, rows - 1)];
-      w[i] = jb + i < rows ? wi : 0.0;
-    }
+      for (int i = 0; i < RB; ++i) {
+        r[i] = HS<T>::template load_buf<0>(rs, (i * Dh + d) * (int)sizeof(T));
+        const double wi = inv[jb + min(i, nr - 1)];
+        w[i] = i < nr ? wi : 0.0;
+      }
 #pragma unroll
-    for (int i = 0; i < RB; ++i) {
-      float f[8];
-      HS<T>::unpack(r[i], f);
+      for (int i = 0; i < RB; ++i) {
+        float f[8];
+        HS<T>::unpack(r[i], f);
 #pragma unroll
-      for (int k = 0; k < 8; ++k) acc[k] = fma((double)f[k], w[i], acc[k]);
+        for (int k = 0; k < 8; ++k) acc[k] = fma((double)f[k], w[i], acc[k]);
+      }
     }
   }
-  double* pp = part + ((size_t)sb * nchunk + c) * Dh + d;
 #pragma unroll
-  for (int k = 0; k < 8; k += 2) *reinterpret_cast<double2*>(pp + k) = make_double2(acc[k], acc[k + 1]);
-}
-
-__global__ void __launch_bounds__(256) txt_dir_sum_kernel(const double* part, int Dh, int nchunk,
-                                                          double* u) {
-  // chunks in batches of CB, every load of a batch in flight together (past
-  // the last chunk the index is clamped and the value not added); the sum
-  // runs in chunk order
-  constexpr int CB = 8;
-  const int sb = blockIdx.y;
-  const int d = blockIdx.x * 256 + threadIdx.x;
-  if (d >= Dh) return;
-  const double* p = part + (size_t)sb * nchunk * Dh + d;
-  double acc = 0.0;
-  for (int c0 = 0; c0 < nchunk; c0 += CB) {
-    double v[CB];
+  for (int k = 0; k < 8; ++k) s_acc[wave][lane * 8 + k] = acc[k];
+  __syncthreads();
+  if (threadIdx.x < 512) {
+    const int dd = blockIdx.x * 512 + threadIdx.x;
+    if (dd < Dh) {
+      double t = 0.0;
 #pragma unroll
-    for (int i = 0; i < CB; ++i) v[i] = p[(size_t)min(c0 + i, nchunk - 1) * Dh];
-#pragma unroll
-    for (int i = 0; i < CB; ++i)
-      if (c0 + i < nchunk) acc += v[i];
+      for (int w = 0; w < kDirWaves; ++w) t += s_acc[w][threadIdx.x];
+      u[(size_t)sb * Dh + dd] = t;
+    }
   }
-  u[(size_t)sb * Dh + d] = acc;
 }
 
 // c_slot = <hv, u_slot> / |hv| (0 for zero norm) for the visual rows.  A
@@ -546,13 +534,10 @@ size_t vis_lds_bytes(int nslots, int Dh) {
   return sizeof(double) * nslots * Dh + (sizeof(double) + sizeof(float)) * kVisRows * nslots * nseg;
 }
 
-int txt_chunks(int64_t n_cap) { return (int)((n_cap + kTxtChunk - 1) / kTxtChunk); }
-
-// inverse norms [2][B][n_cap], u [2][B][Dh], chunk partials [2][B][chunks][Dh], all float64
+// inverse norms [2][B][n_cap], u [2][B][Dh], both float64
 size_t cossim_ws(int B, int Dh, int64_t n_cap) {
   size_t off = align_up(sizeof(double) * 2 * (size_t)B * n_cap, 256);
   off = align_up(off + sizeof(double) * 2 * (size_t)B * Dh, 256);
-  off = align_up(off + sizeof(double) * 2 * (size_t)B * txt_chunks(n_cap) * Dh, 256);
   return off;
 }
 
@@ -563,7 +548,7 @@ template <typename T, bool FUSED = false>
 pvlm_status launch_cossim(int nslots, int64_t voff0, int64_t voff1, int64_t toff0, int64_t toff1,
                           int B, int64_t m_cap, const int32_t* m, int Dh, int64_t n_cap,
                           const int32_t* n_txt, const T* hv, const T* ht, float* outp, double* inv,
-                          double* u, double* part, int32_t* status, hipStream_t stream,
+                          double* u, int32_t* status, hipStream_t stream,
                           const T* dv = nullptr, T* ov = nullptr, const T* dt = nullptr,
                           T* ot = nullptr) {
   const int lds = (int)vis_lds_bytes<T, FUSED>(nslots, Dh);
@@ -579,13 +564,8 @@ pvlm_status launch_cossim(int nslots, int64_t voff0, int64_t voff1, int64_t toff
   hipLaunchKernelGGL((txt_norm_kernel<T, FUSED>), dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream,
                      ht, toff0, toff1, n_txt, nslots, B, n_cap, Dh, inv, status, dt, ot);
   PVLM_LAUNCHED();
-  const int nchunk = txt_chunks(n_cap);
-  hipLaunchKernelGGL(txt_dir_part_kernel<T>, dim3((Dh / 8 + 63) / 64, nchunk, nslots * B), dim3(64), 0,
-                     stream, FUSED ? static_cast<const T*>(ot) : ht, toff0, toff1, n_txt, B, n_cap, Dh,
-                     nchunk, inv, part);
-  PVLM_LAUNCHED();
-  hipLaunchKernelGGL(txt_dir_sum_kernel, dim3((Dh + 255) / 256, nslots * B), dim3(256), 0, stream, part,
-                     Dh, nchunk, u);
+  hipLaunchKernelGGL(txt_dir_kernel<T>, dim3((Dh + 511) / 512, nslots * B), dim3(64 * kDirWaves), 0, stream,
+                     FUSED ? static_cast<const T*>(ot) : ht, toff0, toff1, n_txt, B, n_cap, Dh, inv, u);
   PVLM_LAUNCHED();
   hipLaunchKernelGGL((vis_kernel<T, FUSED>), dim3((unsigned)vis_x, B), dim3(kVisThreads), lds, stream, hv,
                      voff0, voff1, m, nslots, B, m_cap, Dh, u, outp, status, dv, ov);
@@ -606,11 +586,11 @@ pvlm_status run_cossim(int nslots, int L, int B, int64_t m_cap, const int32_t* m
   if (hdt != PVLM_F32 && hdt != PVLM_BF16) return PVLM_ERR_UNSUPPORTED;
   if (B < 1 || m_cap < 1 || n_cap < 1 || Dh < 8 || Dh % 8 != 0) return PVLM_ERR_SHAPE;
   if (Dh > kMaxDh) return PVLM_ERR_UNSUPPORTED;
-  // launch limits: grid y and z of at most 65535 (the text-direction
-  // partials run over 2 * B batch-slots and n_cap / 32 chunks), and one
-  // 64-lane wave per text row of both slots, in one launch of at most
-  // 2^32 - 256 work-items
-  if (m_cap > ((int64_t)1 << 30) || 2 * (int64_t)B > 65535 || txt_chunks(n_cap) > 65535 ||
+  // launch limits: grid y of at most 65535 (the text directions and the
+  // visual rows run over 2 * B batch-slots and B batch rows), and one 64-lane
+  // wave per text row of both slots, in one launch of at most 2^32 - 256
+  // work-items
+  if (m_cap > ((int64_t)1 << 30) || 2 * (int64_t)B > 65535 ||
       ((int64_t)2 * B * n_cap + 3) / 4 * 256 > ((int64_t)1 << 32) - 256)
     return PVLM_ERR_SHAPE;
   if (nslots == 2 && L < 1) return PVLM_ERR_SHAPE;
@@ -620,7 +600,6 @@ pvlm_status run_cossim(int nslots, int L, int B, int64_t m_cap, const int32_t* m
   double* inv = reinterpret_cast<double*>(w);
   const size_t off_u = align_up(sizeof(double) * 2 * (size_t)B * n_cap, 256);
   double* u = reinterpret_cast<double*>(w + off_u);
-  double* part = reinterpret_cast<double*>(w + align_up(off_u + sizeof(double) * 2 * (size_t)B * Dh, 256));
   const int64_t vls = (int64_t)B * m_cap * Dh, tls = (int64_t)B * n_cap * Dh;
   const int64_t l1 = nslots == 2 ? L : 0;
   if (dv) {
@@ -628,22 +607,22 @@ pvlm_status run_cossim(int nslots, int L, int B, int64_t m_cap, const int32_t* m
     if (hdt == PVLM_BF16)
       return launch_cossim<H, true>(1, 0, 0, 0, 0, B, m_cap, m, Dh, n_cap, n_txt,
                                     static_cast<const H*>(hs_vis), static_cast<const H*>(hs_txt),
-                                    outp, inv, u, part, status, stream, static_cast<const H*>(dv),
+                                    outp, inv, u, status, stream, static_cast<const H*>(dv),
                                     static_cast<H*>(ov), static_cast<const H*>(dt), static_cast<H*>(ot));
     return launch_cossim<float, true>(1, 0, 0, 0, 0, B, m_cap, m, Dh, n_cap, n_txt,
                                       static_cast<const float*>(hs_vis),
-                                      static_cast<const float*>(hs_txt), outp, inv, u, part, status,
+                                      static_cast<const float*>(hs_txt), outp, inv, u, status,
                                       stream, static_cast<const float*>(dv), static_cast<float*>(ov),
                                       static_cast<const float*>(dt), static_cast<float*>(ot));
   }
   if (hdt == PVLM_BF16)
     return launch_cossim<uint16_t>(nslots, 0, l1 * vls, 0, l1 * tls, B, m_cap, m, Dh, n_cap, n_txt,
                                    static_cast<const uint16_t*>(hs_vis),
-                                   static_cast<const uint16_t*>(hs_txt), outp, inv, u, part, status,
+                                   static_cast<const uint16_t*>(hs_txt), outp, inv, u, status,
                                    stream);
   return launch_cossim<float>(nslots, 0, l1 * vls, 0, l1 * tls, B, m_cap, m, Dh, n_cap, n_txt,
                               static_cast<const float*>(hs_vis), static_cast<const float*>(hs_txt),
-                              outp, inv, u, part, status, stream);
+                              outp, inv, u, status, stream);
 }
 
 }  // namespace

@@ -137,7 +137,7 @@ def test_uvprune_rejects_more_work_items_than_one_launch_holds():
     assert L.pvlm_uvprune_score(0, 8, 1, 1 << 30, FAKE, FAKE, 0, 0, 0, None, None, None, FAKE,
                                 None, 0, None, None) == 2
     # COSSIM: 64 lanes * 2 * B * n_cap = 64 * 2 * 17 * (2^21 - 32) > 2^32 - 256, while
-    # its n_cap / 32 = 65535 chunks and 2 * B stay within the grid's y and z
+    # 2 * B stays within the grid's y
     assert L.pvlm_uvprune_score(1, 17, 2, 10, FAKE, None, 1, 8, (1 << 21) - 32, FAKE, FAKE, FAKE,
                                 FAKE, FAKE, 1 << 40, None, None) == 2
     assert L.pvlm_uvprune_score(1, 8, 2, 10, FAKE, None, 1, 8, (1 << 21) - 32, FAKE, FAKE, FAKE,
