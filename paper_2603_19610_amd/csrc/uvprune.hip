@@ -91,13 +91,14 @@ struct HS<uint16_t> {
     return {__builtin_amdgcn_raw_buffer_load_b128(rs, boff, 0, AUX)};
   }
   // f holds bf16 values (widened exactly), so their high halves are the bf16 words
+  template <int AUX = kBufNT>
   static __device__ __forceinline__ void store_buf(const float (&f)[8], __amdgpu_buffer_rsrc_t rs, int boff) {
     uint32_t w[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k)
       w[k] = (__float_as_uint(f[2 * k]) >> 16) | (__float_as_uint(f[2 * k + 1]) & 0xFFFF0000u);
     const u32x4 v = {w[0], w[1], w[2], w[3]};
-    __builtin_amdgcn_raw_buffer_store_b128(v, rs, boff, 0, kBufNT);
+    __builtin_amdgcn_raw_buffer_store_b128(v, rs, boff, 0, AUX);
   }
 };
 template <>
@@ -126,10 +127,11 @@ struct HS<float> {
     const u32x4 b = __builtin_amdgcn_raw_buffer_load_b128(rs, boff + 16, 0, AUX);
     return {__builtin_bit_cast(f32x4, a), __builtin_bit_cast(f32x4, b)};
   }
+  template <int AUX = kBufNT>
   static __device__ __forceinline__ void store_buf(const float (&f)[8], __amdgpu_buffer_rsrc_t rs, int boff) {
     const f32x4 a = {f[0], f[1], f[2], f[3]}, b = {f[4], f[5], f[6], f[7]};
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, a), rs, boff, 0, kBufNT);
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, b), rs, boff + 16, 0, kBufNT);
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, a), rs, boff, 0, AUX);
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, b), rs, boff + 16, 0, AUX);
   }
 };
 
@@ -256,12 +258,41 @@ __global__ void __launch_bounds__(256) txt_norm_kernel(const T* ht, int64_t off0
   if (j < nb) {
     const size_t roff = (slot ? off1 : off0) + ((size_t)b * n_cap + j) * Dh;
     double ss = 0.0;
-#pragma unroll 8  // the row's loads in flight together
-    for (int d = lane * 8; d < Dh; d += 512) {
-      float f[8];
-      row8<T, FUSED>(ht, dt, ot, roff + d, f);
+    if constexpr (FUSED) {
+      // every piece of the row (prev and delta) in flight before the first
+      // store: the stores count in the same wait counter as the loads, so
+      // a store between loads would make each later load wait for all
+      // (pieces past the row's end read as zeros, add exact zeros, and
+      // their stores are dropped); the same order as the plain loop below
+      constexpr int NBT = sizeof(T) == 2 ? 16 : 8;
+      const int rb = Dh * (int)sizeof(T);
+      const auto rs = buf_rsrc(ht + roff, rb), rsd = buf_rsrc(dt + roff, rb), os = buf_rsrc(ot + roff, rb);
+      for (int d0 = 0; d0 < Dh; d0 += 512 * NBT) {
+        typename HS<T>::Raw r[NBT], rd[NBT];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) ss = fma((double)f[k], (double)f[k], ss);
+        for (int t = 0; t < NBT; ++t) {
+          r[t] = HS<T>::template load_buf<0>(rs, (d0 + lane * 8 + 512 * t) * (int)sizeof(T));
+          rd[t] = HS<T>::template load_buf<0>(rsd, (d0 + lane * 8 + 512 * t) * (int)sizeof(T));
+        }
+#pragma unroll
+        for (int t = 0; t < NBT; ++t) {
+          float f[8], g[8];
+          HS<T>::unpack(r[t], f);
+          HS<T>::unpack(rd[t], g);
+          add_round8(T(), f, g);
+          HS<T>::template store_buf<0>(f, os, (d0 + lane * 8 + 512 * t) * (int)sizeof(T));
+#pragma unroll
+          for (int k = 0; k < 8; ++k) ss = fma((double)f[k], (double)f[k], ss);
+        }
+      }
+    } else {
+#pragma unroll 8  // the row's loads in flight together
+      for (int d = lane * 8; d < Dh; d += 512) {
+        float f[8];
+        row8<T, FUSED>(ht, dt, ot, roff + d, f);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) ss = fma((double)f[k], (double)f[k], ss);
+      }
     }
     ss = wave_sum_f64(ss);
     inv = ss > 0.0 ? 1.0 / sqrt(ss) : 0.0;
@@ -384,7 +415,7 @@ __device__ __forceinline__ void vis_piece(const typename HS<T>::Raw& r, const ty
     float g[8];
     HS<T>::unpack(rd, g);
     add_round8(T(), f, g);
-    HS<T>::store_buf(f, os, boff);
+    HS<T>::template store_buf<kBufNT>(f, os, boff);
   }
   double2 w[4];
 #pragma unroll
