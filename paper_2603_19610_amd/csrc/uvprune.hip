@@ -365,10 +365,12 @@ __global__ void __launch_bounds__(64 * kDirWaves) txt_dir_kernel(const T* ht, in
 // segment of 64 * kVisPieces 8-element pieces) that its waves take in turn,
 // so every wave carries nearly the same load.  Lane l of a unit handles
 // pieces segment * 64 * kVisPieces + l + 64 t, t < kVisPieces (16-byte
-// loads), kVisBatch of them in registers at a time: as it consumes a piece
-// it issues the next one (of this unit, then of its next unit) into the
-// same registers, so a unit's loads are in flight while the one before is
-// reduced.  A unit's dot product and squared norm (wave totals) go to LDS,
+// loads).  The plain kernel holds a unit's pieces in registers and, as it
+// consumes piece t, issues piece t of its next unit into the same
+// registers, so a unit's loads are in flight while the one before is
+// reduced.  The fused kernel loads a whole unit (prev and delta) before it
+// adds and stores: its stores share the loads' wait counter.
+// A unit's dot product and squared norm (wave totals) go to LDS,
 // and one thread per row then sums the segments in order.  u is staged as
 // s_u[slot][k / 2][d / 8][k % 2]: a lane reads its 8 directions of a piece
 // as four 16-byte words, and the lanes of a wave read consecutive words.
@@ -382,14 +384,10 @@ constexpr int kMaxDh = 8192;
 constexpr int kVisThreads = 1024;
 constexpr int kVisWaves = kVisThreads / 64;
 constexpr int kVisRows = 128;
-// Pieces per lane and unit (the summation grouping, the same for the fused
-// and the plain kernel, so both give the same sums bit for bit), and pieces
-// in flight per lane (the register budget: the fused kernel also holds the
-// deltas).
+// Pieces per lane and unit: the summation grouping, the same for the fused
+// and the plain kernel, so both give the same sums bit for bit.
 template <typename T>
 constexpr int kVisPieces = sizeof(T) == 2 ? 8 : 4;
-template <typename T, bool FUSED>
-constexpr int kVisBatch = FUSED ? kVisPieces<T> / 4 : kVisPieces<T>;
 
 // f(integral_constant<int, I>) for I = 0 .. N-1, unrolled at compile time.
 template <int N, int I = 0, typename F>
@@ -439,7 +437,6 @@ __global__ void __launch_bounds__(kVisThreads) vis_kernel(const T* hv, int64_t o
   // and fp32 squared norms, [kVisRows][nslots][nseg] each
   extern __shared__ __align__(16) double s_u[];
   constexpr int NP = kVisPieces<T>;
-  constexpr int NB = kVisBatch<T, FUSED>;
   constexpr int SEG = 64 * NP;  // pieces per segment
   const int b = blockIdx.y;
   const int lane = threadIdx.x & 63;
@@ -473,67 +470,83 @@ __global__ void __launch_bounds__(kVisThreads) vis_kernel(const T* hv, int64_t o
     const int nr = (int)min((int64_t)kVisRows, r_end - r0);
     const int nv = (int)max((int64_t)0, min((int64_t)nr, (int64_t)mb - r0));  // rows with data
     const int U = nv * per_row;
-    // a ring of NB pieces in registers: piece t of a unit sits in slot
-    // t % NB; consuming it frees the slot for piece t + NB of the unit, or
-    // for the next unit's piece t + NB - NP
-    typename HS<T>::Raw r[NB], rd[NB];
     int q = wave, seg = 0;
     size_t off = 0;
-    if (q < U) {
-      off = unit(r0, q, seg);
-      const auto rs = rsrc(hv, off, seg);
-      const auto rsd = FUSED ? rsrc(dv, off, seg) : rs;
+    if constexpr (FUSED) {
+      // whole units: every piece's loads (prev and delta), then the adds,
+      // stores and sums; the stores count in the same wait counter as the
+      // loads, so a store between loads would make each later load wait
+      // for all
+      for (; q < U; q += kVisWaves) {
+        off = unit(r0, q, seg);
+        const int s = (q % per_row) / nseg;
+        const double* us = s_u + (size_t)s * 8 * D8;
+        const auto rs = rsrc(hv, off, seg), rsd = rsrc(dv, off, seg), os = rsrc(ov, off, seg);
+        typename HS<T>::Raw r[NP], rd[NP];
 #pragma unroll
-      for (int t = 0; t < NB; ++t) {
-        r[t] = HS<T>::load_buf(rs, (lane + 64 * t) * PB);
-        if constexpr (FUSED) rd[t] = HS<T>::load_buf(rsd, (lane + 64 * t) * PB);
-      }
-    }
-    while (q < U) {
-      const int qn = q + kVisWaves;
-      const int s = (q % per_row) / nseg;
-      const double* us = s_u + (size_t)s * 8 * D8;
-      const auto rs = rsrc(hv, off, seg);
-      const auto rsd = FUSED ? rsrc(dv, off, seg) : rs;
-      const auto os = FUSED ? rsrc(ov, off, seg) : rs;
-      double dot = 0.0;
-      float ss = 0.f;
-      const bool more = qn < U;
-      int segn = seg;
-      size_t offn = off;
-      if (more) offn = unit(r0, qn, segn);
-      const auto rsn = rsrc(hv, offn, segn);
-      const auto rsdn = FUSED ? rsrc(dv, offn, segn) : rsn;
-      // consume piece t, then refill its slot; the unit's own pieces first
-      auto step = [&](auto tc, bool next) {
-        constexpr int t = decltype(tc)::value;
-        const int j = min(seg * SEG + lane + 64 * t, D8 - 1);
-        vis_piece<T, FUSED>(r[t % NB], rd[t % NB], os, (lane + 64 * t) * PB, us, D8, j, dot, ss);
-        if constexpr (t + NB < NP) {
-          r[t % NB] = HS<T>::load_buf(rs, (lane + 64 * (t + NB)) * PB);
-          if constexpr (FUSED) rd[t % NB] = HS<T>::load_buf(rsd, (lane + 64 * (t + NB)) * PB);
-        } else if (next) {
-          r[t % NB] = HS<T>::load_buf(rsn, (lane + 64 * (t + NB - NP)) * PB);
-          if constexpr (FUSED) rd[t % NB] = HS<T>::load_buf(rsdn, (lane + 64 * (t + NB - NP)) * PB);
+        for (int t = 0; t < NP; ++t) {
+          r[t] = HS<T>::load_buf(rs, (lane + 64 * t) * PB);
+          rd[t] = HS<T>::load_buf(rsd, (lane + 64 * t) * PB);
         }
-        // keep the order: a load hoisted above the pieces still to be
-        // consumed would hold a second set of registers
-        __builtin_amdgcn_sched_barrier(0);
-      };
-      if (more) {
-        static_for<NP>([&](auto tc) { step(tc, true); });
-      } else {
-        static_for<NP>([&](auto tc) { step(tc, false); });
+        double dot = 0.0;
+        float ss = 0.f;
+#pragma unroll
+        for (int t = 0; t < NP; ++t) {
+          const int j = min(seg * SEG + lane + 64 * t, D8 - 1);
+          vis_piece<T, FUSED>(r[t], rd[t], os, (lane + 64 * t) * PB, us, D8, j, dot, ss);
+        }
+        dot = wave_total_f64(dot);
+        ss = wave_total_f32(ss);
+        if (lane == 0) {
+          s_pd[q] = dot;
+          s_ps[q] = ss;
+        }
       }
-      seg = segn;
-      off = offn;
-      dot = wave_total_f64(dot);
-      ss = wave_total_f32(ss);
-      if (lane == 0) {
-        s_pd[q] = dot;
-        s_ps[q] = ss;
+    } else {
+      // a unit's NP pieces in registers; consuming piece t frees its
+      // registers for piece t of the wave's next unit
+      typename HS<T>::Raw r[NP];
+      if (q < U) {
+        off = unit(r0, q, seg);
+        const auto rs = rsrc(hv, off, seg);
+#pragma unroll
+        for (int t = 0; t < NP; ++t) r[t] = HS<T>::load_buf(rs, (lane + 64 * t) * PB);
       }
-      q = qn;
+      while (q < U) {
+        const int qn = q + kVisWaves;
+        const int s = (q % per_row) / nseg;
+        const double* us = s_u + (size_t)s * 8 * D8;
+        double dot = 0.0;
+        float ss = 0.f;
+        const bool more = qn < U;
+        int segn = seg;
+        size_t offn = off;
+        if (more) offn = unit(r0, qn, segn);
+        const auto rsn = rsrc(hv, offn, segn);
+        auto step = [&](auto tc, bool next) {
+          constexpr int t = decltype(tc)::value;
+          const int j = min(seg * SEG + lane + 64 * t, D8 - 1);
+          vis_piece<T, FUSED>(r[t], r[t], rsn, (lane + 64 * t) * PB, us, D8, j, dot, ss);
+          if (next) r[t] = HS<T>::load_buf(rsn, (lane + 64 * t) * PB);
+          // keep the order: a load hoisted above the pieces still to be
+          // consumed would hold a second set of registers
+          __builtin_amdgcn_sched_barrier(0);
+        };
+        if (more) {
+          static_for<NP>([&](auto tc) { step(tc, true); });
+        } else {
+          static_for<NP>([&](auto tc) { step(tc, false); });
+        }
+        seg = segn;
+        off = offn;
+        dot = wave_total_f64(dot);
+        ss = wave_total_f32(ss);
+        if (lane == 0) {
+          s_pd[q] = dot;
+          s_ps[q] = ss;
+        }
+        q = qn;
+      }
     }
     __syncthreads();
     for (int k = threadIdx.x; k < nr; k += kVisThreads) {
