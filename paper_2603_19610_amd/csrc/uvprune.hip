@@ -135,38 +135,9 @@ struct HS<float> {
   }
 };
 
-// The prefill epilogue's residual add: out = prev + delta, the sum taken in
-// fp32 and rounded once to the storage type; the rounded values are stored
-// and returned, so the criterion uses exactly the stored hidden state.
-template <bool NT>
-__device__ __forceinline__ void add_round_store8(uint16_t* out, float (&f)[8], const float (&g)[8]) {
-  uint32_t w[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const uint16_t lo = f32_to_bf16(f[2 * k] + g[2 * k]), hi = f32_to_bf16(f[2 * k + 1] + g[2 * k + 1]);
-    w[k] = (uint32_t)lo | ((uint32_t)hi << 16);
-    f[2 * k] = bf16_to_f32(lo);
-    f[2 * k + 1] = bf16_to_f32(hi);
-  }
-  const u32x4 v = {w[0], w[1], w[2], w[3]};
-  if constexpr (NT) __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(out));
-  else *reinterpret_cast<u32x4*>(out) = v;
-}
-template <bool NT>
-__device__ __forceinline__ void add_round_store8(float* out, float (&f)[8], const float (&g)[8]) {
-#pragma unroll
-  for (int k = 0; k < 8; ++k) f[k] += g[k];
-  const f32x4 a = {f[0], f[1], f[2], f[3]}, b = {f[4], f[5], f[6], f[7]};
-  if constexpr (NT) {
-    __builtin_nontemporal_store(a, reinterpret_cast<f32x4*>(out));
-    __builtin_nontemporal_store(b, reinterpret_cast<f32x4*>(out + 4));
-  } else {
-    *reinterpret_cast<f32x4*>(out) = a;
-    *reinterpret_cast<f32x4*>(out + 4) = b;
-  }
-}
-
-// The same add without the store: f becomes the stored values.
+// The prefill epilogue's residual add: prev + delta, the sum taken in fp32
+// and rounded once to the storage type.  f (prev) becomes the values that
+// are stored, so the criterion uses exactly the stored hidden state.
 __device__ __forceinline__ void add_round8(uint16_t, float (&f)[8], const float (&g)[8]) {
 #pragma unroll
   for (int k = 0; k < 8; ++k) f[k] = bf16_to_f32(f32_to_bf16(f[k] + g[k]));
@@ -174,21 +145,6 @@ __device__ __forceinline__ void add_round8(uint16_t, float (&f)[8], const float 
 __device__ __forceinline__ void add_round8(float, float (&f)[8], const float (&g)[8]) {
 #pragma unroll
   for (int k = 0; k < 8; ++k) f[k] += g[k];
-}
-
-// 8 consecutive elements of a hidden-state row at element offset `off`: the
-// row itself, or (FUSED) the epilogue's prev + delta, written to `out`.
-// NT: the visual rows, streamed once, go through the non-temporal cache
-// policy; the text rows are read again by the direction sums and keep the
-// ordinary one.
-template <typename T, bool FUSED, bool NT = false>
-__device__ __forceinline__ void row8(const T* h, const T* delta, T* out, size_t off, float (&f)[8]) {
-  HS<T>::template load8<NT>(h + off, f);
-  if constexpr (FUSED) {
-    float g[8];
-    HS<T>::template load8<NT>(delta + off, g);
-    add_round_store8<NT>(out + off, f, g);
-  }
 }
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
@@ -289,7 +245,7 @@ __global__ void __launch_bounds__(256) txt_norm_kernel(const T* ht, int64_t off0
 #pragma unroll 8  // the row's loads in flight together
       for (int d = lane * 8; d < Dh; d += 512) {
         float f[8];
-        row8<T, FUSED>(ht, dt, ot, roff + d, f);
+        HS<T>::load8(ht + roff + d, f);
 #pragma unroll
         for (int k = 0; k < 8; ++k) ss = fma((double)f[k], (double)f[k], ss);
       }
