@@ -69,6 +69,8 @@ def parse():
                     help="profiling helper: one eager step, then N 80-layer gathers, and exit")
     ap.add_argument("--copy-only", type=int, default=0,
                     help="profiling helper: N device copies of 512 MiB (counter calibration)")
+    ap.add_argument("--cossim-only", type=int, default=0,
+                    help="profiling helper: N eager UV-Prune similarity scores (72B hidden shape)")
     return ap.parse_args()
 
 
@@ -474,10 +476,8 @@ def single_layer_record(torch, pv, W, name, dev, steps):
     return rec
 
 
-def cossim_record(torch, pv, W, dev):
-    """UV-Prune similarity criterion on the 72B shape: layers 0 and L of the
-    hidden states (the layer sum telescopes), bf16, hidden size 8192."""
-    w = W.WORKLOADS["llava72b"]
+def cossim_inputs(torch, w, dev):
+    """Seeded hidden states of layers 0 and L (bf16) with the row counts."""
     B, m, n, Dh = w.batch, int(w.m_per_seq().max()), w.n_text, w.hidden
     gen = torch.Generator(device=dev)
     gen.manual_seed(260319610)
@@ -485,6 +485,15 @@ def cossim_record(torch, pv, W, dev):
     ht = torch.randn((2, B, n, Dh), device=dev, generator=gen).to(torch.bfloat16)
     m_t = torch.full((B,), m, dtype=torch.int32, device=dev)
     n_t = torch.full((B,), n, dtype=torch.int32, device=dev)
+    return hv, ht, m_t, n_t
+
+
+def cossim_record(torch, pv, W, dev):
+    """UV-Prune similarity criterion on the 72B shape: layers 0 and L of the
+    hidden states (the layer sum telescopes), bf16, hidden size 8192."""
+    w = W.WORKLOADS["llava72b"]
+    hv, ht, m_t, n_t = cossim_inputs(torch, w, dev)
+    B, m = w.batch, hv.shape[2]
     score = torch.empty((B, m), dtype=torch.float32, device=dev)
     status = torch.zeros(1, dtype=torch.int32, device=dev)
     ws = pv.Workspace(dev)
@@ -810,6 +819,21 @@ def main():
         print(json.dumps({"copy_only": args.copy_only, "bytes_read": COPY_BYTES,
                           "bytes_written": COPY_BYTES}))
         del src, dst
+        teardown(torch, pv)
+        return
+
+    if args.cossim_only:  # the similarity criterion's kernels, eager, on the 72B hidden shape
+        w = W.WORKLOADS["llava72b"]
+        hv, ht, m_t, n_t = cossim_inputs(torch, w, dev)
+        score = torch.empty((w.batch, hv.shape[2]), dtype=torch.float32, device=dev)
+        status = torch.zeros(1, dtype=torch.int32, device=dev)
+        ws = pv.Workspace(dev)
+        for _ in range(args.cossim_only):
+            pv.uvprune_score_cossim(hv, ht, m_t, n_t, score=score, ws=ws, status=status)
+        torch.cuda.synchronize()
+        print(json.dumps({"cossim_only": args.cossim_only, "bytes_per_call": cossim_bytes(w),
+                          "status": int(status.item())}))
+        del hv, ht, score, ws
         teardown(torch, pv)
         return
 
